@@ -1,0 +1,352 @@
+"""CPU oracle for PISA's data-parallel hot path -- TEST INFRASTRUCTURE ONLY.
+
+This is a plain, slow, float64 restatement of what the paper defines, used to
+check the HIP library.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import it; the product path never does.
+It shares no code with the HIP library and imports nothing from the package.
+
+Paper: "Block Sparse Attention with Log-Linear Complexity" (PISA).
+Indices are 0-based here (the paper counts from 1).  All arithmetic is
+float64; bf16 inputs widen to float64 exactly.
+
+Contents and the passage each follows:
+
+* ``level_sizes``       -- hierarchy sizes, Sec. 3.2 eq. (key_hierarchy):
+                           M_1 = ceil(N/C), M_{l+1} = ceil(M_l / g).
+* ``build_pyramid``     -- mean pyramid, Sec. 3.2 eq. (mean_pyramid): leaf
+                           means of raw keys, then means over the *valid*
+                           children one level down.
+* ``lse``               -- natural-log LogSumExp, max-subtracted.
+* ``select_row``        -- coarse-to-fine Top-K, Sec. 3.2 eq.
+                           (hierarchical_topk) with the LSE score of eq.
+                           (direct_child_lse), the grouped-head sum of
+                           Sec. 3.3 eq. (kernel_grouped_score) and the causal
+                           eligibility / forced-block policy of App. B.
+* ``attention_row``     -- selected sparse attention, Sec. 3.1 eq.
+                           (selected_sparse_attention), causal cut of App. B.
+* ``flat_bsa_row``      -- flat block selection, Sec. 3.1 eqs.
+                           (bsa_block_scores, bsa_topk), with the per-head
+                           normalisation before the head sum of App. C.1.
+
+Readings of points the paper leaves open (each also recorded in the design
+notes of the repository):
+
+* R1  levels: the root sits at level L (M_L = 1) and is never scored.
+* R2  forced set: in causal mode the first, previous and current leaf blocks
+      and all their ancestors are kept inside the K budget without scores;
+      causal mode needs K >= 3.
+* R3  the "at most K candidates" test counts every eligible candidate,
+      forced ones included.
+* R4  ties: higher score first, then the smaller block index.
+* R5  eligibility: node i of level l (covering tokens from i*C*g^(l-1)) is a
+      candidate only if it exists and, in causal mode, starts at or before t.
+* R6  query row i sits at absolute position t = N - Nq + i.
+* R7  flat-BSA head normalisation = softmax over the eligible non-forced
+      blocks of each head, then the sum over the group's heads.
+* R8  grouped-query heads: query head h' uses KV head h' // (H / Hkv).
+* R9  outputs: selected leaf indices ascending, padded with -1 to K.
+* R10 attention with no visible token returns o = 0 and lse = -inf.
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+NEG_INF = -math.inf
+POS_INF = math.inf
+
+
+def level_sizes(N: int, C: int, g: int) -> list[int]:
+    """Return [M_1, ..., M_L] of the key hierarchy (Sec. 3.2, eq. key_hierarchy).
+
+    M_1 = ceil(N / C) leaf blocks; each coarser level merges up to g adjacent
+    blocks, M_{l+1} = ceil(M_l / g), until a single root block remains.
+    """
+    if N < 1 or C < 1 or g < 2:
+        raise ValueError("need N >= 1, C >= 1, g >= 2")
+    sizes = [-(-N // C)]
+    while sizes[-1] > 1:
+        sizes.append(-(-sizes[-1] // g))
+    return sizes
+
+
+def build_pyramid(k: np.ndarray, C: int, g: int) -> list[np.ndarray]:
+    """Mean pyramid of one KV head (Sec. 3.2, eq. mean_pyramid).
+
+    k: [N, d] keys.  Returns a list whose entry l-1 is the [M_l, d] array of
+    level-l summaries, l = 1..L.  Level 1 is the mean of the raw keys of each
+    leaf block (the last block may hold fewer than C keys); level l+1 is the
+    mean of the existing children at level l (the denominator counts valid
+    children only).
+    """
+    k = np.asarray(k, dtype=np.float64)
+    N, d = k.shape
+    M = level_sizes(N, C, g)
+    levels = []
+    leaf = np.empty((M[0], d))
+    for i in range(M[0]):
+        leaf[i] = k[i * C:min((i + 1) * C, N)].mean(axis=0)
+    levels.append(leaf)
+    for lv in range(1, len(M)):
+        below = levels[-1]
+        cur = np.empty((M[lv], d))
+        for i in range(M[lv]):
+            cur[i] = below[i * g:min((i + 1) * g, M[lv - 1])].mean(axis=0)
+        levels.append(cur)
+    return levels
+
+
+def lse(z: np.ndarray) -> float:
+    """Natural-log LogSumExp of a 1-D array, max-subtracted."""
+    z = np.asarray(z, dtype=np.float64)
+    if z.size == 0:
+        return NEG_INF
+    m = float(z.max())
+    if m == NEG_INF:
+        return NEG_INF
+    return m + math.log(float(np.exp(z - m).sum()))
+
+
+def forced_leaves(t: int, C: int, causal: bool) -> set[int]:
+    """First, previous and current leaf block of position t (App. B); empty if not causal."""
+    if not causal:
+        return set()
+    c = t // C
+    f = {0, c}
+    if c >= 1:
+        f.add(c - 1)
+    return f
+
+
+def select_row(qg: np.ndarray, k: np.ndarray, levels: list[np.ndarray], t: int,
+               C: int, g: int, K: int, causal: bool, trace: list | None = None):
+    """Pyramid Top-K selection for one query position and one KV head.
+
+    qg: [G, d] the query vectors of the G heads that share this KV head.
+    k:  [N, d] raw keys of the KV head (leaf-level scoring reads them).
+    levels: output of ``build_pyramid`` for the same keys.
+    t: absolute position of the query.
+
+    Returns (selected leaf indices ascending, min_gap) where min_gap is the
+    smallest margin, over all ranked levels, between the lowest kept score
+    and the highest dropped score (+inf if no level needed ranking).  If
+    ``trace`` is a list, one dict per level is appended with the candidate
+    set A, forced set F, kept set I and the scores u.
+
+    Steps (Sec. 3.2 eq. hierarchical_topk, eq. direct_child_lse; Sec. 3.3
+    eq. kernel_grouped_score; App. B):
+      start with the root at level L; at each level l = L..1 keep every
+      candidate if there are at most K of them, otherwise score each
+      non-forced candidate by the sum over the G heads of the LSE of its
+      children's scaled logits (child summaries of level l-1, or the raw keys
+      of the leaf block when l = 1) and keep the forced candidates plus the
+      K - |F| best scored ones; expand the kept blocks to their eligible
+      children at level l-1.
+    """
+    qg = np.asarray(qg, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    N, d = k.shape
+    M = [lv.shape[0] for lv in levels]
+    L = len(M)
+    scale = 1.0 / math.sqrt(d)
+    f_leaf = forced_leaves(t, C, causal)
+
+    def span(lv: int) -> int:
+        return C * g ** (lv - 1)
+
+    def eligible(lv: int, i: int) -> bool:
+        return i < M[lv - 1] and (not causal or i * span(lv) <= t)
+
+    def children(lv: int, i: int) -> range:
+        return range(i * g, min((i + 1) * g, M[lv - 2]))
+
+    A = [0]
+    min_gap = POS_INF
+    I: list[int] = [0]
+    for lv in range(L, 0, -1):
+        F = {j // g ** (lv - 1) for j in f_leaf} & set(A)
+        u: dict[int, float] = {}
+        if len(A) <= K:
+            I = sorted(A)
+        else:
+            free = [i for i in A if i not in F]
+            for i in free:
+                if lv >= 2:
+                    x = levels[lv - 2][list(children(lv, i))]
+                else:
+                    x = k[i * C:min((i + 1) * C, N)]
+                u[i] = sum(lse(x @ qh * scale) for qh in qg)
+            ranked = sorted(free, key=lambda i: (-u[i], i))
+            n_keep = K - len(F)
+            keep, drop = ranked[:n_keep], ranked[n_keep:]
+            if keep and drop:
+                min_gap = min(min_gap, u[keep[-1]] - u[drop[0]])
+            I = sorted(F | set(keep))
+        if trace is not None:
+            trace.append({"level": lv, "A": list(A), "F": set(F), "I": list(I), "u": dict(u)})
+        if lv > 1:
+            A = [r for i in I for r in children(lv, i) if eligible(lv - 1, r)]
+    return I, min_gap
+
+
+def attention_row(q: np.ndarray, k: np.ndarray, v: np.ndarray, blocks, t: int,
+                  C: int, causal: bool):
+    """Attention of one query over the tokens of the selected leaf blocks.
+
+    Sec. 3.1 eq. (selected_sparse_attention): softmax of q.k_j / sqrt(d) over
+    the union of the selected blocks' tokens, weights applied to the original
+    values; App. B: tokens after t are masked in causal mode.
+    Returns (o [d], lse) with lse the natural-log normaliser of the scaled
+    logits.  Negative block indices are padding and ignored.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    N, d = k.shape
+    tokens = sorted({j for i in blocks if i >= 0
+                     for j in range(i * C, min((i + 1) * C, N))
+                     if not causal or j <= t})
+    if not tokens:
+        return np.zeros(d), NEG_INF
+    kk = np.asarray(k[tokens], dtype=np.float64)
+    vv = np.asarray(v[tokens], dtype=np.float64)
+    z = kk @ q / math.sqrt(d)
+    row_lse = lse(z)
+    p = np.exp(z - row_lse)
+    return p @ vv, row_lse
+
+
+def flat_bsa_row(qg: np.ndarray, leaf_means: np.ndarray, t: int, C: int, K: int,
+                 causal: bool):
+    """Flat (single-level) block selection for one position and KV head.
+
+    Sec. 3.1: score every eligible leaf summary, s_i = q.kbar_i / sqrt(d)
+    (eq. bsa_block_scores), keep the K best (eq. bsa_topk).  App. C.1: the
+    scores are normalised within each query head before the sum over heads
+    (reading R7: softmax over the eligible non-forced blocks).  The forced
+    blocks of App. B are kept inside the budget.
+
+    Returns (selected indices ascending, min_gap) with the gap measured in
+    log units of the summed probabilities (equal to logit units when G = 1).
+    """
+    qg = np.asarray(qg, dtype=np.float64)
+    S1 = np.asarray(leaf_means, dtype=np.float64)
+    M1, d = S1.shape
+    c = t // C
+    E = [i for i in range(M1) if not causal or i <= c]
+    if len(E) <= K:
+        return sorted(E), POS_INF
+    F = forced_leaves(t, C, causal) & set(E)
+    free = [i for i in E if i not in F]
+    z = qg @ S1[free].T / math.sqrt(d)          # [G, |free|]
+    u = np.zeros(len(free))
+    for zh in z:
+        u += np.exp(zh - lse(zh))
+    logu = np.log(u)
+    order = sorted(range(len(free)), key=lambda j: (-logu[j], free[j]))
+    n_keep = K - len(F)
+    keep = [free[j] for j in order[:n_keep]]
+    gap = POS_INF
+    if n_keep > 0 and n_keep < len(free):
+        gap = logu[order[n_keep - 1]] - logu[order[n_keep]]
+    return sorted(F | set(keep)), gap
+
+
+# ---------------------------------------------------------------------------
+# Whole-tensor drivers (loops over batch, heads and the requested rows).
+# ---------------------------------------------------------------------------
+
+def pyramid_rows(levels: list[np.ndarray]) -> np.ndarray:
+    """Concatenate levels 1..max(1, L-1) (the root is never scored) into [R, d]."""
+    keep = levels[:-1] if len(levels) > 1 else levels
+    return np.concatenate(keep, axis=0)
+
+
+def _group(H: int, Hkv: int) -> int:
+    if H % Hkv:
+        raise ValueError("H must be a multiple of Hkv")
+    return H // Hkv
+
+
+def pyramid(k: np.ndarray, C: int, g: int) -> np.ndarray:
+    """[B, Hkv, N, d] keys -> [B, Hkv, R, d] concatenated pyramid (float64)."""
+    B, Hkv, N, d = k.shape
+    out = None
+    for b in range(B):
+        for h in range(Hkv):
+            rows = pyramid_rows(build_pyramid(k[b, h], C, g))
+            if out is None:
+                out = np.empty((B, Hkv, rows.shape[0], d))
+            out[b, h] = rows
+    return out
+
+
+def select(q, k, C, g, K, causal, rows=None, heads=None):
+    """Selection for rows of every (batch, KV head).
+
+    q: [B, H, Nq, d], k: [B, Hkv, N, d].  rows: iterable of query-row indices
+    (default all).  Returns (idx [B, Hkv, len(rows), K] int64 padded with -1,
+    gap [B, Hkv, len(rows)]).
+    """
+    B, H, Nq, d = q.shape
+    _, Hkv, N, _ = k.shape
+    G = _group(H, Hkv)
+    rows = list(range(Nq)) if rows is None else list(rows)
+    heads = list(range(Hkv)) if heads is None else list(heads)
+    idx = np.full((B, len(heads), len(rows), K), -1, dtype=np.int64)
+    gap = np.full((B, len(heads), len(rows)), POS_INF)
+    for b in range(B):
+        for hi, h in enumerate(heads):
+            kh = np.asarray(k[b, h], dtype=np.float64)
+            levels = build_pyramid(kh, C, g)
+            for ri, r in enumerate(rows):
+                t = N - Nq + r
+                qg = q[b, h * G:(h + 1) * G, r]
+                sel, gp = select_row(qg, kh, levels, t, C, g, K, causal)
+                idx[b, hi, ri, :len(sel)] = sel
+                gap[b, hi, ri] = gp
+    return idx, gap
+
+
+def sparse_attention(q, k, v, block_idx, C, causal, rows=None, heads=None):
+    """Attention for rows of every query head given selected blocks.
+
+    block_idx: [B, Hkv, Nq_or_len(rows), K] (indexed by position in ``rows``
+    when ``rows`` is given).  Returns (o [B, Hsel, len(rows), d],
+    lse [B, Hsel, len(rows)]) where Hsel enumerates ``heads`` (query heads,
+    default all).
+    """
+    B, H, Nq, d = q.shape
+    _, Hkv, N, _ = k.shape
+    G = _group(H, Hkv)
+    rows = list(range(Nq)) if rows is None else list(rows)
+    heads = list(range(H)) if heads is None else list(heads)
+    o = np.zeros((B, len(heads), len(rows), d))
+    out_lse = np.zeros((B, len(heads), len(rows)))
+    for b in range(B):
+        for hi, hq in enumerate(heads):
+            hk = hq // G
+            for ri, r in enumerate(rows):
+                t = N - Nq + r
+                o[b, hi, ri], out_lse[b, hi, ri] = attention_row(
+                    q[b, hq, r], k[b, hk], v[b, hk], block_idx[b, hk, ri], t, C, causal)
+    return o, out_lse
+
+
+def select_flat_bsa(q, k, C, K, causal, rows=None, heads=None):
+    """Flat-BSA selection for rows of every (batch, KV head); same layout as ``select``."""
+    B, H, Nq, d = q.shape
+    _, Hkv, N, _ = k.shape
+    G = _group(H, Hkv)
+    rows = list(range(Nq)) if rows is None else list(rows)
+    heads = list(range(Hkv)) if heads is None else list(heads)
+    idx = np.full((B, len(heads), len(rows), K), -1, dtype=np.int64)
+    gap = np.full((B, len(heads), len(rows)), POS_INF)
+    for b in range(B):
+        for hi, h in enumerate(heads):
+            S1 = build_pyramid(np.asarray(k[b, h], dtype=np.float64), C, 2)[0]
+            for ri, r in enumerate(rows):
+                t = N - Nq + r
+                sel, gp = flat_bsa_row(q[b, h * G:(h + 1) * G, r], S1, t, C, K, causal)
+                idx[b, hi, ri, :len(sel)] = sel
+                gap[b, hi, ri] = gp
+    return idx, gap

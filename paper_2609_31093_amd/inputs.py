@@ -1,0 +1,151 @@
+"""Seeded synthetic inputs for the PISA hot path.
+
+This module only draws random numbers and rounds them to the storage dtype.
+It holds none of the method's arithmetic: the pyramid, the scores, the
+selection and the attention live in the HIP library (and, independently, in
+the CPU oracle used by the tests).
+
+Workloads (B = batch, H = query heads, Hkv = KV heads, N = keys, Nq = query
+rows, d = head dim, C = leaf block size, g = fan-out, K = block budget):
+
+* ``tiny-fp32``    fp32, B=1, H=Hkv=2, N=4096, d=64, C=64, g=2, K=4;
+                   q, k, v i.i.d. N(0,1).
+* ``gqa-32k``      bf16, B=1, H=16, Hkv=4, N=32768, d=128, C=64, g=2, K=16;
+                   q, k, v i.i.d. N(0,1), q multiplied by 1/sqrt(128) before
+                   rounding.
+* ``needles-128k`` bf16, B=1, H=Hkv=8, N=131072, d=128, C=64, g=2, K=16;
+                   k, v i.i.d. N(0,1); 32 needle leaf blocks (drawn without
+                   replacement from blocks 1..M-1) whose keys in every head
+                   equal 4u for one seeded unit vector u; N/4 seeded query
+                   positions (shared by all heads) set to u + 0.5 N(0, I).
+* ``ar1-512k``     bf16, B=1, H=8, Hkv=2, N=524288, d=128, C=128, g=4, K=32;
+                   q and k follow independent stationary AR(1) processes along
+                   the sequence (rho = 0.999) per (head, dim); v i.i.d. N(0,1).
+* ``decode-128k``  bf16, B=1, H=Hkv=8, N=131072, Nq=1, d=128, C=64, g=2,
+                   K=16; k, v i.i.d. N(0,1); 64 single-token query steps.
+
+Every tensor comes from ``np.random.default_rng(SeedSequence([seed, cfg_id,
+tensor_id]))`` in float32 and is then rounded to bfloat16 (round to nearest
+even) when the workload is bf16.  The arrays returned are float32 holding the
+exact stored values, so the GPU (which receives bf16) and the oracle (which
+widens to float64) see identical numbers.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+WORKLOADS = {
+    "tiny-fp32": dict(cfg_id=1, B=1, H=2, Hkv=2, N=4096, Nq=None, d=64, C=64, g=2, K=4,
+                      causal=1, dtype="f32", dist="iid"),
+    "gqa-32k": dict(cfg_id=2, B=1, H=16, Hkv=4, N=32768, Nq=None, d=128, C=64, g=2, K=16,
+                    causal=1, dtype="bf16", dist="iid_qscaled"),
+    "needles-128k": dict(cfg_id=3, B=1, H=8, Hkv=8, N=131072, Nq=None, d=128, C=64, g=2, K=16,
+                         causal=1, dtype="bf16", dist="needles"),
+    "ar1-512k": dict(cfg_id=4, B=1, H=8, Hkv=2, N=524288, Nq=None, d=128, C=128, g=4, K=32,
+                     causal=1, dtype="bf16", dist="ar1"),
+    "decode-128k": dict(cfg_id=5, B=1, H=8, Hkv=8, N=131072, Nq=1, d=128, C=64, g=2, K=16,
+                        causal=1, dtype="bf16", dist="iid", steps=64),
+}
+
+_Q, _K, _V, _AUX = 0, 1, 2, 3
+
+
+def round_to_bf16(x: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest bfloat16 (ties to even); return float32."""
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    bits = x.view(np.uint32)
+    lsb = (bits >> 16) & 1
+    rounded = (bits + np.uint32(0x7FFF) + lsb) & np.uint32(0xFFFF0000)
+    # NaN/Inf never occur in these generators; keep them untouched anyway.
+    special = (bits & 0x7F800000) == 0x7F800000
+    rounded = np.where(special, bits, rounded).astype(np.uint32)
+    return rounded.view(np.float32)
+
+
+def _rng(seed: int, cfg_id: int, tensor_id: int) -> np.random.Generator:
+    return np.random.default_rng(np.random.SeedSequence([seed, cfg_id, tensor_id]))
+
+
+def _normal(rng, shape) -> np.ndarray:
+    return rng.standard_normal(size=shape, dtype=np.float32)
+
+
+def _ar1(rng, shape, rho: float) -> np.ndarray:
+    """Stationary AR(1) along axis -2: x_0 ~ N(0,1), x_t = rho x_{t-1} + sqrt(1-rho^2) e_t."""
+    from scipy.signal import lfilter
+
+    e = rng.standard_normal(size=shape)  # float64 for the recursion
+    e[..., 0, :] /= np.sqrt(1.0 - rho * rho)  # so that x_0 = e_0 ~ N(0,1) after scaling below
+    x = lfilter([1.0], [1.0, -rho], e, axis=-2) * np.sqrt(1.0 - rho * rho)
+    return x.astype(np.float32)
+
+
+def workload(name: str, **overrides) -> dict:
+    """Return the shape dict of a named workload, with overrides (e.g. N=...)."""
+    if name not in WORKLOADS:
+        raise KeyError(f"unknown workload {name!r}; known: {sorted(WORKLOADS)}")
+    w = dict(WORKLOADS[name])
+    w.update(overrides)
+    w["name"] = name
+    if w.get("Nq") is None:
+        w["Nq"] = w["N"]
+    return w
+
+
+def make_inputs(w: dict, seed: int = 0, step: int = 0) -> dict:
+    """Draw q [B,H,Nq,d], k [B,Hkv,N,d], v [B,Hkv,N,d] for workload dict ``w``.
+
+    ``step`` selects the query of a decode step (decode workloads draw a fresh
+    query per step; k and v do not depend on it).
+    """
+    B, H, Hkv, N, Nq, d, C = w["B"], w["H"], w["Hkv"], w["N"], w["Nq"], w["d"], w["C"]
+    cid = w["cfg_id"]
+    dist = w["dist"]
+    qshape, kshape = (B, H, Nq, d), (B, Hkv, N, d)
+    q_tid = _Q if step == 0 else 16 + step
+    if dist in ("iid", "iid_qscaled"):
+        q = _normal(_rng(seed, cid, q_tid), qshape)
+        if dist == "iid_qscaled":
+            q = q * np.float32(1.0 / np.sqrt(d))
+        k = _normal(_rng(seed, cid, _K), kshape)
+        v = _normal(_rng(seed, cid, _V), kshape)
+    elif dist == "needles":
+        rng_aux = _rng(seed, cid, _AUX)
+        n = rng_aux.standard_normal(d)
+        u = (n / np.linalg.norm(n)).astype(np.float32)
+        M1 = -(-N // C)
+        n_needles = min(32, max(0, M1 - 1))
+        needle_blocks = np.sort(rng_aux.choice(np.arange(1, M1), size=n_needles, replace=False)) \
+            if n_needles else np.zeros(0, dtype=np.int64)
+        n_qpos = Nq // 4
+        qpos = np.sort(rng_aux.choice(Nq, size=n_qpos, replace=False)) if n_qpos else np.zeros(0, np.int64)
+        k = _normal(_rng(seed, cid, _K), kshape)
+        for b in needle_blocks:
+            k[:, :, b * C:min((b + 1) * C, N), :] = 4.0 * u
+        q = _normal(_rng(seed, cid, q_tid), qshape)
+        noise = _normal(_rng(seed, cid, _AUX + 10), (B, H, n_qpos, d))
+        q[:, :, qpos, :] = u + 0.5 * noise
+        v = _normal(_rng(seed, cid, _V), kshape)
+    elif dist == "ar1":
+        q = _ar1(_rng(seed, cid, q_tid), qshape, 0.999)
+        k = _ar1(_rng(seed, cid, _K), kshape, 0.999)
+        v = _normal(_rng(seed, cid, _V), kshape)
+    else:
+        raise ValueError(f"unknown distribution {dist!r}")
+    if w["dtype"] == "bf16":
+        q, k, v = round_to_bf16(q), round_to_bf16(k), round_to_bf16(v)
+    return {"q": np.ascontiguousarray(q, np.float32),
+            "k": np.ascontiguousarray(k, np.float32),
+            "v": np.ascontiguousarray(v, np.float32)}
+
+
+def needle_layout(w: dict, seed: int = 0) -> dict:
+    """Needle block indices and needle query positions of a ``needles`` workload."""
+    N, Nq, C, d, cid = w["N"], w["Nq"], w["C"], w["d"], w["cfg_id"]
+    rng_aux = _rng(seed, cid, _AUX)
+    n = rng_aux.standard_normal(d)
+    M1 = -(-N // C)
+    n_needles = min(32, max(0, M1 - 1))
+    blocks = np.sort(rng_aux.choice(np.arange(1, M1), size=n_needles, replace=False))
+    qpos = np.sort(rng_aux.choice(Nq, size=Nq // 4, replace=False))
+    return {"u": (n / np.linalg.norm(n)).astype(np.float32), "blocks": blocks, "qpos": qpos}

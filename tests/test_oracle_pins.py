@@ -1,0 +1,399 @@
+"""Pins of the CPU oracle against what the paper and mathematics fix.
+
+None of these re-types the oracle: each compares it with a closed form, a
+hand-worked fixture, an invariant the paper proves, a special case that
+reduces to a library routine (scipy / torch), or a differently structured
+brute force on tiny inputs.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+from scipy.special import logsumexp, softmax
+
+import oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rng(seed):
+    return np.random.default_rng(seed)
+
+
+# --------------------------------------------------------------- hierarchy ---
+
+def test_level_sizes_golden():
+    """Sec. 3.2 eq. (key_hierarchy): sizes worked out by hand."""
+    with open(os.path.join(GOLDEN, "level_sizes.json")) as f:
+        cases = json.load(f)["cases"]
+    for c in cases:
+        assert O.level_sizes(c["N"], c["C"], c["g"]) == c["sizes"], c
+
+
+def test_pyramid_ragged_golden():
+    """Sec. 3.2 eq. (mean_pyramid): mean over valid children, hand-worked."""
+    with open(os.path.join(GOLDEN, "pyramid_ragged.json")) as f:
+        gold = json.load(f)
+    levels = O.build_pyramid(np.array(gold["keys"], float), gold["C"], gold["g"])
+    assert [lv.shape[0] for lv in levels] == gold["level_sizes"]
+    for got, want in zip(levels, gold["levels"]):
+        np.testing.assert_array_equal(got, np.array(want, float))
+
+
+@pytest.mark.parametrize("N,C,g", [(1000, 8, 2), (777, 4, 3), (4096, 64, 2), (513, 16, 4)])
+def test_pyramid_complete_nodes_are_raw_means(N, C, g):
+    """Sec. 3.2: with equal-size children the summary is the mean of all raw keys it covers."""
+    k = _rng(1).standard_normal((N, 5))
+    levels = O.build_pyramid(k, C, g)
+    for lv, S in enumerate(levels, start=1):
+        span = C * g ** (lv - 1)
+        for i in range(S.shape[0]):
+            if (i + 1) * span <= N:      # complete node: every descendant is full
+                np.testing.assert_allclose(S[i], k[i * span:(i + 1) * span].mean(0),
+                                           rtol=0, atol=1e-13)
+
+
+def test_pyramid_rows_layout():
+    k = _rng(2).standard_normal((1, 1, 300, 3))
+    P = O.pyramid(k, 8, 2)
+    sizes = O.level_sizes(300, 8, 2)           # 38,19,10,5,3,2,1
+    assert P.shape == (1, 1, sum(sizes[:-1]), 3)
+    single = O.pyramid(k[:, :, :5], 8, 2)      # one leaf block: level 1 only
+    assert single.shape == (1, 1, 1, 3)
+
+
+# ----------------------------------------------------------------- scoring ---
+
+def test_lse_matches_scipy():
+    z = _rng(3).standard_normal(50) * 30
+    assert O.lse(z) == pytest.approx(logsumexp(z), rel=1e-14)
+    assert O.lse(np.array([])) == -math.inf
+
+
+def _tiny_case(seed, N, d, G, scale=1.0):
+    r = _rng(seed)
+    return r.standard_normal((G, d)) * scale, r.standard_normal((N, d))
+
+
+def test_leaf_score_is_raw_key_logsumexp():
+    """Sec. 3.2 eq. (direct_child_lse) at l = 1: exact LSE over the block's raw keys,
+    summed over the grouped heads (Sec. 3.3 eq. kernel_grouped_score)."""
+    N, C, g, K, d, G = 2048, 16, 2, 6, 8, 3
+    qg, k = _tiny_case(4, N, d, G)
+    levels = O.build_pyramid(k, C, g)
+    t = N - 1
+    trace = []
+    O.select_row(qg, k, levels, t, C, g, K, True, trace)
+    leaf = trace[-1]
+    assert leaf["level"] == 1 and leaf["u"], "leaf level must be ranked here"
+    for i, u in leaf["u"].items():
+        want = sum(logsumexp(k[i * C:(i + 1) * C] @ qh / math.sqrt(d)) for qh in qg)
+        assert u == pytest.approx(want, rel=1e-12, abs=1e-12)
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_jensen_chain_on_intermediate_scores(seed):
+    """App. A eq. (equal_child_jensen): for a fully visible node with g equal children,
+    mean_j m_j <= s - log g <= LSE_raw(B) - log|B|, with m_j the child-mean logits."""
+    N, C, g, K, d = 4096, 8, 2, 5, 6
+    qg, k = _tiny_case(10 + seed, N, d, 1, scale=2.0)
+    levels = O.build_pyramid(k, C, g)
+    q = qg[0]
+    checked = 0
+    for t in (N - 1, N // 2 + 3, 1500):
+        trace = []
+        O.select_row(qg, k, levels, t, C, g, K, True, trace)
+        for rec in trace:
+            lv = rec["level"]
+            if lv < 2:
+                continue
+            span = C * g ** (lv - 1)
+            cspan = span // g
+            for i, s in rec["u"].items():
+                lo, hi = i * span, (i + 1) * span
+                assert hi <= t + 1, "scored nodes must lie in the past"
+                z = k[lo:hi] @ q / math.sqrt(d)
+                m = [z[j * cspan:(j + 1) * cspan].mean() for j in range(g)]
+                left = float(np.mean(m))
+                mid = s - math.log(g)
+                right = logsumexp(z) - math.log(hi - lo)
+                assert left <= mid + 1e-12 and mid <= right + 1e-12
+                checked += 1
+    assert checked > 20
+
+
+def test_jensen_equality_when_child_logits_equal():
+    """App. A: F_hat(B) = F_q(B) when all logits within each child are equal.
+    Keys constant inside every leaf block make this hold for level-2 nodes."""
+    N, C, g, K, d = 2048, 8, 2, 4, 6
+    r = _rng(20)
+    leaf_keys = r.standard_normal((N // C, d))
+    k = np.repeat(leaf_keys, C, axis=0)
+    q = r.standard_normal((1, d))
+    levels = O.build_pyramid(k, C, g)
+    trace = []
+    O.select_row(q, k, levels, N - 1, C, g, K, True, trace)
+    rec = [x for x in trace if x["level"] == 2][0]
+    assert rec["u"]
+    for i, s in rec["u"].items():
+        z = k[i * C * g:(i + 1) * C * g] @ q[0] / math.sqrt(d)
+        assert s - math.log(g) == pytest.approx(logsumexp(z) - math.log(C * g), abs=1e-12)
+
+
+# --------------------------------------------------------------- selection ---
+
+@pytest.mark.parametrize("g,K", [(2, 4), (3, 5), (4, 3), (2, 8)])
+def test_candidate_bound(g, K):
+    """Sec. 3.2 eq. (candidate_bound): |I| <= K and |A| <= gK below the root."""
+    N, C, d = 3000, 4, 8
+    qg, k = _tiny_case(30 + g + K, N, d, 2)
+    levels = O.build_pyramid(k, C, g)
+    for t in (N - 1, 2047, 777, 5):
+        trace = []
+        O.select_row(qg, k, levels, t, C, g, K, True, trace)
+        for rec in trace:
+            assert len(rec["I"]) <= K
+            assert len(rec["A"]) <= g * K
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_budget_covering_every_block_selects_all(causal):
+    """With K >= M_1 nothing is ever pruned: every eligible leaf is selected."""
+    N, C, g, d = 999, 16, 2, 4
+    qg, k = _tiny_case(40, N, d, 1)
+    levels = O.build_pyramid(k, C, g)
+    M1 = levels[0].shape[0]
+    for t in range(0, N, 37):
+        sel, gap = O.select_row(qg, k, levels, t, C, g, M1, causal)
+        want = list(range(t // C + 1)) if causal else list(range(M1))
+        assert sel == want and gap == math.inf
+
+
+@pytest.mark.parametrize("seed,G", [(0, 1), (1, 2), (2, 4)])
+def test_no_intermediate_pruning_equals_flat_lse_topk(seed, G):
+    """When M_2 <= K < M_1 no intermediate level prunes, so the pyramid result is the
+    forced blocks plus the best eligible leaves by exact raw-key LSE (brute force)."""
+    N, C, g, d = 1024, 32, 2, 8       # M_1 = 32, M_2 = 16
+    K = 16
+    qg, k = _tiny_case(50 + seed, N, d, G)
+    levels = O.build_pyramid(k, C, g)
+    for t in range(N - 1, 0, -53):
+        sel, _ = O.select_row(qg, k, levels, t, C, g, K, True)
+        c = t // C
+        elig = list(range(c + 1))
+        if len(elig) <= K:
+            assert sel == elig
+            continue
+        forced = {0, c, c - 1}
+        free = [i for i in elig if i not in forced]
+        score = np.array([sum(logsumexp(k[i * C:(i + 1) * C] @ qh / math.sqrt(d)) for qh in qg)
+                          for i in free])
+        order = np.lexsort((np.array(free), -score))
+        want = sorted(forced | {free[j] for j in order[:K - 3]})
+        assert sel == want
+
+
+def test_budget_three_keeps_exactly_forced():
+    """App. B with K = 3: the first, previous and current blocks and nothing else."""
+    N, C, g, d = 2000, 8, 2, 4
+    qg, k = _tiny_case(60, N, d, 1)
+    levels = O.build_pyramid(k, C, g)
+    for t in range(0, N, 13):
+        c = t // C
+        sel, _ = O.select_row(qg, k, levels, t, C, g, 3, True)
+        assert sel == sorted({0, c} | ({c - 1} if c else set()))
+
+
+def test_identical_group_heads_select_as_one_head():
+    """Sec. 3.3: u is the sum of the group's head scores; G identical heads give G*s,
+    which ranks exactly as one head."""
+    N, C, g, K, d = 3000, 8, 2, 6, 8
+    qg, k = _tiny_case(70, N, d, 1)
+    levels = O.build_pyramid(k, C, g)
+    for t in (N - 1, 1777, 901):
+        one, _ = O.select_row(qg, k, levels, t, C, g, K, True)
+        four, _ = O.select_row(np.repeat(qg, 4, axis=0), k, levels, t, C, g, K, True)
+        assert one == four
+
+
+def test_planted_block_wins_every_level():
+    """Keys of one past block aligned with the query and every other key zero: that
+    block and its ancestors carry the top score at every ranked level."""
+    N, C, g, d = 4096, 16, 2, 8
+    r = _rng(80)
+    q = r.standard_normal((1, d))
+    k = np.zeros((N, d))
+    star = 100
+    k[star * C:(star + 1) * C] = 25.0 * q[0] / np.linalg.norm(q[0])
+    levels = O.build_pyramid(k, C, g)
+    t = N - 1
+    trace = []
+    sel, _ = O.select_row(q, k, levels, t, C, g, 4, True, trace)
+    assert star in sel
+    for rec in trace:
+        if rec["u"]:
+            anc = star // g ** (rec["level"] - 1)
+            best = max(rec["u"], key=lambda i: (rec["u"][i], -i))
+            assert best == anc
+
+
+# ------------------------------------------------- brute force on tiny inputs ---
+
+def _brute_select(qg, k, t, C, g, K, causal):
+    """Set-based restatement for tiny inputs: node summaries from a memoised recursive
+    definition, every node's score tabulated densely, selection as set algebra."""
+    N, d = k.shape
+    sizes = O.level_sizes(N, C, g)
+    L = len(sizes)
+    memo = {}
+
+    def summary(lv, i):
+        if (lv, i) not in memo:
+            if lv == 1:
+                memo[(lv, i)] = k[i * C:min(i * C + C, N)].mean(0)
+            else:
+                kids = range(i * g, min(i * g + g, sizes[lv - 2]))
+                memo[(lv, i)] = np.mean([summary(lv - 1, r) for r in kids], axis=0)
+        return memo[(lv, i)]
+
+    def kids(lv, i):
+        if lv == 1:
+            return k[i * C:min(i * C + C, N)]
+        return np.array([summary(lv - 1, r) for r in range(i * g, min(i * g + g, sizes[lv - 2]))])
+
+    table = {lv: np.array([sum(logsumexp(kids(lv, i) @ qh / math.sqrt(d)) for qh in qg)
+                           for i in range(sizes[lv - 1])]) for lv in range(1, L + 1)}
+    c = t // C
+    fl = ({0, c} | ({c - 1} if c else set())) if causal else set()
+    cand = {0}
+    for lv in range(L, 0, -1):
+        forced = {j // g ** (lv - 1) for j in fl} & cand
+        if len(cand) > K:
+            rest = sorted(cand - forced, key=lambda i: (-table[lv][i], i))
+            cand = forced | set(rest[:K - len(forced)])
+        if lv > 1:
+            cand = {r for i in cand for r in range(i * g, min(i * g + g, sizes[lv - 2]))
+                    if not causal or r * C * g ** (lv - 2) <= t}
+    return sorted(cand)
+
+
+CASES = [(N, C, g, K, G, causal, seed)
+         for seed, (N, C, g, K, G, causal) in enumerate([
+             (200, 2, 2, 3, 1, True), (257, 4, 2, 4, 2, True), (300, 4, 3, 5, 1, True),
+             (511, 8, 4, 6, 4, True), (129, 2, 3, 7, 1, False), (100, 4, 2, 3, 2, False),
+             (450, 8, 2, 8, 1, False), (333, 2, 4, 5, 2, True), (64, 2, 2, 4, 1, True),
+             (480, 4, 2, 6, 1, True), (97, 8, 3, 3, 1, False), (512, 2, 2, 8, 2, True)])]
+
+
+@pytest.mark.parametrize("N,C,g,K,G,causal,seed", CASES)
+def test_selection_matches_brute_force(N, C, g, K, G, causal, seed):
+    qg, k = _tiny_case(100 + seed, N, 4, G, scale=1.5)
+    levels = O.build_pyramid(k, C, g)
+    for t in sorted({0, 1, C - 1, C, N // 3, N // 2 + 1, N - 2, N - 1}):
+        sel, _ = O.select_row(qg, k, levels, t, C, g, K, causal)
+        assert sel == _brute_select(qg, k, t, C, g, K, causal), (t,)
+
+
+# --------------------------------------------------------------- attention ---
+
+def _sdpa(q, k, v, mask=None, causal=False):
+    """torch's textbook attention in float64 on the CPU."""
+    Q = torch.from_numpy(q)[None, None]
+    Kt = torch.from_numpy(k)[None, None]
+    V = torch.from_numpy(v)[None, None]
+    m = None if mask is None else torch.from_numpy(mask)[None, None]
+    o = torch.nn.functional.scaled_dot_product_attention(Q, Kt, V, attn_mask=m, is_causal=causal)
+    return o[0, 0].numpy()
+
+
+@pytest.mark.parametrize("causal", [True, False])
+def test_attention_with_all_blocks_is_dense_attention(causal):
+    """With every block selected (K*C >= N) selected attention is dense softmax attention."""
+    N, C, d = 300, 16, 8
+    r = _rng(90)
+    q, k, v = (r.standard_normal((N, d)) for _ in range(3))
+    blocks = list(range(-(-N // C)))
+    want = _sdpa(q, k, v, causal=causal)
+    z = q @ k.T / math.sqrt(d)
+    if causal:
+        z = np.where(np.tril(np.ones((N, N), bool)), z, -np.inf)
+    want_lse = logsumexp(z, axis=1)
+    for t in range(0, N, 7):
+        o, l = O.attention_row(q[t], k, v, blocks, t, C, causal)
+        np.testing.assert_allclose(o, want[t], rtol=1e-12, atol=1e-12)
+        assert l == pytest.approx(want_lse[t], rel=1e-12)
+
+
+def test_attention_matches_block_masked_dense():
+    """Any block set: equal to dense attention under the block (and causal) mask."""
+    N, C, d, K = 256, 8, 8, 5
+    r = _rng(91)
+    q, k, v = (r.standard_normal((N, d)) for _ in range(3))
+    M1 = N // C
+    for t in range(C, N, 11):
+        blocks = sorted(r.choice(t // C + 1, size=min(K, t // C + 1), replace=False))
+        mask = np.zeros((1, N), bool)
+        for i in blocks:
+            mask[0, i * C:(i + 1) * C] = True
+        mask[0, t + 1:] = False
+        want = _sdpa(q[t:t + 1], k, v, mask=mask)[0]
+        o, _ = O.attention_row(q[t], k, v, list(blocks) + [-1], t, C, True)
+        np.testing.assert_allclose(o, want, rtol=1e-12, atol=1e-12)
+    assert M1 == 32
+
+
+# ---------------------------------------------------------------- flat BSA ---
+
+@pytest.mark.parametrize("G,causal", [(1, True), (3, True), (2, False)])
+def test_flat_bsa_brute_force(G, causal):
+    """Sec. 3.1 + App. C.1: dense logits against every leaf mean, per-head softmax over
+    the eligible non-forced blocks, head sum, top-K by lexicographic sort."""
+    N, C, K, d = 1000, 8, 7, 6
+    r = _rng(95 + G)
+    qg = r.standard_normal((G, d))
+    k = r.standard_normal((N, d))
+    M1 = -(-N // C)
+    S1 = np.array([k[i * C:min(i * C + C, N)].mean(0) for i in range(M1)])
+    Z = qg @ S1.T / math.sqrt(d)                      # [G, M1]
+    for t in range(0, N, 29):
+        sel, _ = O.flat_bsa_row(qg, S1, t, C, K, causal)
+        c = t // C
+        elig = np.arange(M1) if not causal else np.arange(c + 1)
+        if len(elig) <= K:
+            assert sel == list(elig)
+            continue
+        forced = ({0, c} | ({c - 1} if c else set())) if causal else set()
+        free = np.array([i for i in elig if i not in forced])
+        u = softmax(Z[:, free], axis=1).sum(0)
+        order = np.lexsort((free, -u))
+        assert sel == sorted(forced | set(free[order[:K - len(forced)]].tolist()))
+    # G = 1: ranking by probability equals ranking by raw score
+    if G == 1:
+        t = N - 1
+        c = t // C
+        free = [i for i in range(c + 1) if i not in {0, c, c - 1}]
+        best = sorted(free, key=lambda i: (-Z[0, i], i))[:K - 3]
+        assert O.flat_bsa_row(qg, S1, t, C, K, True)[0] == sorted({0, c, c - 1} | set(best))
+
+
+def test_exact_ties_prefer_smaller_block_index():
+    """Reading R4: bitwise-equal scores (identical key blocks, as in the needle
+    workload) rank the smaller block index first, at every ranked level."""
+    N, C, g, d = 2048, 16, 2, 8
+    r = _rng(99)
+    q = r.standard_normal((1, d))
+    k = r.standard_normal((N, d)) * 0.01
+    twins = [20, 37, 52, 70, 99]          # five identical strong blocks, budget for two
+    for b in twins:
+        k[b * C:(b + 1) * C] = 10.0 * q[0] / np.linalg.norm(q[0])
+    levels = O.build_pyramid(k, C, g)
+    sel, gap = O.select_row(q, k, levels, N - 1, C, g, 5, True)
+    c = (N - 1) // C
+    assert sel == sorted({0, c - 1, c, 20, 37})
+    assert gap == 0.0
+    S1 = levels[0]
+    sel, gap = O.flat_bsa_row(q, S1, N - 1, C, 5, True)
+    assert sel == sorted({0, c - 1, c, 20, 37}) and gap == 0.0
