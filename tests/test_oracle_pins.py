@@ -385,8 +385,10 @@ def test_exact_ties_prefer_smaller_block_index():
     N, C, g, d = 2048, 16, 2, 8
     r = _rng(99)
     q = r.standard_normal((1, d))
-    k = r.standard_normal((N, d)) * 0.01
-    twins = [20, 37, 52, 70, 99]          # five identical strong blocks, budget for two
+    k = np.zeros((N, d))
+    # five identical strong blocks, each in its own level-5 node (16 leaves), so every
+    # ancestor path is bitwise identical; the budget leaves room for three, then two
+    twins = [20, 37, 52, 70, 99]
     for b in twins:
         k[b * C:(b + 1) * C] = 10.0 * q[0] / np.linalg.norm(q[0])
     levels = O.build_pyramid(k, C, g)
