@@ -1,0 +1,156 @@
+/*
+ * pisa.h -- C ABI of the PISA hot path for AMD Instinct MI355X (gfx950).
+ *
+ * PISA ("Block Sparse Attention with Log-Linear Complexity") selects, for
+ * every query position, K key blocks of C tokens by a coarse-to-fine search
+ * over a mean-pooled key pyramid, then runs softmax attention over the
+ * original keys and values of the selected blocks.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Every buffer pointer is a DEVICE pointer unless stated otherwise and must
+ *   be 16-byte aligned.  The caller allocates and owns every buffer,
+ *   including workspaces; the library never allocates device memory, never
+ *   synchronises and never creates streams.
+ * - Every compute call is asynchronous on `stream` (a hipStream_t; 0 is the
+ *   legacy default stream).
+ * - Indices are 0-based (the paper counts from 1).
+ * - Layouts are contiguous and row-major:
+ *     q, o      [B, H,   Nq, d]   (dtype of the problem)
+ *     k, v      [B, Hkv, N,  d]   (dtype of the problem)
+ *     pyramid   [B, Hkv, R,  d]   float32: summary levels 1 .. max(1, L-1)
+ *               concatenated (level 1 = leaf blocks first); R and the level
+ *               offsets come from pisa_pyramid_layout().  The root (level L)
+ *               is never scored and is not stored.
+ *     block_idx [B, Hkv, Nq, K]   int32, ascending, padded with -1
+ *     lse       [B, H,   Nq]      float32, natural log
+ * - Query row i sits at absolute position t = N - Nq + i (end-aligned), so
+ *   Nq = N is prefill and Nq = 1 is one decode step.
+ * - Query head h' reads KV head h' / (H / Hkv) (grouped-query attention);
+ *   the G = H / Hkv heads of a group share one selected block set.
+ * - Logits are scaled by 1/sqrt(d); scores and lse use the natural log.
+ * - Errors: every call validates all arguments before anything is enqueued.
+ *   On error it returns a negative status, launches nothing and leaves the
+ *   outputs untouched; pisa_last_error() then describes the problem (per
+ *   thread).  PISA_ERR_DEVICE means a HIP launch reported a failure.
+ *
+ * Supported shapes: d in {64, 128}; C a multiple of 32 in [32, 256];
+ * 2 <= fanout <= 16; 1 <= K with fanout*K <= 256 (K >= 3 when causal);
+ * G = H/Hkv <= 16 with fanout*fanout*K*G <= 2048; Nq <= N < 2^31,
+ * Nq < 2^23; B*Hkv <= 65535.
+ */
+#ifndef PISA_H
+#define PISA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef void* pisa_stream_t;
+
+typedef enum { PISA_DTYPE_F32 = 0, PISA_DTYPE_BF16 = 1 } pisa_dtype;
+
+enum {
+  PISA_OK = 0,
+  PISA_ERR_INVALID_ARG = -1, /* malformed problem, null or misaligned pointer */
+  PISA_ERR_UNSUPPORTED = -2, /* well-formed but outside the supported shapes */
+  PISA_ERR_WORKSPACE = -3,   /* workspace smaller than the *_workspace_bytes */
+  PISA_ERR_DEVICE = -4       /* a HIP call or kernel launch failed */
+};
+
+/* Selection schedules (pisa_problem.schedule). */
+enum {
+  PISA_SCHEDULE_AUTO = 0,      /* library picks from the problem size */
+  PISA_SCHEDULE_TWO_STAGE = 1, /* Sec. 3.3 prefill design: intermediate
+                                  levels per query, then leaf blocks scored
+                                  once per key block for a tile of queries,
+                                  then a final Top-K (bf16 only) */
+  PISA_SCHEDULE_FUSED = 2      /* Sec. 3.3 decode design: one program per
+                                  (query, KV head) walks every level down to
+                                  the raw leaf keys */
+};
+
+/* The problem statement of Sec. 3.1-3.2: q/k/v, N, head dim d, block size C,
+ * fan-out g (the paper fixes g = 2; any 2..16 is accepted), budget K. */
+typedef struct {
+  int32_t B, H, Hkv; /* batch, query heads, KV heads (H % Hkv == 0)         */
+  int32_t Nq, N;     /* query rows and key rows, 1 <= Nq <= N               */
+  int32_t d;         /* head dimension                                      */
+  int32_t C;         /* leaf block size (tokens per leaf block)             */
+  int32_t fanout;    /* g: children per node above the leaf level           */
+  int32_t K;         /* block budget per (query, KV head) at every level    */
+  int32_t causal;    /* 1: App. B eligibility + forced first/previous/current
+                        blocks and masked future tokens; 0: plain method    */
+  int32_t dtype;     /* pisa_dtype of q, k, v and o                         */
+  int32_t schedule;  /* PISA_SCHEDULE_* for pisa_select; ignored elsewhere  */
+} pisa_problem;
+
+/* Number of hierarchy levels L (Sec. 3.2 eq. key_hierarchy: M_1 = ceil(N/C),
+ * M_{l+1} = ceil(M_l / fanout) until M_L = 1), or a negative status. */
+int pisa_num_levels(int32_t N, int32_t C, int32_t fanout);
+
+/* Row layout of the stored pyramid.  Writes level_row_offset[l-1] = first row
+ * of level l for l = 1..L (host array with room for L entries; the root's
+ * entry equals R) and *rows_R = R.  Returns L or a negative status. */
+int pisa_pyramid_layout(const pisa_problem* p, int64_t* level_row_offset, int64_t* rows_R);
+
+/* Bytes of the pyramid buffer (B*Hkv*R*d*4), or 0 if the problem is invalid. */
+size_t pisa_pyramid_bytes(const pisa_problem* p);
+
+/* Workspace bytes each call needs (0 is a valid answer); 0 also for invalid
+ * problems, which the call itself then rejects. */
+size_t pisa_select_workspace_bytes(const pisa_problem* p);
+size_t pisa_bsa_workspace_bytes(const pisa_problem* p);
+size_t pisa_attn_workspace_bytes(const pisa_problem* p);
+
+/* Mean pyramid (Sec. 3.2 eq. mean_pyramid): level 1 = mean of each leaf
+ * block's raw keys (the last block may be short), level l+1 = mean of the
+ * existing children at level l.  Accumulates in float32; writes `pyramid`. */
+int pisa_build_pyramid(const pisa_problem* p, const void* k, float* pyramid, pisa_stream_t stream);
+
+/* Pyramid Top-K selection (Sec. 3.2 eqs. hierarchical_topk and
+ * direct_child_lse; grouped heads Sec. 3.3 eq. kernel_grouped_score; causal
+ * policy App. B).  From the root, each level keeps all candidates when there
+ * are at most K, otherwise keeps the forced ones plus the best by the sum over
+ * the group's heads of the LSE of the children's scaled logits (child
+ * summaries above the leaf level, raw keys at the leaf level); kept blocks
+ * expand to their eligible children.  Ties go to the smaller block index.
+ * Writes block_idx.  block_score (nullable, float32 [B,Hkv,Nq,K]) receives the
+ * leaf score of each kept block, +inf for blocks kept without a score, -inf
+ * for padding.  `pyramid` must come from pisa_build_pyramid on the same k. */
+int pisa_select(const pisa_problem* p, const void* q, const void* k, const float* pyramid,
+                int32_t* block_idx, float* block_score, void* ws, size_t ws_bytes,
+                pisa_stream_t stream);
+
+/* Flat block selection baseline (Sec. 3.1 eqs. bsa_block_scores, bsa_topk):
+ * every eligible leaf summary (pyramid level 1) is scored; with G > 1 the
+ * scores are turned into per-head softmax probabilities over the eligible
+ * non-forced blocks and summed over the group (App. C.1); the forced blocks
+ * of App. B are kept inside the budget.  Same block_idx layout as
+ * pisa_select. */
+int pisa_select_flat_bsa(const pisa_problem* p, const void* q, const float* pyramid,
+                         int32_t* block_idx, void* ws, size_t ws_bytes, pisa_stream_t stream);
+
+/* Selected sparse attention (Sec. 3.1 eq. selected_sparse_attention): for
+ * every query row and head, softmax over the tokens of its KV head's selected
+ * blocks (future tokens masked when causal, App. B) applied to the original
+ * values.  Negative indices are padding.  Writes o (problem dtype) and lse
+ * (nullable); a row with no visible token gets o = 0 and lse = -inf. */
+int pisa_sparse_attn_fwd(const pisa_problem* p, const void* q, const void* k, const void* v,
+                         const int32_t* block_idx, void* o, float* lse, void* ws,
+                         size_t ws_bytes, pisa_stream_t stream);
+
+/* Static text for a status code. */
+const char* pisa_status_string(int status);
+
+/* Detail of the last failing call on this thread ("" if none). */
+const char* pisa_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PISA_H */

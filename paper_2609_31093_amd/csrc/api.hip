@@ -1,0 +1,270 @@
+// C ABI of libpisa: argument validation, hierarchy geometry, workspace sizing
+// and dispatch to the kernels.  Nothing is enqueued before every argument has
+// been checked; no call allocates device memory or synchronises.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "../../include/pisa.h"
+#include "common.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+int fail(int status, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return status;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Level sizes of the hierarchy (Sec. 3.2 eq. key_hierarchy).  Returns L or a
+// negative status.
+int compute_geo(int32_t N, int32_t C, int32_t g, pisa::Geo* geo) {
+  if (N < 1 || C < 1 || g < 2) return PISA_ERR_INVALID_ARG;
+  pisa::Geo G{};
+  G.N = N;
+  G.C = C;
+  G.g = g;
+  int64_t m = (static_cast<int64_t>(N) + C - 1) / C;
+  int L = 1;
+  G.M[1] = static_cast<int32_t>(m);
+  while (m > 1) {
+    m = (m + g - 1) / g;
+    ++L;
+    if (L > pisa::kMaxLevels) return PISA_ERR_UNSUPPORTED;
+    G.M[L] = static_cast<int32_t>(m);
+  }
+  G.L = L;
+  G.Lstore = L > 1 ? L - 1 : 1;
+  G.gpow[1] = 1;
+  for (int l = 2; l <= pisa::kMaxLevels; ++l)  // saturate beyond the root
+    G.gpow[l] = G.gpow[l - 1] > (int64_t(1) << 40) ? G.gpow[l - 1] : G.gpow[l - 1] * g;
+  G.off[1] = 0;
+  for (int l = 1; l <= L; ++l) G.off[l + 1] = G.off[l] + (l <= G.Lstore ? G.M[l] : 0);
+  G.R = G.off[G.Lstore + 1];
+  if (geo) *geo = G;
+  return L;
+}
+
+// Full validation of a problem; fills the kernel view on success.
+int check_problem(const pisa_problem* p, pisa::Shape* s, pisa::Geo* geo) {
+  if (!p) return fail(PISA_ERR_INVALID_ARG, "problem is NULL");
+  if (p->B < 1 || p->H < 1 || p->Hkv < 1)
+    return fail(PISA_ERR_INVALID_ARG, "B, H and Hkv must be >= 1 (got %d, %d, %d)", p->B, p->H, p->Hkv);
+  if (p->H % p->Hkv != 0)
+    return fail(PISA_ERR_INVALID_ARG, "H (%d) must be a multiple of Hkv (%d)", p->H, p->Hkv);
+  if (p->N < 1 || p->Nq < 1 || p->Nq > p->N)
+    return fail(PISA_ERR_INVALID_ARG, "need 1 <= Nq <= N (got Nq=%d, N=%d)", p->Nq, p->N);
+  if (p->C < 1 || p->fanout < 2 || p->K < 1)
+    return fail(PISA_ERR_INVALID_ARG, "need C >= 1, fanout >= 2, K >= 1 (got %d, %d, %d)", p->C, p->fanout,
+                p->K);
+  if (p->causal != 0 && p->causal != 1) return fail(PISA_ERR_INVALID_ARG, "causal must be 0 or 1");
+  if (p->causal && p->K < 3)
+    return fail(PISA_ERR_INVALID_ARG, "causal selection keeps the first, previous and current blocks: K >= 3");
+  if (p->dtype != PISA_DTYPE_F32 && p->dtype != PISA_DTYPE_BF16)
+    return fail(PISA_ERR_INVALID_ARG, "unknown dtype %d", p->dtype);
+  if (p->schedule < PISA_SCHEDULE_AUTO || p->schedule > PISA_SCHEDULE_FUSED)
+    return fail(PISA_ERR_INVALID_ARG, "unknown schedule %d", p->schedule);
+  if (p->d != 64 && p->d != 128) return fail(PISA_ERR_UNSUPPORTED, "head dim %d (supported: 64, 128)", p->d);
+  if (p->C % 32 != 0 || p->C > 256)
+    return fail(PISA_ERR_UNSUPPORTED, "block size %d (supported: multiples of 32 up to 256)", p->C);
+  if (p->fanout > 16) return fail(PISA_ERR_UNSUPPORTED, "fanout %d (supported: 2..16)", p->fanout);
+  const int G = p->H / p->Hkv;
+  if (G > 16) return fail(PISA_ERR_UNSUPPORTED, "group size H/Hkv = %d (supported: <= 16)", G);
+  if (static_cast<int64_t>(p->fanout) * p->K > pisa::kMaxCand)
+    return fail(PISA_ERR_UNSUPPORTED, "fanout*K = %lld exceeds %d", static_cast<long long>(p->fanout) * p->K,
+                pisa::kMaxCand);
+  if (static_cast<int64_t>(p->fanout) * p->fanout * p->K * G > 2048)
+    return fail(PISA_ERR_UNSUPPORTED, "fanout^2*K*G = %lld exceeds 2048",
+                static_cast<long long>(p->fanout) * p->fanout * p->K * G);
+  if (p->Nq >= (1 << 23)) return fail(PISA_ERR_UNSUPPORTED, "Nq %d exceeds 2^23-1", p->Nq);
+  if (static_cast<int64_t>(p->B) * p->Hkv > 65535 || static_cast<int64_t>(p->B) * p->H > 65535)
+    return fail(PISA_ERR_UNSUPPORTED, "B*H must be <= 65535");
+  pisa::Geo g{};
+  const int L = compute_geo(p->N, p->C, p->fanout, &g);
+  if (L < 0) return fail(L, "hierarchy too deep");
+  if (g.M[1] > 65535) return fail(PISA_ERR_UNSUPPORTED, "more than 65535 leaf blocks");
+  if (s) {
+    s->B = p->B;
+    s->H = p->H;
+    s->Hkv = p->Hkv;
+    s->G = G;
+    s->Nq = p->Nq;
+    s->N = p->N;
+    s->D = p->d;
+    s->C = p->C;
+    s->g = p->fanout;
+    s->K = p->K;
+    s->causal = p->causal;
+    s->bf16 = p->dtype == PISA_DTYPE_BF16;
+  }
+  if (geo) *geo = g;
+  return PISA_OK;
+}
+
+int check_ptr(const void* ptr, const char* name, bool nullable = false) {
+  if (!ptr) return nullable ? PISA_OK : fail(PISA_ERR_INVALID_ARG, "%s is NULL", name);
+  if (!aligned16(ptr)) return fail(PISA_ERR_INVALID_ARG, "%s is not 16-byte aligned", name);
+  return PISA_OK;
+}
+
+int check_ws(void* ws, size_t ws_bytes, size_t need) {
+  if (need == 0) return PISA_OK;
+  if (ws_bytes < need)
+    return fail(PISA_ERR_WORKSPACE, "workspace of %zu bytes, need %zu", ws_bytes, need);
+  if (!ws) return fail(PISA_ERR_WORKSPACE, "workspace is NULL, need %zu bytes", need);
+  if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return fail(PISA_ERR_INVALID_ARG, "workspace not 256-byte aligned");
+  return PISA_OK;
+}
+
+int device_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return PISA_OK;
+  return fail(PISA_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool use_two_stage(const pisa_problem* p, const pisa::Shape& s) {
+  if (p->schedule == PISA_SCHEDULE_TWO_STAGE) return true;
+  if (p->schedule == PISA_SCHEDULE_FUSED) return false;
+  // Key-block reuse pays once many queries share the key blocks (Sec. 3.3).
+  return s.bf16 && static_cast<int64_t>(s.Nq) * s.BH() >= 4096;
+}
+
+#define PISA_TRY(x)           \
+  do {                        \
+    const int _st = (x);      \
+    if (_st != PISA_OK) return _st; \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+int pisa_num_levels(int32_t N, int32_t C, int32_t fanout) {
+  const int L = compute_geo(N, C, fanout, nullptr);
+  if (L < 0) return fail(L, "invalid N, C or fanout");
+  return L;
+}
+
+int pisa_pyramid_layout(const pisa_problem* p, int64_t* level_row_offset, int64_t* rows_R) {
+  pisa::Geo g{};
+  PISA_TRY(check_problem(p, nullptr, &g));
+  if (!level_row_offset || !rows_R) return fail(PISA_ERR_INVALID_ARG, "output pointers must be non-NULL");
+  for (int l = 1; l <= g.L; ++l) level_row_offset[l - 1] = l <= g.Lstore ? g.off[l] : g.R;
+  *rows_R = g.R;
+  return g.L;
+}
+
+size_t pisa_pyramid_bytes(const pisa_problem* p) {
+  pisa::Geo g{};
+  if (check_problem(p, nullptr, &g) != PISA_OK) return 0;
+  return static_cast<size_t>(p->B) * p->Hkv * g.R * p->d * sizeof(float);
+}
+
+size_t pisa_select_workspace_bytes(const pisa_problem* p) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  if (check_problem(p, &s, &g) != PISA_OK) return 0;
+  return use_two_stage(p, s) ? pisa::select_two_stage_ws(s, g) : 0;
+}
+
+size_t pisa_bsa_workspace_bytes(const pisa_problem* p) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  if (check_problem(p, &s, &g) != PISA_OK) return 0;
+  return pisa::bsa_ws(s, g);
+}
+
+size_t pisa_attn_workspace_bytes(const pisa_problem* p) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  if (check_problem(p, &s, &g) != PISA_OK) return 0;
+  return pisa::attn_ws(s, g);
+}
+
+int pisa_build_pyramid(const pisa_problem* p, const void* k, float* pyramid, pisa_stream_t stream) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  PISA_TRY(check_problem(p, &s, &g));
+  PISA_TRY(check_ptr(k, "k"));
+  PISA_TRY(check_ptr(pyramid, "pyramid"));
+  return device_status(pisa::launch_build_pyramid(g, s.BH(), s.D, s.bf16, k, pyramid,
+                                                  static_cast<hipStream_t>(stream)),
+                       "pisa_build_pyramid");
+}
+
+int pisa_select(const pisa_problem* p, const void* q, const void* k, const float* pyramid, int32_t* block_idx,
+                float* block_score, void* ws, size_t ws_bytes, pisa_stream_t stream) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  PISA_TRY(check_problem(p, &s, &g));
+  PISA_TRY(check_ptr(q, "q"));
+  PISA_TRY(check_ptr(k, "k"));
+  PISA_TRY(check_ptr(pyramid, "pyramid"));
+  PISA_TRY(check_ptr(block_idx, "block_idx"));
+  PISA_TRY(check_ptr(block_score, "block_score", true));
+  const bool two = use_two_stage(p, s);
+  if (two && !s.bf16)
+    return fail(PISA_ERR_UNSUPPORTED, "the two-stage schedule runs on bf16 inputs (use the fused schedule)");
+  const size_t need = two ? pisa::select_two_stage_ws(s, g) : 0;
+  PISA_TRY(check_ws(ws, ws_bytes, need));
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  hipError_t e = two ? pisa::launch_select_two_stage(s, g, q, k, pyramid, block_idx, block_score, ws, st)
+                     : pisa::launch_select_fused(s, g, q, k, pyramid, block_idx, block_score, st);
+  return device_status(e, "pisa_select");
+}
+
+int pisa_select_flat_bsa(const pisa_problem* p, const void* q, const float* pyramid, int32_t* block_idx, void* ws,
+                         size_t ws_bytes, pisa_stream_t stream) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  PISA_TRY(check_problem(p, &s, &g));
+  PISA_TRY(check_ptr(q, "q"));
+  PISA_TRY(check_ptr(pyramid, "pyramid"));
+  PISA_TRY(check_ptr(block_idx, "block_idx"));
+  if ((static_cast<int64_t>(g.M[1]) + s.K) * 4 > 65536)
+    return fail(PISA_ERR_UNSUPPORTED, "flat BSA keeps one score per leaf block in LDS: N/C must be < 16384");
+  PISA_TRY(check_ws(ws, ws_bytes, pisa::bsa_ws(s, g)));
+  return device_status(pisa::launch_flat_bsa(s, g, q, pyramid, block_idx, ws, static_cast<hipStream_t>(stream)),
+                       "pisa_select_flat_bsa");
+}
+
+int pisa_sparse_attn_fwd(const pisa_problem* p, const void* q, const void* k, const void* v,
+                         const int32_t* block_idx, void* o, float* lse, void* ws, size_t ws_bytes,
+                         pisa_stream_t stream) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  PISA_TRY(check_problem(p, &s, &g));
+  PISA_TRY(check_ptr(q, "q"));
+  PISA_TRY(check_ptr(k, "k"));
+  PISA_TRY(check_ptr(v, "v"));
+  PISA_TRY(check_ptr(block_idx, "block_idx"));
+  PISA_TRY(check_ptr(o, "o"));
+  PISA_TRY(check_ptr(lse, "lse", true));
+  PISA_TRY(check_ws(ws, ws_bytes, pisa::attn_ws(s, g)));
+  return device_status(
+      pisa::launch_attention(s, g, q, k, v, block_idx, o, lse, ws, static_cast<hipStream_t>(stream)),
+      "pisa_sparse_attn_fwd");
+}
+
+const char* pisa_status_string(int status) {
+  switch (status) {
+    case PISA_OK: return "ok";
+    case PISA_ERR_INVALID_ARG: return "invalid argument";
+    case PISA_ERR_UNSUPPORTED: return "unsupported shape";
+    case PISA_ERR_WORKSPACE: return "workspace too small";
+    case PISA_ERR_DEVICE: return "device error";
+    default: return "unknown status";
+  }
+}
+
+const char* pisa_last_error(void) { return g_last_error; }
+
+}  // extern "C"

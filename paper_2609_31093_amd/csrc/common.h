@@ -1,0 +1,106 @@
+// Device-side helpers shared by the PISA kernels (gfx950, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pisa {
+
+constexpr int kMaxLevels = 32;
+constexpr int kMaxCand = 256;     // fanout * K upper bound (candidates per level)
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+// Hierarchy geometry of one problem (identical for every batch and KV head).
+// Level l (1-based) has M[l] nodes; node i of level l covers leaf blocks
+// [i*gpow[l], (i+1)*gpow[l]) where gpow[l] = fanout^(l-1); stored levels
+// 1..Lstore start at pyramid row off[l].
+struct Geo {
+  int32_t N, C, g, L, Lstore;
+  int32_t M[kMaxLevels + 1];
+  int64_t gpow[kMaxLevels + 1];
+  int64_t off[kMaxLevels + 2];
+  int64_t R;  // rows per (batch, KV head)
+};
+
+struct bf16x8_t {
+  uint4 raw;
+};
+
+__device__ __forceinline__ float bf16_to_f32(uint16_t h) {
+  return __uint_as_float(static_cast<uint32_t>(h) << 16);
+}
+
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7F800000u) == 0x7F800000u) {  // inf or nan: keep, quiet nan
+    return static_cast<uint16_t>((u >> 16) | ((u & 0xFFFFu) ? 0x40u : 0u));
+  }
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+
+// Load DPL consecutive elements (DPL in {4, 8}) of a bf16 or f32 row as floats.
+template <typename T, int DPL>
+__device__ __forceinline__ void load_row_part(const T* __restrict__ p, float (&x)[DPL]);
+
+template <>
+__device__ __forceinline__ void load_row_part<uint16_t, 8>(const uint16_t* __restrict__ p, float (&x)[8]) {
+  uint4 r = *reinterpret_cast<const uint4*>(p);
+  uint32_t w[4] = {r.x, r.y, r.z, r.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(w[i] << 16);
+    x[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+  }
+}
+
+template <>
+__device__ __forceinline__ void load_row_part<uint16_t, 4>(const uint16_t* __restrict__ p, float (&x)[4]) {
+  uint2 r = *reinterpret_cast<const uint2*>(p);
+  x[0] = __uint_as_float(r.x << 16);
+  x[1] = __uint_as_float(r.x & 0xFFFF0000u);
+  x[2] = __uint_as_float(r.y << 16);
+  x[3] = __uint_as_float(r.y & 0xFFFF0000u);
+}
+
+template <>
+__device__ __forceinline__ void load_row_part<float, 8>(const float* __restrict__ p, float (&x)[8]) {
+  float4 a = *reinterpret_cast<const float4*>(p);
+  float4 b = *reinterpret_cast<const float4*>(p + 4);
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+  x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+}
+
+template <>
+__device__ __forceinline__ void load_row_part<float, 4>(const float* __restrict__ p, float (&x)[4]) {
+  float4 a = *reinterpret_cast<const float4*>(p);
+  x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+}
+
+// Sum over the 16 lanes of a lane group (lanes 16j .. 16j+15).
+__device__ __forceinline__ float sum16(float v) {
+  v += __shfl_xor(v, 8, 16);
+  v += __shfl_xor(v, 4, 16);
+  v += __shfl_xor(v, 2, 16);
+  v += __shfl_xor(v, 1, 16);
+  return v;
+}
+
+// Orders LDS traffic among the lanes of one wavefront (no cross-wave effect).
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// Base-2 exponent / logarithm on the hardware transcendental unit.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
+
+// (score desc, index asc) strict ordering: does (sa, ia) rank before (sb, ib)?
+__device__ __forceinline__ bool ranks_before(float sa, int ia, float sb, int ib) {
+  return sa > sb || (sa == sb && ia < ib);
+}
+
+}  // namespace pisa

@@ -149,3 +149,15 @@ def needle_layout(w: dict, seed: int = 0) -> dict:
     blocks = np.sort(rng_aux.choice(np.arange(1, M1), size=n_needles, replace=False))
     qpos = np.sort(rng_aux.choice(Nq, size=Nq // 4, replace=False))
     return {"u": (n / np.linalg.norm(n)).astype(np.float32), "blocks": blocks, "qpos": qpos}
+
+
+def random_qkv(B: int, H: int, Hkv: int, Nq: int, N: int, d: int, dtype: str = "bf16",
+               seed: int = 0, q_scale: float = 1.0) -> dict:
+    """i.i.d. N(0,1) q, k, v of arbitrary shape (q times q_scale), rounded to dtype."""
+    r = np.random.default_rng(np.random.SeedSequence([seed, 1000 + B, H, Hkv, Nq, N, d]))
+    q = r.standard_normal((B, H, Nq, d), dtype=np.float32) * np.float32(q_scale)
+    k = r.standard_normal((B, Hkv, N, d), dtype=np.float32)
+    v = r.standard_normal((B, Hkv, N, d), dtype=np.float32)
+    if dtype == "bf16":
+        q, k, v = round_to_bf16(q), round_to_bf16(k), round_to_bf16(v)
+    return {"q": q, "k": k, "v": v}

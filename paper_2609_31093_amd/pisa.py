@@ -1,0 +1,216 @@
+"""Thin ctypes binding of libpisa (the C ABI declared in include/pisa.h).
+
+Each ``pisa_*`` function here has the name and argument order of its C
+counterpart; tensors are passed as device pointers and the stream defaults to
+torch's current stream.  Every step of the computation runs in the HIP
+library: this module only marshals arguments, allocates outputs with torch and
+turns negative status codes into :class:`PisaError`.  It raises at import time
+if the library has not been built (there is no fallback path).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libpisa.so")
+
+PISA_DTYPE_F32 = 0
+PISA_DTYPE_BF16 = 1
+PISA_SCHEDULE_AUTO = 0
+PISA_SCHEDULE_TWO_STAGE = 1
+PISA_SCHEDULE_FUSED = 2
+
+PISA_OK = 0
+PISA_ERR_INVALID_ARG = -1
+PISA_ERR_UNSUPPORTED = -2
+PISA_ERR_WORKSPACE = -3
+PISA_ERR_DEVICE = -4
+
+EXPORTS = (
+    "pisa_num_levels", "pisa_pyramid_layout", "pisa_pyramid_bytes",
+    "pisa_select_workspace_bytes", "pisa_bsa_workspace_bytes", "pisa_attn_workspace_bytes",
+    "pisa_build_pyramid", "pisa_select", "pisa_select_flat_bsa", "pisa_sparse_attn_fwd",
+    "pisa_status_string", "pisa_last_error",
+)
+
+
+class PisaError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__(f"{where} failed with status {status}: {detail}")
+        self.status = status
+
+
+class Problem(ctypes.Structure):
+    """Mirror of ``pisa_problem``."""
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("B", "H", "Hkv", "Nq", "N", "d", "C", "fanout", "K", "causal", "dtype", "schedule")]
+
+    def __repr__(self):
+        return "Problem(" + ", ".join(f"{n}={getattr(self, n)}" for n, _ in self._fields_) + ")"
+
+
+def make_problem(B, H, Hkv, Nq, N, d, C, fanout, K, causal=1, dtype="bf16", schedule=PISA_SCHEDULE_AUTO):
+    dt = {"bf16": PISA_DTYPE_BF16, "f32": PISA_DTYPE_F32,
+          torch.bfloat16: PISA_DTYPE_BF16, torch.float32: PISA_DTYPE_F32}[dtype]
+    return Problem(B, H, Hkv, Nq, N, d, C, fanout, K, int(causal), dt, schedule)
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is missing: build it with `python -m paper_2609_31093_amd.build`")
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.POINTER(Problem)
+    vp, sz, i32 = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int32
+    sig = {
+        "pisa_num_levels": (ctypes.c_int, [i32, i32, i32]),
+        "pisa_pyramid_layout": (ctypes.c_int, [P, ctypes.POINTER(ctypes.c_int64), ctypes.POINTER(ctypes.c_int64)]),
+        "pisa_pyramid_bytes": (sz, [P]),
+        "pisa_select_workspace_bytes": (sz, [P]),
+        "pisa_bsa_workspace_bytes": (sz, [P]),
+        "pisa_attn_workspace_bytes": (sz, [P]),
+        "pisa_build_pyramid": (ctypes.c_int, [P, vp, vp, vp]),
+        "pisa_select": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "pisa_select_flat_bsa": (ctypes.c_int, [P, vp, vp, vp, vp, sz, vp]),
+        "pisa_sparse_attn_fwd": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "pisa_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+        "pisa_last_error": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+_lib = _load()
+
+
+def library():
+    """The loaded ctypes.CDLL (its path is ``library()._name``)."""
+    return _lib
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(status: int, where: str):
+    if status != PISA_OK:
+        raise PisaError(status, where, _lib.pisa_last_error().decode())
+    return status
+
+
+# ------------------------------------------------------------ C entry points ---
+
+def pisa_num_levels(N: int, C: int, fanout: int) -> int:
+    L = _lib.pisa_num_levels(N, C, fanout)
+    return _check(L, "pisa_num_levels") if L < 0 else L
+
+
+def pisa_pyramid_layout(p: Problem):
+    offs = (ctypes.c_int64 * 64)()
+    R = ctypes.c_int64()
+    L = _lib.pisa_pyramid_layout(ctypes.byref(p), offs, ctypes.byref(R))
+    if L < 0:
+        _check(L, "pisa_pyramid_layout")
+    return [offs[i] for i in range(L)], R.value
+
+
+def pisa_pyramid_bytes(p: Problem) -> int:
+    return _lib.pisa_pyramid_bytes(ctypes.byref(p))
+
+
+def pisa_select_workspace_bytes(p: Problem) -> int:
+    return _lib.pisa_select_workspace_bytes(ctypes.byref(p))
+
+
+def pisa_bsa_workspace_bytes(p: Problem) -> int:
+    return _lib.pisa_bsa_workspace_bytes(ctypes.byref(p))
+
+
+def pisa_attn_workspace_bytes(p: Problem) -> int:
+    return _lib.pisa_attn_workspace_bytes(ctypes.byref(p))
+
+
+def pisa_build_pyramid(p: Problem, k, pyramid, stream=None) -> int:
+    return _check(_lib.pisa_build_pyramid(ctypes.byref(p), _ptr(k), _ptr(pyramid), _stream(stream)),
+                  "pisa_build_pyramid")
+
+
+def pisa_select(p: Problem, q, k, pyramid, block_idx, block_score=None, ws=None, ws_bytes=0, stream=None) -> int:
+    return _check(_lib.pisa_select(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(pyramid), _ptr(block_idx),
+                                   _ptr(block_score), _ptr(ws), ws_bytes, _stream(stream)), "pisa_select")
+
+
+def pisa_select_flat_bsa(p: Problem, q, pyramid, block_idx, ws=None, ws_bytes=0, stream=None) -> int:
+    return _check(_lib.pisa_select_flat_bsa(ctypes.byref(p), _ptr(q), _ptr(pyramid), _ptr(block_idx),
+                                            _ptr(ws), ws_bytes, _stream(stream)), "pisa_select_flat_bsa")
+
+
+def pisa_sparse_attn_fwd(p: Problem, q, k, v, block_idx, o, lse=None, ws=None, ws_bytes=0, stream=None) -> int:
+    return _check(_lib.pisa_sparse_attn_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(block_idx),
+                                            _ptr(o), _ptr(lse), _ptr(ws), ws_bytes, _stream(stream)),
+                  "pisa_sparse_attn_fwd")
+
+
+def pisa_status_string(status: int) -> str:
+    return _lib.pisa_status_string(status).decode()
+
+
+def pisa_last_error() -> str:
+    return _lib.pisa_last_error().decode()
+
+
+# ----------------------------------------------- allocation-side conveniences ---
+
+def _workspace(nbytes: int, device):
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def build_pyramid(p: Problem, k, stream=None):
+    """Allocate [B, Hkv, R, d] float32 and fill it with pisa_build_pyramid."""
+    _, R = pisa_pyramid_layout(p)
+    pyr = torch.empty((p.B, p.Hkv, R, p.d), dtype=torch.float32, device=k.device)
+    pisa_build_pyramid(p, k, pyr, stream)
+    return pyr
+
+
+def select(p: Problem, q, k, pyramid, with_score=False, stream=None):
+    """Allocate outputs and workspace, run pisa_select; returns idx (and scores)."""
+    idx = torch.empty((p.B, p.Hkv, p.Nq, p.K), dtype=torch.int32, device=q.device)
+    sc = torch.empty((p.B, p.Hkv, p.Nq, p.K), dtype=torch.float32, device=q.device) if with_score else None
+    nb = pisa_select_workspace_bytes(p)
+    ws = _workspace(nb, q.device)
+    pisa_select(p, q, k, pyramid, idx, sc, ws, nb, stream)
+    return (idx, sc) if with_score else idx
+
+
+def select_flat_bsa(p: Problem, q, pyramid, stream=None):
+    idx = torch.empty((p.B, p.Hkv, p.Nq, p.K), dtype=torch.int32, device=q.device)
+    nb = pisa_bsa_workspace_bytes(p)
+    pisa_select_flat_bsa(p, q, pyramid, idx, _workspace(nb, q.device), nb, stream)
+    return idx
+
+
+def sparse_attn_fwd(p: Problem, q, k, v, block_idx, stream=None):
+    o = torch.empty_like(q)
+    lse = torch.empty((p.B, p.H, p.Nq), dtype=torch.float32, device=q.device)
+    nb = pisa_attn_workspace_bytes(p)
+    pisa_sparse_attn_fwd(p, q, k, v, block_idx, o, lse, _workspace(nb, q.device), nb, stream)
+    return o, lse

@@ -1,0 +1,131 @@
+"""C-ABI contract tests that need no GPU: the library loads, exports every
+symbol the header declares, computes the hierarchy geometry, and rejects bad
+arguments (exact status, non-empty detail) before anything is launched."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import oracle as O
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "pisa.h")
+
+pisa = pytest.importorskip("paper_2609_31093_amd.pisa", reason="libpisa.so not built")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(pisa_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_entry_points():
+    names = declared_functions()
+    for must in ("pisa_build_pyramid", "pisa_select", "pisa_sparse_attn_fwd", "pisa_select_flat_bsa"):
+        assert must in names
+    assert set(names) == set(pisa.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = pisa.library()
+    out = subprocess.run(["nm", "-D", "--defined-only", lib._name], capture_output=True, text=True).stdout
+    exported = set(re.findall(r"\bT (pisa_\w+)", out))
+    for name in declared_functions():
+        assert name in exported, name
+        assert getattr(lib, name) is not None
+
+
+@pytest.mark.parametrize("N,C,g", [(4096, 64, 2), (131072, 64, 2), (524288, 128, 4), (1025, 64, 2),
+                                   (700, 32, 3), (64, 64, 2), (1, 32, 5)])
+def test_num_levels_and_layout_match_hierarchy(N, C, g):
+    sizes = O.level_sizes(N, C, g)
+    assert pisa.pisa_num_levels(N, C, g) == len(sizes)
+    p = pisa.make_problem(1, 2, 1, min(N, 16), N, 64, C, g, 3)
+    offs, R = pisa.pisa_pyramid_layout(p)
+    stored = sizes[:-1] if len(sizes) > 1 else sizes
+    assert R == sum(stored)
+    assert offs[0] == 0
+    for lv in range(1, len(stored)):
+        assert offs[lv] == sum(stored[:lv])
+    assert pisa.pisa_pyramid_bytes(p) == 1 * 1 * R * 64 * 4
+
+
+def _good(**kw):
+    base = dict(B=1, H=4, Hkv=2, Nq=256, N=1024, d=128, C=64, fanout=2, K=4, causal=1, dtype="bf16")
+    base.update(kw)
+    return pisa.make_problem(**base)
+
+
+FAKE = 1 << 20  # an aligned, non-null address; never dereferenced because validation fails first
+
+
+BAD = [
+    (dict(H=3, Hkv=2), pisa.PISA_ERR_INVALID_ARG),
+    (dict(Nq=2048), pisa.PISA_ERR_INVALID_ARG),
+    (dict(Nq=0), pisa.PISA_ERR_INVALID_ARG),
+    (dict(K=2), pisa.PISA_ERR_INVALID_ARG),
+    (dict(fanout=1), pisa.PISA_ERR_INVALID_ARG),
+    (dict(causal=2), pisa.PISA_ERR_INVALID_ARG),
+    (dict(d=96), pisa.PISA_ERR_UNSUPPORTED),
+    (dict(C=48), pisa.PISA_ERR_UNSUPPORTED),
+    (dict(C=512), pisa.PISA_ERR_UNSUPPORTED),
+    (dict(fanout=17), pisa.PISA_ERR_UNSUPPORTED),
+    (dict(fanout=16, K=17), pisa.PISA_ERR_UNSUPPORTED),
+    (dict(H=68, Hkv=2), pisa.PISA_ERR_UNSUPPORTED),
+]
+
+
+@pytest.mark.parametrize("kw,status", BAD)
+def test_invalid_problems_are_rejected_before_launch(kw, status):
+    p = _good(**kw)
+    calls = [
+        lambda: pisa.library().pisa_build_pyramid(ctypes.byref(p), FAKE, FAKE, None),
+        lambda: pisa.library().pisa_select(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 40, None),
+        lambda: pisa.library().pisa_select_flat_bsa(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, 1 << 40, None),
+        lambda: pisa.library().pisa_sparse_attn_fwd(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                                     1 << 40, None),
+    ]
+    for call in calls:
+        assert call() == status
+        assert pisa.pisa_last_error() != ""
+    assert pisa.pisa_pyramid_bytes(p) == 0
+    assert pisa.pisa_select_workspace_bytes(p) == 0
+
+
+def test_null_and_misaligned_pointers_are_rejected():
+    p = _good()
+    lib = pisa.library()
+    assert lib.pisa_build_pyramid(ctypes.byref(p), None, FAKE, None) == pisa.PISA_ERR_INVALID_ARG
+    assert "k" in pisa.pisa_last_error()
+    assert lib.pisa_build_pyramid(ctypes.byref(p), FAKE + 2, FAKE, None) == pisa.PISA_ERR_INVALID_ARG
+    assert "aligned" in pisa.pisa_last_error()
+    assert lib.pisa_sparse_attn_fwd(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None, None, None, 0, None) \
+        == pisa.PISA_ERR_INVALID_ARG
+    assert lib.pisa_select(None, FAKE, FAKE, FAKE, FAKE, None, None, 0, None) == pisa.PISA_ERR_INVALID_ARG
+
+
+def test_undersized_workspace_is_rejected():
+    p = _good(schedule=pisa.PISA_SCHEDULE_TWO_STAGE)
+    need = pisa.pisa_select_workspace_bytes(p)
+    assert need > 0
+    lib = pisa.library()
+    st = lib.pisa_select(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None, FAKE, need - 1, None)
+    assert st == pisa.PISA_ERR_WORKSPACE
+    assert str(need) in pisa.pisa_last_error()
+    st = lib.pisa_select(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None, None, need, None)
+    assert st == pisa.PISA_ERR_WORKSPACE
+
+
+def test_two_stage_needs_bf16():
+    p = _good(dtype="f32", schedule=pisa.PISA_SCHEDULE_TWO_STAGE)
+    lib = pisa.library()
+    st = lib.pisa_select(ctypes.byref(p), FAKE, FAKE, FAKE, FAKE, None, FAKE, 1 << 40, None)
+    assert st == pisa.PISA_ERR_UNSUPPORTED
+
+
+def test_status_strings():
+    assert pisa.pisa_status_string(0) == "ok"
+    assert pisa.pisa_status_string(pisa.PISA_ERR_WORKSPACE) == "workspace too small"
