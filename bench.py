@@ -1,0 +1,269 @@
+#!/usr/bin/env python
+"""Benchmark of the PISA hot path on one MI355X.
+
+One step = the whole hot path over one batch of synthetic input already
+resident in HBM: pisa_build_pyramid -> pisa_select -> pisa_sparse_attn_fwd.
+Default workload: needles-128k (B=1, 8 heads, N=131072, d=128, C=64, g=2,
+K=16, bf16, causal prefill).  Prints ONE JSON line on stdout; progress goes
+to stderr.
+
+Also reported: the per-kernel time split (hipEvents recorded by the library
+on the launch stream during the timed steps), the flat-BSA selection
+baseline, the roofline of the dominant kernel and the CPU oracle timed on a
+bounded sample of the same workload (cpu_baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "PISA select+attn tokens/s at N=128K; % HBM peak (select), % MFMA peak (attn)"
+HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+VALU_F32_PEAK_TFLOPS = 78.6   # 256 CU x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz (no packed FP32)
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def algorithmic_work(w, pairs_scored, attn_pairs):
+    """Algorithmic bytes / flops per launch of each kernel (see the design notes)."""
+    B, H, Hkv, N, Nq, d, C, g, K = (w[k] for k in ("B", "H", "Hkv", "N", "Nq", "d", "C", "g", "K"))
+    G = H // Hkv
+    es = 2 if w["dtype"] == "bf16" else 4
+    M = [-(-N // C)]
+    while M[-1] > 1:
+        M.append(-(-M[-1] // g))
+    R = sum(M[:-1]) if len(M) > 1 else M[0]
+    s = 0
+    while g ** (s + 1) <= 16:
+        s += 1
+    leaf_rows = sum(M[:min(s + 1, max(1, len(M) - 1))])
+    out = {}
+    out["pool_leaf"] = ("hbm", B * Hkv * (N * d * es + leaf_rows * d * 4))
+    out["pool_top"] = ("hbm", B * Hkv * (R - leaf_rows) * d * 4 * 2)
+    # Stage 1 upper bound: every ranked intermediate level scores g*K candidates
+    # of g children each, per query head (dot = 2d flops).
+    ranked = 0
+    for lv in range(len(M), 1, -1):
+        if M[lv - 1] > K:      # this level can hold more than K candidates
+            ranked += 1
+    stage1_flops = B * Hkv * Nq * G * ranked * g * K * g * 2 * d
+    out["select_stage1"] = ("alu", stage1_flops)
+    out["leaf_score"] = ("mfma", pairs_scored * G * C * d * 2)
+    out["attn_rows"] = ("mfma", attn_pairs * 4 * d)
+    out["attn_block"] = ("mfma", attn_pairs * 4 * d)
+    n_part = B * Hkv * Nq * K * G
+    out["attn_combine"] = ("hbm", n_part * (2 * d + 4) + B * H * Nq * (2 * d + 4))
+    rows = B * Hkv * Nq
+    out["final_topk"] = ("hbm", rows * (g * K * 8 + 4 + K * 4))
+    out["cluster_build"] = ("hbm", rows * g * K * 4 * 3)
+    return out
+
+
+def cpu_baseline(x, w, n_rows):
+    """The oracle, as it stands, on a bounded sample: pyramid of KV head 0 plus
+    selection + attention of n_rows evenly spaced rows of head 0; extrapolated
+    to the whole job (all heads, all rows) as tokens/s."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+
+    import oracle as O
+
+    N, Nq, d, C, g, K, H, Hkv = (w[k] for k in ("N", "Nq", "d", "C", "g", "K", "H", "Hkv"))
+    G = H // Hkv
+    with threadpool_limits(1):
+        k0 = x["k"][0, 0].astype(np.float64)
+        v0 = x["v"][0, 0]
+        t0 = time.perf_counter()
+        levels = O.build_pyramid(k0, C, g)
+        t_pyr = time.perf_counter() - t0
+        rows = np.unique(np.linspace(0, Nq - 1, n_rows).astype(int))
+        t0 = time.perf_counter()
+        for r in rows:
+            t = N - Nq + r
+            sel, _ = O.select_row(x["q"][0, 0:G, r], k0, levels, t, C, g, K, bool(w["causal"]))
+            for hh in range(G):
+                O.attention_row(x["q"][0, hh, r], k0, v0, sel, t, C, bool(w["causal"]))
+        t_rows = time.perf_counter() - t0
+    per_row = t_rows / len(rows)              # one (row, KV head) incl. its G heads' attention
+    total = w["B"] * Hkv * (t_pyr + Nq * per_row)
+    return {"value": w["B"] * Nq / total, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"pyramid of 1 KV head + selection and attention of {len(rows)} evenly spaced rows "
+                      f"of that head ({t_pyr + t_rows:.1f} s), extrapolated to {w['B'] * Hkv} KV heads x "
+                      f"{Nq} rows; float64 numpy, 1 thread"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="needles-128k")
+    ap.add_argument("--cpu-rows", type=int, default=4096)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-bsa", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one MI355X: this build has no multi-GPU path "
+              "(the hot path shards by KV head with no exchange); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2609_31093_amd import inputs, pisa
+
+    torch.cuda.set_device(0)
+    w = inputs.workload(args.workload)
+    B, H, Hkv, N, Nq, d, C, g, K = (w[k] for k in ("B", "H", "Hkv", "N", "Nq", "d", "C", "g", "K"))
+    log(f"[bench] generating {args.workload} inputs")
+    x = inputs.make_inputs(w, seed=0)
+    tdt = torch.bfloat16 if w["dtype"] == "bf16" else torch.float32
+    q, k, v = (torch.from_numpy(x[n]).to(tdt).cuda() for n in "qkv")
+    p = pisa.make_problem(B, H, Hkv, Nq, N, d, C, g, K, w["causal"], w["dtype"])
+    _, R = pisa.pisa_pyramid_layout(p)
+    pyr = torch.empty((B, Hkv, R, d), dtype=torch.float32, device="cuda")
+    idx = torch.empty((B, Hkv, Nq, K), dtype=torch.int32, device="cuda")
+    o = torch.empty_like(q)
+    lse = torch.empty((B, H, Nq), dtype=torch.float32, device="cuda")
+    ws_sel_n = pisa.pisa_select_workspace_bytes(p)
+    ws_att_n = pisa.pisa_attn_workspace_bytes(p)
+    ws_sel = torch.empty(max(ws_sel_n, 1), dtype=torch.uint8, device="cuda")
+    ws_att = torch.empty(max(ws_att_n, 1), dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    ev = {n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for n in ("pool", "select", "attn")}
+
+    def step(timed=False):
+        if timed:
+            ev["pool"][0].record(stream)
+        pisa.pisa_build_pyramid(p, k, pyr, stream)
+        if timed:
+            ev["pool"][1].record(stream)
+            ev["select"][0].record(stream)
+        pisa.pisa_select(p, q, k, pyr, idx, None, ws_sel, ws_sel_n, stream)
+        if timed:
+            ev["select"][1].record(stream)
+            ev["attn"][0].record(stream)
+        pisa.pisa_sparse_attn_fwd(p, q, k, v, idx, o, lse, ws_att, ws_att_n, stream)
+        if timed:
+            ev["attn"][1].record(stream)
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    log(f"[bench] timing {args.steps} steps")
+    pisa.pisa_profile_enable(True)
+    pisa.pisa_profile_report()  # clear
+    split = {n: 0.0 for n in ev}
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step(timed=True)
+        torch.cuda.synchronize()   # per-step sync so the phase events can be read
+        for n, (a, b) in ev.items():
+            split[n] += a.elapsed_time(b)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    kern = pisa.pisa_profile_report()
+    pisa.pisa_profile_enable(False)
+    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    tokens_per_s = B * Nq / (ms_per_step / 1e3)
+    log(f"[bench] {ms_per_step:.3f} ms/step, {tokens_per_s / 1e6:.2f} M tokens/s")
+
+    # Algorithmic work of this workload (counted from the outputs, outside the timed region).
+    idx_t = idx.long()
+    t_pos = torch.arange(N - Nq, N, device="cuda").view(1, 1, Nq, 1)
+    starts = idx_t * C
+    valid = (idx_t >= 0)
+    cnt = torch.clamp(torch.minimum(t_pos - starts + 1, torch.full_like(starts, C)), min=0)
+    cnt = torch.minimum(cnt, torch.clamp(N - starts, min=0))
+    attn_pairs = int((cnt * valid).sum().item()) * (H // Hkv)
+    # leaf pairs scored (upper bound): every row may score g*K candidates minus the 3 forced
+    pairs_scored = B * Hkv * Nq * max(0, g * K - (3 if w["causal"] else 0))
+    work = algorithmic_work(w, pairs_scored, attn_pairs)
+    kernels = {name: {"launches": n // args.steps if n >= args.steps else n,
+                      "ms_per_step": tot / args.steps, "avg_ms": tot / max(n, 1)}
+               for name, (n, tot) in kern.items()}
+    dom = max(kernels, key=lambda n: kernels[n]["ms_per_step"]) if kernels else None
+    roof = None
+    if dom in work:
+        bound, amount = work[dom]
+        avg_s = kernels[dom]["avg_ms"] / 1e3
+        if bound == "hbm":
+            roof = {"kernel": dom, "bound": "hbm", "achieved": amount / avg_s / 1e9, "peak": HBM_PEAK_GBS,
+                    "unit": "GB/s"}
+        elif bound == "mfma":
+            roof = {"kernel": dom, "bound": "mfma", "achieved": amount / avg_s / 1e12,
+                    "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
+        else:
+            roof = {"kernel": dom, "bound": "alu", "achieved": amount / avg_s / 1e12,
+                    "peak": VALU_F32_PEAK_TFLOPS, "unit": "TFLOP/s"}
+        roof["frac"] = roof["achieved"] / roof["peak"]
+        roof["traffic"] = None
+
+    bsa_ms = None
+    if not args.no_bsa:
+        log("[bench] flat-BSA baseline")
+        idx_b = torch.empty_like(idx)
+        nb = pisa.pisa_bsa_workspace_bytes(p)
+        ws_b = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda")
+        for _ in range(2):
+            pisa.pisa_select_flat_bsa(p, q, pyr, idx_b, ws_b, nb, stream)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        nrep = 3
+        e0.record(stream)
+        for _ in range(nrep):
+            pisa.pisa_build_pyramid(p, k, pyr, stream)
+            pisa.pisa_select_flat_bsa(p, q, pyr, idx_b, ws_b, nb, stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        bsa_ms = e0.elapsed_time(e1) / nrep
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"[bench] cpu baseline: oracle on {args.cpu_rows} rows")
+        cpu = cpu_baseline(x, w, args.cpu_rows)
+
+    sel_ms = (split["pool"] + split["select"]) / args.steps
+    res = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w["dtype"],
+        "data": "synthetic",
+        "config": {"workload": args.workload, "B": B, "H": H, "Hkv": Hkv, "N": N, "Nq": Nq, "d": d, "C": C,
+                   "fanout": g, "K": K, "causal": bool(w["causal"]), "parallelism": "single GPU"},
+        "split_ms": {"pool": split["pool"] / args.steps, "select": split["select"] / args.steps,
+                     "attn": split["attn"] / args.steps},
+        "selection_ms_incl_pool": sel_ms,
+        "flat_bsa_selection_ms_incl_pool": bsa_ms,
+        "kernels": kernels,
+        "roofline": roof,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

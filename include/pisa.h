@@ -143,6 +143,16 @@ int pisa_sparse_attn_fwd(const pisa_problem* p, const void* q, const void* k, co
                          const int32_t* block_idx, void* o, float* lse, void* ws,
                          size_t ws_bytes, pisa_stream_t stream);
 
+/* Per-kernel timing for benchmarks (not needed for computing anything).
+ * pisa_profile_enable(1) makes every later call bracket each kernel it
+ * launches with two hipEvents recorded on that call's stream (host-side
+ * bookkeeping only; no device memory).  pisa_profile_report() waits for the
+ * recorded events, writes one line "kernel_name launches total_ms" per kernel
+ * into buf (host, NUL-terminated, truncated to cap) and clears the totals; it
+ * returns the untruncated text length. */
+int pisa_profile_enable(int on);
+int pisa_profile_report(char* buf, size_t cap);
+
 /* Static text for a status code. */
 const char* pisa_status_string(int status);
 

@@ -130,11 +130,15 @@ int device_status(hipError_t e, const char* what) {
   return fail(PISA_ERR_DEVICE, "%s: %s", what, hipGetErrorString(e));
 }
 
-bool use_two_stage(const pisa_problem* p, const pisa::Shape& s) {
+// The cluster histogram of the two-stage schedule lives in LDS (one int per
+// leaf block).
+constexpr int kMaxClusterBins = 16384;
+
+bool use_two_stage(const pisa_problem* p, const pisa::Shape& s, const pisa::Geo& g) {
   if (p->schedule == PISA_SCHEDULE_TWO_STAGE) return true;
   if (p->schedule == PISA_SCHEDULE_FUSED) return false;
   // Key-block reuse pays once many queries share the key blocks (Sec. 3.3).
-  return s.bf16 && static_cast<int64_t>(s.Nq) * s.BH() >= 4096;
+  return s.bf16 && static_cast<int64_t>(s.Nq) * s.BH() >= 4096 && g.M[1] <= kMaxClusterBins;
 }
 
 #define PISA_TRY(x)           \
@@ -172,7 +176,7 @@ size_t pisa_select_workspace_bytes(const pisa_problem* p) {
   pisa::Shape s{};
   pisa::Geo g{};
   if (check_problem(p, &s, &g) != PISA_OK) return 0;
-  return use_two_stage(p, s) ? pisa::select_two_stage_ws(s, g) : 0;
+  return use_two_stage(p, s, g) ? pisa::select_two_stage_ws(s, g) : 0;
 }
 
 size_t pisa_bsa_workspace_bytes(const pisa_problem* p) {
@@ -210,9 +214,11 @@ int pisa_select(const pisa_problem* p, const void* q, const void* k, const float
   PISA_TRY(check_ptr(pyramid, "pyramid"));
   PISA_TRY(check_ptr(block_idx, "block_idx"));
   PISA_TRY(check_ptr(block_score, "block_score", true));
-  const bool two = use_two_stage(p, s);
+  const bool two = use_two_stage(p, s, g);
   if (two && !s.bf16)
     return fail(PISA_ERR_UNSUPPORTED, "the two-stage schedule runs on bf16 inputs (use the fused schedule)");
+  if (two && g.M[1] > kMaxClusterBins)
+    return fail(PISA_ERR_UNSUPPORTED, "the two-stage schedule needs N/C <= %d", kMaxClusterBins);
   const size_t need = two ? pisa::select_two_stage_ws(s, g) : 0;
   PISA_TRY(check_ws(ws, ws_bytes, need));
   hipStream_t st = static_cast<hipStream_t>(stream);

@@ -8,6 +8,8 @@
 // row and one value row per group, and the groups' states are merged at the
 // end.  Outputs: o in the input dtype (round to nearest even for bf16), lse in
 // natural log.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -161,6 +163,240 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(AttnArgs a) {
   }
 }
 
+
+// ----------------------------------------------------------------------------
+// Block-centric attention for many rows (bf16).
+//
+// attn_block_kernel: one workgroup per tile of up to kClusterTile (row, slot)
+// pairs of one (batch x KV head, key block) cluster.  The block's C keys are staged in LDS row-major and its values transposed
+// (V^T, so that the PV product reads contiguous 8-byte runs); every (row,
+// slot) pair that selected the block is processed 32 per wavefront tile:
+// S^T = K q^T (v_mfma_f32_32x32x16_bf16, keys along M, queries along N), the
+// causal mask, the block-local max and sum, P in bf16, then O^T = V^T P with
+// the key order of P's accumulator layout reproduced in the V^T reads.  Each
+// pair leaves a partial: o normalised by its own sum (bf16) and its log2-sum
+// (fp32).  attn_combine_kernel merges the K partials of each (row, head) with
+// the usual log-sum-exp weights.
+// ----------------------------------------------------------------------------
+
+typedef __bf16 bf16x8a __attribute__((ext_vector_type(8)));
+typedef float f32x16a __attribute__((ext_vector_type(16)));
+
+struct AttnBlockArgs {
+  int H, Hkv, G, Nq, N, C, K, causal, M1;
+  int row0, nrows;  // row chunk handled by this launch
+  float qscale2;
+};
+
+__device__ __forceinline__ bf16x8a u4_as_bf16x8(uint4 r) { return __builtin_bit_cast(bf16x8a, r); }
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
+  return static_cast<uint32_t>(f32_to_bf16_rne(a)) | (static_cast<uint32_t>(f32_to_bf16_rne(b)) << 16);
+}
+
+template <int D, int CT>
+__global__ __launch_bounds__(256) void attn_block_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
+                                                         const uint16_t* __restrict__ k,
+                                                         const uint16_t* __restrict__ v,
+                                                         const int32_t* __restrict__ offs,
+                                                         const int32_t* __restrict__ toffs, int64_t ncl,
+                                                         const int32_t* __restrict__ pairs,
+                                                         uint16_t* __restrict__ part_o,
+                                                         float* __restrict__ part_lse) {
+  constexpr int KS = D / 16;       // k-steps of QK^T
+  constexpr int LDK = D + 8;       // padded K row (bf16 elements)
+  constexpr int C = CT * 32;       // keys per block
+  constexpr int LDV = C + 8;       // padded V^T row
+  constexpr int DT = D / 32;       // output d tiles
+  extern __shared__ uint16_t lds[];
+  uint16_t* klds = lds;
+  uint16_t* vt = lds + C * LDK;
+
+  int64_t cl;
+  int beg, end;
+  if (!cluster_tile(offs, toffs, ncl, blockIdx.x, cl, beg, end)) return;
+  const int bh = static_cast<int>(cl / a.M1);
+  const int blk = static_cast<int>(cl - static_cast<int64_t>(bh) * a.M1);
+  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+  const int r0 = blk * C;
+  const int nkeys = min(C, a.N - r0);
+
+  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.N + r0) * D;
+  const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.N + r0) * D;
+  for (int e = threadIdx.x; e < C * (D / 8); e += 256) {
+    const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
+    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+    if (r < nkeys) {
+      kv = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
+      vv = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(r) * D + c8);
+    }
+    *reinterpret_cast<uint4*>(klds + r * LDK + c8) = kv;
+    const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      vt[(c8 + 2 * i) * LDV + r] = static_cast<uint16_t>(w[i] & 0xFFFFu);
+      vt[(c8 + 2 * i + 1) * LDV + r] = static_cast<uint16_t>(w[i] >> 16);
+    }
+  }
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int col = lane & 31;
+  const int half = lane >> 5;
+  const int ntile = (end - beg + 31) / 32;
+  for (int tile = wave; tile < ntile; tile += 4) {
+    const int p = beg + tile * 32 + col;
+    const bool valid = p < end;
+    const int pr = valid ? pairs[p] : 0;
+    const int rr = pr >> 8, slot = pr & 255;   // row within the chunk, slot
+    const int row = a.row0 + rr;
+    const int t = a.N - a.Nq + row;
+    for (int hh = 0; hh < a.G; ++hh) {
+      const uint16_t* qrow = q + ((static_cast<int64_t>(b) * a.H + h * a.G + hh) * a.Nq + row) * D + half * 8;
+      bf16x8a qb[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        uint4 u = make_uint4(0, 0, 0, 0);
+        if (valid) u = *reinterpret_cast<const uint4*>(qrow + ks * 16);
+        qb[ks] = u4_as_bf16x8(u);
+      }
+      f32x16a sacc[CT];
+      float m = -INFINITY;
+#pragma unroll
+      for (int kt = 0; kt < CT; ++kt) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) sacc[kt][r] = 0.f;
+        const uint16_t* arow = klds + (kt * 32 + col) * LDK + half * 8;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8a av = u4_as_bf16x8(*reinterpret_cast<const uint4*>(arow + ks * 16));
+          sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qb[ks], sacc[kt], 0, 0, 0);
+        }
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          const bool ok = key < nkeys && (!a.causal || r0 + key <= t);
+          sacc[kt][r] = ok ? sacc[kt][r] * a.qscale2 : -INFINITY;
+          m = fmaxf(m, sacc[kt][r]);
+        }
+      }
+      m = fmaxf(m, __shfl_xor(m, 32));
+      const float msafe = (m == -INFINITY) ? 0.f : m;
+      float l = 0.f;
+      bf16x8a pb[CT][2];
+#pragma unroll
+      for (int kt = 0; kt < CT; ++kt) {
+        float pv[16];
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          pv[r] = fast_exp2(sacc[kt][r] - msafe);
+          l += pv[r];
+        }
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          uint4 u;
+          u.x = pack_bf16x2(pv[8 * j + 0], pv[8 * j + 1]);
+          u.y = pack_bf16x2(pv[8 * j + 2], pv[8 * j + 3]);
+          u.z = pack_bf16x2(pv[8 * j + 4], pv[8 * j + 5]);
+          u.w = pack_bf16x2(pv[8 * j + 6], pv[8 * j + 7]);
+          pb[kt][j] = u4_as_bf16x8(u);
+        }
+      }
+      l += __shfl_xor(l, 32);
+      // O^T[d][query] = sum_keys V^T[d][key] P[key][query]; the k index of
+      // PV step (kt, j) maps to keys kt*32 + 16j + 4*half + {0..3} (i < 4)
+      // and kt*32 + 16j + 8 + 4*half + {0..3} (i >= 4).
+      const float inv = l > 0.f ? 1.0f / l : 0.f;
+      const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + slot) * a.G + hh;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        f32x16a oacc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[r] = 0.f;
+        const uint16_t* vrow = vt + (dt * 32 + col) * LDV + 4 * half;
+#pragma unroll
+        for (int kt = 0; kt < CT; ++kt) {
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const uint2 lo = *reinterpret_cast<const uint2*>(vrow + kt * 32 + 16 * j);
+            const uint2 hi = *reinterpret_cast<const uint2*>(vrow + kt * 32 + 16 * j + 8);
+            const bf16x8a av = u4_as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+            oacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[kt][j], oacc, 0, 0, 0);
+          }
+        }
+        // oacc[r] = O[d = dt*32 + 8*(r/4) + 4*half + r%4][query col]
+        if (valid) {
+          uint16_t* dst = part_o + pidx * D + dt * 32 + 4 * half;
+#pragma unroll
+          for (int g4 = 0; g4 < 4; ++g4) {
+            uint2 w;
+            w.x = pack_bf16x2(oacc[4 * g4 + 0] * inv, oacc[4 * g4 + 1] * inv);
+            w.y = pack_bf16x2(oacc[4 * g4 + 2] * inv, oacc[4 * g4 + 3] * inv);
+            *reinterpret_cast<uint2*>(dst + 8 * g4) = w;
+          }
+        }
+      }
+      if (valid && half == 0) part_lse[pidx] = l > 0.f ? m + fast_log2(l) : -INFINITY;
+    }
+  }
+}
+
+// One wavefront per (row of the chunk, query head): merge the row's K
+// partials.  16 lanes cover one partial (8 bf16 each for d = 128).
+template <int D>
+__global__ __launch_bounds__(256) void attn_combine_kernel(AttnBlockArgs a, const int32_t* __restrict__ idx,
+                                                           const uint16_t* __restrict__ part_o,
+                                                           const float* __restrict__ part_lse,
+                                                           uint16_t* __restrict__ o, float* __restrict__ lse) {
+  constexpr int DPL = D / 16;
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int grp = lane >> 4, sub = lane & 15;
+  const int rr = blockIdx.x * 4 + wave;
+  if (rr >= a.nrows) return;
+  const int hq = blockIdx.y % a.H;
+  const int b = blockIdx.y / a.H;
+  const int hk = hq / a.G, hh = hq - hk * a.G;
+  const int bh = b * a.Hkv + hk;
+  const int row = a.row0 + rr;
+  const int32_t* sel = idx + (static_cast<int64_t>(bh) * a.Nq + row) * a.K;
+  float m = -INFINITY, s = 0.f, acc[DPL];
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
+  for (int slot = grp; slot < a.K; slot += 4) {
+    if (sel[slot] < 0) continue;
+    const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + slot) * a.G + hh;
+    const float ls = part_lse[pidx];
+    if (ls == -INFINITY) continue;
+    float x[DPL];
+    load_row_part<uint16_t, DPL>(part_o + pidx * D + sub * DPL, x);
+    const float mn = fmaxf(m, ls);
+    const float c0 = fast_exp2(m - mn), c1 = fast_exp2(ls - mn);
+    s = s * c0 + c1;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) acc[e] = acc[e] * c0 + x[e] * c1;
+    m = mn;
+  }
+#pragma unroll
+  for (int msk = 16; msk <= 32; msk <<= 1) {
+    float o2[DPL];
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) o2[e] = __shfl_xor(acc[e], msk);
+    const float m2 = __shfl_xor(m, msk), s2 = __shfl_xor(s, msk);
+    merge_state<DPL>(m, s, acc, m2, s2, o2);
+  }
+  if (grp == 0) {
+    const int64_t orow = (static_cast<int64_t>(b) * a.H + hq) * a.Nq + row;
+    float res[DPL];
+    const float inv = s > 0.f ? 1.0f / s : 0.f;
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) res[e] = acc[e] * inv;
+    store_row_part<uint16_t, DPL>(o + orow * D + sub * DPL, res);
+    if (lse && sub == 0) lse[orow] = s > 0.f ? (m + fast_log2(s)) * kLn2 : -INFINITY;
+  }
+}
+
 template <typename T, int D, int TEAM>
 static void launch_rows(const Shape& s, const AttnArgs& a, hipStream_t st) {
   constexpr int ROWS = 256 / TEAM;
@@ -176,14 +412,96 @@ static void launch_rows_team(const Shape& s, const AttnArgs& a, hipStream_t st) 
     launch_rows<T, D, 64>(s, a, st);
 }
 
-size_t attn_ws(const Shape&, const Geo&) { return 0; }
+// Block-centric path: bf16, many rows, cluster histogram fits in LDS.
+static bool use_block_path(const Shape& s, const Geo& geo) {
+  return s.bf16 && static_cast<int64_t>(s.BH()) * s.Nq >= 4096 && geo.M[1] <= 16384 && s.C <= 128;
+}
+
+// Rows per chunk: the partials of a chunk (K slots x G heads x (d bf16 + lse))
+// are bounded by kPartialBudget bytes.
+constexpr size_t kPartialBudget = size_t(6) << 30;
+
+static int attn_chunk_rows(const Shape& s) {
+  const size_t per_row = static_cast<size_t>(s.BH()) * s.K * s.G * (s.D * 2 + 4);
+  const size_t rows = kPartialBudget / per_row;
+  return static_cast<int>(std::min<size_t>(s.Nq, std::max<size_t>(rows, 1)));
+}
+
+struct AttnWs {
+  size_t part_o, part_lse, cl, total;
+};
+
+static AttnWs attn_layout(const Shape& s, const Geo& geo) {
+  const size_t ch = attn_chunk_rows(s);
+  const size_t np = static_cast<size_t>(s.BH()) * ch * s.K;  // pairs per chunk
+  AttnWs w{};
+  size_t o = 0;
+  auto al = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
+  w.part_o = o;   o += al(np * s.G * s.D * 2);
+  w.part_lse = o; o += al(np * s.G * 4);
+  w.cl = o;       o += al(cluster_ws(s.BH(), geo.M[1], static_cast<int64_t>(np)));
+  w.total = o;
+  return w;
+}
+
+size_t attn_ws(const Shape& s, const Geo& geo) { return use_block_path(s, geo) ? attn_layout(s, geo).total : 0; }
+
+template <int D>
+static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* q, const void* k, const void* v,
+                                    const int32_t* idx, void* o, float* lse, void* ws, hipStream_t st) {
+  const AttnWs w = attn_layout(s, geo);
+  char* base = static_cast<char*>(ws);
+  uint16_t* part_o = reinterpret_cast<uint16_t*>(base + w.part_o);
+  float* part_lse = reinterpret_cast<float*>(base + w.part_lse);
+  const int ch = attn_chunk_rows(s);
+  hipError_t e;
+  for (int row0 = 0; row0 < s.Nq; row0 += ch) {
+    const int nrows = std::min(ch, s.Nq - row0);
+    ClusterArgs ca{idx, nullptr, s.K, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], kClusterAttn, row0, nrows};
+    ClusterOut co{};
+    if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st)) != hipSuccess) return e;
+    AttnBlockArgs a{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], row0, nrows,
+                    kLog2e / sqrtf(static_cast<float>(s.D))};
+    {
+      ProfScope ps("attn_block", st);
+      dim3 grid(static_cast<unsigned>(cluster_max_tiles(s.BH(), geo.M[1], static_cast<int64_t>(s.BH()) * nrows * s.K)));
+      const size_t lds = (static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 8)) * 2;
+      const uint16_t* qq = static_cast<const uint16_t*>(q);
+      const uint16_t* kk = static_cast<const uint16_t*>(k);
+      const uint16_t* vv = static_cast<const uint16_t*>(v);
+      auto go = [&](auto kern) {
+        if (lds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        kern<<<grid, 256, lds, st>>>(a, qq, kk, vv, co.offs, co.toffs, co.ncl, co.pairs, part_o, part_lse);
+      };
+      if (s.C == 32)
+        go(attn_block_kernel<D, 1>);
+      else if (s.C == 64)
+        go(attn_block_kernel<D, 2>);
+      else if (s.C == 96)
+        go(attn_block_kernel<D, 3>);
+      else
+        go(attn_block_kernel<D, 4>);
+    }
+    {
+      ProfScope ps("attn_combine", st);
+      dim3 grid((nrows + 3) / 4, s.B * s.H);
+      attn_combine_kernel<D><<<grid, 256, 0, st>>>(a, idx, part_o, part_lse, static_cast<uint16_t*>(o), lse);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
 
 hipError_t launch_attention(const Shape& s, const Geo& geo, const void* q, const void* k, const void* v,
                             const int32_t* idx, void* o, float* lse, void* ws, hipStream_t st) {
-  (void)geo;
-  (void)ws;
+  if (use_block_path(s, geo)) {
+    return s.D == 128 ? launch_block_path<128>(s, geo, q, k, v, idx, o, lse, ws, st)
+                      : launch_block_path<64>(s, geo, q, k, v, idx, o, lse, ws, st);
+  }
   AttnArgs a{q, k, v, idx, o, lse, s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal,
              kLog2e / sqrtf(static_cast<float>(s.D))};
+  ProfScope ps("attn_rows", st);
   if (s.bf16) {
     if (s.D == 128)
       launch_rows_team<uint16_t, 128>(s, a, st);

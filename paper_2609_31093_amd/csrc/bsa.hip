@@ -177,6 +177,7 @@ hipError_t launch_flat_bsa(const Shape& s, const Geo& geo, const void* q, const 
   (void)ws;
   BsaArgs a{q, pyr, idx, s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], geo.R,
             kLog2e / sqrtf(static_cast<float>(s.D))};
+  ProfScope ps("bsa_rows", st);
   if (s.bf16) {
     if (s.D == 128)
       launch_bsa_g<uint16_t, 128>(s, a, st);

@@ -1,0 +1,180 @@
+// Grouping of (query row, slot) pairs by key block, the "query clustering"
+// step of the two-stage design (Sec. 3.3, Stage 2), shared by the leaf
+// scorer and the block-centric attention.
+//
+// A workgroup owns a chunk of rows of one (batch, KV head) and builds an LDS
+// histogram of the blocks its pairs reference; only the non-zero bins reach
+// global memory (one atomic per bin per chunk instead of one per pair).  An
+// exclusive scan turns the global counts into cluster offsets; the scatter
+// pass rebuilds the chunk histogram, reserves one contiguous range per
+// non-zero bin with a single global atomic, and places each pair with an LDS
+// atomic inside its range.  The order of pairs inside a cluster is therefore
+// not fixed, which no consumer depends on (every pair is processed on its
+// own).
+#include <algorithm>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace pisa {
+
+constexpr int kClusterThreads = 1024;
+constexpr int kClusterRows = 1024;  // rows per workgroup chunk
+
+__device__ __forceinline__ bool cluster_pair(const ClusterArgs& a, int bh, int r, int slot, int& blk) {
+  const int64_t rg = static_cast<int64_t>(bh) * a.Nq + a.row0 + r;
+  const int32_t* lst = a.list + rg * a.S;
+  blk = lst[slot];
+  if (blk < 0) return false;
+  if (a.mode == kClusterLeaf) {
+    const int n = a.cnt[rg];
+    if (slot >= n || n <= a.K) return false;
+    const int c = (a.N - a.Nq + a.row0 + r) / a.C;
+    if (a.causal && (blk == 0 || blk == c || blk == c - 1)) return false;
+  }
+  return true;
+}
+
+__global__ __launch_bounds__(256) void fill_zero_kernel(int32_t* p, int64_t n) {
+  for (int64_t i = blockIdx.x * 256LL + threadIdx.x; i < n; i += 256LL * gridDim.x) p[i] = 0;
+}
+
+__global__ __launch_bounds__(kClusterThreads) void cluster_hist_kernel(ClusterArgs a, int32_t* __restrict__ hist) {
+  extern __shared__ int32_t h[];
+  const int bh = blockIdx.y;
+  const int r0 = blockIdx.x * kClusterRows;
+  const int nr = min(kClusterRows, a.nrows - r0);
+  for (int i = threadIdx.x; i < a.M1; i += kClusterThreads) h[i] = 0;
+  __syncthreads();
+  const int npairs = nr * a.S;
+  for (int e = threadIdx.x; e < npairs; e += kClusterThreads) {
+    const int r = r0 + e / a.S, slot = e % a.S;
+    int blk;
+    if (cluster_pair(a, bh, r, slot, blk)) atomicAdd(&h[blk], 1);
+  }
+  __syncthreads();
+  int32_t* gh = hist + static_cast<int64_t>(bh) * a.M1;
+  for (int i = threadIdx.x; i < a.M1; i += kClusterThreads) {
+    const int n = h[i];
+    if (n) atomicAdd(&gh[i], n);
+  }
+}
+
+// Exclusive scans of the n counts into offs[0..n] (pair offsets, also copied
+// to cursor) and of their tile counts ceil(count / tile) into toffs[0..n].
+__global__ __launch_bounds__(1024) void cluster_scan_kernel(const int32_t* __restrict__ hist,
+                                                            int32_t* __restrict__ offs,
+                                                            int32_t* __restrict__ cursor,
+                                                            int32_t* __restrict__ toffs, int64_t n, int tile) {
+  __shared__ int wsum[16], wtile[16];
+  const int tid = threadIdx.x;
+  const int64_t per = (n + 1023) / 1024;
+  const int64_t i0 = tid * per, i1 = min(n, i0 + per);
+  int local = 0, ltile = 0;
+  for (int64_t i = i0; i < i1; ++i) {
+    const int c = hist[i];
+    local += c;
+    ltile += (c + tile - 1) / tile;
+  }
+  const int lane = tid & 63, w = tid >> 6;
+  int x = local, y = ltile;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int xs = __shfl_up(x, o), ys = __shfl_up(y, o);
+    if (lane >= o) {
+      x += xs;
+      y += ys;
+    }
+  }
+  if (lane == 63) {
+    wsum[w] = x;
+    wtile[w] = y;
+  }
+  __syncthreads();
+  int pre = 0, tot = 0, tpre = 0, ttot = 0;
+  for (int i = 0; i < 16; ++i) {
+    pre += (i < w) ? wsum[i] : 0;
+    tot += wsum[i];
+    tpre += (i < w) ? wtile[i] : 0;
+    ttot += wtile[i];
+  }
+  int run = pre + x - local, trun = tpre + y - ltile;
+  for (int64_t i = i0; i < i1; ++i) {
+    const int c = hist[i];
+    offs[i] = run;
+    cursor[i] = run;
+    toffs[i] = trun;
+    run += c;
+    trun += (c + tile - 1) / tile;
+  }
+  if (tid == 0) {
+    offs[n] = tot;
+    toffs[n] = ttot;
+  }
+}
+
+__global__ __launch_bounds__(kClusterThreads) void cluster_scatter_kernel(ClusterArgs a, int32_t* __restrict__ cursor,
+                                                                          int32_t* __restrict__ pairs) {
+  extern __shared__ int32_t h[];
+  const int bh = blockIdx.y;
+  const int r0 = blockIdx.x * kClusterRows;
+  const int nr = min(kClusterRows, a.nrows - r0);
+  for (int i = threadIdx.x; i < a.M1; i += kClusterThreads) h[i] = 0;
+  __syncthreads();
+  const int npairs = nr * a.S;
+  for (int e = threadIdx.x; e < npairs; e += kClusterThreads) {
+    const int r = r0 + e / a.S, slot = e % a.S;
+    int blk;
+    if (cluster_pair(a, bh, r, slot, blk)) atomicAdd(&h[blk], 1);
+  }
+  __syncthreads();
+  int32_t* gc = cursor + static_cast<int64_t>(bh) * a.M1;
+  for (int i = threadIdx.x; i < a.M1; i += kClusterThreads) {
+    const int n = h[i];
+    if (n) h[i] = atomicAdd(&gc[i], n);  // base of this chunk's range in bin i
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < npairs; e += kClusterThreads) {
+    const int r = r0 + e / a.S, slot = e % a.S;
+    int blk;
+    if (cluster_pair(a, bh, r, slot, blk)) {
+      const int pos = atomicAdd(&h[blk], 1);
+      pairs[pos] = (r << 8) | slot;
+    }
+  }
+}
+
+size_t cluster_ws(int BH, int M1, int64_t max_pairs) {
+  const size_t ncl = static_cast<size_t>(BH) * M1;
+  return 4 * ((ncl + 1) * 4 + 256) + static_cast<size_t>(max_pairs) * 4 + 256;
+}
+
+int64_t cluster_max_tiles(int BH, int M1, int64_t max_pairs) {
+  return (max_pairs + kClusterTile - 1) / kClusterTile + static_cast<int64_t>(BH) * M1;
+}
+
+static size_t al(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* out, hipStream_t st) {
+  const int64_t ncl = static_cast<int64_t>(BH) * a.M1;
+  char* base = static_cast<char*>(ws);
+  int32_t* hist = reinterpret_cast<int32_t*>(base);
+  int32_t* offs = reinterpret_cast<int32_t*>(base + al((ncl + 1) * 4));
+  int32_t* cursor = reinterpret_cast<int32_t*>(base + 2 * al((ncl + 1) * 4));
+  int32_t* toffs = reinterpret_cast<int32_t*>(base + 3 * al((ncl + 1) * 4));
+  int32_t* pairs = reinterpret_cast<int32_t*>(base + 4 * al((ncl + 1) * 4));
+  out->offs = offs;
+  out->toffs = toffs;
+  out->pairs = pairs;
+  out->ncl = ncl;
+  ProfScope ps("cluster_build", st);
+  fill_zero_kernel<<<static_cast<unsigned>(std::min<int64_t>((ncl + 255) / 256, 4096)), 256, 0, st>>>(hist, ncl);
+  dim3 grid((a.nrows + kClusterRows - 1) / kClusterRows, BH);
+  const size_t lds = static_cast<size_t>(a.M1) * 4;
+  cluster_hist_kernel<<<grid, kClusterThreads, lds, st>>>(a, hist);
+  cluster_scan_kernel<<<1, 1024, 0, st>>>(hist, offs, cursor, toffs, ncl, kClusterTile);
+  cluster_scatter_kernel<<<grid, kClusterThreads, lds, st>>>(a, cursor, pairs);
+  return hipGetLastError();
+}
+
+}  // namespace pisa

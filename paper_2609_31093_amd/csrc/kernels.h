@@ -9,6 +9,21 @@
 
 namespace pisa {
 
+// Brackets the kernel launches of its scope with timing events when
+// per-kernel profiling is enabled (pisa_profile_enable); otherwise inert.
+class ProfScope {
+ public:
+  ProfScope(const char* name, hipStream_t st);
+  ~ProfScope();
+  ProfScope(const ProfScope&) = delete;
+  ProfScope& operator=(const ProfScope&) = delete;
+
+ private:
+  const char* name_;
+  hipStream_t st_;
+  void* a_;
+};
+
 // Problem shape as the kernels see it (validated by the ABI layer).
 struct Shape {
   int B, H, Hkv, G, Nq, N, D, C, g, K, causal;
@@ -16,6 +31,42 @@ struct Shape {
   int BH() const { return B * Hkv; }
   int gK() const { return g * K; }
 };
+
+// Pair clustering by key block (cluster.hip).
+constexpr int kClusterLeaf = 0;  // leaf scoring: rows with more than K candidates, forced blocks skipped
+constexpr int kClusterAttn = 1;  // attention: every non-negative slot
+struct ClusterArgs {
+  const int32_t* list;  // [BH, Nq, S] block per slot, -1 = none
+  const int32_t* cnt;   // [BH, Nq] candidates per row (leaf mode only)
+  int S, Nq, N, C, K, causal, M1, mode;
+  int row0, nrows;      // rows [row0, row0 + nrows) of every (batch, KV head)
+};
+constexpr int kClusterTile = 256;  // pairs per workgroup tile of a cluster consumer
+struct ClusterOut {
+  const int32_t* offs;   // [BH*M1 + 1] cluster start offsets into pairs
+  const int32_t* toffs;  // [BH*M1 + 1] first tile of each cluster (kClusterTile pairs per tile)
+  const int32_t* pairs;  // (row - row0) << 8 | slot, grouped by (bh, block)
+  int64_t ncl;           // BH*M1
+};
+size_t cluster_ws(int BH, int M1, int64_t max_pairs);
+int64_t cluster_max_tiles(int BH, int M1, int64_t max_pairs);
+
+// Tile w of the cluster list: its cluster (largest cl with toffs[cl] <= w)
+// and pair range; false when w is past the last tile.
+__device__ __forceinline__ bool cluster_tile(const int32_t* __restrict__ offs, const int32_t* __restrict__ toffs,
+                                             int64_t ncl, int64_t w, int64_t& cl, int& beg, int& end) {
+  if (w >= toffs[ncl]) return false;
+  int64_t lo = 0, hi = ncl - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (toffs[mid] <= w) lo = mid; else hi = mid - 1;
+  }
+  cl = lo;
+  beg = offs[cl] + static_cast<int>(w - toffs[cl]) * kClusterTile;
+  end = min(offs[cl + 1], beg + kClusterTile);
+  return true;
+}
+hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* out, hipStream_t st);
 
 hipError_t launch_build_pyramid(const Geo& geo, int BH, int D, bool bf16, const void* k, float* pyr,
                                 hipStream_t st);

@@ -140,6 +140,8 @@ hipError_t launch_build_pyramid(const Geo& geo, int BH, int D, bool bf16, const 
   for (int i = 0; i < s; ++i) lpb *= geo.g;
   dim3 grid((geo.M[1] + lpb - 1) / lpb, BH);
   const size_t lds = 2 * static_cast<size_t>(lpb) * D * sizeof(float);
+  {
+  ProfScope ps("pool_leaf", st);
   if (bf16) {
     if (D == 128)
       pool_leaf_kernel<uint16_t, 128><<<grid, 256, lds, st>>>(static_cast<const uint16_t*>(k), pyr, geo, s, lpb);
@@ -151,9 +153,11 @@ hipError_t launch_build_pyramid(const Geo& geo, int BH, int D, bool bf16, const 
     else
       pool_leaf_kernel<float, 64><<<grid, 256, lds, st>>>(static_cast<const float*>(k), pyr, geo, s, lpb);
   }
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   if (geo.Lstore >= s + 2) {
+    ProfScope ps("pool_top", st);
     pool_top_kernel<<<BH, 256, 0, st>>>(pyr, geo, s + 2, D);
     e = hipGetLastError();
   }

@@ -44,6 +44,11 @@ struct SelArgs {
   float qscale2;    // log2(e) / sqrt(d)
 };
 
+struct TopkArgsP {
+  int Nq, N, C, K, gK, causal;
+  int64_t rows;
+};
+
 template <int TEAM>
 __device__ __forceinline__ void team_sync() {
   if constexpr (TEAM == 64) {
@@ -145,6 +150,8 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
   int* flag = L + 3 * gK;
   int* misc = L + 4 * gK;
   float* zbuf = reinterpret_cast<float*>(L + 4 * gK + 8);
+  float* zself = zbuf + gK * g * G;   // logit of each candidate (per head), NaN if unknown
+  float* zself2 = zself + gK * G;
 
   const int row = blockIdx.x * ROWS + team;
   if (row >= a.Nq) return;  // the whole team leaves together
@@ -172,6 +179,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
   }
 
   if (tid == 0) cand[0] = 0;
+  for (int hh = tid; hh < G; hh += TEAM) zself[hh] = __builtin_nanf("");
   int nA = 1;
   team_sync<TEAM>();
 
@@ -182,30 +190,50 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
     ranked = nA > a.K;
     if (ranked) {
       if (lev >= 2) {
-        // Child logits of every (candidate, child) pair into zbuf.
+        // Child logits of every (candidate, child) pair into zbuf, UNR loads in
+        // flight per lane group.  A candidate whose own logit is known from
+        // the level above (zself) skips its last child: the mean pyramid
+        // makes the node logit the mean of its children's logits, so that
+        // child's logit is nch * z_node - (sum of the others).
         const int Mb = geo.M[lev - 1];
         const float* pbase = a.pyr + (static_cast<int64_t>(bh) * geo.R + geo.off[lev - 1]) * D + sub * DPL;
         const int npairs = nA * g;
-        for (int p = grp; p < npairs; p += NGRP) {
-          const int ci = p / g;
-          const int node = cand[ci];
-          const int r = node * g + (p - ci * g);
-          const bool valid = r < Mb && !fz.is(node);
-          float x[DPL];
-          if (valid) {
-            load_row_part<float, DPL>(pbase + static_cast<int64_t>(r) * D, x);
-          } else {
+        constexpr int UNR = 4;
+        for (int p0 = grp; p0 < npairs; p0 += NGRP * UNR) {
+          float x[UNR][DPL];
+          bool ld[UNR];
 #pragma unroll
-            for (int e = 0; e < DPL; ++e) x[e] = 0.f;
+          for (int u = 0; u < UNR; ++u) {
+            const int p = p0 + u * NGRP;
+            ld[u] = false;
+            int r = 0;
+            if (p < npairs) {
+              const int ci = p / g, j = p - ci * g;
+              const int node = cand[ci];
+              const int nch = min(g, Mb - node * g);
+              const bool derived = j == nch - 1 && !__builtin_isnan(zself[ci * G]);
+              r = node * g + j;
+              ld[u] = j < nch && !fz.is(node) && !derived;
+            }
+            if (ld[u]) {
+              load_row_part<float, DPL>(pbase + static_cast<int64_t>(r) * D, x[u]);
+            } else {
+#pragma unroll
+              for (int e = 0; e < DPL; ++e) x[u][e] = 0.f;
+            }
           }
 #pragma unroll
-          for (int hh = 0; hh < GMAX; ++hh) {
-            if (hh < G) {
-              float d0 = 0.f;
+          for (int u = 0; u < UNR; ++u) {
+            const int p = p0 + u * NGRP;
 #pragma unroll
-              for (int e = 0; e < DPL; ++e) d0 = fmaf(qv[hh][e], x[e], d0);
-              d0 = sum16(d0);
-              if (sub == 0) zbuf[p * G + hh] = valid ? d0 : -INFINITY;
+            for (int hh = 0; hh < GMAX; ++hh) {
+              if (hh < G) {
+                float d0 = 0.f;
+#pragma unroll
+                for (int e = 0; e < DPL; ++e) d0 = fmaf(qv[hh][e], x[u][e], d0);
+                d0 = sum16(d0);
+                if (sub == 0 && p < npairs) zbuf[p * G + hh] = ld[u] ? d0 : -INFINITY;
+              }
             }
           }
         }
@@ -215,11 +243,18 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
           float u = 0.f;
           if (!fz.is(node)) {
             const int nch = min(g, Mb - node * g);
+            const bool has_self = !__builtin_isnan(zself[ci * G]);
             for (int hh = 0; hh < G; ++hh) {
+              float* zc = zbuf + ci * g * G + hh;
+              if (has_self) {
+                float others = 0.f;
+                for (int j = 0; j < nch - 1; ++j) others += zc[j * G];
+                zc[(nch - 1) * G] = static_cast<float>(nch) * zself[ci * G + hh] - others;
+              }
               float m = -INFINITY;
-              for (int j = 0; j < nch; ++j) m = fmaxf(m, zbuf[(ci * g + j) * G + hh]);
+              for (int j = 0; j < nch; ++j) m = fmaxf(m, zc[j * G]);
               float s = 0.f;
-              for (int j = 0; j < nch; ++j) s += fast_exp2(zbuf[(ci * g + j) * G + hh] - m);
+              for (int j = 0; j < nch; ++j) s += fast_exp2(zc[j * G] - m);
               u += m + fast_log2(s);
             }
           }
@@ -311,16 +346,25 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
       }
       int total;
       int pos = team_scan<TEAM>(mine, misc, total);
+      const bool logits_known = ranked && lev >= 2;
       for (int ci = i0; ci < i1; ++ci) {
         if (flag[ci]) {
           const int c0 = cand[ci] * g;
           const int n = max(0, min(c0 + g - 1, rmax) - c0 + 1);
-          for (int j = 0; j < n; ++j) cand2[pos + j] = c0 + j;
+          const bool known = logits_known && !fz.is(cand[ci]);
+          for (int j = 0; j < n; ++j) {
+            cand2[pos + j] = c0 + j;
+            for (int hh = 0; hh < G; ++hh)
+              zself2[(pos + j) * G + hh] = known ? zbuf[(ci * g + j) * G + hh] : __builtin_nanf("");
+          }
           pos += n;
         }
       }
       team_sync<TEAM>();
-      for (int ci = tid; ci < total; ci += TEAM) cand[ci] = cand2[ci];
+      for (int ci = tid; ci < total; ci += TEAM) {
+        cand[ci] = cand2[ci];
+        for (int hh = 0; hh < G; ++hh) zself[ci * G + hh] = zself2[ci * G + hh];
+      }
       nA = total;
       team_sync<TEAM>();
     }
@@ -360,86 +404,262 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
 }
 
 // ----------------------------------------------------------------------------
-// Two-stage remainder: cluster build, MFMA leaf scoring, final Top-K.
+// Stage 1 for g*K <= 32: two query rows per wavefront, one candidate per lane.
+//
+// Lanes 0-31 own row 2w and lanes 32-63 row 2w+1 (lane hl of a half holds
+// candidate hl).  Per ranked level: the candidates needing child logits build
+// a compact load list (a candidate whose own logit is known loads one child
+// fewer, see select_kernel), the two 16-lane groups of each half compute the
+// listed dots, each lane turns its children's logits into its LSE score, and
+// a 32-lane bitonic sort on (score desc, node asc) with forced nodes keyed
+// +inf ranks the half: the first K survive.  Survivors expand through an LDS
+// staging list.  The leaf candidate set is sorted ascending before it is
+// stored.
 // ----------------------------------------------------------------------------
 
-struct PairArgs {
-  int Nq, N, C, K, gK, M1, causal;
-  int64_t rows;  // BH * Nq
-};
-
-__device__ __forceinline__ bool pair_needs_score(const PairArgs& a, const int32_t* a1, const int32_t* a1cnt,
-                                                 int64_t gid, int& bh, int& row, int& slot, int& blk) {
-  const int64_t rg = gid / a.gK;
-  slot = static_cast<int>(gid - rg * a.gK);
-  const int n = a1cnt[rg];
-  if (slot >= n || n <= a.K) return false;
-  blk = a1[gid];
-  bh = static_cast<int>(rg / a.Nq);
-  row = static_cast<int>(rg - static_cast<int64_t>(bh) * a.Nq);
-  const int c = (a.N - a.Nq + row) / a.C;
-  if (a.causal && (blk == 0 || blk == c || blk == c - 1)) return false;
-  return true;
+// Does (ka, pa) rank before (kb, pb)?  Higher key first, then smaller pack.
+__device__ __forceinline__ bool better(float ka, int pa, float kb, int pb) {
+  return ka > kb || (ka == kb && pa < pb);
 }
 
-__global__ __launch_bounds__(256) void fill_zero_kernel(int32_t* p, int64_t n) {
-  for (int64_t i = blockIdx.x * 256LL + threadIdx.x; i < n; i += 256LL * gridDim.x) p[i] = 0;
-}
-
-__global__ __launch_bounds__(256) void cluster_count_kernel(PairArgs a, const int32_t* __restrict__ a1,
-                                                            const int32_t* __restrict__ a1cnt,
-                                                            int32_t* __restrict__ hist) {
-  const int64_t gid = blockIdx.x * 256LL + threadIdx.x;
-  if (gid >= a.rows * a.gK) return;
-  int bh, row, slot, blk;
-  if (!pair_needs_score(a, a1, a1cnt, gid, bh, row, slot, blk)) return;
-  atomicAdd(&hist[static_cast<int64_t>(bh) * a.M1 + blk], 1);
-}
-
-// Exclusive scan of n counts into offs[0..n] and cursor[0..n), one workgroup.
-__global__ __launch_bounds__(1024) void cluster_scan_kernel(const int32_t* __restrict__ hist,
-                                                            int32_t* __restrict__ offs,
-                                                            int32_t* __restrict__ cursor, int64_t n) {
-  __shared__ int wsum[16];
-  const int tid = threadIdx.x;
-  const int64_t per = (n + 1023) / 1024;
-  const int64_t i0 = tid * per, i1 = min(n, i0 + per);
-  int local = 0;
-  for (int64_t i = i0; i < i1; ++i) local += hist[i];
-  const int lane = tid & 63, w = tid >> 6;
-  int x = local;
+// Bitonic sort of the 32 lanes of each wavefront half into rank order.
+__device__ __forceinline__ void sort32(float& key, int& pack, int hl) {
 #pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const int y = __shfl_up(x, o);
-    if (lane >= o) x += y;
+  for (int k = 2; k <= 32; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const float ok = __shfl_xor(key, j, 32);
+      const int op = __shfl_xor(pack, j, 32);
+      const bool dir = (hl & k) == 0;
+      const bool lower = (hl & j) == 0;
+      const bool take = (lower == dir) ? better(ok, op, key, pack) : better(key, pack, ok, op);
+      if (take) {
+        key = ok;
+        pack = op;
+      }
+    }
   }
-  if (lane == 63) wsum[w] = x;
-  __syncthreads();
-  int pre = 0, tot = 0;
-  for (int i = 0; i < 16; ++i) {
-    pre += (i < w) ? wsum[i] : 0;
-    tot += wsum[i];
-  }
-  int run = pre + x - local;
-  for (int64_t i = i0; i < i1; ++i) {
-    offs[i] = run;
-    cursor[i] = run;
-    run += hist[i];
-  }
-  if (tid == 0) offs[n] = tot;
 }
 
-__global__ __launch_bounds__(256) void cluster_scatter_kernel(PairArgs a, const int32_t* __restrict__ a1,
-                                                              const int32_t* __restrict__ a1cnt,
-                                                              int32_t* __restrict__ cursor,
-                                                              int32_t* __restrict__ pairs) {
-  const int64_t gid = blockIdx.x * 256LL + threadIdx.x;
-  if (gid >= a.rows * a.gK) return;
-  int bh, row, slot, blk;
-  if (!pair_needs_score(a, a1, a1cnt, gid, bh, row, slot, blk)) return;
-  const int pos = atomicAdd(&cursor[static_cast<int64_t>(bh) * a.M1 + blk], 1);
-  pairs[pos] = (row << 8) | slot;
+// Inclusive prefix sum over the 32 lanes of a wavefront half.
+__device__ __forceinline__ int scan32(int v, int hl) {
+#pragma unroll
+  for (int o = 1; o < 32; o <<= 1) {
+    const int y = __shfl_up(v, o, 32);
+    if (hl >= o) v += y;
+  }
+  return v;
 }
+
+template <int D, int GMAX>
+__global__ __launch_bounds__(256, (GMAX == 1 ? 8 : 2)) void stage1_pair_kernel(SelArgs a, int row_words) {
+  constexpr int DPL = D / 16;
+  constexpr int UNR = 4;
+  extern __shared__ int lds_i[];
+  const Geo& geo = a.geo;
+  const int g = geo.g, G = a.G, K = a.K, gK = a.gK;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5, hl = lane & 31;
+  const int gr = (lane >> 4) & 1;  // lane group within the half
+  const int sub = lane & 15;
+  int* L = lds_i + (wave * 2 + half) * row_words;
+  int* lst_r = L;                                   // [gK*g] child row to load
+  int* lst_s = lst_r + gK * g;                      // [gK*g] zbuf slot of that child
+  int* cand2 = lst_s + gK * g;                      // [gK]
+  float* zbuf = reinterpret_cast<float*>(cand2 + gK);  // [gK*g*G]
+  float* zs2 = zbuf + gK * g * G;                   // [gK*G]
+
+  const int row = (blockIdx.x * 4 + wave) * 2 + half;
+  const bool live = row < a.Nq;
+  const int rowc = live ? row : a.Nq - 1;
+  const int bh = blockIdx.y;
+  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+  const int t = geo.N - a.Nq + rowc;
+  const int c = t / geo.C;
+
+  float qv[GMAX][DPL];
+  {
+    const uint16_t* qb = static_cast<const uint16_t*>(a.q);
+#pragma unroll
+    for (int hh = 0; hh < GMAX; ++hh) {
+      if (hh < G) {
+        const int64_t off = ((static_cast<int64_t>(b) * a.H + h * G + hh) * a.Nq + rowc) * D + sub * DPL;
+        load_row_part<uint16_t, DPL>(qb + off, qv[hh]);
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) qv[hh][e] *= a.qscale2;
+      } else {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) qv[hh][e] = 0.f;
+      }
+    }
+  }
+
+  int node = hl == 0 ? 0 : -1;  // candidate of this lane (-1: none)
+  float zs[GMAX];               // its logit per head, NaN if unknown
+#pragma unroll
+  for (int hh = 0; hh < GMAX; ++hh) zs[hh] = __builtin_nanf("");
+  int nA = 1;
+
+  for (int lev = geo.L; lev >= 2; --lev) {
+    const Forced fz = forced_at(geo, lev, c, a.causal);
+    const bool ranked = nA > K;
+    const int Mb = geo.M[lev - 1];
+    const bool valid = node >= 0;
+    const bool isf = valid && fz.is(node);
+    const int nch = valid ? min(g, Mb - node * g) : 0;
+    float key = valid ? INFINITY : -INFINITY;
+    if (ranked) {
+      // 1) compact list of the child rows to load
+      const bool has_self = !__builtin_isnan(zs[0]);
+      const int nl = (valid && !isf) ? (has_self ? nch - 1 : nch) : 0;
+      const int incl = scan32(nl, hl);
+      const int T = __shfl(incl, (lane & 32) + 31);
+      int pos = incl - nl;
+      for (int j = 0; j < nl; ++j) {
+        lst_r[pos + j] = node * g + j;
+        lst_s[pos + j] = hl * g + j;
+      }
+      wave_sync();
+      // 2) child logits, UNR loads in flight per 16-lane group
+      const float* pbase = a.pyr + (static_cast<int64_t>(bh) * geo.R + geo.off[lev - 1]) * D + sub * DPL;
+      for (int e0 = gr; e0 < T; e0 += 2 * UNR) {
+        float x[UNR][DPL];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          const int e = e0 + 2 * u;
+          if (e < T) {
+            load_row_part<float, DPL>(pbase + static_cast<int64_t>(lst_r[e]) * D, x[u]);
+          } else {
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) x[u][i] = 0.f;
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          const int e = e0 + 2 * u;
+#pragma unroll
+          for (int hh = 0; hh < GMAX; ++hh) {
+            if (hh < G) {
+              float d0 = 0.f;
+#pragma unroll
+              for (int i = 0; i < DPL; ++i) d0 = fmaf(qv[hh][i], x[u][i], d0);
+              d0 = sum16(d0);
+              if (sub == 0 && e < T) zbuf[lst_s[e] * G + hh] = d0;
+            }
+          }
+        }
+      }
+      wave_sync();
+      // 3) this lane's candidate score
+      if (valid && !isf) {
+        float u = 0.f;
+#pragma unroll
+        for (int hh = 0; hh < GMAX; ++hh) {
+          if (hh < G) {
+            float* zc = zbuf + hl * g * G + hh;
+            if (has_self) {
+              float others = 0.f;
+              for (int j = 0; j < nch - 1; ++j) others += zc[j * G];
+              zc[(nch - 1) * G] = static_cast<float>(nch) * zs[hh] - others;
+            }
+            float m = -INFINITY;
+            for (int j = 0; j < nch; ++j) m = fmaxf(m, zc[j * G]);
+            float ssum = 0.f;
+            for (int j = 0; j < nch; ++j) ssum += fast_exp2(zc[j * G] - m);
+            u += m + fast_log2(ssum);
+          }
+        }
+        key = u;
+      }
+    }
+    // 4) rank: the first K in (key desc, node asc) order survive
+    int pack = valid ? (node << 6) | hl : 0x7FFFFFC0 | hl;
+    float skey = key;
+    sort32(skey, pack, hl);
+    int knode, korig;
+    bool kept;
+    if (ranked) {
+      kept = hl < K && skey != -INFINITY;
+      knode = pack >> 6;
+      korig = pack & 63;
+    } else {
+      kept = valid;
+      knode = node;
+      korig = hl;
+    }
+    const bool known = ranked && kept && !fz.is(knode);
+    wave_sync();  // zbuf reads of step 3 are done before cand2/zs2 are written
+    // 5) expand survivors to their eligible children
+    const int64_t span_below = geo.gpow[lev - 1] * geo.C;
+    const int rmax = a.causal ? static_cast<int>(min<int64_t>(t / span_below, Mb - 1)) : Mb - 1;
+    const int c0 = knode * g;
+    const int nk = kept ? max(0, min(c0 + g - 1, rmax) - c0 + 1) : 0;
+    const int incl = scan32(nk, hl);
+    const int nA2 = __shfl(incl, (lane & 32) + 31);
+    int pos = incl - nk;
+    for (int j = 0; j < nk; ++j) {
+      cand2[pos + j] = c0 + j;
+      for (int hh = 0; hh < G; ++hh)
+        zs2[(pos + j) * G + hh] = known ? zbuf[(korig * g + j) * G + hh] : __builtin_nanf("");
+    }
+    wave_sync();
+    node = hl < nA2 ? cand2[hl] : -1;
+#pragma unroll
+    for (int hh = 0; hh < GMAX; ++hh) zs[hh] = (hh < G && hl < nA2) ? zs2[hl * G + hh] : __builtin_nanf("");
+    nA = nA2;
+    wave_sync();
+  }
+
+  // Leaf candidate set ascending.
+  float akey = node >= 0 ? -static_cast<float>(node) : -INFINITY;
+  int apack = node >= 0 ? node : 0x7FFFFFC0 | hl;
+  sort32(akey, apack, hl);
+  if (live) {
+    const int64_t orow = static_cast<int64_t>(bh) * a.Nq + row;
+    if (hl < gK) a.a1[orow * gK + hl] = hl < nA ? apack : -1;
+    if (hl == 0) a.a1cnt[orow] = nA;
+  }
+}
+
+// Final Top-K for g*K <= 32: two rows per wavefront, one candidate per lane.
+// A first sort32 puts the candidates in rank order (forced and unranked rows
+// keyed +inf); the survivors are the first min(n, K) lanes; a second sort32
+// orders them by block index and carries the lane that holds each score.
+__global__ __launch_bounds__(256) void final_topk_pair_kernel(TopkArgsP a, const int32_t* __restrict__ a1,
+                                                              const int32_t* __restrict__ a1cnt,
+                                                              const float* __restrict__ u1,
+                                                              int32_t* __restrict__ idx, float* __restrict__ score) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5, hl = lane & 31;
+  const int64_t rg = (blockIdx.x * 4LL + wave) * 2 + half;
+  const bool live = rg < a.rows;
+  const int64_t rgc = live ? rg : a.rows - 1;
+  const int row = static_cast<int>(rgc % a.Nq);
+  const int c = (a.N - a.Nq + row) / a.C;
+  const int n = a1cnt[rgc];
+  const bool ranked = n > a.K;
+  const bool valid = hl < n;
+  const int node = valid ? a1[rgc * a.gK + hl] : -1;
+  const bool isf = a.causal && valid && (node == 0 || node == c || node == c - 1);
+  float key = -INFINITY;
+  if (valid) key = (ranked && !isf) ? u1[rgc * a.gK + hl] : INFINITY;
+  int pack = valid ? node : 0x7FFFFFC0 | hl;
+  sort32(key, pack, hl);
+  const bool kept = hl < min(n, a.K) && key != -INFINITY;
+  float k2 = kept ? -static_cast<float>(pack) : -INFINITY;
+  int p2 = kept ? (pack << 6) | hl : 0x7FFFFFC0 | hl;
+  sort32(k2, p2, hl);
+  const float sc = __shfl(key, (lane & 32) + (p2 & 63));
+  if (live && hl < a.K) {
+    const bool out = k2 != -INFINITY;
+    idx[rg * a.K + hl] = out ? (p2 >> 6) : -1;
+    if (score) score[rg * a.K + hl] = !out ? -INFINITY : (sc == INFINITY ? INFINITY : sc * kLn2);
+  }
+}
+
+// ----------------------------------------------------------------------------
+// Two-stage remainder: cluster build, MFMA leaf scoring, final Top-K.
+// ----------------------------------------------------------------------------
 
 typedef __bf16 bf16x8v __attribute__((ext_vector_type(8)));
 typedef float f32x16v __attribute__((ext_vector_type(16)));
@@ -453,24 +673,25 @@ struct LeafArgs {
   float qscale2;
 };
 
-// One workgroup per (leaf block, batch x KV head): the C x D key block is
-// staged in LDS once (rows padded by 16 B against bank conflicts) and every
-// (query, slot) pair of the block's cluster is scored against it, 32 pairs
-// per wavefront tile.
+// One workgroup per tile of up to kClusterTile pairs of one (batch x KV head,
+// leaf block) cluster: the C x D key block is staged in LDS (rows padded by
+// 16 B against bank conflicts) and the tile's (query, slot) pairs are scored
+// against it, 32 pairs per wavefront MFMA tile.
 template <int D>
 __global__ __launch_bounds__(256) void leaf_score_kernel(LeafArgs a, const uint16_t* __restrict__ q,
                                                          const uint16_t* __restrict__ k,
                                                          const int32_t* __restrict__ offs,
+                                                         const int32_t* __restrict__ toffs, int64_t ncl,
                                                          const int32_t* __restrict__ pairs,
                                                          float* __restrict__ u1) {
   constexpr int LDR = D + 8;  // padded LDS row, in bf16 elements
   constexpr int KS = D / 16;
   extern __shared__ uint16_t klds[];
-  const int blk = blockIdx.x;
-  const int bh = blockIdx.y;
-  const int64_t cl = static_cast<int64_t>(bh) * a.M1 + blk;
-  const int beg = offs[cl], end = offs[cl + 1];
-  if (beg == end) return;
+  int64_t cl;
+  int beg, end;
+  if (!cluster_tile(offs, toffs, ncl, blockIdx.x, cl, beg, end)) return;
+  const int bh = static_cast<int>(cl / a.M1);
+  const int blk = static_cast<int>(cl - static_cast<int64_t>(bh) * a.M1);
   const int b = bh / a.Hkv, h = bh - b * a.Hkv;
   const int r0 = blk * a.C;
   const int nrows = min(a.C, a.N - r0);
@@ -616,7 +837,7 @@ __global__ __launch_bounds__(256) void final_topk_kernel(TopkArgs a, const int32
 
 static int sel_lds_words(const Shape& s) {
   const int gK = s.gK();
-  int w = 4 * gK + 8 + gK * s.g * s.G;
+  int w = 4 * gK + 8 + gK * s.g * s.G + 2 * gK * s.G;
   return (w + 3) & ~3;
 }
 
@@ -666,6 +887,7 @@ hipError_t launch_select_fused(const Shape& s, const Geo& geo, const void* q, co
   a.score = score;
   // Few rows: a whole workgroup per row to cut latency; many rows: a wave per row.
   const bool wide = static_cast<int64_t>(s.BH()) * s.Nq <= 2048;
+  ProfScope ps("select_fused", st);
   if (s.bf16) {
     if (wide)
       launch_sel_d<uint16_t, 256, true>(s, a, st);
@@ -683,21 +905,17 @@ hipError_t launch_select_fused(const Shape& s, const Geo& geo, const void* q, co
 static size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 struct TwoStageWs {
-  size_t a1, a1cnt, u1, hist, offs, cursor, pairs, total;
+  size_t a1, a1cnt, u1, cl, total;
 };
 
 static TwoStageWs two_stage_layout(const Shape& s, const Geo& geo) {
   const size_t rows = static_cast<size_t>(s.BH()) * s.Nq;
-  const size_t ncl = static_cast<size_t>(s.BH()) * geo.M[1];
   TwoStageWs w{};
   size_t o = 0;
   w.a1 = o;     o += align256(rows * s.gK() * 4);
   w.a1cnt = o;  o += align256(rows * 4);
   w.u1 = o;     o += align256(rows * s.gK() * 4);
-  w.hist = o;   o += align256(ncl * 4);
-  w.offs = o;   o += align256((ncl + 1) * 4);
-  w.cursor = o; o += align256(ncl * 4);
-  w.pairs = o;  o += align256(rows * s.gK() * 4);
+  w.cl = o;     o += align256(cluster_ws(s.BH(), geo.M[1], static_cast<int64_t>(rows) * s.gK()));
   w.total = o;
   return w;
 }
@@ -711,45 +929,70 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
   int32_t* a1 = reinterpret_cast<int32_t*>(base + w.a1);
   int32_t* a1cnt = reinterpret_cast<int32_t*>(base + w.a1cnt);
   float* u1 = reinterpret_cast<float*>(base + w.u1);
-  int32_t* hist = reinterpret_cast<int32_t*>(base + w.hist);
-  int32_t* offs = reinterpret_cast<int32_t*>(base + w.offs);
-  int32_t* cursor = reinterpret_cast<int32_t*>(base + w.cursor);
-  int32_t* pairs = reinterpret_cast<int32_t*>(base + w.pairs);
   hipError_t e;
 
-  // Stage 1: intermediate levels, one wavefront per (row, KV head).
+  // Stage 1: intermediate levels.
   SelArgs a = make_sel_args(s, geo, q, k, pyr);
   a.a1 = a1;
   a.a1cnt = a1cnt;
-  launch_sel_d<uint16_t, 64, false>(s, a, st);
+  const bool narrow = s.gK() <= 32;
+  {
+    ProfScope ps("select_stage1", st);
+    if (narrow) {
+      const int gK = s.gK();
+      const int words = gK * s.g * 2 + gK + gK * s.g * s.G + gK * s.G;
+      dim3 grid((s.Nq + 7) / 8, s.BH());
+      const size_t lds = static_cast<size_t>(8) * words * sizeof(int);
+      auto go = [&](auto kern) { kern<<<grid, 256, lds, st>>>(a, words); };
+      if (s.D == 128) {
+        if (s.G == 1) go(stage1_pair_kernel<128, 1>);
+        else if (s.G <= 4) go(stage1_pair_kernel<128, 4>);
+        else go(stage1_pair_kernel<128, 16>);
+      } else {
+        if (s.G == 1) go(stage1_pair_kernel<64, 1>);
+        else if (s.G <= 4) go(stage1_pair_kernel<64, 4>);
+        else go(stage1_pair_kernel<64, 16>);
+      }
+    } else {
+      launch_sel_d<uint16_t, 64, false>(s, a, st);
+    }
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
   // Cluster the (row, slot) pairs by leaf block.
   const int64_t rows = static_cast<int64_t>(s.BH()) * s.Nq;
-  const int64_t ncl = static_cast<int64_t>(s.BH()) * geo.M[1];
-  PairArgs pa{s.Nq, s.N, s.C, s.K, s.gK(), geo.M[1], s.causal, rows};
-  fill_zero_kernel<<<static_cast<unsigned>(std::min<int64_t>((ncl + 255) / 256, 4096)), 256, 0, st>>>(hist, ncl);
-  const unsigned pgrid = static_cast<unsigned>((rows * s.gK() + 255) / 256);
-  cluster_count_kernel<<<pgrid, 256, 0, st>>>(pa, a1, a1cnt, hist);
-  cluster_scan_kernel<<<1, 1024, 0, st>>>(hist, offs, cursor, ncl);
-  cluster_scatter_kernel<<<pgrid, 256, 0, st>>>(pa, a1, a1cnt, cursor, pairs);
-  if ((e = hipGetLastError()) != hipSuccess) return e;
+  ClusterArgs ca{a1, a1cnt, s.gK(), s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], kClusterLeaf, 0, s.Nq};
+  ClusterOut co{};
+  if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st)) != hipSuccess) return e;
 
   // Stage 2: leaf scoring against each key block once per cluster.
   LeafArgs la{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, geo.M[1], s.gK(), kLog2e / sqrtf(static_cast<float>(s.D))};
-  dim3 lgrid(geo.M[1], s.BH());
+  dim3 lgrid(static_cast<unsigned>(cluster_max_tiles(s.BH(), geo.M[1], rows * s.gK())));
   const size_t llds = static_cast<size_t>(s.C) * (s.D + 8) * 2;
+  {
+  ProfScope ps("leaf_score", st);
+  auto go = [&](auto kern) {
+    if (llds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                          hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(llds));
+    kern<<<lgrid, 256, llds, st>>>(la, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), co.offs,
+                                   co.toffs, co.ncl, co.pairs, u1);
+  };
   if (s.D == 128)
-    leaf_score_kernel<128><<<lgrid, 256, llds, st>>>(la, static_cast<const uint16_t*>(q),
-                                                     static_cast<const uint16_t*>(k), offs, pairs, u1);
+    go(leaf_score_kernel<128>);
   else
-    leaf_score_kernel<64><<<lgrid, 256, llds, st>>>(la, static_cast<const uint16_t*>(q),
-                                                    static_cast<const uint16_t*>(k), offs, pairs, u1);
+    go(leaf_score_kernel<64>);
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
   // Final Top-K per row.
-  TopkArgs ta{s.Nq, s.N, s.C, s.K, s.gK(), s.causal, rows};
-  final_topk_kernel<<<static_cast<unsigned>((rows + 3) / 4), 256, 0, st>>>(ta, a1, a1cnt, u1, idx, score);
+  ProfScope ps("final_topk", st);
+  if (narrow) {
+    TopkArgsP ta{s.Nq, s.N, s.C, s.K, s.gK(), s.causal, rows};
+    final_topk_pair_kernel<<<static_cast<unsigned>((rows + 7) / 8), 256, 0, st>>>(ta, a1, a1cnt, u1, idx, score);
+  } else {
+    TopkArgs ta{s.Nq, s.N, s.C, s.K, s.gK(), s.causal, rows};
+    final_topk_kernel<<<static_cast<unsigned>((rows + 3) / 4), 256, 0, st>>>(ta, a1, a1cnt, u1, idx, score);
+  }
   return hipGetLastError();
 }
 

@@ -24,9 +24,11 @@ rows, d = head dim, C = leaf block size, g = fan-out, K = block budget):
 * ``decode-128k``  bf16, B=1, H=Hkv=8, N=131072, Nq=1, d=128, C=64, g=2,
                    K=16; k, v i.i.d. N(0,1); 64 single-token query steps.
 
-Every tensor comes from ``np.random.default_rng(SeedSequence([seed, cfg_id,
-tensor_id]))`` in float32 and is then rounded to bfloat16 (round to nearest
-even) when the workload is bf16.  The arrays returned are float32 holding the
+Every (batch, head) slice of every tensor comes from its own stream
+``np.random.default_rng(SeedSequence([seed, cfg_id, tensor_id, b, h]))`` in
+float32 (needle positions and the needle direction from stream
+``[seed, cfg_id, 3]``) and is then rounded to bfloat16 (round to nearest even)
+when the workload is bf16.  The arrays returned are float32 holding the
 exact stored values, so the GPU (which receives bf16) and the oracle (which
 widens to float64) see identical numbers.
 """
@@ -52,25 +54,39 @@ _Q, _K, _V, _AUX = 0, 1, 2, 3
 
 def round_to_bf16(x: np.ndarray) -> np.ndarray:
     """Round float32 values to the nearest bfloat16 (ties to even); return float32."""
-    x = np.ascontiguousarray(x, dtype=np.float32)
-    bits = x.view(np.uint32)
-    lsb = (bits >> 16) & 1
-    rounded = (bits + np.uint32(0x7FFF) + lsb) & np.uint32(0xFFFF0000)
-    # NaN/Inf never occur in these generators; keep them untouched anyway.
-    special = (bits & 0x7F800000) == 0x7F800000
-    rounded = np.where(special, bits, rounded).astype(np.uint32)
-    return rounded.view(np.float32)
+    import torch
+
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32))
+    return t.to(torch.bfloat16).to(torch.float32).numpy()
 
 
 def _rng(seed: int, cfg_id: int, tensor_id: int) -> np.random.Generator:
     return np.random.default_rng(np.random.SeedSequence([seed, cfg_id, tensor_id]))
 
 
-def _normal(rng, shape) -> np.ndarray:
+def _per_head(seed: int, cfg_id: int, tensor_id: int, shape, fill) -> np.ndarray:
+    """Fill a [B, Hx, ...] float32 array one (b, h) slice at a time, each slice
+    from its own stream SeedSequence([seed, cfg_id, tensor_id, b, h])."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    out = np.empty(shape, dtype=np.float32)
+    B, Hx = shape[0], shape[1]
+
+    def one(i):
+        b, h = divmod(i, Hx)
+        rng = np.random.default_rng(np.random.SeedSequence([seed, cfg_id, tensor_id, b, h]))
+        out[b, h] = fill(rng, shape[2:])
+
+    with ThreadPoolExecutor(max_workers=max(1, min(16, B * Hx))) as ex:
+        list(ex.map(one, range(B * Hx)))
+    return out
+
+
+def _normal_fill(rng, shape):
     return rng.standard_normal(size=shape, dtype=np.float32)
 
 
-def _ar1(rng, shape, rho: float) -> np.ndarray:
+def _ar1_fill(rng, shape, rho: float = 0.999) -> np.ndarray:
     """Stationary AR(1) along axis -2: x_0 ~ N(0,1), x_t = rho x_{t-1} + sqrt(1-rho^2) e_t."""
     from scipy.signal import lfilter
 
@@ -104,11 +120,11 @@ def make_inputs(w: dict, seed: int = 0, step: int = 0) -> dict:
     qshape, kshape = (B, H, Nq, d), (B, Hkv, N, d)
     q_tid = _Q if step == 0 else 16 + step
     if dist in ("iid", "iid_qscaled"):
-        q = _normal(_rng(seed, cid, q_tid), qshape)
+        q = _per_head(seed, cid, q_tid, qshape, _normal_fill)
         if dist == "iid_qscaled":
-            q = q * np.float32(1.0 / np.sqrt(d))
-        k = _normal(_rng(seed, cid, _K), kshape)
-        v = _normal(_rng(seed, cid, _V), kshape)
+            q *= np.float32(1.0 / np.sqrt(d))
+        k = _per_head(seed, cid, _K, kshape, _normal_fill)
+        v = _per_head(seed, cid, _V, kshape, _normal_fill)
     elif dist == "needles":
         rng_aux = _rng(seed, cid, _AUX)
         n = rng_aux.standard_normal(d)
@@ -119,17 +135,18 @@ def make_inputs(w: dict, seed: int = 0, step: int = 0) -> dict:
             if n_needles else np.zeros(0, dtype=np.int64)
         n_qpos = Nq // 4
         qpos = np.sort(rng_aux.choice(Nq, size=n_qpos, replace=False)) if n_qpos else np.zeros(0, np.int64)
-        k = _normal(_rng(seed, cid, _K), kshape)
+        k = _per_head(seed, cid, _K, kshape, _normal_fill)
         for b in needle_blocks:
             k[:, :, b * C:min((b + 1) * C, N), :] = 4.0 * u
-        q = _normal(_rng(seed, cid, q_tid), qshape)
-        noise = _normal(_rng(seed, cid, _AUX + 10), (B, H, n_qpos, d))
-        q[:, :, qpos, :] = u + 0.5 * noise
-        v = _normal(_rng(seed, cid, _V), kshape)
+        q = _per_head(seed, cid, q_tid, qshape, _normal_fill)
+        if n_qpos:
+            noise = _per_head(seed, cid, _AUX + 10, (B, H, n_qpos, d), _normal_fill)
+            q[:, :, qpos, :] = u + 0.5 * noise
+        v = _per_head(seed, cid, _V, kshape, _normal_fill)
     elif dist == "ar1":
-        q = _ar1(_rng(seed, cid, q_tid), qshape, 0.999)
-        k = _ar1(_rng(seed, cid, _K), kshape, 0.999)
-        v = _normal(_rng(seed, cid, _V), kshape)
+        q = _per_head(seed, cid, q_tid, qshape, _ar1_fill)
+        k = _per_head(seed, cid, _K, kshape, _ar1_fill)
+        v = _per_head(seed, cid, _V, kshape, _normal_fill)
     else:
         raise ValueError(f"unknown distribution {dist!r}")
     if w["dtype"] == "bf16":

@@ -32,7 +32,7 @@ EXPORTS = (
     "pisa_num_levels", "pisa_pyramid_layout", "pisa_pyramid_bytes",
     "pisa_select_workspace_bytes", "pisa_bsa_workspace_bytes", "pisa_attn_workspace_bytes",
     "pisa_build_pyramid", "pisa_select", "pisa_select_flat_bsa", "pisa_sparse_attn_fwd",
-    "pisa_status_string", "pisa_last_error",
+    "pisa_profile_enable", "pisa_profile_report", "pisa_status_string", "pisa_last_error",
 )
 
 
@@ -74,6 +74,8 @@ def _load():
         "pisa_select": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pisa_select_flat_bsa": (ctypes.c_int, [P, vp, vp, vp, vp, sz, vp]),
         "pisa_sparse_attn_fwd": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "pisa_profile_enable": (ctypes.c_int, [ctypes.c_int]),
+        "pisa_profile_report": (ctypes.c_int, [ctypes.c_char_p, sz]),
         "pisa_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "pisa_last_error": (ctypes.c_char_p, []),
     }
@@ -165,6 +167,22 @@ def pisa_sparse_attn_fwd(p: Problem, q, k, v, block_idx, o, lse=None, ws=None, w
     return _check(_lib.pisa_sparse_attn_fwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(block_idx),
                                             _ptr(o), _ptr(lse), _ptr(ws), ws_bytes, _stream(stream)),
                   "pisa_sparse_attn_fwd")
+
+
+def pisa_profile_enable(on: bool) -> int:
+    return _lib.pisa_profile_enable(1 if on else 0)
+
+
+def pisa_profile_report() -> dict:
+    """{kernel: (launches, total_ms)} since the last report (waits for the events)."""
+    cap = 1 << 16
+    buf = ctypes.create_string_buffer(cap)
+    _lib.pisa_profile_report(buf, cap)
+    out = {}
+    for line in buf.value.decode().splitlines():
+        name, cnt, ms = line.split()
+        out[name] = (int(cnt), float(ms))
+    return out
 
 
 def pisa_status_string(status: int) -> str:

@@ -48,6 +48,7 @@ SHAPES = {
     "decode-row": (1, 4, 4, 1, 10000, 128, 64, 2, 8, 1, "bf16"),
     "big-budget": (1, 2, 2, 2048, 2048, 64, 32, 2, 64, 1, "f32"),
     "noncausal-f32-ragged": (1, 2, 1, 777, 777, 64, 32, 2, 4, 0, "f32"),
+    "c128-g4-gqa": (1, 8, 2, 6000, 6000, 128, 128, 4, 8, 1, "bf16"),
 }
 
 
