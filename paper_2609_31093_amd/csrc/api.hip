@@ -44,7 +44,13 @@ int compute_geo(int32_t N, int32_t C, int32_t g, pisa::Geo* geo) {
   }
   G.L = L;
   G.Lstore = L > 1 ? L - 1 : 1;
+  G.lg = -1;
+  for (int b = 0; b < 31; ++b)
+    if ((1 << b) == g) G.lg = b;
   G.gpow[1] = 1;
+  G.gp[1] = 1;
+  for (int l = 2; l <= pisa::kMaxLevels; ++l)
+    G.gp[l] = G.gp[l - 1] > (1 << 26) ? (1 << 30) : G.gp[l - 1] * g;
   for (int l = 2; l <= pisa::kMaxLevels; ++l)  // saturate beyond the root
     G.gpow[l] = G.gpow[l - 1] > (int64_t(1) << 40) ? G.gpow[l - 1] : G.gpow[l - 1] * g;
   G.off[1] = 0;

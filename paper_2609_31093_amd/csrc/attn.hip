@@ -32,17 +32,17 @@ __device__ __forceinline__ void store_row_part(T* p, const float (&x)[DPL]);
 template <>
 __device__ __forceinline__ void store_row_part<uint16_t, 8>(uint16_t* p, const float (&x)[8]) {
   uint4 r;
-  r.x = f32_to_bf16_rne(x[0]) | (static_cast<uint32_t>(f32_to_bf16_rne(x[1])) << 16);
-  r.y = f32_to_bf16_rne(x[2]) | (static_cast<uint32_t>(f32_to_bf16_rne(x[3])) << 16);
-  r.z = f32_to_bf16_rne(x[4]) | (static_cast<uint32_t>(f32_to_bf16_rne(x[5])) << 16);
-  r.w = f32_to_bf16_rne(x[6]) | (static_cast<uint32_t>(f32_to_bf16_rne(x[7])) << 16);
+  r.x = pack2_bf16(x[0], x[1]);
+  r.y = pack2_bf16(x[2], x[3]);
+  r.z = pack2_bf16(x[4], x[5]);
+  r.w = pack2_bf16(x[6], x[7]);
   *reinterpret_cast<uint4*>(p) = r;
 }
 template <>
 __device__ __forceinline__ void store_row_part<uint16_t, 4>(uint16_t* p, const float (&x)[4]) {
   uint2 r;
-  r.x = f32_to_bf16_rne(x[0]) | (static_cast<uint32_t>(f32_to_bf16_rne(x[1])) << 16);
-  r.y = f32_to_bf16_rne(x[2]) | (static_cast<uint32_t>(f32_to_bf16_rne(x[3])) << 16);
+  r.x = pack2_bf16(x[0], x[1]);
+  r.y = pack2_bf16(x[2], x[3]);
   *reinterpret_cast<uint2*>(p) = r;
 }
 template <>
@@ -190,10 +190,6 @@ struct AttnBlockArgs {
 
 __device__ __forceinline__ bf16x8a u4_as_bf16x8(uint4 r) { return __builtin_bit_cast(bf16x8a, r); }
 
-__device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
-  return static_cast<uint32_t>(f32_to_bf16_rne(a)) | (static_cast<uint32_t>(f32_to_bf16_rne(b)) << 16);
-}
-
 template <int D, int CT>
 __global__ __launch_bounds__(256) void attn_block_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
                                                          const uint16_t* __restrict__ k,
@@ -206,11 +202,12 @@ __global__ __launch_bounds__(256) void attn_block_kernel(AttnBlockArgs a, const 
   constexpr int KS = D / 16;       // k-steps of QK^T
   constexpr int LDK = D + 8;       // padded K row (bf16 elements)
   constexpr int C = CT * 32;       // keys per block
-  constexpr int LDV = C + 8;       // padded V^T row
+  constexpr int LDV = C + 4;       // padded V^T row: (LDV/2) is 2 mod 4 dwords
   constexpr int DT = D / 32;       // output d tiles
   extern __shared__ uint16_t lds[];
   uint16_t* klds = lds;
   uint16_t* vt = lds + C * LDK;
+  uint32_t* vt32 = reinterpret_cast<uint32_t*>(vt);
 
   int64_t cl;
   int beg, end;
@@ -221,21 +218,26 @@ __global__ __launch_bounds__(256) void attn_block_kernel(AttnBlockArgs a, const 
   const int r0 = blk * C;
   const int nkeys = min(C, a.N - r0);
 
+  // K block row-major; V block transposed, two keys per 32-bit word.
   const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.N + r0) * D;
   const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.N + r0) * D;
   for (int e = threadIdx.x; e < C * (D / 8); e += 256) {
     const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
-    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
-    if (r < nkeys) {
-      kv = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
-      vv = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(r) * D + c8);
-    }
+    uint4 kv = make_uint4(0, 0, 0, 0);
+    if (r < nkeys) kv = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
     *reinterpret_cast<uint4*>(klds + r * LDK + c8) = kv;
-    const uint32_t w[4] = {vv.x, vv.y, vv.z, vv.w};
+  }
+  for (int e = threadIdx.x; e < (C / 2) * (D / 8); e += 256) {
+    const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
+    uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
+    if (2 * kp < nkeys) v0 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp) * D + c8);
+    if (2 * kp + 1 < nkeys) v1 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp + 1) * D + c8);
+    const uint32_t w0[4] = {v0.x, v0.y, v0.z, v0.w};
+    const uint32_t w1[4] = {v1.x, v1.y, v1.z, v1.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      vt[(c8 + 2 * i) * LDV + r] = static_cast<uint16_t>(w[i] & 0xFFFFu);
-      vt[(c8 + 2 * i + 1) * LDV + r] = static_cast<uint16_t>(w[i] >> 16);
+      vt32[(c8 + 2 * i) * (LDV / 2) + kp] = (w0[i] & 0xFFFFu) | (w1[i] << 16);
+      vt32[(c8 + 2 * i + 1) * (LDV / 2) + kp] = (w0[i] >> 16) | (w1[i] & 0xFFFF0000u);
     }
   }
   __syncthreads();
@@ -252,6 +254,8 @@ __global__ __launch_bounds__(256) void attn_block_kernel(AttnBlockArgs a, const 
     const int rr = pr >> 8, slot = pr & 255;   // row within the chunk, slot
     const int row = a.row0 + rr;
     const int t = a.N - a.Nq + row;
+    // keys [0, kmax) of the block are visible to this query (contiguous)
+    const int kmax = a.causal ? min(nkeys, t - r0 + 1) : nkeys;
     for (int hh = 0; hh < a.G; ++hh) {
       const uint16_t* qrow = q + ((static_cast<int64_t>(b) * a.H + h * a.G + hh) * a.Nq + row) * D + half * 8;
       bf16x8a qb[KS];
@@ -276,8 +280,7 @@ __global__ __launch_bounds__(256) void attn_block_kernel(AttnBlockArgs a, const 
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          const bool ok = key < nkeys && (!a.causal || r0 + key <= t);
-          sacc[kt][r] = ok ? sacc[kt][r] * a.qscale2 : -INFINITY;
+          sacc[kt][r] = key < kmax ? sacc[kt][r] * a.qscale2 : -INFINITY;
           m = fmaxf(m, sacc[kt][r]);
         }
       }
@@ -296,10 +299,10 @@ __global__ __launch_bounds__(256) void attn_block_kernel(AttnBlockArgs a, const 
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           uint4 u;
-          u.x = pack_bf16x2(pv[8 * j + 0], pv[8 * j + 1]);
-          u.y = pack_bf16x2(pv[8 * j + 2], pv[8 * j + 3]);
-          u.z = pack_bf16x2(pv[8 * j + 4], pv[8 * j + 5]);
-          u.w = pack_bf16x2(pv[8 * j + 6], pv[8 * j + 7]);
+          u.x = pack2_bf16(pv[8 * j + 0], pv[8 * j + 1]);
+          u.y = pack2_bf16(pv[8 * j + 2], pv[8 * j + 3]);
+          u.z = pack2_bf16(pv[8 * j + 4], pv[8 * j + 5]);
+          u.w = pack2_bf16(pv[8 * j + 6], pv[8 * j + 7]);
           pb[kt][j] = u4_as_bf16x8(u);
         }
       }
@@ -309,7 +312,7 @@ __global__ __launch_bounds__(256) void attn_block_kernel(AttnBlockArgs a, const 
       // and kt*32 + 16j + 8 + 4*half + {0..3} (i >= 4).
       const float inv = l > 0.f ? 1.0f / l : 0.f;
       const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + slot) * a.G + hh;
-#pragma unroll
+#pragma unroll 1
       for (int dt = 0; dt < DT; ++dt) {
         f32x16a oacc;
 #pragma unroll
@@ -331,8 +334,8 @@ __global__ __launch_bounds__(256) void attn_block_kernel(AttnBlockArgs a, const 
 #pragma unroll
           for (int g4 = 0; g4 < 4; ++g4) {
             uint2 w;
-            w.x = pack_bf16x2(oacc[4 * g4 + 0] * inv, oacc[4 * g4 + 1] * inv);
-            w.y = pack_bf16x2(oacc[4 * g4 + 2] * inv, oacc[4 * g4 + 3] * inv);
+            w.x = pack2_bf16(oacc[4 * g4 + 0] * inv, oacc[4 * g4 + 1] * inv);
+            w.y = pack2_bf16(oacc[4 * g4 + 2] * inv, oacc[4 * g4 + 3] * inv);
             *reinterpret_cast<uint2*>(dst + 8 * g4) = w;
           }
         }
@@ -465,7 +468,7 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
     {
       ProfScope ps("attn_block", st);
       dim3 grid(static_cast<unsigned>(cluster_max_tiles(s.BH(), geo.M[1], static_cast<int64_t>(s.BH()) * nrows * s.K)));
-      const size_t lds = (static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 8)) * 2;
+      const size_t lds = (static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 4)) * 2;
       const uint16_t* qq = static_cast<const uint16_t*>(q);
       const uint16_t* kk = static_cast<const uint16_t*>(k);
       const uint16_t* vv = static_cast<const uint16_t*>(v);

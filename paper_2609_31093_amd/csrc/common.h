@@ -17,7 +17,9 @@ constexpr float kLn2 = 0.6931471805599453f;
 // 1..Lstore start at pyramid row off[l].
 struct Geo {
   int32_t N, C, g, L, Lstore;
+  int32_t lg;  // log2(g) when g is a power of two, else -1
   int32_t M[kMaxLevels + 1];
+  int32_t gp[kMaxLevels + 1];  // g^(l-1), saturated at 2^30 (exact wherever it matters: <= g*M_1)
   int64_t gpow[kMaxLevels + 1];
   int64_t off[kMaxLevels + 2];
   int64_t R;  // rows per (batch, KV head)
@@ -38,6 +40,21 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
   }
   u += 0x7FFFu + ((u >> 16) & 1u);
   return static_cast<uint16_t>(u >> 16);
+}
+
+// x / g^(l-1) for 0 <= x < 2^31 (leaf-block index -> its level-l ancestor).
+__device__ __forceinline__ int anc_at(const Geo& geo, int x, int l) {
+  if (geo.lg >= 0) return x >> min(geo.lg * (l - 1), 31);
+  return static_cast<int>(static_cast<uint32_t>(x) / static_cast<uint32_t>(geo.gp[l]));
+}
+
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// Two floats to packed bf16 (round to nearest even, hardware conversion).
+__device__ __forceinline__ uint32_t pack2_bf16(float a, float b) {
+  const f32x2_t v = {a, b};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
 }
 
 // Load DPL consecutive elements (DPL in {4, 8}) of a bf16 or f32 row as floats.
@@ -85,6 +102,50 @@ __device__ __forceinline__ float sum16(float v) {
   v += __shfl_xor(v, 2, 16);
   v += __shfl_xor(v, 1, 16);
   return v;
+}
+
+// ---- cross-lane moves on the VALU (DPP) or the LDS swizzle unit -------------
+// dpp_ctrl encodings: quad_perm 0x00-0xFF, row_shr:n 0x110+n, row_ror:n
+// 0x120+n, row_bcast15 0x142.  Lanes without a source (or masked rows) read 0.
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ int dpp_i(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, ROW_MASK, 0xF, true);
+}
+template <int CTRL, int ROW_MASK = 0xF>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, dpp_i<CTRL, ROW_MASK>(__builtin_bit_cast(int, v)));
+}
+
+// Sum over each 16-lane row; the total lands in lane 15 of the row.
+__device__ __forceinline__ float rowsum16_to15(float v) {
+  v += dpp_f<0x111>(v);
+  v += dpp_f<0x112>(v);
+  v += dpp_f<0x114>(v);
+  v += dpp_f<0x118>(v);
+  return v;
+}
+
+// Inclusive prefix sum within each 32-lane half of the wavefront.
+__device__ __forceinline__ int scan32_incl(int v) {
+  v += dpp_i<0x111>(v);
+  v += dpp_i<0x112>(v);
+  v += dpp_i<0x114>(v);
+  v += dpp_i<0x118>(v);
+  v += dpp_i<0x142, 0xA>(v);  // row_bcast15 into rows 1 and 3
+  return v;
+}
+
+// Value of lane (j XOR lane) within a 32-lane half, for j in {1,2,4,8,16}.
+template <int J>
+__device__ __forceinline__ int xor32_i(int v) {
+  if constexpr (J == 1) return dpp_i<0xB1>(v);        // quad_perm [1,0,3,2]
+  else if constexpr (J == 2) return dpp_i<0x4E>(v);   // quad_perm [2,3,0,1]
+  else if constexpr (J == 8) return dpp_i<0x128>(v);  // row_ror:8
+  else return __builtin_amdgcn_ds_swizzle(v, (J << 10) | 0x1F);
+}
+template <int J>
+__device__ __forceinline__ float xor32_f(float v) {
+  return __builtin_bit_cast(float, xor32_i<J>(__builtin_bit_cast(int, v)));
 }
 
 // Orders LDS traffic among the lanes of one wavefront (no cross-wave effect).

@@ -83,9 +83,9 @@ __global__ __launch_bounds__(256) void pool_leaf_kernel(const T* __restrict__ k,
   float* dstb = buf1;
   for (int lv = 2; lv <= top; ++lv) {
     const int g = geo.g;
-    const int first = static_cast<int>(leaf0 / geo.gpow[lv]);          // node index of the run start
-    const int below_first = static_cast<int>(leaf0 / geo.gpow[lv - 1]);
-    const int nnode = min(static_cast<int>(lpb / geo.gpow[lv]), geo.M[lv] - first);
+    const int first = anc_at(geo, leaf0, lv);  // node index of the run start
+    const int below_first = anc_at(geo, leaf0, lv - 1);
+    const int nnode = min(lpb / geo.gp[lv], geo.M[lv] - first);
     for (int e = threadIdx.x; e < nnode * D; e += blockDim.x) {
       const int j = e / D, col = e - j * D;
       const int node = first + j;

@@ -106,8 +106,8 @@ struct Forced {
 __device__ __forceinline__ Forced forced_at(const Geo& geo, int lev, int c, int causal) {
   Forced f;
   f.causal = causal;
-  f.f2 = static_cast<int>(c / geo.gpow[lev]);
-  f.f1 = (c >= 1) ? static_cast<int>((c - 1) / geo.gpow[lev]) : -1;
+  f.f2 = anc_at(geo, c, lev);
+  f.f1 = (c >= 1) ? anc_at(geo, c - 1, lev) : -1;
   return f;
 }
 
@@ -333,8 +333,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
     if (lev > last_level || (!FUSED && lev == 2)) {
       // Expand kept nodes to their eligible children at level lev-1.
       const int Mb = geo.M[lev - 1];
-      const int64_t span_below = geo.gpow[lev - 1] * geo.C;
-      const int rmax = a.causal ? static_cast<int>(min<int64_t>(t / span_below, Mb - 1)) : Mb - 1;
+      const int rmax = a.causal ? min(anc_at(geo, c, lev - 1), Mb - 1) : Mb - 1;
       const int E = (nA + TEAM - 1) / TEAM;
       const int i0 = tid * E, i1 = min(nA, i0 + E);
       int mine = 0;
@@ -422,37 +421,50 @@ __device__ __forceinline__ bool better(float ka, int pa, float kb, int pb) {
   return ka > kb || (ka == kb && pa < pb);
 }
 
+template <int K2, int J>
+__device__ __forceinline__ void sort32_step(float& key, int& pack, int hl) {
+  const float ok = xor32_f<J>(key);
+  const int op = xor32_i<J>(pack);
+  const bool dir = (hl & K2) == 0;
+  const bool lower = (hl & J) == 0;
+  const bool take = (lower == dir) ? better(ok, op, key, pack) : better(key, pack, ok, op);
+  if (take) {
+    key = ok;
+    pack = op;
+  }
+}
+
 // Bitonic sort of the 32 lanes of each wavefront half into rank order.
 __device__ __forceinline__ void sort32(float& key, int& pack, int hl) {
-#pragma unroll
-  for (int k = 2; k <= 32; k <<= 1) {
-#pragma unroll
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      const float ok = __shfl_xor(key, j, 32);
-      const int op = __shfl_xor(pack, j, 32);
-      const bool dir = (hl & k) == 0;
-      const bool lower = (hl & j) == 0;
-      const bool take = (lower == dir) ? better(ok, op, key, pack) : better(key, pack, ok, op);
-      if (take) {
-        key = ok;
-        pack = op;
-      }
-    }
-  }
+  sort32_step<2, 1>(key, pack, hl);
+  sort32_step<4, 2>(key, pack, hl);
+  sort32_step<4, 1>(key, pack, hl);
+  sort32_step<8, 4>(key, pack, hl);
+  sort32_step<8, 2>(key, pack, hl);
+  sort32_step<8, 1>(key, pack, hl);
+  sort32_step<16, 8>(key, pack, hl);
+  sort32_step<16, 4>(key, pack, hl);
+  sort32_step<16, 2>(key, pack, hl);
+  sort32_step<16, 1>(key, pack, hl);
+  sort32_step<32, 16>(key, pack, hl);
+  sort32_step<32, 8>(key, pack, hl);
+  sort32_step<32, 4>(key, pack, hl);
+  sort32_step<32, 2>(key, pack, hl);
+  sort32_step<32, 1>(key, pack, hl);
 }
 
 // Inclusive prefix sum over the 32 lanes of a wavefront half.
-__device__ __forceinline__ int scan32(int v, int hl) {
-#pragma unroll
-  for (int o = 1; o < 32; o <<= 1) {
-    const int y = __shfl_up(v, o, 32);
-    if (hl >= o) v += y;
-  }
-  return v;
+__device__ __forceinline__ int scan32(int v, int) { return scan32_incl(v); }
+
+// Total of a 32-lane half from an inclusive scan.
+__device__ __forceinline__ int half_total(int incl, int lane) {
+  const int t0 = __builtin_amdgcn_readlane(incl, 31);
+  const int t1 = __builtin_amdgcn_readlane(incl, 63);
+  return lane < 32 ? t0 : t1;
 }
 
 template <int D, int GMAX>
-__global__ __launch_bounds__(256, (GMAX == 1 ? 8 : 2)) void stage1_pair_kernel(SelArgs a, int row_words) {
+__global__ __launch_bounds__(256) void stage1_pair_kernel(SelArgs a, int row_words) {
   constexpr int DPL = D / 16;
   constexpr int UNR = 4;
   extern __shared__ int lds_i[];
@@ -513,7 +525,7 @@ __global__ __launch_bounds__(256, (GMAX == 1 ? 8 : 2)) void stage1_pair_kernel(S
       const bool has_self = !__builtin_isnan(zs[0]);
       const int nl = (valid && !isf) ? (has_self ? nch - 1 : nch) : 0;
       const int incl = scan32(nl, hl);
-      const int T = __shfl(incl, (lane & 32) + 31);
+      const int T = half_total(incl, lane);
       int pos = incl - nl;
       for (int j = 0; j < nl; ++j) {
         lst_r[pos + j] = node * g + j;
@@ -543,8 +555,8 @@ __global__ __launch_bounds__(256, (GMAX == 1 ? 8 : 2)) void stage1_pair_kernel(S
               float d0 = 0.f;
 #pragma unroll
               for (int i = 0; i < DPL; ++i) d0 = fmaf(qv[hh][i], x[u][i], d0);
-              d0 = sum16(d0);
-              if (sub == 0 && e < T) zbuf[lst_s[e] * G + hh] = d0;
+              d0 = rowsum16_to15(d0);
+              if (sub == 15 && e < T) zbuf[lst_s[e] * G + hh] = d0;
             }
           }
         }
@@ -590,12 +602,11 @@ __global__ __launch_bounds__(256, (GMAX == 1 ? 8 : 2)) void stage1_pair_kernel(S
     const bool known = ranked && kept && !fz.is(knode);
     wave_sync();  // zbuf reads of step 3 are done before cand2/zs2 are written
     // 5) expand survivors to their eligible children
-    const int64_t span_below = geo.gpow[lev - 1] * geo.C;
-    const int rmax = a.causal ? static_cast<int>(min<int64_t>(t / span_below, Mb - 1)) : Mb - 1;
+    const int rmax = a.causal ? min(anc_at(geo, c, lev - 1), Mb - 1) : Mb - 1;
     const int c0 = knode * g;
     const int nk = kept ? max(0, min(c0 + g - 1, rmax) - c0 + 1) : 0;
     const int incl = scan32(nk, hl);
-    const int nA2 = __shfl(incl, (lane & 32) + 31);
+    const int nA2 = half_total(incl, lane);
     int pos = incl - nk;
     for (int j = 0; j < nk; ++j) {
       cand2[pos + j] = c0 + j;
