@@ -70,6 +70,29 @@ def algorithmic_work(w, pairs_scored, attn_pairs):
     return out
 
 
+def committed_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (profiles/traffic.json), or None when absent or when the kernel's source
+    file has changed since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        table = json.load(f)
+    ent = table.get("kernels", {}).get(kernel)
+    if not ent:
+        return None
+    src = os.path.join(ROOT, ent["source"])
+    if not os.path.exists(src):
+        return None
+    with open(src, "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != ent["source_sha256"]:
+            return None
+    return ent["bytes_per_launch"]
+
+
 def cpu_baseline(x, w, n_rows):
     """The oracle, as it stands, on a bounded sample: pyramid of KV head 0 plus
     selection + attention of n_rows evenly spaced rows of head 0; extrapolated
@@ -112,6 +135,8 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=4096)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bsa", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="after the run, copy a cold buffer of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one MI355X: this build has no multi-GPU path "
@@ -213,7 +238,7 @@ def main():
             roof = {"kernel": dom, "bound": "alu", "achieved": amount / avg_s / 1e12,
                     "peak": VALU_F32_PEAK_TFLOPS, "unit": "TFLOP/s"}
         roof["frac"] = roof["achieved"] / roof["peak"]
-        roof["traffic"] = None
+        roof["traffic"] = committed_traffic(dom)
 
     bsa_ms = None
     if not args.no_bsa:
@@ -263,6 +288,19 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)
+
+    if args.copy_probe_mib:
+        # A plain device copy of known size from a buffer evicted from the caches
+        # (a 2 GiB write in between), for scaling FETCH_SIZE / WRITE_SIZE.
+        n = args.copy_probe_mib << 20
+        src = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda")
+        evict = torch.empty(1 << 30, dtype=torch.float16, device="cuda")
+        evict.fill_(1.0)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] copy probe: {n} bytes read, {n} bytes written")
 
 
 if __name__ == "__main__":

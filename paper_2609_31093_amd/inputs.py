@@ -108,11 +108,13 @@ def workload(name: str, **overrides) -> dict:
     return w
 
 
-def make_inputs(w: dict, seed: int = 0, step: int = 0) -> dict:
+def make_inputs(w: dict, seed: int = 0, step: int = 0, parts: str = "qkv") -> dict:
     """Draw q [B,H,Nq,d], k [B,Hkv,N,d], v [B,Hkv,N,d] for workload dict ``w``.
 
     ``step`` selects the query of a decode step (decode workloads draw a fresh
-    query per step; k and v do not depend on it).
+    query per step; k and v do not depend on it).  ``parts`` limits which
+    tensors are returned for the i.i.d. workloads (e.g. "q" for later decode
+    steps); the others always return all three.
     """
     B, H, Hkv, N, Nq, d, C = w["B"], w["H"], w["Hkv"], w["N"], w["Nq"], w["d"], w["C"]
     cid = w["cfg_id"]
@@ -123,6 +125,8 @@ def make_inputs(w: dict, seed: int = 0, step: int = 0) -> dict:
         q = _per_head(seed, cid, q_tid, qshape, _normal_fill)
         if dist == "iid_qscaled":
             q *= np.float32(1.0 / np.sqrt(d))
+        if parts == "q":
+            return {"q": round_to_bf16(q) if w["dtype"] == "bf16" else q}
         k = _per_head(seed, cid, _K, kshape, _normal_fill)
         v = _per_head(seed, cid, _V, kshape, _normal_fill)
     elif dist == "needles":
