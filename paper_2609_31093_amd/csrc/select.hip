@@ -506,15 +506,35 @@ __global__ __launch_bounds__(256) void stage1_pair_kernel(SelArgs a, int row_wor
     }
   }
 
-  int node = hl == 0 ? 0 : -1;  // candidate of this lane (-1: none)
-  float zs[GMAX];               // its logit per head, NaN if unknown
+  // Levels whose eligible nodes number at most K keep everything, so the
+  // candidate set of the first level that can hold more than K is simply
+  // all its eligible nodes: each row starts there (the root level when none
+  // can, i.e. the whole set reaches the leaf level unpruned).
+  auto n_eligible = [&](int lev) { return a.causal ? min(anc_at(geo, c, lev) + 1, geo.M[lev]) : geo.M[lev]; };
+  int start = 1;
+  for (int lev = geo.L; lev >= 2; --lev) {
+    if (n_eligible(lev) > K) {
+      start = lev;
+      break;
+    }
+  }
+  // start == 1: fewer than K+1 eligible leaves; start >= 2: first ranked level.
+  const int wave_start = max(start, __shfl_xor(start, 32));
+
+  int node = -1;  // candidate of this lane (-1: none)
+  float zs[GMAX];  // its logit per head, NaN if unknown
 #pragma unroll
   for (int hh = 0; hh < GMAX; ++hh) zs[hh] = __builtin_nanf("");
-  int nA = 1;
+  int nA = 0;
 
-  for (int lev = geo.L; lev >= 2; --lev) {
+  for (int lev = wave_start; lev >= 2; --lev) {
+    if (lev == start) {
+      nA = n_eligible(lev);
+      node = hl < nA ? hl : -1;
+    }
+    const bool active = lev <= start;
     const Forced fz = forced_at(geo, lev, c, a.causal);
-    const bool ranked = nA > K;
+    const bool ranked = active && nA > K;
     const int Mb = geo.M[lev - 1];
     const bool valid = node >= 0;
     const bool isf = valid && fz.is(node);
@@ -532,19 +552,16 @@ __global__ __launch_bounds__(256) void stage1_pair_kernel(SelArgs a, int row_wor
         lst_s[pos + j] = hl * g + j;
       }
       wave_sync();
-      // 2) child logits, UNR loads in flight per 16-lane group
+      // 2) child logits, UNR loads in flight per 16-lane group (loads past the
+      //    list end fetch row 0 and are discarded)
       const float* pbase = a.pyr + (static_cast<int64_t>(bh) * geo.R + geo.off[lev - 1]) * D + sub * DPL;
       for (int e0 = gr; e0 < T; e0 += 2 * UNR) {
         float x[UNR][DPL];
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
           const int e = e0 + 2 * u;
-          if (e < T) {
-            load_row_part<float, DPL>(pbase + static_cast<int64_t>(lst_r[e]) * D, x[u]);
-          } else {
-#pragma unroll
-            for (int i = 0; i < DPL; ++i) x[u][i] = 0.f;
-          }
+          const int r = e < T ? lst_r[e] : 0;
+          load_row_part<float, DPL>(pbase + static_cast<int64_t>(r) * D, x[u]);
         }
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
@@ -585,19 +602,17 @@ __global__ __launch_bounds__(256) void stage1_pair_kernel(SelArgs a, int row_wor
       }
     }
     // 4) rank: the first K in (key desc, node asc) order survive
-    int pack = valid ? (node << 6) | hl : 0x7FFFFFC0 | hl;
-    float skey = key;
-    sort32(skey, pack, hl);
-    int knode, korig;
-    bool kept;
-    if (ranked) {
-      kept = hl < K && skey != -INFINITY;
-      knode = pack >> 6;
-      korig = pack & 63;
-    } else {
-      kept = valid;
-      knode = node;
-      korig = hl;
+    int knode = node, korig = hl;
+    bool kept = active && valid;
+    if (__ballot(ranked) != 0) {
+      int pack = valid ? (node << 6) | hl : 0x7FFFFFC0 | hl;
+      float skey = key;
+      sort32(skey, pack, hl);
+      if (ranked) {
+        kept = hl < K && skey != -INFINITY;
+        knode = pack >> 6;
+        korig = pack & 63;
+      }
     }
     const bool known = ranked && kept && !fz.is(knode);
     wave_sync();  // zbuf reads of step 3 are done before cand2/zs2 are written
@@ -614,11 +629,17 @@ __global__ __launch_bounds__(256) void stage1_pair_kernel(SelArgs a, int row_wor
         zs2[(pos + j) * G + hh] = known ? zbuf[(korig * g + j) * G + hh] : __builtin_nanf("");
     }
     wave_sync();
-    node = hl < nA2 ? cand2[hl] : -1;
+    if (active) {
+      node = hl < nA2 ? cand2[hl] : -1;
 #pragma unroll
-    for (int hh = 0; hh < GMAX; ++hh) zs[hh] = (hh < G && hl < nA2) ? zs2[hl * G + hh] : __builtin_nanf("");
-    nA = nA2;
+      for (int hh = 0; hh < GMAX; ++hh) zs[hh] = (hh < G && hl < nA2) ? zs2[hl * G + hh] : __builtin_nanf("");
+      nA = nA2;
+    }
     wave_sync();
+  }
+  if (start == 1) {  // every eligible leaf survives unranked
+    nA = n_eligible(1);
+    node = hl < nA ? hl : -1;
   }
 
   // Leaf candidate set ascending.
