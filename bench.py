@@ -132,9 +132,13 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="needles-128k")
-    ap.add_argument("--cpu-rows", type=int, default=4096)
+    ap.add_argument("--cpu-rows", type=int, default=12288)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bsa", action="store_true")
+    ap.add_argument("--sweep", default="",
+                    help="comma-separated N values: time PISA selection and flat-BSA selection "
+                         "(each including pooling) at every N with the workload's other shapes, "
+                         "random inputs drawn on the GPU; printed as one extra JSON line")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the run, copy a cold buffer of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -288,6 +292,51 @@ def main():
         "cpu_baseline": cpu,
     }
     print(json.dumps(res), flush=True)
+
+    if args.sweep:
+        sweep = []
+        for n_s in (int(x) for x in args.sweep.split(",")):
+            gen = torch.Generator(device="cuda").manual_seed(n_s)
+            qs = torch.randn((B, H, n_s, d), device="cuda", generator=gen).to(tdt)
+            ks = torch.randn((B, Hkv, n_s, d), device="cuda", generator=gen).to(tdt)
+            ps = pisa.make_problem(B, H, Hkv, n_s, n_s, d, C, g, K, w["causal"], w["dtype"])
+            _, Rs = pisa.pisa_pyramid_layout(ps)
+            pyr_s = torch.empty((B, Hkv, Rs, d), dtype=torch.float32, device="cuda")
+            idx_s = torch.empty((B, Hkv, n_s, K), dtype=torch.int32, device="cuda")
+            nsel = pisa.pisa_select_workspace_bytes(ps)
+            nbsa = pisa.pisa_bsa_workspace_bytes(ps)
+            ws_s = torch.empty(max(nsel, nbsa, 1), dtype=torch.uint8, device="cuda")
+
+            def timed(fn, reps=3):
+                fn()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                for _ in range(reps):
+                    fn()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                return e0.elapsed_time(e1) / reps
+
+            def pisa_sel():
+                pisa.pisa_build_pyramid(ps, ks, pyr_s, stream)
+                pisa.pisa_select(ps, qs, ks, pyr_s, idx_s, None, ws_s, nsel, stream)
+
+            def bsa_sel():
+                pisa.pisa_build_pyramid(ps, ks, pyr_s, stream)
+                pisa.pisa_select_flat_bsa(ps, qs, pyr_s, idx_s, ws_s, nbsa, stream)
+
+            row = {"N": n_s, "pisa_ms": timed(pisa_sel)}
+            try:
+                row["bsa_ms"] = timed(bsa_sel)
+            except pisa.PisaError as err:  # flat BSA keeps N/C scores per row in LDS
+                row["bsa_ms"] = None
+                row["bsa_error"] = str(err)
+            log(f"[bench] sweep N={n_s}: {row}")
+            sweep.append(row)
+            del qs, ks, pyr_s, idx_s, ws_s
+        print(json.dumps({"sweep": sweep, "workload": args.workload, "what": "selection incl. pooling, ms"}),
+              flush=True)
 
     if args.copy_probe_mib:
         # A plain device copy of known size from a buffer evicted from the caches

@@ -241,8 +241,9 @@ int pisa_select_flat_bsa(const pisa_problem* p, const void* q, const float* pyra
   PISA_TRY(check_ptr(q, "q"));
   PISA_TRY(check_ptr(pyramid, "pyramid"));
   PISA_TRY(check_ptr(block_idx, "block_idx"));
-  if ((static_cast<int64_t>(g.M[1]) + s.K) * 4 > 65536)
-    return fail(PISA_ERR_UNSUPPORTED, "flat BSA keeps one score per leaf block in LDS: N/C must be < 16384");
+  const bool mfma_bsa = s.bf16 && s.K <= 32;
+  if (!mfma_bsa && (static_cast<int64_t>(g.M[1]) + s.K) * 4 > 65536)
+    return fail(PISA_ERR_UNSUPPORTED, "flat BSA on fp32 or K > 32 keeps one score per leaf block in LDS: N/C < 16384");
   PISA_TRY(check_ws(ws, ws_bytes, pisa::bsa_ws(s, g)));
   return device_status(pisa::launch_flat_bsa(s, g, q, pyramid, block_idx, ws, static_cast<hipStream_t>(stream)),
                        "pisa_select_flat_bsa");

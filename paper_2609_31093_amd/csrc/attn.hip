@@ -345,6 +345,168 @@ __global__ __launch_bounds__(256) void attn_block_kernel(AttnBlockArgs a, const 
   }
 }
 
+// Same work as attn_block_kernel with 16-query tiles on
+// v_mfma_f32_16x16x32_bf16 (A lane l: row l%16, k 8*(l/16)..+7; B lane l:
+// k 8*(l/16)..+7, column l%16; D lane l: rows 4*(l/16)..+3, column l%16):
+// half the accumulator and operand registers of the 32x32 tiles, so twice
+// the wavefronts per SIMD to hide the query gathers.
+typedef float f32x4a __attribute__((ext_vector_type(4)));
+
+template <int D, int CT>
+__global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
+                                                           const uint16_t* __restrict__ k,
+                                                           const uint16_t* __restrict__ v,
+                                                           const int32_t* __restrict__ offs,
+                                                           const int32_t* __restrict__ toffs, int64_t ncl,
+                                                           const int32_t* __restrict__ pairs,
+                                                           uint16_t* __restrict__ part_o,
+                                                           float* __restrict__ part_lse) {
+  constexpr int KS = D / 32;       // k-steps of QK^T (32 dims each)
+  constexpr int LDK = D + 8;       // padded K row (bf16 elements)
+  constexpr int C = CT * 32;       // keys per block
+  constexpr int MT = C / 16;       // 16-key tiles of S
+  constexpr int LDV = C + 4;       // padded V^T row
+  constexpr int DT = D / 16;       // 16-row d tiles of O
+  extern __shared__ uint16_t lds[];
+  uint16_t* klds = lds;
+  uint16_t* vt = lds + C * LDK;
+  uint32_t* vt32 = reinterpret_cast<uint32_t*>(vt);
+
+  int64_t cl;
+  int beg, end;
+  if (!cluster_tile(offs, toffs, ncl, blockIdx.x, cl, beg, end)) return;
+  const int bh = static_cast<int>(cl / a.M1);
+  const int blk = static_cast<int>(cl - static_cast<int64_t>(bh) * a.M1);
+  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+  const int r0 = blk * C;
+  const int nkeys = min(C, a.N - r0);
+
+  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.N + r0) * D;
+  const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.N + r0) * D;
+  for (int e = threadIdx.x; e < C * (D / 8); e += 256) {
+    const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
+    uint4 kv = make_uint4(0, 0, 0, 0);
+    if (r < nkeys) kv = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
+    *reinterpret_cast<uint4*>(klds + r * LDK + c8) = kv;
+  }
+  for (int e = threadIdx.x; e < (C / 2) * (D / 8); e += 256) {
+    const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
+    uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
+    if (2 * kp < nkeys) v0 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp) * D + c8);
+    if (2 * kp + 1 < nkeys) v1 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp + 1) * D + c8);
+    const uint32_t w0[4] = {v0.x, v0.y, v0.z, v0.w};
+    const uint32_t w1[4] = {v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      vt32[(c8 + 2 * i) * (LDV / 2) + kp] = (w0[i] & 0xFFFFu) | (w1[i] << 16);
+      vt32[(c8 + 2 * i + 1) * (LDV / 2) + kp] = (w0[i] >> 16) | (w1[i] & 0xFFFF0000u);
+    }
+  }
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int col = lane & 15;   // query column
+  const int grp = lane >> 4;   // 0..3: k slice of the operands, row group of the results
+  const int ntile = (end - beg + 15) / 16;
+  for (int tile = wave; tile < ntile; tile += 4) {
+    const int p = beg + tile * 16 + col;
+    const bool valid = p < end;
+    const int pr = valid ? pairs[p] : 0;
+    const int rr = pr >> 8, slot = pr & 255;
+    const int row = a.row0 + rr;
+    const int t = a.N - a.Nq + row;
+    const int kmax = a.causal ? min(nkeys, t - r0 + 1) : nkeys;
+    for (int hh = 0; hh < a.G; ++hh) {
+      const uint16_t* qrow = q + ((static_cast<int64_t>(b) * a.H + h * a.G + hh) * a.Nq + row) * D + grp * 8;
+      bf16x8a qb[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        uint4 u = make_uint4(0, 0, 0, 0);
+        if (valid) u = *reinterpret_cast<const uint4*>(qrow + ks * 32);
+        qb[ks] = u4_as_bf16x8(u);
+      }
+      // S^T tile mt holds keys mt*16 + 4*grp + i (i = 0..3) of query `col`.
+      auto s_tile = [&](int mt) {
+        f32x4a acc = {0.f, 0.f, 0.f, 0.f};
+        const uint16_t* arow = klds + (mt * 16 + col) * LDK + grp * 8;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8a av = u4_as_bf16x8(*reinterpret_cast<const uint4*>(arow + ks * 32));
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qb[ks], acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = mt * 16 + 4 * grp + i;
+          acc[i] = key < kmax ? acc[i] * a.qscale2 : -INFINITY;
+        }
+        return acc;
+      };
+      // pass A: the block-local maximum of the query's logits
+      float m = -INFINITY;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const f32x4a sa = s_tile(mt);
+        m = fmaxf(m, fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])));
+      }
+      m = fmaxf(m, __shfl_xor(m, 16));
+      m = fmaxf(m, __shfl_xor(m, 32));
+      const float msafe = (m == -INFINITY) ? 0.f : m;
+      // keep pass A's tiles from being reused (recomputing S is cheaper than
+      // holding it in registers)
+      asm volatile("" ::: "memory");
+      // pass B: P = 2^(S - m) per 32-key step and O^T += V^T P.  The P operand
+      // k = 8*grp + i holds key 32s + 4*grp + i (i < 4) or 32s + 16 + 4*grp +
+      // (i - 4) (i >= 4); the V^T operand reads the same keys.
+      f32x4a oacc[DT];
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x4a{0.f, 0.f, 0.f, 0.f};
+      float l = 0.f;
+#pragma unroll
+      for (int s2 = 0; s2 < MT / 2; ++s2) {
+        const f32x4a sa = s_tile(2 * s2), sb = s_tile(2 * s2 + 1);
+        float pv[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          pv[i] = fast_exp2(sa[i] - msafe);
+          pv[4 + i] = fast_exp2(sb[i] - msafe);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) l += pv[i];
+        uint4 u;
+        u.x = pack2_bf16(pv[0], pv[1]);
+        u.y = pack2_bf16(pv[2], pv[3]);
+        u.z = pack2_bf16(pv[4], pv[5]);
+        u.w = pack2_bf16(pv[6], pv[7]);
+        const bf16x8a pb = u4_as_bf16x8(u);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const uint16_t* vrow = vt + (dt * 16 + col) * LDV + 4 * grp + 32 * s2;
+          const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
+          const bf16x8a av = u4_as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+          oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb, oacc[dt], 0, 0, 0);
+        }
+      }
+      l += __shfl_xor(l, 16);
+      l += __shfl_xor(l, 32);
+      const float inv = l > 0.f ? 1.0f / l : 0.f;
+      const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + slot) * a.G + hh;
+      if (valid) {
+        // oacc[dt][i] = O[d = dt*16 + 4*grp + i][query col]
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          uint2 w;
+          w.x = pack2_bf16(oacc[dt][0] * inv, oacc[dt][1] * inv);
+          w.y = pack2_bf16(oacc[dt][2] * inv, oacc[dt][3] * inv);
+          *reinterpret_cast<uint2*>(part_o + pidx * D + dt * 16 + 4 * grp) = w;
+        }
+        if (grp == 0) part_lse[pidx] = l > 0.f ? m + fast_log2(l) : -INFINITY;
+      }
+    }
+  }
+}
+
 // One wavefront per (row of the chunk, query head): merge the row's K
 // partials.  16 lanes cover one partial (8 bf16 each for d = 128).
 template <int D>
@@ -478,13 +640,13 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
         kern<<<grid, 256, lds, st>>>(a, qq, kk, vv, co.offs, co.toffs, co.ncl, co.pairs, part_o, part_lse);
       };
       if (s.C == 32)
-        go(attn_block_kernel<D, 1>);
+        go(attn_block16_kernel<D, 1>);
       else if (s.C == 64)
-        go(attn_block_kernel<D, 2>);
+        go(attn_block16_kernel<D, 2>);
       else if (s.C == 96)
-        go(attn_block_kernel<D, 3>);
+        go(attn_block16_kernel<D, 3>);
       else
-        go(attn_block_kernel<D, 4>);
+        go(attn_block16_kernel<D, 4>);
     }
     {
       ProfScope ps("attn_combine", st);

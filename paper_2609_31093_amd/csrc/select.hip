@@ -668,13 +668,18 @@ __global__ __launch_bounds__(256) void final_topk_pair_kernel(TopkArgsP a, const
   const int64_t rgc = live ? rg : a.rows - 1;
   const int row = static_cast<int>(rgc % a.Nq);
   const int c = (a.N - a.Nq + row) / a.C;
+  // the three loads of a row are independent (slots past the count hold
+  // stale workspace values that are masked below)
+  const int slot = min(hl, a.gK - 1);
   const int n = a1cnt[rgc];
+  const int node_raw = a1[rgc * a.gK + slot];
+  const float u_raw = u1[rgc * a.gK + slot];
   const bool ranked = n > a.K;
   const bool valid = hl < n;
-  const int node = valid ? a1[rgc * a.gK + hl] : -1;
+  const int node = valid ? node_raw : -1;
   const bool isf = a.causal && valid && (node == 0 || node == c || node == c - 1);
   float key = -INFINITY;
-  if (valid) key = (ranked && !isf) ? u1[rgc * a.gK + hl] : INFINITY;
+  if (valid) key = (ranked && !isf) ? u_raw : INFINITY;
   int pack = valid ? node : 0x7FFFFFC0 | hl;
   sort32(key, pack, hl);
   const bool kept = hl < min(n, a.K) && key != -INFINITY;

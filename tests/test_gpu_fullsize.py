@@ -62,7 +62,7 @@ def _run(w, x):
     pyr = pisa.build_pyramid(p, k)
     idx = pisa.select(p, q, k, pyr)
     o, lse = pisa.sparse_attn_fwd(p, q, k, v, idx)
-    bsa = pisa.select_flat_bsa(p, q, pyr) if -(-N // C) < 16384 else None
+    bsa = pisa.select_flat_bsa(p, q, pyr)
     torch.cuda.synchronize()
     return pyr, idx, o, lse, bsa
 
