@@ -653,14 +653,16 @@ __global__ __launch_bounds__(256) void stage1_pair_kernel(SelArgs a, int row_wor
   }
 }
 
-// Final Top-K for g*K <= 32: two rows per wavefront, one candidate per lane.
-// A first sort32 puts the candidates in rank order (forced and unranked rows
-// keyed +inf); the survivors are the first min(n, K) lanes; a second sort32
-// orders them by block index and carries the lane that holds each score.
+// Final Top-K for g*K <= 32: two rows per wavefront, one candidate per lane
+// (the candidates arrive in ascending block order).  sort32 ranks them
+// (forced and unranked rows keyed +inf); the rank of each lane's own
+// candidate comes back through LDS and the kept ones are compacted in their
+// original, ascending order with a prefix sum.
 __global__ __launch_bounds__(256) void final_topk_pair_kernel(TopkArgsP a, const int32_t* __restrict__ a1,
                                                               const int32_t* __restrict__ a1cnt,
                                                               const float* __restrict__ u1,
                                                               int32_t* __restrict__ idx, float* __restrict__ score) {
+  __shared__ int s_rank[4][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, hl = lane & 31;
   const int64_t rg = (blockIdx.x * 4LL + wave) * 2 + half;
@@ -680,17 +682,24 @@ __global__ __launch_bounds__(256) void final_topk_pair_kernel(TopkArgsP a, const
   const bool isf = a.causal && valid && (node == 0 || node == c || node == c - 1);
   float key = -INFINITY;
   if (valid) key = (ranked && !isf) ? u_raw : INFINITY;
-  int pack = valid ? node : 0x7FFFFFC0 | hl;
+  const float own = key;
+  int pack = valid ? (node << 6) | hl : 0x7FFFFFC0 | hl;
   sort32(key, pack, hl);
-  const bool kept = hl < min(n, a.K) && key != -INFINITY;
-  float k2 = kept ? -static_cast<float>(pack) : -INFINITY;
-  int p2 = kept ? (pack << 6) | hl : 0x7FFFFFC0 | hl;
-  sort32(k2, p2, hl);
-  const float sc = __shfl(key, (lane & 32) + (p2 & 63));
-  if (live && hl < a.K) {
-    const bool out = k2 != -INFINITY;
-    idx[rg * a.K + hl] = out ? (p2 >> 6) : -1;
-    if (score) score[rg * a.K + hl] = !out ? -INFINITY : (sc == INFINITY ? INFINITY : sc * kLn2);
+  // lane p of the sorted half holds rank p; send it back to the source lane
+  s_rank[wave][(lane & 32) + (pack & 63)] = hl;
+  wave_sync();
+  const bool kept = valid && s_rank[wave][lane] < a.K;
+  const int incl = scan32(kept ? 1 : 0, hl);
+  if (live) {
+    const int total = half_total(incl, lane);
+    if (kept) {
+      idx[rg * a.K + incl - 1] = node;
+      if (score) score[rg * a.K + incl - 1] = (own == INFINITY) ? INFINITY : own * kLn2;
+    }
+    if (hl >= total && hl < a.K) {
+      idx[rg * a.K + hl] = -1;
+      if (score) score[rg * a.K + hl] = -INFINITY;
+    }
   }
 }
 
