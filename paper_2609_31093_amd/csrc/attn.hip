@@ -622,7 +622,7 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
   hipError_t e;
   for (int row0 = 0; row0 < s.Nq; row0 += ch) {
     const int nrows = std::min(ch, s.Nq - row0);
-    ClusterArgs ca{idx, nullptr, s.K, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], kClusterAttn, row0, nrows};
+    ClusterArgs ca{idx, nullptr, s.K, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], kClusterAttn, row0, nrows, s.g};
     ClusterOut co{};
     if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st)) != hipSuccess) return e;
     AttnBlockArgs a{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], row0, nrows,

@@ -26,11 +26,23 @@ __device__ __forceinline__ bool cluster_pair(const ClusterArgs& a, int bh, int r
   const int32_t* lst = a.list + rg * a.S;
   blk = lst[slot];
   if (blk < 0) return false;
-  if (a.mode == kClusterLeaf) {
+  if (a.mode == kClusterLeaf || a.mode == kClusterLeafParent) {
     const int n = a.cnt[rg];
     if (slot >= n || n <= a.K) return false;
     const int c = (a.N - a.Nq + a.row0 + r) / a.C;
-    if (a.causal && (blk == 0 || blk == c || blk == c - 1)) return false;
+    auto forced = [&](int x) { return a.causal && (x == 0 || x == c || x == c - 1); };
+    if (forced(blk)) return false;
+    if (a.mode == kClusterLeafParent) {
+      // the candidate list is ascending, so siblings are adjacent: emit only
+      // at the first non-forced child of the parent
+      const int par = blk / a.g;
+      for (int i = 1; i < a.g && slot - i >= 0; ++i) {
+        const int o = lst[slot - i];
+        if (o / a.g != par) break;
+        if (!forced(o)) return false;
+      }
+      blk = par;
+    }
   }
   return true;
 }
@@ -156,6 +168,10 @@ int64_t cluster_max_tiles(int BH, int M1, int64_t max_pairs) {
 static size_t al(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* out, hipStream_t st) {
+  // the rows read are [row0, row0 + nrows) of [0, Nq): refuse anything else
+  if (a.row0 < 0 || a.nrows < 1 || a.row0 + a.nrows > a.Nq || a.M1 < 1 ||
+      (a.mode == kClusterLeafParent && a.g < 2))
+    return hipErrorInvalidValue;
   const int64_t ncl = static_cast<int64_t>(BH) * a.M1;
   char* base = static_cast<char*>(ws);
   int32_t* hist = reinterpret_cast<int32_t*>(base);

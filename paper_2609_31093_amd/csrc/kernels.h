@@ -35,11 +35,14 @@ struct Shape {
 // Pair clustering by key block (cluster.hip).
 constexpr int kClusterLeaf = 0;  // leaf scoring: rows with more than K candidates, forced blocks skipped
 constexpr int kClusterAttn = 1;  // attention: every non-negative slot
+constexpr int kClusterLeafParent = 2;  // leaf scoring grouped by parent node: one entry per
+                                       // (row, parent) at the slot of its first non-forced child
 struct ClusterArgs {
   const int32_t* list;  // [BH, Nq, S] block per slot, -1 = none
   const int32_t* cnt;   // [BH, Nq] candidates per row (leaf mode only)
-  int S, Nq, N, C, K, causal, M1, mode;
+  int S, Nq, N, C, K, causal, M1, mode;  // M1: number of bins (leaf blocks, or parents)
   int row0, nrows;      // rows [row0, row0 + nrows) of every (batch, KV head)
+  int g;                // fan-out (parent mode)
 };
 constexpr int kClusterTile = 256;  // pairs per workgroup tile of a cluster consumer
 struct ClusterOut {

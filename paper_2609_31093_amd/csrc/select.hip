@@ -804,6 +804,128 @@ __global__ __launch_bounds__(256) void leaf_score_kernel(LeafArgs a, const uint1
   }
 }
 
+struct LeafParentArgs {
+  int H, Hkv, G, Nq, N, C, g, M1, M2, gK, K, causal;
+  float qscale2;
+};
+
+// Leaf scoring grouped by parent node (g*C <= 128 keys): one workgroup per
+// tile of up to kClusterTile (row, first-child slot) entries of one parent;
+// the parent's children key blocks are staged in LDS together and each query
+// row is gathered once for all of them; every 32-key MFMA tile belongs to
+// one child, whose LSE is accumulated separately.
+template <int D>
+__global__ __launch_bounds__(256) void leaf_parent_kernel(LeafParentArgs a, const uint16_t* __restrict__ q,
+                                                          const uint16_t* __restrict__ k,
+                                                          const int32_t* __restrict__ a1,
+                                                          const int32_t* __restrict__ a1cnt,
+                                                          const int32_t* __restrict__ offs,
+                                                          const int32_t* __restrict__ toffs, int64_t ncl,
+                                                          const int32_t* __restrict__ pairs,
+                                                          float* __restrict__ u1) {
+  constexpr int LDR = D + 8;
+  constexpr int KS = D / 16;
+  extern __shared__ uint16_t klds[];
+  int64_t cl;
+  int beg, end;
+  if (!cluster_tile(offs, toffs, ncl, blockIdx.x, cl, beg, end)) return;
+  const int bh = static_cast<int>(cl / a.M2);
+  const int par = static_cast<int>(cl - static_cast<int64_t>(bh) * a.M2);
+  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+  const int r0 = par * a.g * a.C;                  // first key of the parent
+  const int nkeys = min(a.g * a.C, a.N - r0);      // keys of its existing children
+  const int nkt = (nkeys + 31) / 32;
+
+  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.N + r0) * D;
+  for (int e = threadIdx.x; e < nkt * 32 * (D / 8); e += 256) {
+    const int r = e / (D / 8), cidx = (e - r * (D / 8)) * 8;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (r < nkeys) v = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + cidx);
+    *reinterpret_cast<uint4*>(klds + r * LDR + cidx) = v;
+  }
+  __syncthreads();
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int col = lane & 31;
+  const int half = lane >> 5;
+  const int ntile = (end - beg + 31) / 32;
+  const int kt_per_child = a.C / 32;
+  for (int tile = wave; tile < ntile; tile += 4) {
+    const int p = beg + tile * 32 + col;
+    const bool valid = p < end;
+    const int pr = valid ? pairs[p] : 0;
+    const int row = pr >> 8, slot0 = pr & 255;
+    float uc[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int hh = 0; hh < a.G; ++hh) {
+      const uint16_t* qrow = q + ((static_cast<int64_t>(b) * a.H + h * a.G + hh) * a.Nq + row) * D + half * 8;
+      bf16x8v qb[KS];
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (valid) v = *reinterpret_cast<const uint4*>(qrow + ks * 16);
+        qb[ks] = as_bf16x8(v);
+      }
+      float mc[4], sc[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        mc[j] = -INFINITY;
+        sc[j] = 0.f;
+      }
+#pragma unroll
+      for (int kt = 0; kt < 4; ++kt) {
+        if (kt >= nkt) break;
+        f32x16v acc;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+        const uint16_t* arow = klds + (kt * 32 + col) * LDR + half * 8;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8v av = as_bf16x8(*reinterpret_cast<const uint4*>(arow + ks * 16));
+          acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qb[ks], acc, 0, 0, 0);
+        }
+        float tm = -INFINITY;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+          acc[r] = key < nkeys ? acc[r] * a.qscale2 : -INFINITY;
+          tm = fmaxf(tm, acc[r]);
+        }
+        float ts = 0.f;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) ts += fast_exp2(acc[r] - tm);
+        const int j = kt / kt_per_child;
+#pragma unroll
+        for (int jj = 0; jj < 4; ++jj)
+          if (jj == j) lse_merge(mc[jj], sc[jj], tm, ts);
+      }
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const float m2 = __shfl_xor(mc[j], 32), s2 = __shfl_xor(sc[j], 32);
+        lse_merge(mc[j], sc[j], m2, s2);
+        uc[j] += mc[j] + fast_log2(sc[j]);
+      }
+    }
+    if (valid && half == 0) {
+      // the row's children of this parent sit at consecutive slots from slot0
+      const int64_t rgi = static_cast<int64_t>(bh) * a.Nq + row;
+      const int n = a1cnt[rgi];
+      const int c = (a.N - a.Nq + row) / a.C;
+      for (int i = 0; i < a.g && slot0 + i < n; ++i) {
+        const int node = a1[rgi * a.gK + slot0 + i];
+        if (node / a.g != par) break;
+        if (a.causal && (node == 0 || node == c || node == c - 1)) continue;
+        const int j = node - par * a.g;
+        float uj = uc[0];
+#pragma unroll
+        for (int jj = 1; jj < 4; ++jj)
+          if (jj == j) uj = uc[jj];
+        u1[rgi * a.gK + slot0 + i] = uj;
+      }
+    }
+  }
+}
+
 struct TopkArgs {
   int Nq, N, C, K, gK, causal;
   int64_t rows;
@@ -1005,11 +1127,34 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
 
-  // Cluster the (row, slot) pairs by leaf block.
+  // Cluster the (row, slot) pairs by leaf block, or by parent node when a
+  // parent's children fit one tile (each query row is then gathered once per
+  // parent instead of once per child).
   const int64_t rows = static_cast<int64_t>(s.BH()) * s.Nq;
-  ClusterArgs ca{a1, a1cnt, s.gK(), s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], kClusterLeaf, 0, s.Nq};
+  const bool by_parent = geo.L >= 2 && s.g * s.C <= 128;
+  const int M2 = geo.L >= 2 ? geo.M[2] : 1;
+  ClusterArgs ca{a1, a1cnt, s.gK(), s.Nq, s.N, s.C, s.K, s.causal, by_parent ? M2 : geo.M[1],
+                 by_parent ? kClusterLeafParent : kClusterLeaf, 0, s.Nq, s.g};
   ClusterOut co{};
   if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st)) != hipSuccess) return e;
+  if (by_parent) {
+    LeafParentArgs lp{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.g, geo.M[1], M2, s.gK(), s.K, s.causal,
+                      kLog2e / sqrtf(static_cast<float>(s.D))};
+    dim3 pgrid(static_cast<unsigned>(cluster_max_tiles(s.BH(), M2, rows * s.gK())));
+    const size_t plds = static_cast<size_t>(128) * (s.D + 8) * 2;
+    {
+      ProfScope ps("leaf_score", st);
+      if (s.D == 128)
+        leaf_parent_kernel<128><<<pgrid, 256, plds, st>>>(lp, static_cast<const uint16_t*>(q),
+                                                          static_cast<const uint16_t*>(k), a1, a1cnt, co.offs,
+                                                          co.toffs, co.ncl, co.pairs, u1);
+      else
+        leaf_parent_kernel<64><<<pgrid, 256, plds, st>>>(lp, static_cast<const uint16_t*>(q),
+                                                         static_cast<const uint16_t*>(k), a1, a1cnt, co.offs,
+                                                         co.toffs, co.ncl, co.pairs, u1);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  } else {
 
   // Stage 2: leaf scoring against each key block once per cluster.
   LeafArgs la{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, geo.M[1], s.gK(), kLog2e / sqrtf(static_cast<float>(s.D))};
@@ -1029,6 +1174,7 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
     go(leaf_score_kernel<64>);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
 
   // Final Top-K per row.
   ProfScope ps("final_topk", st);
