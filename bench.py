@@ -139,6 +139,9 @@ def main():
                     help="comma-separated N values: time PISA selection and flat-BSA selection "
                          "(each including pooling) at every N with the workload's other shapes, "
                          "random inputs drawn on the GPU; printed as one extra JSON line")
+    ap.add_argument("--decode", action="store_true",
+                    help="also time the decode workload: single-token selection + attention steps against one "
+                         "prebuilt 128K pyramid (extra JSON line)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the run, copy a cold buffer of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -337,6 +340,39 @@ def main():
             del qs, ks, pyr_s, idx_s, ws_s
         print(json.dumps({"sweep": sweep, "workload": args.workload, "what": "selection incl. pooling, ms"}),
               flush=True)
+
+    if args.decode:
+        wd = inputs.workload("decode-128k")
+        xd = inputs.make_inputs(wd, seed=0, step=0)
+        Bd, Hd, Hkvd, Nd, dd, Cd, gd, Kd = (wd[k_] for k_ in ("B", "H", "Hkv", "N", "d", "C", "g", "K"))
+        kd = torch.from_numpy(xd["k"]).to(torch.bfloat16).cuda()
+        vd = torch.from_numpy(xd["v"]).to(torch.bfloat16).cuda()
+        pd = pisa.make_problem(Bd, Hd, Hkvd, 1, Nd, dd, Cd, gd, Kd, 1, "bf16")
+        pyr_d = pisa.build_pyramid(pd, kd)
+        qsteps = [torch.from_numpy(inputs.make_inputs(wd, seed=0, step=i, parts="q")["q"]).to(torch.bfloat16).cuda()
+                  for i in range(wd["steps"])]
+        idx_d = torch.empty((Bd, Hkvd, 1, Kd), dtype=torch.int32, device="cuda")
+        o_d = torch.empty_like(qsteps[0])
+        lse_d = torch.empty((Bd, Hd, 1), dtype=torch.float32, device="cuda")
+        nsd = pisa.pisa_select_workspace_bytes(pd)
+        nad = pisa.pisa_attn_workspace_bytes(pd)
+        ws_d = torch.empty(max(nsd, nad, 1), dtype=torch.uint8, device="cuda")
+        lat = []
+        for rep in range(2):
+            for qd in qsteps:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                pisa.pisa_select(pd, qd, kd, pyr_d, idx_d, None, ws_d, nsd, stream)
+                pisa.pisa_sparse_attn_fwd(pd, qd, kd, vd, idx_d, o_d, lse_d, ws_d, nad, stream)
+                e1.record(stream)
+                torch.cuda.synchronize()
+                if rep == 1:
+                    lat.append(e0.elapsed_time(e1) * 1e3)
+        lat.sort()
+        print(json.dumps({"decode": {"workload": "decode-128k", "steps": len(lat),
+                                     "median_us": lat[len(lat) // 2], "p90_us": lat[int(0.9 * len(lat))],
+                                     "what": "one step = pisa_select + pisa_sparse_attn_fwd for 8 heads x 1 token "
+                                             "at KV length 131072, pyramid prebuilt"}}), flush=True)
 
     if args.copy_probe_mib:
         # A plain device copy of known size from a buffer evicted from the caches

@@ -416,41 +416,55 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
 // stored.
 // ----------------------------------------------------------------------------
 
-// Does (ka, pa) rank before (kb, pb)?  Higher key first, then smaller pack.
-__device__ __forceinline__ bool better(float ka, int pa, float kb, int pb) {
-  return ka > kb || (ka == kb && pa < pb);
+// Rank order (key desc, pack asc) as one ascending 64-bit integer: the high
+// word maps the float key to an unsigned value that decreases as the key
+// grows (total order, -inf last), the low word is the non-negative pack.
+__device__ __forceinline__ uint32_t desc_bits(float key) {
+  const uint32_t u = __float_as_uint(key + 0.0f);  // -0 ranks as +0
+  const uint32_t m = static_cast<uint32_t>(static_cast<int32_t>(u) >> 31);
+  return u ^ (~m & 0x7FFFFFFFu);
+}
+__device__ __forceinline__ float desc_bits_inv(uint32_t d) {
+  const uint32_t m = static_cast<uint32_t>(static_cast<int32_t>(d) >> 31);
+  return __uint_as_float(d ^ (~m & 0x7FFFFFFFu));
 }
 
+// One compare-exchange stage of the bitonic network, without branches: the
+// lane keeps the smaller of (itself, partner) where the stage wants the
+// smaller, else the larger.
 template <int K2, int J>
-__device__ __forceinline__ void sort32_step(float& key, int& pack, int hl) {
-  const float ok = xor32_f<J>(key);
-  const int op = xor32_i<J>(pack);
-  const bool dir = (hl & K2) == 0;
-  const bool lower = (hl & J) == 0;
-  const bool take = (lower == dir) ? better(ok, op, key, pack) : better(key, pack, ok, op);
-  if (take) {
-    key = ok;
-    pack = op;
-  }
+__device__ __forceinline__ void sort32_step(uint32_t& hi, uint32_t& lo, int hl) {
+  const uint32_t ohi = static_cast<uint32_t>(xor32_i<J>(static_cast<int>(hi)));
+  const uint32_t olo = static_cast<uint32_t>(xor32_i<J>(static_cast<int>(lo)));
+  const uint64_t mine = (static_cast<uint64_t>(hi) << 32) | lo;
+  const uint64_t other = (static_cast<uint64_t>(ohi) << 32) | olo;
+  const bool want_small = ((hl & K2) == 0) == ((hl & J) == 0);
+  const bool take = (other < mine) == want_small;
+  hi = take ? ohi : hi;
+  lo = take ? olo : lo;
 }
 
-// Bitonic sort of the 32 lanes of each wavefront half into rank order.
+// Bitonic sort of the 32 lanes of each wavefront half into rank order
+// (key desc, pack asc); packs are non-negative.
 __device__ __forceinline__ void sort32(float& key, int& pack, int hl) {
-  sort32_step<2, 1>(key, pack, hl);
-  sort32_step<4, 2>(key, pack, hl);
-  sort32_step<4, 1>(key, pack, hl);
-  sort32_step<8, 4>(key, pack, hl);
-  sort32_step<8, 2>(key, pack, hl);
-  sort32_step<8, 1>(key, pack, hl);
-  sort32_step<16, 8>(key, pack, hl);
-  sort32_step<16, 4>(key, pack, hl);
-  sort32_step<16, 2>(key, pack, hl);
-  sort32_step<16, 1>(key, pack, hl);
-  sort32_step<32, 16>(key, pack, hl);
-  sort32_step<32, 8>(key, pack, hl);
-  sort32_step<32, 4>(key, pack, hl);
-  sort32_step<32, 2>(key, pack, hl);
-  sort32_step<32, 1>(key, pack, hl);
+  uint32_t hi = desc_bits(key), lo = static_cast<uint32_t>(pack);
+  sort32_step<2, 1>(hi, lo, hl);
+  sort32_step<4, 2>(hi, lo, hl);
+  sort32_step<4, 1>(hi, lo, hl);
+  sort32_step<8, 4>(hi, lo, hl);
+  sort32_step<8, 2>(hi, lo, hl);
+  sort32_step<8, 1>(hi, lo, hl);
+  sort32_step<16, 8>(hi, lo, hl);
+  sort32_step<16, 4>(hi, lo, hl);
+  sort32_step<16, 2>(hi, lo, hl);
+  sort32_step<16, 1>(hi, lo, hl);
+  sort32_step<32, 16>(hi, lo, hl);
+  sort32_step<32, 8>(hi, lo, hl);
+  sort32_step<32, 4>(hi, lo, hl);
+  sort32_step<32, 2>(hi, lo, hl);
+  sort32_step<32, 1>(hi, lo, hl);
+  key = desc_bits_inv(hi);
+  pack = static_cast<int>(lo);
 }
 
 // Inclusive prefix sum over the 32 lanes of a wavefront half.
