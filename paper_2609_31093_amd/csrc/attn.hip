@@ -167,20 +167,22 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(AttnArgs a) {
 // ----------------------------------------------------------------------------
 // Block-centric attention for many rows (bf16).
 //
-// attn_block_kernel: one workgroup per tile of up to kClusterTile (row, slot)
-// pairs of one (batch x KV head, key block) cluster.  The block's C keys are staged in LDS row-major and its values transposed
-// (V^T, so that the PV product reads contiguous 8-byte runs); every (row,
-// slot) pair that selected the block is processed 32 per wavefront tile:
-// S^T = K q^T (v_mfma_f32_32x32x16_bf16, keys along M, queries along N), the
-// causal mask, the block-local max and sum, P in bf16, then O^T = V^T P with
-// the key order of P's accumulator layout reproduced in the V^T reads.  Each
-// pair leaves a partial: o normalised by its own sum (bf16) and its log2-sum
-// (fp32).  attn_combine_kernel merges the K partials of each (row, head) with
-// the usual log-sum-exp weights.
+// attn_block16_kernel: one workgroup per tile of up to kClusterTile (row,
+// slot) pairs of one (batch x KV head, key block) cluster.  The block's C
+// keys are staged in LDS row-major and its values transposed (V^T, two keys
+// per 32-bit word, so that the PV product reads contiguous 8-byte runs);
+// the pairs are processed 16 per wavefront tile on v_mfma_f32_16x16x32_bf16
+// (A lane l: row l%16, k 8*(l/16)..+7; B lane l: k 8*(l/16)..+7, column
+// l%16; D lane l: rows 4*(l/16)..+3, column l%16): S^T = K q^T (keys along
+// M, queries along N), the causal mask, the block-local max, P = 2^(S - m)
+// in bf16, then O^T = V^T P with the key order of P's operand reproduced in
+// the V^T reads.  Each pair leaves a partial: o normalised by its own sum
+// (bf16) and its log2-sum (fp32).  attn_combine_kernel merges the K
+// partials of each (row, head) with the usual log-sum-exp weights.
 // ----------------------------------------------------------------------------
 
 typedef __bf16 bf16x8a __attribute__((ext_vector_type(8)));
-typedef float f32x16a __attribute__((ext_vector_type(16)));
+typedef float f32x4a __attribute__((ext_vector_type(4)));
 
 struct AttnBlockArgs {
   int H, Hkv, G, Nq, N, C, K, causal, M1;
@@ -189,168 +191,6 @@ struct AttnBlockArgs {
 };
 
 __device__ __forceinline__ bf16x8a u4_as_bf16x8(uint4 r) { return __builtin_bit_cast(bf16x8a, r); }
-
-template <int D, int CT>
-__global__ __launch_bounds__(256) void attn_block_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
-                                                         const uint16_t* __restrict__ k,
-                                                         const uint16_t* __restrict__ v,
-                                                         const int32_t* __restrict__ offs,
-                                                         const int32_t* __restrict__ toffs, int64_t ncl,
-                                                         const int32_t* __restrict__ pairs,
-                                                         uint16_t* __restrict__ part_o,
-                                                         float* __restrict__ part_lse) {
-  constexpr int KS = D / 16;       // k-steps of QK^T
-  constexpr int LDK = D + 8;       // padded K row (bf16 elements)
-  constexpr int C = CT * 32;       // keys per block
-  constexpr int LDV = C + 4;       // padded V^T row: (LDV/2) is 2 mod 4 dwords
-  constexpr int DT = D / 32;       // output d tiles
-  extern __shared__ uint16_t lds[];
-  uint16_t* klds = lds;
-  uint16_t* vt = lds + C * LDK;
-  uint32_t* vt32 = reinterpret_cast<uint32_t*>(vt);
-
-  int64_t cl;
-  int beg, end;
-  if (!cluster_tile(offs, toffs, ncl, blockIdx.x, cl, beg, end)) return;
-  const int bh = static_cast<int>(cl / a.M1);
-  const int blk = static_cast<int>(cl - static_cast<int64_t>(bh) * a.M1);
-  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
-  const int r0 = blk * C;
-  const int nkeys = min(C, a.N - r0);
-
-  // K block row-major; V block transposed, two keys per 32-bit word.
-  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.N + r0) * D;
-  const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.N + r0) * D;
-  for (int e = threadIdx.x; e < C * (D / 8); e += 256) {
-    const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
-    uint4 kv = make_uint4(0, 0, 0, 0);
-    if (r < nkeys) kv = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
-    *reinterpret_cast<uint4*>(klds + r * LDK + c8) = kv;
-  }
-  for (int e = threadIdx.x; e < (C / 2) * (D / 8); e += 256) {
-    const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
-    uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
-    if (2 * kp < nkeys) v0 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp) * D + c8);
-    if (2 * kp + 1 < nkeys) v1 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp + 1) * D + c8);
-    const uint32_t w0[4] = {v0.x, v0.y, v0.z, v0.w};
-    const uint32_t w1[4] = {v1.x, v1.y, v1.z, v1.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      vt32[(c8 + 2 * i) * (LDV / 2) + kp] = (w0[i] & 0xFFFFu) | (w1[i] << 16);
-      vt32[(c8 + 2 * i + 1) * (LDV / 2) + kp] = (w0[i] >> 16) | (w1[i] & 0xFFFF0000u);
-    }
-  }
-  __syncthreads();
-
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int col = lane & 31;
-  const int half = lane >> 5;
-  const int ntile = (end - beg + 31) / 32;
-  for (int tile = wave; tile < ntile; tile += 4) {
-    const int p = beg + tile * 32 + col;
-    const bool valid = p < end;
-    const int pr = valid ? pairs[p] : 0;
-    const int rr = pr >> 8, slot = pr & 255;   // row within the chunk, slot
-    const int row = a.row0 + rr;
-    const int t = a.N - a.Nq + row;
-    // keys [0, kmax) of the block are visible to this query (contiguous)
-    const int kmax = a.causal ? min(nkeys, t - r0 + 1) : nkeys;
-    for (int hh = 0; hh < a.G; ++hh) {
-      const uint16_t* qrow = q + ((static_cast<int64_t>(b) * a.H + h * a.G + hh) * a.Nq + row) * D + half * 8;
-      bf16x8a qb[KS];
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        uint4 u = make_uint4(0, 0, 0, 0);
-        if (valid) u = *reinterpret_cast<const uint4*>(qrow + ks * 16);
-        qb[ks] = u4_as_bf16x8(u);
-      }
-      f32x16a sacc[CT];
-      float m = -INFINITY;
-#pragma unroll
-      for (int kt = 0; kt < CT; ++kt) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[kt][r] = 0.f;
-        const uint16_t* arow = klds + (kt * 32 + col) * LDK + half * 8;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const bf16x8a av = u4_as_bf16x8(*reinterpret_cast<const uint4*>(arow + ks * 16));
-          sacc[kt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qb[ks], sacc[kt], 0, 0, 0);
-        }
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          sacc[kt][r] = key < kmax ? sacc[kt][r] * a.qscale2 : -INFINITY;
-          m = fmaxf(m, sacc[kt][r]);
-        }
-      }
-      m = fmaxf(m, __shfl_xor(m, 32));
-      const float msafe = (m == -INFINITY) ? 0.f : m;
-      float l = 0.f;
-      bf16x8a pb[CT][2];
-#pragma unroll
-      for (int kt = 0; kt < CT; ++kt) {
-        float pv[16];
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          pv[r] = fast_exp2(sacc[kt][r] - msafe);
-          l += pv[r];
-        }
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-          uint4 u;
-          u.x = pack2_bf16(pv[8 * j + 0], pv[8 * j + 1]);
-          u.y = pack2_bf16(pv[8 * j + 2], pv[8 * j + 3]);
-          u.z = pack2_bf16(pv[8 * j + 4], pv[8 * j + 5]);
-          u.w = pack2_bf16(pv[8 * j + 6], pv[8 * j + 7]);
-          pb[kt][j] = u4_as_bf16x8(u);
-        }
-      }
-      l += __shfl_xor(l, 32);
-      // O^T[d][query] = sum_keys V^T[d][key] P[key][query]; the k index of
-      // PV step (kt, j) maps to keys kt*32 + 16j + 4*half + {0..3} (i < 4)
-      // and kt*32 + 16j + 8 + 4*half + {0..3} (i >= 4).
-      const float inv = l > 0.f ? 1.0f / l : 0.f;
-      const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + slot) * a.G + hh;
-#pragma unroll 1
-      for (int dt = 0; dt < DT; ++dt) {
-        f32x16a oacc;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[r] = 0.f;
-        const uint16_t* vrow = vt + (dt * 32 + col) * LDV + 4 * half;
-#pragma unroll
-        for (int kt = 0; kt < CT; ++kt) {
-#pragma unroll
-          for (int j = 0; j < 2; ++j) {
-            const uint2 lo = *reinterpret_cast<const uint2*>(vrow + kt * 32 + 16 * j);
-            const uint2 hi = *reinterpret_cast<const uint2*>(vrow + kt * 32 + 16 * j + 8);
-            const bf16x8a av = u4_as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-            oacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pb[kt][j], oacc, 0, 0, 0);
-          }
-        }
-        // oacc[r] = O[d = dt*32 + 8*(r/4) + 4*half + r%4][query col]
-        if (valid) {
-          uint16_t* dst = part_o + pidx * D + dt * 32 + 4 * half;
-#pragma unroll
-          for (int g4 = 0; g4 < 4; ++g4) {
-            uint2 w;
-            w.x = pack2_bf16(oacc[4 * g4 + 0] * inv, oacc[4 * g4 + 1] * inv);
-            w.y = pack2_bf16(oacc[4 * g4 + 2] * inv, oacc[4 * g4 + 3] * inv);
-            *reinterpret_cast<uint2*>(dst + 8 * g4) = w;
-          }
-        }
-      }
-      if (valid && half == 0) part_lse[pidx] = l > 0.f ? m + fast_log2(l) : -INFINITY;
-    }
-  }
-}
-
-// Same work as attn_block_kernel with 16-query tiles on
-// v_mfma_f32_16x16x32_bf16 (A lane l: row l%16, k 8*(l/16)..+7; B lane l:
-// k 8*(l/16)..+7, column l%16; D lane l: rows 4*(l/16)..+3, column l%16):
-// half the accumulator and operand registers of the 32x32 tiles, so twice
-// the wavefronts per SIMD to hide the query gathers.
-typedef float f32x4a __attribute__((ext_vector_type(4)));
 
 template <int D, int CT>
 __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,

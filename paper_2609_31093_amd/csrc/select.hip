@@ -408,9 +408,9 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
 // Lanes 0-31 own row 2w and lanes 32-63 row 2w+1 (lane hl of a half holds
 // candidate hl).  Per ranked level: the candidates needing child logits build
 // a compact load list (a candidate whose own logit is known loads one child
-// fewer, see select_kernel), the two 16-lane groups of each half compute the
-// listed dots, each lane turns its children's logits into its LSE score, and
-// a 32-lane bitonic sort on (score desc, node asc) with forced nodes keyed
+// fewer, see select_kernel), the lane groups of each half (4, 8 or 16 lanes
+// per dot) compute the listed dots, each lane turns its children's logits
+// into its LSE score, and a 32-lane bitonic sort on (score desc, node asc) with forced nodes keyed
 // +inf ranks the half: the first K survive.  Survivors expand through an LDS
 // staging list.  The leaf candidate set is sorted ascending before it is
 // stored.
@@ -477,17 +477,33 @@ __device__ __forceinline__ int half_total(int incl, int lane) {
   return lane < 32 ? t0 : t1;
 }
 
-template <int D, int GMAX>
+// Sum over each aligned group of LPE lanes (LPE in {4, 8, 16}); the total
+// lands in the group's last lane.
+template <int LPE>
+__device__ __forceinline__ float group_sum_to_last(float v) {
+  v += dpp_f<0x111>(v);
+  v += dpp_f<0x112>(v);
+  if constexpr (LPE >= 8) v += dpp_f<0x114>(v);
+  if constexpr (LPE >= 16) v += dpp_f<0x118>(v);
+  return v;
+}
+
+// LPE lanes share one child dot; lane s of a group holds the 16-byte chunks
+// s, s + LPE, s + 2 LPE, ... of the row, so each load instruction reads
+// whole 128-byte lines.
+template <int D, int GMAX, int LPE>
 __global__ __launch_bounds__(256) void stage1_pair_kernel(SelArgs a, int row_words) {
-  constexpr int DPL = D / 16;
-  constexpr int UNR = 4;
+  constexpr int DPL = D / LPE;      // floats per lane
+  constexpr int NCH = DPL / 4;      // 16-byte chunks per lane
+  constexpr int NG = 32 / LPE;      // lane groups per half
+  constexpr int UNR = DPL >= 32 ? 1 : (32 / DPL > 4 ? 4 : 32 / DPL);
   extern __shared__ int lds_i[];
   const Geo& geo = a.geo;
   const int g = geo.g, G = a.G, K = a.K, gK = a.gK;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, hl = lane & 31;
-  const int gr = (lane >> 4) & 1;  // lane group within the half
-  const int sub = lane & 15;
+  const int gr = hl / LPE;  // lane group within the half
+  const int sub = hl % LPE;
   int* L = lds_i + (wave * 2 + half) * row_words;
   int* lst_r = L;                                   // [gK*g] child row to load
   int* lst_s = lst_r + gK * g;                      // [gK*g] zbuf slot of that child
@@ -509,10 +525,14 @@ __global__ __launch_bounds__(256) void stage1_pair_kernel(SelArgs a, int row_wor
 #pragma unroll
     for (int hh = 0; hh < GMAX; ++hh) {
       if (hh < G) {
-        const int64_t off = ((static_cast<int64_t>(b) * a.H + h * G + hh) * a.Nq + rowc) * D + sub * DPL;
-        load_row_part<uint16_t, DPL>(qb + off, qv[hh]);
+        const int64_t off = ((static_cast<int64_t>(b) * a.H + h * G + hh) * a.Nq + rowc) * D + sub * 4;
 #pragma unroll
-        for (int e = 0; e < DPL; ++e) qv[hh][e] *= a.qscale2;
+        for (int ch = 0; ch < NCH; ++ch) {
+          float x4[4];
+          load_row_part<uint16_t, 4>(qb + off + ch * 4 * LPE, x4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) qv[hh][ch * 4 + e] = x4[e] * a.qscale2;
+        }
       } else {
 #pragma unroll
         for (int e = 0; e < DPL; ++e) qv[hh][e] = 0.f;
@@ -568,26 +588,33 @@ __global__ __launch_bounds__(256) void stage1_pair_kernel(SelArgs a, int row_wor
       wave_sync();
       // 2) child logits, UNR loads in flight per 16-lane group (loads past the
       //    list end fetch row 0 and are discarded)
-      const float* pbase = a.pyr + (static_cast<int64_t>(bh) * geo.R + geo.off[lev - 1]) * D + sub * DPL;
-      for (int e0 = gr; e0 < T; e0 += 2 * UNR) {
+      const float* pbase = a.pyr + (static_cast<int64_t>(bh) * geo.R + geo.off[lev - 1]) * D + sub * 4;
+      for (int e0 = gr; e0 < T; e0 += NG * UNR) {
         float x[UNR][DPL];
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
-          const int e = e0 + 2 * u;
+          const int e = e0 + NG * u;
           const int r = e < T ? lst_r[e] : 0;
-          load_row_part<float, DPL>(pbase + static_cast<int64_t>(r) * D, x[u]);
+#pragma unroll
+          for (int ch = 0; ch < NCH; ++ch) {
+            const float4 v4 = *reinterpret_cast<const float4*>(pbase + static_cast<int64_t>(r) * D + ch * 4 * LPE);
+            x[u][ch * 4 + 0] = v4.x;
+            x[u][ch * 4 + 1] = v4.y;
+            x[u][ch * 4 + 2] = v4.z;
+            x[u][ch * 4 + 3] = v4.w;
+          }
         }
 #pragma unroll
         for (int u = 0; u < UNR; ++u) {
-          const int e = e0 + 2 * u;
+          const int e = e0 + NG * u;
 #pragma unroll
           for (int hh = 0; hh < GMAX; ++hh) {
             if (hh < G) {
               float d0 = 0.f;
 #pragma unroll
               for (int i = 0; i < DPL; ++i) d0 = fmaf(qv[hh][i], x[u][i], d0);
-              d0 = rowsum16_to15(d0);
-              if (sub == 15 && e < T) zbuf[lst_s[e] * G + hh] = d0;
+              d0 = group_sum_to_last<LPE>(d0);
+              if (sub == LPE - 1 && e < T) zbuf[lst_s[e] * G + hh] = d0;
             }
           }
         }
@@ -1127,13 +1154,13 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
       const size_t lds = static_cast<size_t>(8) * words * sizeof(int);
       auto go = [&](auto kern) { kern<<<grid, 256, lds, st>>>(a, words); };
       if (s.D == 128) {
-        if (s.G == 1) go(stage1_pair_kernel<128, 1>);
-        else if (s.G <= 4) go(stage1_pair_kernel<128, 4>);
-        else go(stage1_pair_kernel<128, 16>);
+        if (s.G == 1) go(stage1_pair_kernel<128, 1, 4>);
+        else if (s.G <= 4) go(stage1_pair_kernel<128, 4, 16>);
+        else go(stage1_pair_kernel<128, 16, 16>);
       } else {
-        if (s.G == 1) go(stage1_pair_kernel<64, 1>);
-        else if (s.G <= 4) go(stage1_pair_kernel<64, 4>);
-        else go(stage1_pair_kernel<64, 16>);
+        if (s.G == 1) go(stage1_pair_kernel<64, 1, 4>);
+        else if (s.G <= 4) go(stage1_pair_kernel<64, 4, 16>);
+        else go(stage1_pair_kernel<64, 16, 16>);
       }
     } else {
       launch_sel_d<uint16_t, 64, false>(s, a, st);
