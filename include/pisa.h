@@ -68,9 +68,15 @@ enum {
                                   levels per query, then leaf blocks scored
                                   once per key block for a tile of queries,
                                   then a final Top-K (bf16 only) */
-  PISA_SCHEDULE_FUSED = 2      /* Sec. 3.3 decode design: one program per
+  PISA_SCHEDULE_FUSED = 2,     /* Sec. 3.3 decode design: one program per
                                   (query, KV head) walks every level down to
                                   the raw leaf keys */
+  PISA_SCHEDULE_SPLIT = 3      /* few rows (decode): intermediate levels with
+                                  a workgroup per (query, KV head), then each
+                                  leaf candidate scored by a workgroup of its
+                                  own, then the final Top-K; the same
+                                  selection as the other schedules, spread
+                                  over the whole GPU */
 };
 
 /* The problem statement of Sec. 3.1-3.2: q/k/v, N, head dim d, block size C,

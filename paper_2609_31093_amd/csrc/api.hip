@@ -77,10 +77,10 @@ int check_problem(const pisa_problem* p, pisa::Shape* s, pisa::Geo* geo) {
     return fail(PISA_ERR_INVALID_ARG, "causal selection keeps the first, previous and current blocks: K >= 3");
   if (p->dtype != PISA_DTYPE_F32 && p->dtype != PISA_DTYPE_BF16)
     return fail(PISA_ERR_INVALID_ARG, "unknown dtype %d", p->dtype);
-  if (p->schedule < PISA_SCHEDULE_AUTO || p->schedule > PISA_SCHEDULE_FUSED)
+  if (p->schedule < PISA_SCHEDULE_AUTO || p->schedule > PISA_SCHEDULE_SPLIT)
     return fail(PISA_ERR_INVALID_ARG, "unknown schedule %d", p->schedule);
   if (p->d != 64 && p->d != 128) return fail(PISA_ERR_UNSUPPORTED, "head dim %d (supported: 64, 128)", p->d);
-  if (p->C % 32 != 0 || p->C > 256)
+  if (p->C % 32 != 0 || p->C > pisa::kMaxLeafKeys)
     return fail(PISA_ERR_UNSUPPORTED, "block size %d (supported: multiples of 32 up to 256)", p->C);
   if (p->fanout > 16) return fail(PISA_ERR_UNSUPPORTED, "fanout %d (supported: 2..16)", p->fanout);
   const int G = p->H / p->Hkv;
@@ -140,11 +140,22 @@ int device_status(hipError_t e, const char* what) {
 // leaf block).
 constexpr int kMaxClusterBins = 16384;
 
-bool use_two_stage(const pisa_problem* p, const pisa::Shape& s, const pisa::Geo& g) {
-  if (p->schedule == PISA_SCHEDULE_TWO_STAGE) return true;
-  if (p->schedule == PISA_SCHEDULE_FUSED) return false;
+// Rows (query rows x batch x KV heads) up to which the automatic schedule
+// spreads each row's leaf candidates over workgroups of their own.
+constexpr int64_t kSplitMaxRows = 2048;
+
+int pick_schedule(const pisa_problem* p, const pisa::Shape& s, const pisa::Geo& g) {
+  if (p->schedule != PISA_SCHEDULE_AUTO) return p->schedule;
+  const int64_t rows = static_cast<int64_t>(s.Nq) * s.BH();
   // Key-block reuse pays once many queries share the key blocks (Sec. 3.3).
-  return s.bf16 && static_cast<int64_t>(s.Nq) * s.BH() >= 4096 && g.M[1] <= kMaxClusterBins;
+  if (s.bf16 && rows >= 4096 && g.M[1] <= kMaxClusterBins) return PISA_SCHEDULE_TWO_STAGE;
+  return rows <= kSplitMaxRows ? PISA_SCHEDULE_SPLIT : PISA_SCHEDULE_FUSED;
+}
+
+size_t select_ws(int sched, const pisa::Shape& s, const pisa::Geo& g) {
+  if (sched == PISA_SCHEDULE_TWO_STAGE) return pisa::select_two_stage_ws(s, g);
+  if (sched == PISA_SCHEDULE_SPLIT) return pisa::select_split_ws(s);
+  return 0;
 }
 
 #define PISA_TRY(x)           \
@@ -182,7 +193,7 @@ size_t pisa_select_workspace_bytes(const pisa_problem* p) {
   pisa::Shape s{};
   pisa::Geo g{};
   if (check_problem(p, &s, &g) != PISA_OK) return 0;
-  return use_two_stage(p, s, g) ? pisa::select_two_stage_ws(s, g) : 0;
+  return select_ws(pick_schedule(p, s, g), s, g);
 }
 
 size_t pisa_bsa_workspace_bytes(const pisa_problem* p) {
@@ -220,16 +231,21 @@ int pisa_select(const pisa_problem* p, const void* q, const void* k, const float
   PISA_TRY(check_ptr(pyramid, "pyramid"));
   PISA_TRY(check_ptr(block_idx, "block_idx"));
   PISA_TRY(check_ptr(block_score, "block_score", true));
-  const bool two = use_two_stage(p, s, g);
+  const int sched = pick_schedule(p, s, g);
+  const bool two = sched == PISA_SCHEDULE_TWO_STAGE;
   if (two && !s.bf16)
     return fail(PISA_ERR_UNSUPPORTED, "the two-stage schedule runs on bf16 inputs (use the fused schedule)");
   if (two && g.M[1] > kMaxClusterBins)
     return fail(PISA_ERR_UNSUPPORTED, "the two-stage schedule needs N/C <= %d", kMaxClusterBins);
-  const size_t need = two ? pisa::select_two_stage_ws(s, g) : 0;
-  PISA_TRY(check_ws(ws, ws_bytes, need));
+  PISA_TRY(check_ws(ws, ws_bytes, select_ws(sched, s, g)));
   hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e = two ? pisa::launch_select_two_stage(s, g, q, k, pyramid, block_idx, block_score, ws, st)
-                     : pisa::launch_select_fused(s, g, q, k, pyramid, block_idx, block_score, st);
+  hipError_t e;
+  if (two)
+    e = pisa::launch_select_two_stage(s, g, q, k, pyramid, block_idx, block_score, ws, st);
+  else if (sched == PISA_SCHEDULE_SPLIT)
+    e = pisa::launch_select_split(s, g, q, k, pyramid, block_idx, block_score, ws, st);
+  else
+    e = pisa::launch_select_fused(s, g, q, k, pyramid, block_idx, block_score, st);
   return device_status(e, "pisa_select");
 }
 

@@ -402,6 +402,128 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnBlockArgs a, cons
   }
 }
 
+// Attention for few rows (decode): one workgroup per (row, slot) attends the
+// slot's key block for the G query heads of the KV head and leaves the same
+// partial as attn_block16_kernel (o normalised by its own sum in bf16, the
+// log2-sum in fp32); attn_combine_kernel merges the K partials of each row.
+// The block's keys and values are staged in LDS with every load in flight
+// at once, so a step costs a few memory round trips whatever the row count.
+template <int D, int GMAX>
+__global__ __launch_bounds__(256) void attn_slot_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
+                                                        const uint16_t* __restrict__ k,
+                                                        const uint16_t* __restrict__ v,
+                                                        const int32_t* __restrict__ idx,
+                                                        uint16_t* __restrict__ part_o,
+                                                        float* __restrict__ part_lse) {
+  constexpr int DPL = D / 16;
+  constexpr int NPART = 256 / D;  // key subsets summed separately in the PV product
+  extern __shared__ uint16_t lds[];
+  const int C = a.C;
+  uint16_t* ks = lds;                                          // [C][D]
+  uint16_t* vs = lds + C * D;                                  // [C][D]
+  float* z = reinterpret_cast<float*>(lds + 2 * C * D);        // [C][G] logits, then weights
+  float* red = z + C * GMAX;                                   // [256] PV partial sums
+  float* ml = red + 256;                                       // [GMAX][2] max, sum
+
+  const int slot = blockIdx.x;
+  const int rr = blockIdx.y % a.nrows;
+  const int bh = blockIdx.y / a.nrows;
+  const int row = a.row0 + rr;
+  const int blk = idx[(static_cast<int64_t>(bh) * a.Nq + row) * a.K + slot];
+  if (blk < 0) return;  // the combine skips empty slots
+  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+  const int G = a.G;
+  const int t = a.N - a.Nq + row;
+  const int r0 = blk * C;
+  const int nkeys = min(C, a.N - r0);
+  const int kmax = a.causal ? min(nkeys, t - r0 + 1) : nkeys;
+  const int tid = threadIdx.x;
+
+  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.N + r0) * D;
+  const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.N + r0) * D;
+  for (int e = tid; e < C * (D / 8); e += 256) {
+    const int r = e / (D / 8);
+    uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
+    if (r < nkeys) {
+      kv = reinterpret_cast<const uint4*>(kb)[e];
+      vv = reinterpret_cast<const uint4*>(vb)[e];
+    }
+    reinterpret_cast<uint4*>(ks)[e] = kv;
+    reinterpret_cast<uint4*>(vs)[e] = vv;
+  }
+  const int grp = tid >> 4, sub = tid & 15;
+  float qv[GMAX][DPL];
+#pragma unroll
+  for (int hh = 0; hh < GMAX; ++hh) {
+    if (hh < G) {
+      const int64_t off = ((static_cast<int64_t>(b) * a.H + h * G + hh) * a.Nq + row) * D + sub * DPL;
+      load_row_part<uint16_t, DPL>(q + off, qv[hh]);
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) qv[hh][e] *= a.qscale2;
+    } else {
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) qv[hh][e] = 0.f;
+    }
+  }
+  __syncthreads();
+  // logits of the visible keys (16 lanes per key)
+  for (int r = grp; r < C; r += 16) {
+    float x[DPL];
+    load_row_part<uint16_t, DPL>(ks + r * D + sub * DPL, x);
+#pragma unroll
+    for (int hh = 0; hh < GMAX; ++hh) {
+      if (hh < G) {
+        float d0 = 0.f;
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) d0 = fmaf(qv[hh][e], x[e], d0);
+        d0 = sum16(d0);
+        if (sub == 0) z[r * G + hh] = r < kmax ? d0 : -INFINITY;
+      }
+    }
+  }
+  __syncthreads();
+  // per head: block-local max and sum, z turned into weights 2^(z - m)
+  const int wave = tid >> 6, lane = tid & 63;
+  for (int hh = wave; hh < G; hh += 4) {
+    float m = -INFINITY;
+    for (int r = lane; r < C; r += 64) m = fmaxf(m, z[r * G + hh]);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    const float msafe = m == -INFINITY ? 0.f : m;
+    float sm = 0.f;
+    for (int r = lane; r < C; r += 64) {
+      const float p = fast_exp2(z[r * G + hh] - msafe);
+      z[r * G + hh] = p;
+      sm += p;
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) sm += __shfl_xor(sm, o);
+    if (lane == 0) {
+      ml[2 * hh] = m;
+      ml[2 * hh + 1] = sm;
+    }
+  }
+  __syncthreads();
+  // O[hh][d] = sum_r w[r][hh] V[r][d] / l: thread (part, d) sums keys part, part + NPART, ...
+  const int dcol = tid % D, part = tid / D;
+  for (int hh = 0; hh < G; ++hh) {
+    float acc = 0.f;
+    for (int r = part; r < kmax; r += NPART) acc = fmaf(z[r * G + hh], bf16_to_f32(vs[r * D + dcol]), acc);
+    red[tid] = acc;
+    __syncthreads();
+    if (tid < D) {
+      float o = red[tid];
+#pragma unroll
+      for (int pp = 1; pp < NPART; ++pp) o += red[tid + pp * D];
+      const float m = ml[2 * hh], l = ml[2 * hh + 1];
+      const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + slot) * G + hh;
+      part_o[pidx * D + tid] = f32_to_bf16_rne(l > 0.f ? o / l : 0.f);
+      if (tid == 0) part_lse[pidx] = l > 0.f ? m + fast_log2(l) : -INFINITY;
+    }
+    __syncthreads();
+  }
+}
+
 template <typename T, int D, int TEAM>
 static void launch_rows(const Shape& s, const AttnArgs& a, hipStream_t st) {
   constexpr int ROWS = 256 / TEAM;
@@ -432,6 +554,12 @@ static int attn_chunk_rows(const Shape& s) {
   return static_cast<int>(std::min<size_t>(s.Nq, std::max<size_t>(rows, 1)));
 }
 
+// Split path for few rows: bf16, a workgroup per (row, slot), partials for
+// every row at once (rows * K * G of them).
+static bool use_split_path(const Shape& s, const Geo& geo) {
+  return s.bf16 && !use_block_path(s, geo) && static_cast<int64_t>(s.BH()) * s.Nq <= 2048;
+}
+
 struct AttnWs {
   size_t part_o, part_lse, cl, total;
 };
@@ -449,7 +577,59 @@ static AttnWs attn_layout(const Shape& s, const Geo& geo) {
   return w;
 }
 
-size_t attn_ws(const Shape& s, const Geo& geo) { return use_block_path(s, geo) ? attn_layout(s, geo).total : 0; }
+static AttnWs split_attn_layout(const Shape& s) {
+  const size_t np = static_cast<size_t>(s.BH()) * s.Nq * s.K;
+  AttnWs w{};
+  size_t o = 0;
+  auto al = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
+  w.part_o = o;   o += al(np * s.G * s.D * 2);
+  w.part_lse = o; o += al(np * s.G * 4);
+  w.cl = o;
+  w.total = o;
+  return w;
+}
+
+size_t attn_ws(const Shape& s, const Geo& geo) {
+  if (use_block_path(s, geo)) return attn_layout(s, geo).total;
+  if (use_split_path(s, geo)) return split_attn_layout(s).total;
+  return 0;
+}
+
+template <int D>
+static hipError_t launch_split_path(const Shape& s, const void* q, const void* k, const void* v,
+                                    const int32_t* idx, void* o, float* lse, void* ws, hipStream_t st) {
+  const AttnWs w = split_attn_layout(s);
+  char* base = static_cast<char*>(ws);
+  uint16_t* part_o = reinterpret_cast<uint16_t*>(base + w.part_o);
+  float* part_lse = reinterpret_cast<float*>(base + w.part_lse);
+  AttnBlockArgs a{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, 0, 0, s.Nq,
+                  kLog2e / sqrtf(static_cast<float>(s.D))};
+  const uint16_t* qq = static_cast<const uint16_t*>(q);
+  const uint16_t* kk = static_cast<const uint16_t*>(k);
+  const uint16_t* vv = static_cast<const uint16_t*>(v);
+  {
+    ProfScope ps("attn_slot", st);
+    dim3 grid(s.K, static_cast<unsigned>(static_cast<int64_t>(s.BH()) * s.Nq));
+    auto go = [&](auto kern, int gmax) {
+      const size_t lds = static_cast<size_t>(2) * s.C * D * 2 + (static_cast<size_t>(s.C) * gmax + 256 + 2 * gmax) * 4;
+      if (lds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+      kern<<<grid, 256, lds, st>>>(a, qq, kk, vv, idx, part_o, part_lse);
+    };
+    if (s.G == 1)
+      go(attn_slot_kernel<D, 1>, 1);
+    else if (s.G <= 4)
+      go(attn_slot_kernel<D, 4>, 4);
+    else
+      go(attn_slot_kernel<D, 16>, 16);
+  }
+  {
+    ProfScope ps("attn_combine", st);
+    dim3 grid((s.Nq + 3) / 4, s.B * s.H);
+    attn_combine_kernel<D><<<grid, 256, 0, st>>>(a, idx, part_o, part_lse, static_cast<uint16_t*>(o), lse);
+  }
+  return hipGetLastError();
+}
 
 template <int D>
 static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* q, const void* k, const void* v,
@@ -503,6 +683,10 @@ hipError_t launch_attention(const Shape& s, const Geo& geo, const void* q, const
   if (use_block_path(s, geo)) {
     return s.D == 128 ? launch_block_path<128>(s, geo, q, k, v, idx, o, lse, ws, st)
                       : launch_block_path<64>(s, geo, q, k, v, idx, o, lse, ws, st);
+  }
+  if (use_split_path(s, geo)) {
+    return s.D == 128 ? launch_split_path<128>(s, q, k, v, idx, o, lse, ws, st)
+                      : launch_split_path<64>(s, q, k, v, idx, o, lse, ws, st);
   }
   AttnArgs a{q, k, v, idx, o, lse, s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal,
              kLog2e / sqrtf(static_cast<float>(s.D))};

@@ -8,6 +8,7 @@ namespace pisa {
 
 constexpr int kMaxLevels = 32;
 constexpr int kMaxCand = 256;     // fanout * K upper bound (candidates per level)
+constexpr int kMaxLeafKeys = 256;  // leaf block size C upper bound
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 

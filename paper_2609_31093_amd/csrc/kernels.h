@@ -78,6 +78,11 @@ hipError_t launch_build_pyramid(const Geo& geo, int BH, int D, bool bf16, const 
 hipError_t launch_select_fused(const Shape& s, const Geo& geo, const void* q, const void* k,
                                const float* pyr, int32_t* idx, float* score, hipStream_t st);
 
+// Split selector for few rows (decode): workspace of select_split_ws().
+size_t select_split_ws(const Shape& s);
+hipError_t launch_select_split(const Shape& s, const Geo& geo, const void* q, const void* k, const float* pyr,
+                               int32_t* idx, float* score, void* ws, hipStream_t st);
+
 // Two-stage selector: workspace layout is computed by select_two_stage_ws().
 size_t select_two_stage_ws(const Shape& s, const Geo& geo);
 hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q, const void* k,

@@ -1041,6 +1041,309 @@ __global__ __launch_bounds__(256) void final_topk_kernel(TopkArgs a, const int32
 }
 
 // ----------------------------------------------------------------------------
+// Stage 1 for few rows (decode) and g*K <= 64: one workgroup per row.
+//
+// Latency is the cost here, so each ranked level is one memory round trip
+// and no more: the row starts at its first ranked level (every coarser level
+// keeps all of its eligible nodes, so that level's candidates are simply its
+// eligible nodes), all 256 threads fetch every child row of the level at
+// once (16 lanes per row) and leave the logits in LDS, and wavefront 0 holds
+// one candidate per lane, forms the LSE scores, ranks them with a 64-lane
+// bitonic sort (forced nodes keyed +inf), keeps the first K and expands them
+// to their eligible children through a lane scan.
+// ----------------------------------------------------------------------------
+template <int K2, int J>
+__device__ __forceinline__ void sort64_step(uint32_t& hi, uint32_t& lo, int lane) {
+  uint32_t ohi, olo;
+  if constexpr (J == 32) {
+    ohi = static_cast<uint32_t>(__shfl_xor(static_cast<int>(hi), 32));
+    olo = static_cast<uint32_t>(__shfl_xor(static_cast<int>(lo), 32));
+  } else {
+    ohi = static_cast<uint32_t>(xor32_i<J>(static_cast<int>(hi)));
+    olo = static_cast<uint32_t>(xor32_i<J>(static_cast<int>(lo)));
+  }
+  const uint64_t mine = (static_cast<uint64_t>(hi) << 32) | lo;
+  const uint64_t other = (static_cast<uint64_t>(ohi) << 32) | olo;
+  const bool want_small = ((lane & K2) == 0) == ((lane & J) == 0);
+  const bool take = (other < mine) == want_small;
+  hi = take ? ohi : hi;
+  lo = take ? olo : lo;
+}
+
+// Bitonic sort of the 64 lanes of a wavefront into rank order (key desc,
+// pack asc); packs are non-negative.
+__device__ __forceinline__ void sort64(float& key, int& pack, int lane) {
+  uint32_t hi = desc_bits(key), lo = static_cast<uint32_t>(pack);
+  sort64_step<2, 1>(hi, lo, lane);
+  sort64_step<4, 2>(hi, lo, lane);
+  sort64_step<4, 1>(hi, lo, lane);
+  sort64_step<8, 4>(hi, lo, lane);
+  sort64_step<8, 2>(hi, lo, lane);
+  sort64_step<8, 1>(hi, lo, lane);
+  sort64_step<16, 8>(hi, lo, lane);
+  sort64_step<16, 4>(hi, lo, lane);
+  sort64_step<16, 2>(hi, lo, lane);
+  sort64_step<16, 1>(hi, lo, lane);
+  sort64_step<32, 16>(hi, lo, lane);
+  sort64_step<32, 8>(hi, lo, lane);
+  sort64_step<32, 4>(hi, lo, lane);
+  sort64_step<32, 2>(hi, lo, lane);
+  sort64_step<32, 1>(hi, lo, lane);
+  sort64_step<64, 32>(hi, lo, lane);
+  sort64_step<64, 16>(hi, lo, lane);
+  sort64_step<64, 8>(hi, lo, lane);
+  sort64_step<64, 4>(hi, lo, lane);
+  sort64_step<64, 2>(hi, lo, lane);
+  sort64_step<64, 1>(hi, lo, lane);
+  key = desc_bits_inv(hi);
+  pack = static_cast<int>(lo);
+}
+
+// Inclusive prefix sum over the 64 lanes of a wavefront.
+__device__ __forceinline__ int scan64_incl(int v, int lane) {
+  const int x = scan32_incl(v);
+  return x + (lane >= 32 ? __builtin_amdgcn_readlane(x, 31) : 0);
+}
+
+template <typename T, int D, int GMAX>
+__global__ __launch_bounds__(256) void stage1_row_kernel(SelArgs a) {
+  constexpr int DPL = D / 16;
+  constexpr int UNR = 4;  // child rows per 16-lane group in flight: 64 per round
+  __shared__ int s_cand[64];
+  __shared__ int s_n;
+  extern __shared__ float s_z[];  // [candidate * g + child][head], g*K*g*G floats
+  const Geo& geo = a.geo;
+  const int g = geo.g, G = a.G, K = a.K;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int grp = tid >> 4, sub = tid & 15;
+  const int row = blockIdx.x;
+  const int bh = blockIdx.y;
+  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+  const int t = geo.N - a.Nq + row;
+  const int c = t / geo.C;
+
+  float qv[GMAX][DPL];
+  {
+    const T* qb = static_cast<const T*>(a.q);
+#pragma unroll
+    for (int hh = 0; hh < GMAX; ++hh) {
+      if (hh < G) {
+        const int64_t off = ((static_cast<int64_t>(b) * a.H + h * G + hh) * a.Nq + row) * D + sub * DPL;
+        load_row_part<T, DPL>(qb + off, qv[hh]);
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) qv[hh][e] *= a.qscale2;
+      } else {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) qv[hh][e] = 0.f;
+      }
+    }
+  }
+  auto n_eligible = [&](int lev) { return a.causal ? min(anc_at(geo, c, lev) + 1, geo.M[lev]) : geo.M[lev]; };
+  int start = 1;
+  for (int lev = geo.L; lev >= 2; --lev) {
+    if (n_eligible(lev) > K) {
+      start = lev;
+      break;
+    }
+  }
+  // wavefront 0 keeps the candidate of each lane in a register
+  int node = -1, nA = n_eligible(start);
+  if (wave == 0) {
+    node = lane < nA ? lane : -1;
+    if (lane < nA) s_cand[lane] = lane;
+    if (lane == 0) s_n = nA;
+  }
+  __syncthreads();
+
+  for (int lev = start; lev >= 2; --lev) {
+    nA = s_n;
+    const int Mb = geo.M[lev - 1];
+    const int nch_all = nA * g;
+    // 1) logits of every child row of every candidate (non-existent children
+    //    past the level's end are skipped)
+    const float* pbase = a.pyr + (static_cast<int64_t>(bh) * geo.R + geo.off[lev - 1]) * D + sub * DPL;
+    for (int e0 = grp; e0 < nch_all; e0 += 16 * UNR) {
+      float x[UNR][DPL];
+      bool ok[UNR];
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int e = e0 + 16 * u;
+        const int r = e < nch_all ? s_cand[e / g] * g + (e % g) : Mb;
+        ok[u] = r < Mb;
+        if (ok[u]) {
+          load_row_part<float, DPL>(pbase + static_cast<int64_t>(r) * D, x[u]);
+        } else {
+#pragma unroll
+          for (int i = 0; i < DPL; ++i) x[u][i] = 0.f;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < UNR; ++u) {
+        const int e = e0 + 16 * u;
+#pragma unroll
+        for (int hh = 0; hh < GMAX; ++hh) {
+          if (hh < G) {
+            float d0 = 0.f;
+#pragma unroll
+            for (int i = 0; i < DPL; ++i) d0 = fmaf(qv[hh][i], x[u][i], d0);
+            d0 = rowsum16_to15(d0);
+            if (sub == 15 && e < nch_all) s_z[e * G + hh] = ok[u] ? d0 : -INFINITY;
+          }
+        }
+      }
+    }
+    __syncthreads();
+    if (wave == 0) {
+      // 2) scores, rank, keep
+      const Forced fz = forced_at(geo, lev, c, a.causal);
+      const bool valid = node >= 0;
+      const bool isf = valid && fz.is(node);
+      const bool ranked = nA > K;
+      float key = valid ? INFINITY : -INFINITY;
+      if (ranked && valid && !isf) {
+        const int nch = min(g, Mb - node * g);
+        float u = 0.f;
+        for (int hh = 0; hh < G; ++hh) {
+          const float* zc = s_z + lane * g * G + hh;
+          float m = -INFINITY;
+          for (int j = 0; j < nch; ++j) m = fmaxf(m, zc[j * G]);
+          float sm = 0.f;
+          for (int j = 0; j < nch; ++j) sm += fast_exp2(zc[j * G] - m);
+          u += m + fast_log2(sm);
+        }
+        key = u;
+      }
+      int knode = node;
+      bool kept = valid;
+      if (ranked) {
+        int pack = valid ? node : 0x7FFFFFC0 | lane;
+        sort64(key, pack, lane);
+        kept = lane < K && key != -INFINITY;
+        knode = pack;
+      }
+      // 3) expand the kept nodes to their eligible children
+      const int rmax = a.causal ? min(anc_at(geo, c, lev - 1), Mb - 1) : Mb - 1;
+      const int c0 = knode * g;
+      const int nk = kept ? max(0, min(c0 + g - 1, rmax) - c0 + 1) : 0;
+      const int incl = scan64_incl(nk, lane);
+      const int n2 = __builtin_amdgcn_readlane(incl, 63);
+      for (int j = 0; j < nk; ++j) s_cand[incl - nk + j] = c0 + j;
+      wave_sync();
+      node = lane < n2 ? s_cand[lane] : -1;
+      if (lane == 0) s_n = n2;
+    }
+    __syncthreads();
+  }
+  if (wave == 0) {
+    if (start == 1) node = lane < nA ? lane : -1;
+    nA = start == 1 ? nA : s_n;
+    // leaf candidate set, ascending
+    float akey = node >= 0 ? -static_cast<float>(node) : -INFINITY;
+    int apack = node >= 0 ? node : 0x7FFFFFC0 | lane;
+    sort64(akey, apack, lane);
+    const int64_t orow = static_cast<int64_t>(bh) * a.Nq + row;
+    if (lane < a.gK) a.a1[orow * a.gK + lane] = lane < nA ? apack : -1;
+    if (lane == 0) a.a1cnt[orow] = nA;
+  }
+}
+
+// ----------------------------------------------------------------------------
+// Leaf scoring for few rows (decode): one workgroup per (row, candidate slot)
+// computes the exact LSE over the candidate block's raw keys for the G query
+// heads of the KV head (Sec. 3.3 leaf level; the same u as the clustered
+// scorers, in log2 units).  Up to 64 key rows are requested at once, so a
+// step costs a few memory round trips whatever the number of rows; key-block
+// reuse across queries, the reason for clustering, does not arise here.
+// ----------------------------------------------------------------------------
+template <typename T, int D, int GMAX>
+__global__ __launch_bounds__(256) void leaf_slot_kernel(SelArgs a, const int32_t* __restrict__ a1,
+                                                        const int32_t* __restrict__ a1cnt, float* __restrict__ u1) {
+  constexpr int DPL = D / 16;
+  constexpr int UNR = 4;  // rounds of 16 key rows in flight
+  __shared__ float z[kMaxLeafKeys * GMAX];
+  __shared__ float lse_h[GMAX];
+  const Geo& geo = a.geo;
+  const int slot = blockIdx.x;
+  const int64_t rg = blockIdx.y;  // bh * Nq + row
+  const int n = a1cnt[rg];
+  if (slot >= n || n <= a.K) return;
+  const int node = a1[rg * a.gK + slot];
+  const int bh = static_cast<int>(rg / a.Nq), row = static_cast<int>(rg - static_cast<int64_t>(bh) * a.Nq);
+  const int c = (geo.N - a.Nq + row) / geo.C;
+  if (a.causal && (node == 0 || node == c || node == c - 1)) return;  // forced: never scored
+  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+  const int G = a.G;
+  const int tid = threadIdx.x, grp = tid >> 4, sub = tid & 15;
+
+  float qv[GMAX][DPL];
+  {
+    const T* qb = static_cast<const T*>(a.q);
+#pragma unroll
+    for (int hh = 0; hh < GMAX; ++hh) {
+      if (hh < G) {
+        const int64_t off = ((static_cast<int64_t>(b) * a.H + h * G + hh) * a.Nq + row) * D + sub * DPL;
+        load_row_part<T, DPL>(qb + off, qv[hh]);
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) qv[hh][e] *= a.qscale2;
+      } else {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) qv[hh][e] = 0.f;
+      }
+    }
+  }
+  const int r0 = node * geo.C;
+  const int nrows = min(geo.C, geo.N - r0);
+  const T* kb = static_cast<const T*>(a.k) + (static_cast<int64_t>(bh) * geo.N + r0) * D + sub * DPL;
+  for (int base = 0; base < nrows; base += 16 * UNR) {
+    float x[UNR][DPL];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int r = base + grp + 16 * u;
+      if (r < nrows) {
+        load_row_part<T, DPL>(kb + static_cast<int64_t>(r) * D, x[u]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) x[u][e] = 0.f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int r = base + grp + 16 * u;
+#pragma unroll
+      for (int hh = 0; hh < GMAX; ++hh) {
+        if (hh < G) {
+          float d0 = 0.f;
+#pragma unroll
+          for (int e = 0; e < DPL; ++e) d0 = fmaf(qv[hh][e], x[u][e], d0);
+          d0 = sum16(d0);
+          if (sub == 0 && r < nrows) z[r * G + hh] = d0;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  // LSE per head: wave w takes heads w, w + 4, ...
+  const int wave = tid >> 6, lane = tid & 63;
+  for (int hh = wave; hh < G; hh += 4) {
+    float m = -INFINITY;
+    for (int r = lane; r < nrows; r += 64) m = fmaxf(m, z[r * G + hh]);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
+    float sm = 0.f;
+    for (int r = lane; r < nrows; r += 64) sm += fast_exp2(z[r * G + hh] - m);
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) sm += __shfl_xor(sm, o);
+    if (lane == 0) lse_h[hh] = m + fast_log2(sm);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    float u = 0.f;
+    for (int hh = 0; hh < G; ++hh) u += lse_h[hh];
+    u1[rg * a.gK + slot] = u;
+  }
+}
+
+// ----------------------------------------------------------------------------
 // Host launchers.
 // ----------------------------------------------------------------------------
 
@@ -1131,6 +1434,21 @@ static TwoStageWs two_stage_layout(const Shape& s, const Geo& geo) {
 
 size_t select_two_stage_ws(const Shape& s, const Geo& geo) { return two_stage_layout(s, geo).total; }
 
+// Final Top-K per row over the scored leaf candidates.
+static hipError_t launch_final_topk(const Shape& s, const int32_t* a1, const int32_t* a1cnt, const float* u1,
+                                    int32_t* idx, float* score, hipStream_t st) {
+  const int64_t rows = static_cast<int64_t>(s.BH()) * s.Nq;
+  ProfScope ps("final_topk", st);
+  if (s.gK() <= 32) {
+    TopkArgsP ta{s.Nq, s.N, s.C, s.K, s.gK(), s.causal, rows};
+    final_topk_pair_kernel<<<static_cast<unsigned>((rows + 7) / 8), 256, 0, st>>>(ta, a1, a1cnt, u1, idx, score);
+  } else {
+    TopkArgs ta{s.Nq, s.N, s.C, s.K, s.gK(), s.causal, rows};
+    final_topk_kernel<<<static_cast<unsigned>((rows + 3) / 4), 256, 0, st>>>(ta, a1, a1cnt, u1, idx, score);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q, const void* k,
                                    const float* pyr, int32_t* idx, float* score, void* ws, hipStream_t st) {
   const TwoStageWs w = two_stage_layout(s, geo);
@@ -1196,37 +1514,121 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   } else {
+    // Stage 2: leaf scoring against each key block once per cluster.
+    LeafArgs la{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, geo.M[1], s.gK(), kLog2e / sqrtf(static_cast<float>(s.D))};
+    dim3 lgrid(static_cast<unsigned>(cluster_max_tiles(s.BH(), geo.M[1], rows * s.gK())));
+    const size_t llds = static_cast<size_t>(s.C) * (s.D + 8) * 2;
+    {
+      ProfScope ps("leaf_score", st);
+      auto go = [&](auto kern) {
+        if (llds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(llds));
+        kern<<<lgrid, 256, llds, st>>>(la, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                                       co.offs, co.toffs, co.ncl, co.pairs, u1);
+      };
+      if (s.D == 128)
+        go(leaf_score_kernel<128>);
+      else
+        go(leaf_score_kernel<64>);
+    }
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
 
-  // Stage 2: leaf scoring against each key block once per cluster.
-  LeafArgs la{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, geo.M[1], s.gK(), kLog2e / sqrtf(static_cast<float>(s.D))};
-  dim3 lgrid(static_cast<unsigned>(cluster_max_tiles(s.BH(), geo.M[1], rows * s.gK())));
-  const size_t llds = static_cast<size_t>(s.C) * (s.D + 8) * 2;
-  {
-  ProfScope ps("leaf_score", st);
-  auto go = [&](auto kern) {
-    if (llds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                          hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(llds));
-    kern<<<lgrid, 256, llds, st>>>(la, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), co.offs,
-                                   co.toffs, co.ncl, co.pairs, u1);
-  };
-  if (s.D == 128)
-    go(leaf_score_kernel<128>);
+  return launch_final_topk(s, a1, a1cnt, u1, idx, score, st);
+}
+
+// Split schedule: stage 1 with a workgroup per row, every scored leaf
+// candidate on a workgroup of its own, then the final Top-K.
+struct SplitWs {
+  size_t a1, a1cnt, u1, total;
+};
+
+static SplitWs split_layout(const Shape& s) {
+  const size_t rows = static_cast<size_t>(s.BH()) * s.Nq;
+  SplitWs w{};
+  size_t o = 0;
+  w.a1 = o;     o += align256(rows * s.gK() * 4);
+  w.a1cnt = o;  o += align256(rows * 4);
+  w.u1 = o;     o += align256(rows * s.gK() * 4);
+  w.total = o;
+  return w;
+}
+
+size_t select_split_ws(const Shape& s) { return split_layout(s).total; }
+
+template <typename T, int D>
+static void launch_leaf_slot(const Shape& s, const SelArgs& a, const int32_t* a1, const int32_t* a1cnt, float* u1,
+                             hipStream_t st) {
+  dim3 grid(s.gK(), static_cast<unsigned>(static_cast<int64_t>(s.BH()) * s.Nq));
+  if (s.G == 1)
+    leaf_slot_kernel<T, D, 1><<<grid, 256, 0, st>>>(a, a1, a1cnt, u1);
+  else if (s.G <= 4)
+    leaf_slot_kernel<T, D, 4><<<grid, 256, 0, st>>>(a, a1, a1cnt, u1);
   else
-    go(leaf_score_kernel<64>);
+    leaf_slot_kernel<T, D, 16><<<grid, 256, 0, st>>>(a, a1, a1cnt, u1);
+}
+
+hipError_t launch_select_split(const Shape& s, const Geo& geo, const void* q, const void* k, const float* pyr,
+                               int32_t* idx, float* score, void* ws, hipStream_t st) {
+  const SplitWs w = split_layout(s);
+  char* base = static_cast<char*>(ws);
+  int32_t* a1 = reinterpret_cast<int32_t*>(base + w.a1);
+  int32_t* a1cnt = reinterpret_cast<int32_t*>(base + w.a1cnt);
+  float* u1 = reinterpret_cast<float*>(base + w.u1);
+  hipError_t e;
+  SelArgs a = make_sel_args(s, geo, q, k, pyr);
+  a.a1 = a1;
+  a.a1cnt = a1cnt;
+  {
+    ProfScope ps("select_stage1", st);
+    if (s.gK() <= 64) {
+      dim3 grid(s.Nq, s.BH());
+      const size_t lds = static_cast<size_t>(s.gK()) * s.g * s.G * sizeof(float);
+      auto go = [&](auto tag) {
+        using T = decltype(tag);
+        auto run = [&](auto kern) {
+          if (lds > 60000)  // beyond the default dynamic limit once the static arrays are added
+            hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                static_cast<int>(lds));
+          kern<<<grid, 256, lds, st>>>(a);
+        };
+        if (s.D == 128) {
+          if (s.G == 1) run(stage1_row_kernel<T, 128, 1>);
+          else if (s.G <= 4) run(stage1_row_kernel<T, 128, 4>);
+          else run(stage1_row_kernel<T, 128, 16>);
+        } else {
+          if (s.G == 1) run(stage1_row_kernel<T, 64, 1>);
+          else if (s.G <= 4) run(stage1_row_kernel<T, 64, 4>);
+          else run(stage1_row_kernel<T, 64, 16>);
+        }
+      };
+      if (s.bf16)
+        go(uint16_t{});
+      else
+        go(float{});
+    } else if (s.bf16) {
+      launch_sel_d<uint16_t, 256, false>(s, a, st);
+    } else {
+      launch_sel_d<float, 256, false>(s, a, st);
+    }
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  {
+    ProfScope ps("leaf_score", st);
+    if (s.bf16) {
+      if (s.D == 128)
+        launch_leaf_slot<uint16_t, 128>(s, a, a1, a1cnt, u1, st);
+      else
+        launch_leaf_slot<uint16_t, 64>(s, a, a1, a1cnt, u1, st);
+    } else {
+      if (s.D == 128)
+        launch_leaf_slot<float, 128>(s, a, a1, a1cnt, u1, st);
+      else
+        launch_leaf_slot<float, 64>(s, a, a1, a1cnt, u1, st);
+    }
   }
-
-  // Final Top-K per row.
-  ProfScope ps("final_topk", st);
-  if (narrow) {
-    TopkArgsP ta{s.Nq, s.N, s.C, s.K, s.gK(), s.causal, rows};
-    final_topk_pair_kernel<<<static_cast<unsigned>((rows + 7) / 8), 256, 0, st>>>(ta, a1, a1cnt, u1, idx, score);
-  } else {
-    TopkArgs ta{s.Nq, s.N, s.C, s.K, s.gK(), s.causal, rows};
-    final_topk_kernel<<<static_cast<unsigned>((rows + 3) / 4), 256, 0, st>>>(ta, a1, a1cnt, u1, idx, score);
-  }
-  return hipGetLastError();
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  return launch_final_topk(s, a1, a1cnt, u1, idx, score, st);
 }
 
 }  // namespace pisa

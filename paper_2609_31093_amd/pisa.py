@@ -21,6 +21,7 @@ PISA_DTYPE_BF16 = 1
 PISA_SCHEDULE_AUTO = 0
 PISA_SCHEDULE_TWO_STAGE = 1
 PISA_SCHEDULE_FUSED = 2
+PISA_SCHEDULE_SPLIT = 3
 
 PISA_OK = 0
 PISA_ERR_INVALID_ARG = -1

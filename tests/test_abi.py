@@ -75,6 +75,8 @@ BAD = [
     (dict(fanout=17), pisa.PISA_ERR_UNSUPPORTED),
     (dict(fanout=16, K=17), pisa.PISA_ERR_UNSUPPORTED),
     (dict(H=68, Hkv=2), pisa.PISA_ERR_UNSUPPORTED),
+    (dict(schedule=4), pisa.PISA_ERR_INVALID_ARG),
+    (dict(schedule=-1), pisa.PISA_ERR_INVALID_ARG),
 ]
 
 
@@ -107,8 +109,10 @@ def test_null_and_misaligned_pointers_are_rejected():
     assert lib.pisa_select(None, FAKE, FAKE, FAKE, FAKE, None, None, 0, None) == pisa.PISA_ERR_INVALID_ARG
 
 
-def test_undersized_workspace_is_rejected():
-    p = _good(schedule=pisa.PISA_SCHEDULE_TWO_STAGE)
+@pytest.mark.parametrize("schedule", [pisa.PISA_SCHEDULE_TWO_STAGE, pisa.PISA_SCHEDULE_SPLIT],
+                         ids=["two_stage", "split"])
+def test_undersized_workspace_is_rejected(schedule):
+    p = _good(schedule=schedule)
     need = pisa.pisa_select_workspace_bytes(p)
     assert need > 0
     lib = pisa.library()
@@ -129,3 +133,7 @@ def test_two_stage_needs_bf16():
 def test_status_strings():
     assert pisa.pisa_status_string(0) == "ok"
     assert pisa.pisa_status_string(pisa.PISA_ERR_WORKSPACE) == "workspace too small"
+
+
+def test_fused_schedule_needs_no_workspace():
+    assert pisa.pisa_select_workspace_bytes(_good(schedule=pisa.PISA_SCHEDULE_FUSED)) == 0

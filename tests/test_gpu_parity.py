@@ -49,6 +49,10 @@ SHAPES = {
     "big-budget": (1, 2, 2, 2048, 2048, 64, 32, 2, 64, 1, "f32"),
     "noncausal-f32-ragged": (1, 2, 1, 777, 777, 64, 32, 2, 4, 0, "f32"),
     "c128-g4-gqa": (1, 8, 2, 6000, 6000, 128, 128, 4, 8, 1, "bf16"),
+    # bf16 row counts between the split and the block-centric attention paths
+    "mid-rows-bf16": (1, 4, 2, 1500, 1500, 64, 32, 2, 6, 1, "bf16"),
+    # few rows (split paths) with GQA, C = 128 and no causal mask
+    "split-gqa-c128-noncausal": (1, 8, 2, 700, 5000, 128, 128, 2, 6, 0, "bf16"),
 }
 
 
@@ -86,11 +90,11 @@ def _run_select(shape, schedule, x):
     return idx.cpu().numpy(), sc.cpu().numpy()
 
 
-SCHEDULES = [pisa_s for pisa_s in (2, 1)]
+SCHEDULES = (2, 1, 3)  # fused, two-stage, split
 
 
 @pytest.mark.parametrize("name", list(SHAPES))
-@pytest.mark.parametrize("schedule", SCHEDULES, ids=["fused", "two_stage"])
+@pytest.mark.parametrize("schedule", SCHEDULES, ids=["fused", "two_stage", "split"])
 def test_select_parity(name, schedule):
     shape = SHAPES[name]
     B, H, Hkv, Nq, N, d, C, g, K, causal, dtype = shape
@@ -111,11 +115,12 @@ def test_schedules_agree_on_decisive_rows():
     shape = SHAPES["gqa-ragged-bf16"]
     x = _data(shape, seed=3)
     a, _ = _run_select(shape, 2, x)
-    b, _ = _run_select(shape, 1, x)
     B, H, Hkv, Nq, N, d, C, g, K, causal, dtype = shape
     rows = _rows_sample(Nq, 16, 32)
     _, gap = O.select(x["q"], x["k"], C, g, K, bool(causal), rows=rows)
-    assert not ((a[:, :, rows] != b[:, :, rows]).any(-1) & (gap > 1e-3)).any()
+    for other in (1, 3):
+        b, _ = _run_select(shape, other, x)
+        assert not ((a[:, :, rows] != b[:, :, rows]).any(-1) & (gap > 1e-3)).any(), other
 
 
 @pytest.mark.parametrize("name", list(SHAPES))
