@@ -221,6 +221,40 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
   const int r0 = blk * C;
   const int nkeys = min(C, a.N - r0);
 
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int col = lane & 15;   // query column
+  const int grp = lane >> 4;   // 0..3: k slice of the operands, row group of the results
+  // This wavefront's 16-pair tiles are wave, wave + 4, ... (at most 4 of a
+  // 256-pair tile); iteration it covers tile it / G and query head it % G.
+  // The pair words of all of them are read up front, and the query operand
+  // of the next iteration is gathered while the current one computes.
+  static_assert(kClusterTile == 256, "four 16-pair tiles per wavefront");
+  const int ntile = (end - beg + 15) / 16;
+  const int nmine = ntile > wave ? (ntile - wave + 3) / 4 : 0;
+  const int nit = nmine * a.G;
+  int prw[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int p = beg + (wave + 4 * j) * 16 + col;
+    prw[j] = (j < nmine && p < end) ? pairs[p] : -1;
+  }
+  auto pair_of = [&](int j) { return j == 0 ? prw[0] : j == 1 ? prw[1] : j == 2 ? prw[2] : prw[3]; };
+  auto gather = [&](int it, bf16x8a (&dst)[KS]) {
+    const int j = it / a.G, hh = it - j * a.G;
+    const int pr = pair_of(j);
+    const int row = a.row0 + (pr >= 0 ? (pr >> 8) : 0);
+    const uint16_t* qrow = q + ((static_cast<int64_t>(b) * a.H + h * a.G + hh) * a.Nq + row) * D + grp * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      uint4 u = make_uint4(0, 0, 0, 0);
+      if (pr >= 0) u = *reinterpret_cast<const uint4*>(qrow + ks * 32);
+      dst[ks] = u4_as_bf16x8(u);
+    }
+  };
+  bf16x8a qn[KS];
+  if (nit > 0) gather(0, qn);
+
   const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.N + r0) * D;
   const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.N + r0) * D;
   for (int e = threadIdx.x; e < C * (D / 8); e += 256) {
@@ -244,28 +278,19 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
   }
   __syncthreads();
 
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
-  const int col = lane & 15;   // query column
-  const int grp = lane >> 4;   // 0..3: k slice of the operands, row group of the results
-  const int ntile = (end - beg + 15) / 16;
-  for (int tile = wave; tile < ntile; tile += 4) {
-    const int p = beg + tile * 16 + col;
-    const bool valid = p < end;
-    const int pr = valid ? pairs[p] : 0;
-    const int rr = pr >> 8, slot = pr & 255;
+  for (int it = 0; it < nit; ++it) {
+    bf16x8a qb[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qb[ks] = qn[ks];
+    if (it + 1 < nit) gather(it + 1, qn);
+    const int j = it / a.G, hh = it - j * a.G;
+    const int pr = pair_of(j);
+    const bool valid = pr >= 0;
+    const int rr = valid ? pr >> 8 : 0, slot = pr & 255;
     const int row = a.row0 + rr;
     const int t = a.N - a.Nq + row;
     const int kmax = a.causal ? min(nkeys, t - r0 + 1) : nkeys;
-    for (int hh = 0; hh < a.G; ++hh) {
-      const uint16_t* qrow = q + ((static_cast<int64_t>(b) * a.H + h * a.G + hh) * a.Nq + row) * D + grp * 8;
-      bf16x8a qb[KS];
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        uint4 u = make_uint4(0, 0, 0, 0);
-        if (valid) u = *reinterpret_cast<const uint4*>(qrow + ks * 32);
-        qb[ks] = u4_as_bf16x8(u);
-      }
+    {
       // S^T tile mt holds keys mt*16 + 4*grp + i (i = 0..3) of query `col`.
       auto s_tile = [&](int mt) {
         f32x4a acc = {0.f, 0.f, 0.f, 0.f};
