@@ -17,11 +17,13 @@
  * - Indices are 0-based (the paper counts from 1).
  * - Layouts are contiguous and row-major:
  *     q, o      [B, H,   Nq, d]   (dtype of the problem)
- *     k, v      [B, Hkv, N,  d]   (dtype of the problem)
+ *     k, v      [B, Hkv, Ncap, d] (dtype of the problem; Ncap = N unless
+ *               the problem reserves more rows, see pisa_problem.Ncap)
  *     pyramid   [B, Hkv, R,  d]   float32: summary levels 1 .. max(1, L-1)
- *               concatenated (level 1 = leaf blocks first); R and the level
- *               offsets come from pisa_pyramid_layout().  The root (level L)
- *               is never scored and is not stored.
+ *               concatenated (level 1 = leaf blocks first), each level laid
+ *               out for Ncap tokens; R and the level offsets come from
+ *               pisa_pyramid_layout().  The root (level L) is never scored
+ *               and is not stored.
  *     block_idx [B, Hkv, Nq, K]   int32, ascending, padded with -1
  *     lse       [B, H,   Nq]      float32, natural log
  * - Query row i sits at absolute position t = N - Nq + i (end-aligned), so
@@ -92,6 +94,11 @@ typedef struct {
                         blocks and masked future tokens; 0: plain method    */
   int32_t dtype;     /* pisa_dtype of q, k, v and o                         */
   int32_t schedule;  /* PISA_SCHEDULE_* for pisa_select; ignored elsewhere  */
+  int32_t Ncap;      /* rows reserved per (batch, KV head): k and v are
+                        [B,Hkv,Ncap,d] of which the first N rows are used,
+                        and the pyramid is laid out for Ncap tokens, so a
+                        decode loop grows N in place (App. B decode cache);
+                        0 means N, otherwise N <= Ncap                       */
 } pisa_problem;
 
 /* Number of hierarchy levels L (Sec. 3.2 eq. key_hierarchy: M_1 = ceil(N/C),
@@ -116,6 +123,19 @@ size_t pisa_attn_workspace_bytes(const pisa_problem* p);
  * block's raw keys (the last block may be short), level l+1 = mean of the
  * existing children at level l.  Accumulates in float32; writes `pyramid`. */
 int pisa_build_pyramid(const pisa_problem* p, const void* k, float* pyramid, pisa_stream_t stream);
+
+/* Decode cache update (App. B "decode cache": each new token updates the
+ * mean of its leaf block and of that block's ancestors).  `pyramid` holds
+ * the pyramid of the first n_old keys, as left by pisa_build_pyramid or an
+ * earlier append with the same C, fanout and Ncap; k holds the first p->N
+ * keys.  The leaf blocks containing rows [n_old, N) and all of their
+ * ancestors are recomputed, and levels that did not exist at n_old are
+ * computed whole, with the arithmetic of pisa_build_pyramid: the result
+ * equals a full build at N bit for bit.  0 <= n_old <= N (n_old = 0 rebuilds
+ * every block, on one workgroup per (batch, KV head)); one launch, no
+ * workspace. */
+int pisa_pyramid_append(const pisa_problem* p, const void* k, float* pyramid, int32_t n_old,
+                        pisa_stream_t stream);
 
 /* Pyramid Top-K selection (Sec. 3.2 eqs. hierarchical_topk and
  * direct_child_lse; grouped heads Sec. 3.3 eq. kernel_grouped_score; causal

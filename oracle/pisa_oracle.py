@@ -16,6 +16,9 @@ Contents and the passage each follows:
 * ``build_pyramid``     -- mean pyramid, Sec. 3.2 eq. (mean_pyramid): leaf
                            means of raw keys, then means over the *valid*
                            children one level down.
+* ``pyramid_append``    -- decode-cache update, App. B ("Decode cache"):
+                           per token, the running mean of its leaf and the
+                           ancestor path (pinned against build_pyramid).
 * ``lse``               -- natural-log LogSumExp, max-subtracted.
 * ``select_row``        -- coarse-to-fine Top-K, Sec. 3.2 eq.
                            (hierarchical_topk) with the LSE score of eq.
@@ -95,6 +98,54 @@ def build_pyramid(k: np.ndarray, C: int, g: int) -> list[np.ndarray]:
             cur[i] = below[i * g:min((i + 1) * g, M[lv - 1])].mean(axis=0)
         levels.append(cur)
     return levels
+
+
+def pyramid_append(levels: list[np.ndarray], k: np.ndarray, n_old: int, C: int, g: int) -> list[np.ndarray]:
+    """Decode-cache update (App. B, paragraph "Decode cache"): extend the
+    pyramid of the first n_old keys (``levels`` as from build_pyramid; an
+    empty list when n_old = 0) to all len(k) keys, one token at a time.
+
+    A new token moves the running mean of its leaf block (or opens a new
+    block).  Going up, a parent is the mean of its existing children: when one
+    child moves by delta the parent moves by delta / (number of children);
+    when a child is new the parent becomes prev + (child - prev) / n; a parent
+    that did not exist is created from its first child; and when the top
+    level gains a second node a new root (the mean of the top level) is
+    added.  Returns the new list of levels (same form as build_pyramid).
+    """
+    k = np.asarray(k, dtype=np.float64)
+    rows = [[r.copy() for r in lv] for lv in levels] or [[]]
+    for t in range(n_old, k.shape[0]):
+        c, cnt = divmod(t, C)
+        leaf = rows[0]
+        if cnt == 0:
+            leaf.append(k[t].copy())
+            before = None
+        else:
+            before = leaf[c].copy()
+            leaf[c] = before + (k[t] - before) / (cnt + 1)
+        child, lv = c, 0
+        while True:
+            cur = rows[lv]
+            if lv == len(rows) - 1:          # the top level
+                if len(cur) > 1:             # it outgrew the root: one level more
+                    rows.append([np.mean(np.array(cur[:g]), axis=0)])
+                break
+            parent = child // g
+            n_children = min(g, len(cur) - parent * g)
+            up = rows[lv + 1]
+            if parent == len(up):            # first child of a new parent
+                up.append(cur[child].copy())
+                before = None
+            else:
+                prev = up[parent].copy()
+                if before is None:           # one child more in the mean
+                    up[parent] = prev + (cur[child] - prev) / n_children
+                else:                        # the child's share moved
+                    up[parent] = prev + (cur[child] - before) / n_children
+                before = prev
+            child, lv = parent, lv + 1
+    return [np.array(lv) for lv in rows]
 
 
 def lse(z: np.ndarray) -> float:

@@ -27,21 +27,36 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 // Level sizes of the hierarchy (Sec. 3.2 eq. key_hierarchy).  Returns L or a
 // negative status.
-int compute_geo(int32_t N, int32_t C, int32_t g, pisa::Geo* geo) {
-  if (N < 1 || C < 1 || g < 2) return PISA_ERR_INVALID_ARG;
-  pisa::Geo G{};
-  G.N = N;
-  G.C = C;
-  G.g = g;
-  int64_t m = (static_cast<int64_t>(N) + C - 1) / C;
+// Level sizes of an N-token hierarchy (M[1..L]); returns L or a negative status.
+int level_sizes(int64_t N, int32_t C, int32_t g, int32_t* M) {
+  int64_t m = (N + C - 1) / C;
   int L = 1;
-  G.M[1] = static_cast<int32_t>(m);
+  M[1] = static_cast<int32_t>(m);
   while (m > 1) {
     m = (m + g - 1) / g;
     ++L;
     if (L > pisa::kMaxLevels) return PISA_ERR_UNSUPPORTED;
-    G.M[L] = static_cast<int32_t>(m);
+    M[L] = static_cast<int32_t>(m);
   }
+  return L;
+}
+
+// Geometry of an N-token problem whose pyramid (and k/v rows) are laid out
+// for cap >= N tokens.
+int compute_geo(int32_t N, int32_t C, int32_t g, pisa::Geo* geo, int32_t cap = 0) {
+  if (N < 1 || C < 1 || g < 2) return PISA_ERR_INVALID_ARG;
+  if (cap == 0) cap = N;
+  if (cap < N) return PISA_ERR_INVALID_ARG;
+  pisa::Geo G{};
+  G.N = N;
+  G.Nkv = cap;
+  G.C = C;
+  G.g = g;
+  const int L = level_sizes(N, C, g, G.M);
+  if (L < 0) return L;
+  int32_t Mc[pisa::kMaxLevels + 1] = {};
+  const int Lc = level_sizes(cap, C, g, Mc);
+  if (Lc < 0) return Lc;
   G.L = L;
   G.Lstore = L > 1 ? L - 1 : 1;
   G.lg = -1;
@@ -53,9 +68,12 @@ int compute_geo(int32_t N, int32_t C, int32_t g, pisa::Geo* geo) {
     G.gp[l] = G.gp[l - 1] > (1 << 26) ? (1 << 30) : G.gp[l - 1] * g;
   for (int l = 2; l <= pisa::kMaxLevels; ++l)  // saturate beyond the root
     G.gpow[l] = G.gpow[l - 1] > (int64_t(1) << 40) ? G.gpow[l - 1] : G.gpow[l - 1] * g;
+  // Row offsets of the capacity layout: levels 1 .. max(1, Lc - 1) of a
+  // cap-token hierarchy (which contain the stored levels of N).
+  const int Lcs = Lc > 1 ? Lc - 1 : 1;
   G.off[1] = 0;
-  for (int l = 1; l <= L; ++l) G.off[l + 1] = G.off[l] + (l <= G.Lstore ? G.M[l] : 0);
-  G.R = G.off[G.Lstore + 1];
+  for (int l = 1; l <= pisa::kMaxLevels; ++l) G.off[l + 1] = G.off[l] + (l <= Lcs ? Mc[l] : 0);
+  G.R = G.off[Lcs + 1];
   if (geo) *geo = G;
   return L;
 }
@@ -94,10 +112,13 @@ int check_problem(const pisa_problem* p, pisa::Shape* s, pisa::Geo* geo) {
   if (p->Nq >= (1 << 23)) return fail(PISA_ERR_UNSUPPORTED, "Nq %d exceeds 2^23-1", p->Nq);
   if (static_cast<int64_t>(p->B) * p->Hkv > 65535 || static_cast<int64_t>(p->B) * p->H > 65535)
     return fail(PISA_ERR_UNSUPPORTED, "B*H must be <= 65535");
+  if (p->Ncap != 0 && p->Ncap < p->N)
+    return fail(PISA_ERR_INVALID_ARG, "Ncap (%d) must be 0 or >= N (%d)", p->Ncap, p->N);
   pisa::Geo g{};
-  const int L = compute_geo(p->N, p->C, p->fanout, &g);
+  const int L = compute_geo(p->N, p->C, p->fanout, &g, p->Ncap);
   if (L < 0) return fail(L, "hierarchy too deep");
-  if (g.M[1] > 65535) return fail(PISA_ERR_UNSUPPORTED, "more than 65535 leaf blocks");
+  if ((static_cast<int64_t>(g.Nkv) + p->C - 1) / p->C > 65535)
+    return fail(PISA_ERR_UNSUPPORTED, "more than 65535 leaf blocks");
   if (s) {
     s->B = p->B;
     s->H = p->H;
@@ -110,6 +131,7 @@ int check_problem(const pisa_problem* p, pisa::Shape* s, pisa::Geo* geo) {
     s->g = p->fanout;
     s->K = p->K;
     s->causal = p->causal;
+    s->Nkv = g.Nkv;
     s->bf16 = p->dtype == PISA_DTYPE_BF16;
   }
   if (geo) *geo = g;
@@ -219,6 +241,21 @@ int pisa_build_pyramid(const pisa_problem* p, const void* k, float* pyramid, pis
   return device_status(pisa::launch_build_pyramid(g, s.BH(), s.D, s.bf16, k, pyramid,
                                                   static_cast<hipStream_t>(stream)),
                        "pisa_build_pyramid");
+}
+
+int pisa_pyramid_append(const pisa_problem* p, const void* k, float* pyramid, int32_t n_old, pisa_stream_t stream) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  PISA_TRY(check_problem(p, &s, &g));
+  PISA_TRY(check_ptr(k, "k"));
+  PISA_TRY(check_ptr(pyramid, "pyramid"));
+  if (n_old < 0 || n_old > p->N) return fail(PISA_ERR_INVALID_ARG, "need 0 <= n_old <= N (got %d, N=%d)", n_old, p->N);
+  if (n_old == p->N) return PISA_OK;
+  pisa::Geo g_old{};
+  if (n_old > 0) compute_geo(n_old, p->C, p->fanout, &g_old, g.Nkv);
+  return device_status(pisa::launch_pyramid_append(g, g_old, s.BH(), s.D, s.bf16, k, pyramid, n_old,
+                                                   static_cast<hipStream_t>(stream)),
+                       "pisa_pyramid_append");
 }
 
 int pisa_select(const pisa_problem* p, const void* q, const void* k, const float* pyramid, int32_t* block_idx,

@@ -24,6 +24,7 @@ struct AttnArgs {
   float* lse;
   int H, Hkv, G, Nq, N, C, K, causal;
   float qscale2;
+  int Nkv;  // rows per (batch, KV head) in k and v
 };
 
 template <typename T, int DPL>
@@ -95,8 +96,8 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(AttnArgs a) {
 #pragma unroll
   for (int e = 0; e < DPL; ++e) qv[e] *= a.qscale2;
 
-  const T* kb = static_cast<const T*>(a.k) + static_cast<int64_t>(bh) * a.N * D + sub * DPL;
-  const T* vb = static_cast<const T*>(a.v) + static_cast<int64_t>(bh) * a.N * D + sub * DPL;
+  const T* kb = static_cast<const T*>(a.k) + static_cast<int64_t>(bh) * a.Nkv * D + sub * DPL;
+  const T* vb = static_cast<const T*>(a.v) + static_cast<int64_t>(bh) * a.Nkv * D + sub * DPL;
   const int32_t* sel = a.idx + (static_cast<int64_t>(bh) * a.Nq + row) * a.K;
 
   float m = -INFINITY, s = 0.f, o[DPL];
@@ -188,6 +189,7 @@ struct AttnBlockArgs {
   int H, Hkv, G, Nq, N, C, K, causal, M1;
   int row0, nrows;  // row chunk handled by this launch
   float qscale2;
+  int Nkv;          // rows per (batch, KV head) in k and v
 };
 
 __device__ __forceinline__ bf16x8a u4_as_bf16x8(uint4 r) { return __builtin_bit_cast(bf16x8a, r); }
@@ -255,8 +257,8 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
   bf16x8a qn[KS];
   if (nit > 0) gather(0, qn);
 
-  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.N + r0) * D;
-  const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.N + r0) * D;
+  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
+  const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
   for (int e = threadIdx.x; e < C * (D / 8); e += 256) {
     const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
     uint4 kv = make_uint4(0, 0, 0, 0);
@@ -464,8 +466,8 @@ __global__ __launch_bounds__(256) void attn_slot_kernel(AttnBlockArgs a, const u
   const int kmax = a.causal ? min(nkeys, t - r0 + 1) : nkeys;
   const int tid = threadIdx.x;
 
-  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.N + r0) * D;
-  const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.N + r0) * D;
+  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
+  const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
   for (int e = tid; e < C * (D / 8); e += 256) {
     const int r = e / (D / 8);
     uint4 kv = make_uint4(0, 0, 0, 0), vv = make_uint4(0, 0, 0, 0);
@@ -628,7 +630,7 @@ static hipError_t launch_split_path(const Shape& s, const void* q, const void* k
   uint16_t* part_o = reinterpret_cast<uint16_t*>(base + w.part_o);
   float* part_lse = reinterpret_cast<float*>(base + w.part_lse);
   AttnBlockArgs a{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, 0, 0, s.Nq,
-                  kLog2e / sqrtf(static_cast<float>(s.D))};
+                  kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv};
   const uint16_t* qq = static_cast<const uint16_t*>(q);
   const uint16_t* kk = static_cast<const uint16_t*>(k);
   const uint16_t* vv = static_cast<const uint16_t*>(v);
@@ -671,7 +673,7 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
     ClusterOut co{};
     if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st)) != hipSuccess) return e;
     AttnBlockArgs a{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], row0, nrows,
-                    kLog2e / sqrtf(static_cast<float>(s.D))};
+                    kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv};
     {
       ProfScope ps("attn_block", st);
       dim3 grid(static_cast<unsigned>(cluster_max_tiles(s.BH(), geo.M[1], static_cast<int64_t>(s.BH()) * nrows * s.K)));
@@ -714,7 +716,7 @@ hipError_t launch_attention(const Shape& s, const Geo& geo, const void* q, const
                       : launch_split_path<64>(s, q, k, v, idx, o, lse, ws, st);
   }
   AttnArgs a{q, k, v, idx, o, lse, s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal,
-             kLog2e / sqrtf(static_cast<float>(s.D))};
+             kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv};
   ProfScope ps("attn_rows", st);
   if (s.bf16) {
     if (s.D == 128)

@@ -15,9 +15,11 @@ constexpr float kLn2 = 0.6931471805599453f;
 // Hierarchy geometry of one problem (identical for every batch and KV head).
 // Level l (1-based) has M[l] nodes; node i of level l covers leaf blocks
 // [i*gpow[l], (i+1)*gpow[l]) where gpow[l] = fanout^(l-1); stored levels
-// 1..Lstore start at pyramid row off[l].
+// 1..Lstore start at pyramid row off[l].  Level sizes follow N; the row
+// offsets and R follow the capacity the pyramid is laid out for (>= N).
 struct Geo {
   int32_t N, C, g, L, Lstore;
+  int32_t Nkv;  // rows per (batch, KV head) in k and v (row stride), >= N
   int32_t lg;  // log2(g) when g is a power of two, else -1
   int32_t M[kMaxLevels + 1];
   int32_t gp[kMaxLevels + 1];  // g^(l-1), saturated at 2^30 (exact wherever it matters: <= g*M_1)

@@ -27,6 +27,7 @@ class ProfScope {
 // Problem shape as the kernels see it (validated by the ABI layer).
 struct Shape {
   int B, H, Hkv, G, Nq, N, D, C, g, K, causal;
+  int Nkv;  // rows per (batch, KV head) in k and v (row stride), >= N
   bool bf16;
   int BH() const { return B * Hkv; }
   int gK() const { return g * K; }
@@ -73,6 +74,10 @@ hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* ou
 
 hipError_t launch_build_pyramid(const Geo& geo, int BH, int D, bool bf16, const void* k, float* pyr,
                                 hipStream_t st);
+// Recompute the leaves holding rows [n_old, N), their ancestors, and whole
+// levels absent at n_old (geo_old: the geometry at n_old, same layout).
+hipError_t launch_pyramid_append(const Geo& geo, const Geo& geo_old, int BH, int D, bool bf16, const void* k,
+                                 float* pyr, int n_old, hipStream_t st);
 
 // Fused single-stage selector (all levels, raw leaf keys scored per query).
 hipError_t launch_select_fused(const Shape& s, const Geo& geo, const void* q, const void* k,

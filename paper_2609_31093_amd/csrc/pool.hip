@@ -12,6 +12,58 @@
 
 namespace pisa {
 
+// Mean of leaf block `leaf` (rows [leaf*C, min((leaf+1)*C, N))) computed by
+// one wavefront: 16 lanes cover a key row, the 4 row groups take every 4th
+// row; lanes of row group 0 return the D/16 means of their column slice.
+// Both the full build and the decode-cache update use this, so their leaf
+// means agree bit for bit.
+template <typename T, int D>
+__device__ __forceinline__ void leaf_mean(const T* __restrict__ kb, const Geo& geo, int leaf, int sub, int rg,
+                                          float (&m)[D / 16]) {
+  constexpr int DPL = D / 16;
+  const int64_t row0 = static_cast<int64_t>(leaf) * geo.C;
+  const int nrows = min(geo.C, geo.N - static_cast<int>(row0));
+  float acc[DPL];
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
+  const T* base = kb + row0 * D + sub * DPL;
+  int r = rg;
+  for (; r + 12 < nrows; r += 16) {
+    float x0[DPL], x1[DPL], x2[DPL], x3[DPL];
+    load_row_part<T, DPL>(base + static_cast<int64_t>(r) * D, x0);
+    load_row_part<T, DPL>(base + static_cast<int64_t>(r + 4) * D, x1);
+    load_row_part<T, DPL>(base + static_cast<int64_t>(r + 8) * D, x2);
+    load_row_part<T, DPL>(base + static_cast<int64_t>(r + 12) * D, x3);
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) acc[e] += (x0[e] + x1[e]) + (x2[e] + x3[e]);
+  }
+  for (; r < nrows; r += 4) {
+    float x0[DPL];
+    load_row_part<T, DPL>(base + static_cast<int64_t>(r) * D, x0);
+#pragma unroll
+    for (int e = 0; e < DPL; ++e) acc[e] += x0[e];
+  }
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) {
+    acc[e] += __shfl_xor(acc[e], 16);
+    acc[e] += __shfl_xor(acc[e], 32);
+  }
+  const float inv = 1.0f / static_cast<float>(nrows);
+#pragma unroll
+  for (int e = 0; e < DPL; ++e) m[e] = acc[e] * inv;
+}
+
+// Node `node` of level lv (>= 2): the mean of its existing children, summed
+// in index order; `child(ch, col)` reads column col of child ch.
+template <typename F>
+__device__ __forceinline__ float node_mean(const Geo& geo, int lv, int node, int col, F child) {
+  const int c0 = node * geo.g;
+  const int c1 = min(c0 + geo.g, geo.M[lv - 1]);
+  float s = 0.f;
+  for (int ch = c0; ch < c1; ++ch) s += child(ch, col);
+  return s / static_cast<float>(c1 - c0);
+}
+
 template <typename T, int D>
 __global__ __launch_bounds__(256) void pool_leaf_kernel(const T* __restrict__ k, float* __restrict__ pyr,
                                                         Geo geo, int s_levels, int lpb) {
@@ -23,7 +75,7 @@ __global__ __launch_bounds__(256) void pool_leaf_kernel(const T* __restrict__ k,
   const int bh = blockIdx.y;
   const int leaf0 = blockIdx.x * lpb;
   const int nleaf = min(lpb, geo.M[1] - leaf0);
-  const T* kb = k + static_cast<int64_t>(bh) * geo.N * D;
+  const T* kb = k + static_cast<int64_t>(bh) * geo.Nkv * D;
   float* pb = pyr + static_cast<int64_t>(bh) * geo.R * D;
 
   const int lane = threadIdx.x & 63;
@@ -33,38 +85,9 @@ __global__ __launch_bounds__(256) void pool_leaf_kernel(const T* __restrict__ k,
 
   for (int lf = wave; lf < nleaf; lf += 4) {
     const int leaf = leaf0 + lf;
-    const int64_t row0 = static_cast<int64_t>(leaf) * geo.C;
-    const int nrows = min(geo.C, geo.N - static_cast<int>(row0));
-    float acc[DPL];
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
-    const T* base = kb + row0 * D + sub * DPL;
-    int r = rg;
-    for (; r + 12 < nrows; r += 16) {
-      float x0[DPL], x1[DPL], x2[DPL], x3[DPL];
-      load_row_part<T, DPL>(base + static_cast<int64_t>(r) * D, x0);
-      load_row_part<T, DPL>(base + static_cast<int64_t>(r + 4) * D, x1);
-      load_row_part<T, DPL>(base + static_cast<int64_t>(r + 8) * D, x2);
-      load_row_part<T, DPL>(base + static_cast<int64_t>(r + 12) * D, x3);
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) acc[e] += (x0[e] + x1[e]) + (x2[e] + x3[e]);
-    }
-    for (; r < nrows; r += 4) {
-      float x0[DPL];
-      load_row_part<T, DPL>(base + static_cast<int64_t>(r) * D, x0);
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) acc[e] += x0[e];
-    }
-#pragma unroll
-    for (int e = 0; e < DPL; ++e) {
-      acc[e] += __shfl_xor(acc[e], 16);
-      acc[e] += __shfl_xor(acc[e], 32);
-    }
+    float m[DPL];
+    leaf_mean<T, D>(kb, geo, leaf, sub, rg, m);
     if (rg == 0) {
-      const float inv = 1.0f / static_cast<float>(nrows);
-      float m[DPL];
-#pragma unroll
-      for (int e = 0; e < DPL; ++e) m[e] = acc[e] * inv;
       float* dst = pb + (geo.off[1] + leaf) * D + sub * DPL;
       float* ldst = buf0 + lf * D + sub * DPL;
 #pragma unroll
@@ -82,18 +105,13 @@ __global__ __launch_bounds__(256) void pool_leaf_kernel(const T* __restrict__ k,
   float* src = buf0;
   float* dstb = buf1;
   for (int lv = 2; lv <= top; ++lv) {
-    const int g = geo.g;
     const int first = anc_at(geo, leaf0, lv);  // node index of the run start
     const int below_first = anc_at(geo, leaf0, lv - 1);
     const int nnode = min(lpb / geo.gp[lv], geo.M[lv] - first);
     for (int e = threadIdx.x; e < nnode * D; e += blockDim.x) {
       const int j = e / D, col = e - j * D;
       const int node = first + j;
-      const int c0 = node * g;
-      const int c1 = min(c0 + g, geo.M[lv - 1]);
-      float s = 0.f;
-      for (int ch = c0; ch < c1; ++ch) s += src[(ch - below_first) * D + col];
-      const float mval = s / static_cast<float>(c1 - c0);
+      const float mval = node_mean(geo, lv, node, col, [&](int ch, int cc) { return src[(ch - below_first) * D + cc]; });
       dstb[j * D + col] = mval;
       pb[(geo.off[lv] + node) * D + col] = mval;
     }
@@ -114,14 +132,141 @@ __global__ __launch_bounds__(256) void pool_top_kernel(float* __restrict__ pyr, 
     const int n = geo.M[lv] * D;
     for (int e = threadIdx.x; e < n; e += blockDim.x) {
       const int node = e / D, col = e - node * D;
-      const int c0 = node * geo.g;
-      const int c1 = min(c0 + geo.g, geo.M[lv - 1]);
-      float s = 0.f;
-      for (int ch = c0; ch < c1; ++ch) s += pb[(geo.off[lv - 1] + ch) * D + col];
-      pb[(geo.off[lv] + node) * D + col] = s / static_cast<float>(c1 - c0);
+      pb[(geo.off[lv] + node) * D + col] =
+          node_mean(geo, lv, node, col, [&](int ch, int cc) { return pb[(geo.off[lv - 1] + ch) * D + cc]; });
     }
     __syncthreads();
   }
+}
+
+// Decode-cache update (App. B): one workgroup per (batch, KV head).  The
+// leaf blocks from c_first (the block holding row n_old) to the end are
+// recomputed, then level by level the nodes from the ancestor of c_first to
+// the end of the level (exactly the ancestors of the recomputed leaves), or
+// the whole level where it did not exist at n_old (l > old_lstore).  Same
+// arithmetic as the full build, so the result equals it bit for bit.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void pool_append_kernel(const T* __restrict__ k, float* __restrict__ pyr, Geo geo,
+                                                          int c_first, int old_lstore) {
+  constexpr int DPL = D / 16;
+  const int bh = blockIdx.x;
+  const T* kb = k + static_cast<int64_t>(bh) * geo.Nkv * D;
+  float* pb = pyr + static_cast<int64_t>(bh) * geo.R * D;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int sub = lane & 15, rg = lane >> 4;
+  for (int leaf = c_first + wave; leaf < geo.M[1]; leaf += 4) {
+    float m[DPL];
+    leaf_mean<T, D>(kb, geo, leaf, sub, rg, m);
+    if (rg == 0) {
+      float* dst = pb + (geo.off[1] + leaf) * D + sub * DPL;
+#pragma unroll
+      for (int e = 0; e < DPL; e += 4)
+        *reinterpret_cast<float4*>(dst + e) = make_float4(m[e], m[e + 1], m[e + 2], m[e + 3]);
+    }
+  }
+  __syncthreads();
+  for (int lv = 2; lv <= geo.Lstore; ++lv) {
+    const int first = lv > old_lstore ? 0 : anc_at(geo, c_first, lv);
+    const int n = (geo.M[lv] - first) * D;
+    for (int e = threadIdx.x; e < n; e += blockDim.x) {
+      const int node = first + e / D, col = e % D;
+      pb[(geo.off[lv] + node) * D + col] =
+          node_mean(geo, lv, node, col, [&](int ch, int cc) { return pb[(geo.off[lv - 1] + ch) * D + cc]; });
+    }
+    __syncthreads();
+  }
+}
+
+// The decode case of the update: only the last leaf block changed and no
+// level is new, so the changed nodes are the last node of every level and
+// each one's changed child is its last child.  While wavefront 0 recomputes
+// the leaf mean, the other wavefronts fetch every ancestor's unchanged
+// children into LDS; then thread d walks column d up all levels on its own
+// (children summed in index order, as in the full build), with no barrier
+// and no dependent memory round trip per level.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void pool_append_path_kernel(const T* __restrict__ k, float* __restrict__ pyr,
+                                                               Geo geo) {
+  constexpr int DPL = D / 16;
+  extern __shared__ float lds[];  // [D] changed child, then per level (g - 1) x D siblings
+  float* val = lds;
+  float* sib = lds + D;
+  const int bh = blockIdx.x;
+  const T* kb = k + static_cast<int64_t>(bh) * geo.Nkv * D;
+  float* pb = pyr + static_cast<int64_t>(bh) * geo.R * D;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int g = geo.g;
+  const int leaf = geo.M[1] - 1;
+  if (wave == 0) {
+    const int sub = lane & 15, rg = lane >> 4;
+    float m[DPL];
+    leaf_mean<T, D>(kb, geo, leaf, sub, rg, m);
+    if (rg == 0) {
+      float* dst = pb + (geo.off[1] + leaf) * D + sub * DPL;
+#pragma unroll
+      for (int e = 0; e < DPL; e += 4) {
+        const float4 v4 = make_float4(m[e], m[e + 1], m[e + 2], m[e + 3]);
+        *reinterpret_cast<float4*>(dst + e) = v4;
+        *reinterpret_cast<float4*>(val + sub * DPL + e) = v4;
+      }
+    }
+  } else {
+    // siblings of level lv's last node: children c0 .. M[lv-1]-2 at level lv-1
+    for (int lv = 2; lv <= geo.Lstore; ++lv) {
+      const int c0 = (geo.M[lv] - 1) * g;
+      const int ns = geo.M[lv - 1] - 1 - c0;
+      float* dst = sib + (lv - 2) * (g - 1) * D;
+      for (int e = tid - 64; e < ns * D; e += 192) dst[e] = pb[(geo.off[lv - 1] + c0) * D + e];
+    }
+  }
+  __syncthreads();
+  if (tid < D) {
+    float x = val[tid];
+    for (int lv = 2; lv <= geo.Lstore; ++lv) {
+      const int c0 = (geo.M[lv] - 1) * g;
+      const int ns = geo.M[lv - 1] - 1 - c0;
+      const float* sv = sib + (lv - 2) * (g - 1) * D + tid;
+      float sum = 0.f;
+      for (int j = 0; j < ns; ++j) sum += sv[j * D];
+      sum += x;
+      x = sum / static_cast<float>(ns + 1);
+      pb[(geo.off[lv] + geo.M[lv] - 1) * D + tid] = x;
+    }
+  }
+}
+
+hipError_t launch_pyramid_append(const Geo& geo, const Geo& geo_old, int BH, int D, bool bf16, const void* k,
+                                 float* pyr, int n_old, hipStream_t st) {
+  const int c_first = n_old / geo.C;
+  const int old_lstore = n_old > 0 ? geo_old.Lstore : 0;
+  ProfScope ps("pool_append", st);
+  if (n_old > 0 && c_first == geo.M[1] - 1 && old_lstore == geo.Lstore) {
+    const size_t lds = (static_cast<size_t>(D) + static_cast<size_t>(geo.Lstore) * (geo.g - 1) * D) * sizeof(float);
+    if (bf16) {
+      if (D == 128)
+        pool_append_path_kernel<uint16_t, 128><<<BH, 256, lds, st>>>(static_cast<const uint16_t*>(k), pyr, geo);
+      else
+        pool_append_path_kernel<uint16_t, 64><<<BH, 256, lds, st>>>(static_cast<const uint16_t*>(k), pyr, geo);
+    } else {
+      if (D == 128)
+        pool_append_path_kernel<float, 128><<<BH, 256, lds, st>>>(static_cast<const float*>(k), pyr, geo);
+      else
+        pool_append_path_kernel<float, 64><<<BH, 256, lds, st>>>(static_cast<const float*>(k), pyr, geo);
+    }
+    return hipGetLastError();
+  }
+  if (bf16) {
+    if (D == 128)
+      pool_append_kernel<uint16_t, 128><<<BH, 256, 0, st>>>(static_cast<const uint16_t*>(k), pyr, geo, c_first, old_lstore);
+    else
+      pool_append_kernel<uint16_t, 64><<<BH, 256, 0, st>>>(static_cast<const uint16_t*>(k), pyr, geo, c_first, old_lstore);
+  } else {
+    if (D == 128)
+      pool_append_kernel<float, 128><<<BH, 256, 0, st>>>(static_cast<const float*>(k), pyr, geo, c_first, old_lstore);
+    else
+      pool_append_kernel<float, 64><<<BH, 256, 0, st>>>(static_cast<const float*>(k), pyr, geo, c_first, old_lstore);
+  }
+  return hipGetLastError();
 }
 
 // s = number of coarser levels computed inside pool_leaf_kernel: the largest

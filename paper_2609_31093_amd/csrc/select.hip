@@ -262,7 +262,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
         }
       } else if constexpr (FUSED) {
         // Leaf level: exact LSE over each candidate block's raw keys.
-        const T* kb = static_cast<const T*>(a.k) + static_cast<int64_t>(bh) * geo.N * D + sub * DPL;
+        const T* kb = static_cast<const T*>(a.k) + static_cast<int64_t>(bh) * geo.Nkv * D + sub * DPL;
         for (int ci = wave_in_team; ci < nA; ci += NW) {
           const int node = cand[ci];
           if (fz.is(node)) {
@@ -758,6 +758,7 @@ __device__ __forceinline__ bf16x8v as_bf16x8(uint4 r) {
 struct LeafArgs {
   int H, Hkv, G, Nq, N, C, M1, gK;
   float qscale2;
+  int Nkv;  // rows per (batch, KV head) in k
 };
 
 // One workgroup per tile of up to kClusterTile pairs of one (batch x KV head,
@@ -784,7 +785,7 @@ __global__ __launch_bounds__(256) void leaf_score_kernel(LeafArgs a, const uint1
   const int nrows = min(a.C, a.N - r0);
 
   // Stage the key block (zero rows past the end of the sequence).
-  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.N + r0) * D;
+  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
   for (int e = threadIdx.x; e < a.C * (D / 8); e += 256) {
     const int r = e / (D / 8), cidx = (e - r * (D / 8)) * 8;
     uint4 v = make_uint4(0, 0, 0, 0);
@@ -848,6 +849,7 @@ __global__ __launch_bounds__(256) void leaf_score_kernel(LeafArgs a, const uint1
 struct LeafParentArgs {
   int H, Hkv, G, Nq, N, C, g, M1, M2, gK, K, causal;
   float qscale2;
+  int Nkv;  // rows per (batch, KV head) in k
 };
 
 // Leaf scoring grouped by parent node (g*C <= 128 keys): one workgroup per
@@ -877,7 +879,7 @@ __global__ __launch_bounds__(256) void leaf_parent_kernel(LeafParentArgs a, cons
   const int nkeys = min(a.g * a.C, a.N - r0);      // keys of its existing children
   const int nkt = (nkeys + 31) / 32;
 
-  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.N + r0) * D;
+  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
   for (int e = threadIdx.x; e < nkt * 32 * (D / 8); e += 256) {
     const int r = e / (D / 8), cidx = (e - r * (D / 8)) * 8;
     uint4 v = make_uint4(0, 0, 0, 0);
@@ -1293,7 +1295,7 @@ __global__ __launch_bounds__(256) void leaf_slot_kernel(SelArgs a, const int32_t
   }
   const int r0 = node * geo.C;
   const int nrows = min(geo.C, geo.N - r0);
-  const T* kb = static_cast<const T*>(a.k) + (static_cast<int64_t>(bh) * geo.N + r0) * D + sub * DPL;
+  const T* kb = static_cast<const T*>(a.k) + (static_cast<int64_t>(bh) * geo.Nkv + r0) * D + sub * DPL;
   for (int base = 0; base < nrows; base += 16 * UNR) {
     float x[UNR][DPL];
 #pragma unroll
@@ -1498,7 +1500,7 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
   if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st)) != hipSuccess) return e;
   if (by_parent) {
     LeafParentArgs lp{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.g, geo.M[1], M2, s.gK(), s.K, s.causal,
-                      kLog2e / sqrtf(static_cast<float>(s.D))};
+                      kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv};
     dim3 pgrid(static_cast<unsigned>(cluster_max_tiles(s.BH(), M2, rows * s.gK())));
     const size_t plds = static_cast<size_t>(128) * (s.D + 8) * 2;
     {
@@ -1515,7 +1517,7 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
     if ((e = hipGetLastError()) != hipSuccess) return e;
   } else {
     // Stage 2: leaf scoring against each key block once per cluster.
-    LeafArgs la{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, geo.M[1], s.gK(), kLog2e / sqrtf(static_cast<float>(s.D))};
+    LeafArgs la{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, geo.M[1], s.gK(), kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv};
     dim3 lgrid(static_cast<unsigned>(cluster_max_tiles(s.BH(), geo.M[1], rows * s.gK())));
     const size_t llds = static_cast<size_t>(s.C) * (s.D + 8) * 2;
     {

@@ -32,7 +32,7 @@ PISA_ERR_DEVICE = -4
 EXPORTS = (
     "pisa_num_levels", "pisa_pyramid_layout", "pisa_pyramid_bytes",
     "pisa_select_workspace_bytes", "pisa_bsa_workspace_bytes", "pisa_attn_workspace_bytes",
-    "pisa_build_pyramid", "pisa_select", "pisa_select_flat_bsa", "pisa_sparse_attn_fwd",
+    "pisa_build_pyramid", "pisa_pyramid_append", "pisa_select", "pisa_select_flat_bsa", "pisa_sparse_attn_fwd",
     "pisa_profile_enable", "pisa_profile_report", "pisa_status_string", "pisa_last_error",
 )
 
@@ -46,16 +46,17 @@ class PisaError(RuntimeError):
 class Problem(ctypes.Structure):
     """Mirror of ``pisa_problem``."""
     _fields_ = [(n, ctypes.c_int32) for n in
-                ("B", "H", "Hkv", "Nq", "N", "d", "C", "fanout", "K", "causal", "dtype", "schedule")]
+                ("B", "H", "Hkv", "Nq", "N", "d", "C", "fanout", "K", "causal", "dtype", "schedule", "Ncap")]
 
     def __repr__(self):
         return "Problem(" + ", ".join(f"{n}={getattr(self, n)}" for n, _ in self._fields_) + ")"
 
 
-def make_problem(B, H, Hkv, Nq, N, d, C, fanout, K, causal=1, dtype="bf16", schedule=PISA_SCHEDULE_AUTO):
+def make_problem(B, H, Hkv, Nq, N, d, C, fanout, K, causal=1, dtype="bf16", schedule=PISA_SCHEDULE_AUTO, Ncap=0):
+    """A pisa_problem; Ncap > N reserves rows of k, v and the pyramid for a growing N."""
     dt = {"bf16": PISA_DTYPE_BF16, "f32": PISA_DTYPE_F32,
           torch.bfloat16: PISA_DTYPE_BF16, torch.float32: PISA_DTYPE_F32}[dtype]
-    return Problem(B, H, Hkv, Nq, N, d, C, fanout, K, int(causal), dt, schedule)
+    return Problem(B, H, Hkv, Nq, N, d, C, fanout, K, int(causal), dt, schedule, Ncap)
 
 
 def _load():
@@ -72,6 +73,7 @@ def _load():
         "pisa_bsa_workspace_bytes": (sz, [P]),
         "pisa_attn_workspace_bytes": (sz, [P]),
         "pisa_build_pyramid": (ctypes.c_int, [P, vp, vp, vp]),
+        "pisa_pyramid_append": (ctypes.c_int, [P, vp, vp, i32, vp]),
         "pisa_select": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pisa_select_flat_bsa": (ctypes.c_int, [P, vp, vp, vp, vp, sz, vp]),
         "pisa_sparse_attn_fwd": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
@@ -152,6 +154,11 @@ def pisa_attn_workspace_bytes(p: Problem) -> int:
 def pisa_build_pyramid(p: Problem, k, pyramid, stream=None) -> int:
     return _check(_lib.pisa_build_pyramid(ctypes.byref(p), _ptr(k), _ptr(pyramid), _stream(stream)),
                   "pisa_build_pyramid")
+
+
+def pisa_pyramid_append(p: Problem, k, pyramid, n_old: int, stream=None) -> int:
+    return _check(_lib.pisa_pyramid_append(ctypes.byref(p), _ptr(k), _ptr(pyramid), n_old, _stream(stream)),
+                  "pisa_pyramid_append")
 
 
 def pisa_select(p: Problem, q, k, pyramid, block_idx, block_score=None, ws=None, ws_bytes=0, stream=None) -> int:

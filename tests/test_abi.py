@@ -76,6 +76,7 @@ BAD = [
     (dict(fanout=16, K=17), pisa.PISA_ERR_UNSUPPORTED),
     (dict(H=68, Hkv=2), pisa.PISA_ERR_UNSUPPORTED),
     (dict(schedule=4), pisa.PISA_ERR_INVALID_ARG),
+    (dict(Ncap=1000), pisa.PISA_ERR_INVALID_ARG),
     (dict(schedule=-1), pisa.PISA_ERR_INVALID_ARG),
 ]
 
@@ -137,3 +138,34 @@ def test_status_strings():
 
 def test_fused_schedule_needs_no_workspace():
     assert pisa.pisa_select_workspace_bytes(_good(schedule=pisa.PISA_SCHEDULE_FUSED)) == 0
+
+
+def test_pyramid_append_validates_n_old():
+    p = _good()
+    lib = pisa.library()
+    for bad in (-1, p.N + 1):
+        assert lib.pisa_pyramid_append(ctypes.byref(p), FAKE, FAKE, bad, None) == pisa.PISA_ERR_INVALID_ARG
+        assert "n_old" in pisa.pisa_last_error()
+    assert lib.pisa_pyramid_append(ctypes.byref(p), None, FAKE, 0, None) == pisa.PISA_ERR_INVALID_ARG
+    # n_old == N: nothing to do, nothing launched
+    assert lib.pisa_pyramid_append(ctypes.byref(p), FAKE, FAKE, p.N, None) == pisa.PISA_OK
+
+
+def test_capacity_layout():
+    """With Ncap > N the pyramid is laid out for Ncap tokens; N's levels sit at
+    the capacity offsets and the buffer size follows Ncap."""
+    p = _good(N=1000, Ncap=4096, C=64)
+    q = _good(N=4096, C=64)
+    L = pisa.library()
+    offs = (ctypes.c_int64 * 32)()
+    R = ctypes.c_int64()
+    Lp = L.pisa_pyramid_layout(ctypes.byref(p), offs, ctypes.byref(R))
+    offs_q = (ctypes.c_int64 * 32)()
+    Rq = ctypes.c_int64()
+    Lq = L.pisa_pyramid_layout(ctypes.byref(q), offs_q, ctypes.byref(Rq))
+    assert Lp == 5 and Lq == 7  # 16 and 64 leaf blocks with fanout 2
+    assert R.value == Rq.value == 64 + 32 + 16 + 8 + 4 + 2
+    assert list(offs[:Lp - 1]) == list(offs_q[:Lp - 1]) == [0, 64, 96, 112]
+    assert offs[Lp - 1] == R.value  # the root is not stored
+    assert pisa.pisa_pyramid_bytes(p) == pisa.pisa_pyramid_bytes(q)
+

@@ -399,3 +399,33 @@ def test_exact_ties_prefer_smaller_block_index():
     S1 = levels[0]
     sel, gap = O.flat_bsa_row(q, S1, N - 1, C, 5, True)
     assert sel == sorted({0, c - 1, c, 20, 37}) and gap == 0.0
+
+
+# Decode cache (App. B): the per-token incremental rule must land on the
+# direct definition of the pyramid (eq. mean_pyramid) at every length,
+# including new blocks, new parents, ragged tails and a growing root.
+@pytest.mark.parametrize("N,n_old,C,g", [
+    (1, 0, 4, 2), (37, 0, 4, 2), (64, 1, 8, 2), (100, 31, 8, 2), (100, 32, 8, 2), (130, 63, 4, 3),
+    (300, 299, 8, 4), (513, 200, 16, 2), (257, 0, 4, 2),
+])
+def test_pyramid_append_equals_rebuild(N, n_old, C, g):
+    r = np.random.default_rng(N * 7 + n_old)
+    k = r.standard_normal((N, 5))
+    start = O.build_pyramid(k[:n_old], C, g) if n_old else []
+    got = O.pyramid_append(start, k, n_old, C, g)
+    want = O.build_pyramid(k, C, g)
+    assert [x.shape for x in got] == [x.shape for x in want]
+    for a, b in zip(got, want):
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+
+
+def test_pyramid_append_in_steps_equals_one_append():
+    r = np.random.default_rng(5)
+    k = r.standard_normal((200, 3))
+    lv, n = O.build_pyramid(k[:10], 8, 2), 10
+    for n_new in (11, 16, 17, 63, 64, 65, 199, 200):
+        lv, n = O.pyramid_append(lv, k[:n_new], n, 8, 2), n_new
+    want = O.build_pyramid(k, 8, 2)
+    for a, b in zip(lv, want):
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+
