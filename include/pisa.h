@@ -81,6 +81,16 @@ enum {
                                   over the whole GPU */
 };
 
+/* Block scores of pisa_select (pisa_problem.score): for one candidate and
+ * query head with child logits z_1..z_m (child summaries above the leaf
+ * level, raw keys at it), summed over the group's query heads. */
+enum {
+  PISA_SCORE_LSE = 0,      /* PISA, eq. direct_child_lse: log sum_j exp(z_j) */
+  PISA_SCORE_MEAN = 1,     /* PISA-1, App. A: the mean of the z_j             */
+  PISA_SCORE_MEAN_VAR = 2  /* PISA-2, App. A: the mean plus half the
+                              population variance of the z_j                   */
+};
+
 /* The problem statement of Sec. 3.1-3.2: q/k/v, N, head dim d, block size C,
  * fan-out g (the paper fixes g = 2; any 2..16 is accepted), budget K. */
 typedef struct {
@@ -99,6 +109,8 @@ typedef struct {
                         and the pyramid is laid out for Ncap tokens, so a
                         decode loop grows N in place (App. B decode cache);
                         0 means N, otherwise N <= Ncap                       */
+  int32_t score;     /* PISA_SCORE_* reducer of pisa_select (ignored by flat
+                        BSA and everywhere else)                            */
 } pisa_problem;
 
 /* Number of hierarchy levels L (Sec. 3.2 eq. key_hierarchy: M_1 = ceil(N/C),

@@ -1,5 +1,5 @@
 """CPU oracle of the PISA hot path (test infrastructure; see pisa_oracle)."""
 from .pisa_oracle import (  # noqa: F401
-    level_sizes, build_pyramid, pyramid_append, lse, forced_leaves, select_row, attention_row,
+    level_sizes, build_pyramid, pyramid_append, lse, score_mean, score_mean_var, SCORES, forced_leaves, select_row, attention_row,
     flat_bsa_row, pyramid_rows, pyramid, select, sparse_attention, select_flat_bsa,
 )

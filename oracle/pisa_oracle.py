@@ -20,6 +20,8 @@ Contents and the passage each follows:
                            per token, the running mean of its leaf and the
                            ancestor path (pinned against build_pyramid).
 * ``lse``               -- natural-log LogSumExp, max-subtracted.
+* ``score_mean``, ``score_mean_var`` -- the PISA-1 / PISA-2 block scores,
+                           App. A "First- and second-order approximations".
 * ``select_row``        -- coarse-to-fine Top-K, Sec. 3.2 eq.
                            (hierarchical_topk) with the LSE score of eq.
                            (direct_child_lse), the grouped-head sum of
@@ -159,6 +161,23 @@ def lse(z: np.ndarray) -> float:
     return m + math.log(float(np.exp(z - m).sum()))
 
 
+def score_mean(z: np.ndarray) -> float:
+    """PISA-1 block score (App. A, first-order truncation): the mean logit."""
+    z = np.asarray(z, dtype=np.float64)
+    return float(z.sum() / z.size)
+
+
+def score_mean_var(z: np.ndarray) -> float:
+    """PISA-2 block score (App. A, second-order truncation): the mean logit
+    plus half the population variance (denominator m)."""
+    z = np.asarray(z, dtype=np.float64)
+    mean = z.sum() / z.size
+    return float(mean + 0.5 * ((z - mean) ** 2).sum() / z.size)
+
+
+SCORES = {"lse": lse, "mean": score_mean, "mean_var": score_mean_var}
+
+
 def forced_leaves(t: int, C: int, causal: bool) -> set[int]:
     """First, previous and current leaf block of position t (App. B); empty if not causal."""
     if not causal:
@@ -171,7 +190,7 @@ def forced_leaves(t: int, C: int, causal: bool) -> set[int]:
 
 
 def select_row(qg: np.ndarray, k: np.ndarray, levels: list[np.ndarray], t: int,
-               C: int, g: int, K: int, causal: bool, trace: list | None = None):
+               C: int, g: int, K: int, causal: bool, trace: list | None = None, score: str = "lse"):
     """Pyramid Top-K selection for one query position and one KV head.
 
     qg: [G, d] the query vectors of the G heads that share this KV head.
@@ -183,7 +202,9 @@ def select_row(qg: np.ndarray, k: np.ndarray, levels: list[np.ndarray], t: int,
     smallest margin, over all ranked levels, between the lowest kept score
     and the highest dropped score (+inf if no level needed ranking).  If
     ``trace`` is a list, one dict per level is appended with the candidate
-    set A, forced set F, kept set I and the scores u.
+    set A, forced set F, kept set I and the scores u.  ``score`` names the
+    per-head block score: "lse" (PISA), "mean" (PISA-1) or "mean_var"
+    (PISA-2, App. A); the group's per-head scores are summed in every case.
 
     Steps (Sec. 3.2 eq. hierarchical_topk, eq. direct_child_lse; Sec. 3.3
     eq. kernel_grouped_score; App. B):
@@ -202,6 +223,7 @@ def select_row(qg: np.ndarray, k: np.ndarray, levels: list[np.ndarray], t: int,
     L = len(M)
     scale = 1.0 / math.sqrt(d)
     f_leaf = forced_leaves(t, C, causal)
+    reduce = SCORES[score]
 
     def span(lv: int) -> int:
         return C * g ** (lv - 1)
@@ -227,7 +249,7 @@ def select_row(qg: np.ndarray, k: np.ndarray, levels: list[np.ndarray], t: int,
                     x = levels[lv - 2][list(children(lv, i))]
                 else:
                     x = k[i * C:min((i + 1) * C, N)]
-                u[i] = sum(lse(x @ qh * scale) for qh in qg)
+                u[i] = sum(reduce(x @ qh * scale) for qh in qg)
             ranked = sorted(free, key=lambda i: (-u[i], i))
             n_keep = K - len(F)
             keep, drop = ranked[:n_keep], ranked[n_keep:]
@@ -331,7 +353,7 @@ def pyramid(k: np.ndarray, C: int, g: int) -> np.ndarray:
     return out
 
 
-def select(q, k, C, g, K, causal, rows=None, heads=None):
+def select(q, k, C, g, K, causal, rows=None, heads=None, score="lse"):
     """Selection for rows of every (batch, KV head).
 
     q: [B, H, Nq, d], k: [B, Hkv, N, d].  rows: iterable of query-row indices
@@ -352,7 +374,7 @@ def select(q, k, C, g, K, causal, rows=None, heads=None):
             for ri, r in enumerate(rows):
                 t = N - Nq + r
                 qg = q[b, h * G:(h + 1) * G, r]
-                sel, gp = select_row(qg, kh, levels, t, C, g, K, causal)
+                sel, gp = select_row(qg, kh, levels, t, C, g, K, causal, score=score)
                 idx[b, hi, ri, :len(sel)] = sel
                 gap[b, hi, ri] = gp
     return idx, gap

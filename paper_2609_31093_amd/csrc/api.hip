@@ -112,6 +112,8 @@ int check_problem(const pisa_problem* p, pisa::Shape* s, pisa::Geo* geo) {
   if (p->Nq >= (1 << 23)) return fail(PISA_ERR_UNSUPPORTED, "Nq %d exceeds 2^23-1", p->Nq);
   if (static_cast<int64_t>(p->B) * p->Hkv > 65535 || static_cast<int64_t>(p->B) * p->H > 65535)
     return fail(PISA_ERR_UNSUPPORTED, "B*H must be <= 65535");
+  if (p->score < PISA_SCORE_LSE || p->score > PISA_SCORE_MEAN_VAR)
+    return fail(PISA_ERR_INVALID_ARG, "unknown score %d", p->score);
   if (p->Ncap != 0 && p->Ncap < p->N)
     return fail(PISA_ERR_INVALID_ARG, "Ncap (%d) must be 0 or >= N (%d)", p->Ncap, p->N);
   pisa::Geo g{};
@@ -132,6 +134,7 @@ int check_problem(const pisa_problem* p, pisa::Shape* s, pisa::Geo* geo) {
     s->K = p->K;
     s->causal = p->causal;
     s->Nkv = g.Nkv;
+    s->score = p->score;
     s->bf16 = p->dtype == PISA_DTYPE_BF16;
   }
   if (geo) *geo = g;

@@ -27,7 +27,8 @@ class ProfScope {
 // Problem shape as the kernels see it (validated by the ABI layer).
 struct Shape {
   int B, H, Hkv, G, Nq, N, D, C, g, K, causal;
-  int Nkv;  // rows per (batch, KV head) in k and v (row stride), >= N
+  int Nkv;    // rows per (batch, KV head) in k and v (row stride), >= N
+  int score;  // PISA_SCORE_* reducer of the selection
   bool bf16;
   int BH() const { return B * Hkv; }
   int gK() const { return g * K; }

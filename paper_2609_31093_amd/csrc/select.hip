@@ -41,6 +41,7 @@ struct SelArgs {
   int32_t* a1;      // stage 1: [BH, Nq, gK]
   int32_t* a1cnt;   // stage 1: [BH, Nq]
   int H, Hkv, G, Nq, K, causal, gK;
+  int score_kind;   // kScoreLse / kScoreMean / kScoreMeanVar
   float qscale2;    // log2(e) / sqrt(d)
 };
 
@@ -121,6 +122,110 @@ __device__ __forceinline__ void lse_merge(float& m, float& s, float m2, float s2
   }
   s = s * fast_exp2(m - mn) + s2 * fast_exp2(m2 - mn);
   m = mn;
+}
+
+// ----------------------------------------------------------------------------
+// Score reducers over the logits of one candidate and query head (log2 units):
+// the LSE of eq. direct_child_lse (PISA) and its first- and second-order
+// truncations of App. A "First- and second-order approximations": the mean
+// (PISA-1) and the mean plus half the population variance (PISA-2; ln 2
+// rescales the variance of log2-unit logits so that the score is the natural-
+// log one times log2(e), which ranks identically).
+// ----------------------------------------------------------------------------
+constexpr int kScoreLse = 0, kScoreMean = 1, kScoreMeanVar = 2;
+
+// LSE: (max, sum of 2^(v - max)); moments: (count, mean, sum of squared
+// deviations from the mean).
+struct ScoreAcc {
+  float x, y, z;
+};
+
+__device__ __forceinline__ ScoreAcc acc_empty(int kind) {
+  return kind == kScoreLse ? ScoreAcc{-INFINITY, 0.f, 0.f} : ScoreAcc{0.f, 0.f, 0.f};
+}
+
+// Merge two states (the moments by Chan et al.'s pairwise update).
+__device__ __forceinline__ void acc_merge(int kind, ScoreAcc& a, const ScoreAcc& b) {
+  if (kind == kScoreLse) {
+    lse_merge(a.x, a.y, b.x, b.y);
+    return;
+  }
+  if (b.x == 0.f) return;
+  if (a.x == 0.f) {
+    a = b;
+    return;
+  }
+  const float n = a.x + b.x;
+  const float d = b.y - a.y;
+  a.y += d * (b.x / n);
+  a.z += b.z + d * d * (a.x * b.x / n);
+  a.x = n;
+}
+
+__device__ __forceinline__ void acc_push(int kind, ScoreAcc& a, float v) {
+  acc_merge(kind, a, kind == kScoreLse ? ScoreAcc{v, 1.f, 0.f} : ScoreAcc{1.f, v, 0.f});
+}
+
+// State of NV register values; -inf marks an absent value.
+template <int NV>
+__device__ __forceinline__ ScoreAcc acc_of(int kind, const float (&v)[NV]) {
+  if (kind == kScoreLse) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) m = fmaxf(m, v[i]);
+    if (m == -INFINITY) return ScoreAcc{-INFINITY, 0.f, 0.f};
+    float sm = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) sm += fast_exp2(v[i] - m);
+    return ScoreAcc{m, sm, 0.f};
+  }
+  float n = 0.f, sum = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const bool ok = v[i] != -INFINITY;
+    n += ok ? 1.f : 0.f;
+    sum += ok ? v[i] : 0.f;
+  }
+  if (n == 0.f) return ScoreAcc{0.f, 0.f, 0.f};
+  const float mean = sum / n;
+  float m2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < NV; ++i) {
+    const float dv = v[i] - mean;
+    m2 += v[i] != -INFINITY ? dv * dv : 0.f;
+  }
+  return ScoreAcc{n, mean, m2};
+}
+
+__device__ __forceinline__ ScoreAcc acc_shfl_xor(const ScoreAcc& a, int mask) {
+  return ScoreAcc{__shfl_xor(a.x, mask), __shfl_xor(a.y, mask), __shfl_xor(a.z, mask)};
+}
+
+__device__ __forceinline__ float acc_value(int kind, const ScoreAcc& a) {
+  if (kind == kScoreLse) return a.x + fast_log2(a.y);
+  if (kind == kScoreMean) return a.y;
+  return a.y + 0.5f * kLn2 * (a.z / a.x);
+}
+
+// Score of the n >= 1 logits z[0], z[stride], ... (two passes).
+__device__ __forceinline__ float reduce_logits(int kind, const float* z, int n, int stride) {
+  if (kind == kScoreLse) {
+    float m = -INFINITY;
+    for (int j = 0; j < n; ++j) m = fmaxf(m, z[j * stride]);
+    float sm = 0.f;
+    for (int j = 0; j < n; ++j) sm += fast_exp2(z[j * stride] - m);
+    return m + fast_log2(sm);
+  }
+  float sum = 0.f;
+  for (int j = 0; j < n; ++j) sum += z[j * stride];
+  const float mean = sum / static_cast<float>(n);
+  if (kind == kScoreMean) return mean;
+  float m2 = 0.f;
+  for (int j = 0; j < n; ++j) {
+    const float dv = z[j * stride] - mean;
+    m2 += dv * dv;
+  }
+  return mean + 0.5f * kLn2 * (m2 / static_cast<float>(n));
 }
 
 template <typename T, int D, int TEAM, int GMAX, bool FUSED>
@@ -251,11 +356,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
                 for (int j = 0; j < nch - 1; ++j) others += zc[j * G];
                 zc[(nch - 1) * G] = static_cast<float>(nch) * zself[ci * G + hh] - others;
               }
-              float m = -INFINITY;
-              for (int j = 0; j < nch; ++j) m = fmaxf(m, zc[j * G]);
-              float s = 0.f;
-              for (int j = 0; j < nch; ++j) s += fast_exp2(zc[j * G] - m);
-              u += m + fast_log2(s);
+              u += reduce_logits(a.score_kind, zc, nch, G);
             }
           }
           score[ci] = u;
@@ -271,12 +372,9 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
           }
           const int r0 = node * geo.C;
           const int nrows = min(geo.C, geo.N - r0);
-          float m[GMAX], s[GMAX];
+          ScoreAcc st[GMAX];
 #pragma unroll
-          for (int hh = 0; hh < GMAX; ++hh) {
-            m[hh] = -INFINITY;
-            s[hh] = 0.f;
-          }
+          for (int hh = 0; hh < GMAX; ++hh) st[hh] = acc_empty(a.score_kind);
           for (int r = grp_in_wave; r < nrows; r += 4) {
             float x[DPL];
             load_row_part<T, DPL>(kb + static_cast<int64_t>(r0 + r) * D, x);
@@ -287,9 +385,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
 #pragma unroll
                 for (int e = 0; e < DPL; ++e) d0 = fmaf(qv[hh][e], x[e], d0);
                 d0 = sum16(d0);
-                const float mn = fmaxf(m[hh], d0);
-                s[hh] = s[hh] * fast_exp2(m[hh] - mn) + fast_exp2(d0 - mn);
-                m[hh] = mn;
+                acc_push(a.score_kind, st[hh], d0);
               }
             }
           }
@@ -297,12 +393,9 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
 #pragma unroll
           for (int hh = 0; hh < GMAX; ++hh) {
             if (hh < G) {
-              float m2 = __shfl_xor(m[hh], 16), s2 = __shfl_xor(s[hh], 16);
-              lse_merge(m[hh], s[hh], m2, s2);
-              m2 = __shfl_xor(m[hh], 32);
-              s2 = __shfl_xor(s[hh], 32);
-              lse_merge(m[hh], s[hh], m2, s2);
-              u += m[hh] + fast_log2(s[hh]);
+              acc_merge(a.score_kind, st[hh], acc_shfl_xor(st[hh], 16));
+              acc_merge(a.score_kind, st[hh], acc_shfl_xor(st[hh], 32));
+              u += acc_value(a.score_kind, st[hh]);
             }
           }
           if (lane == 0) score[ci] = u;
@@ -632,11 +725,7 @@ __global__ __launch_bounds__(256) void stage1_pair_kernel(SelArgs a, int row_wor
               for (int j = 0; j < nch - 1; ++j) others += zc[j * G];
               zc[(nch - 1) * G] = static_cast<float>(nch) * zs[hh] - others;
             }
-            float m = -INFINITY;
-            for (int j = 0; j < nch; ++j) m = fmaxf(m, zc[j * G]);
-            float ssum = 0.f;
-            for (int j = 0; j < nch; ++j) ssum += fast_exp2(zc[j * G] - m);
-            u += m + fast_log2(ssum);
+            u += reduce_logits(a.score_kind, zc, nch, G);
           }
         }
         key = u;
@@ -765,7 +854,7 @@ struct LeafArgs {
 // leaf block) cluster: the C x D key block is staged in LDS (rows padded by
 // 16 B against bank conflicts) and the tile's (query, slot) pairs are scored
 // against it, 32 pairs per wavefront MFMA tile.
-template <int D>
+template <int D, int KIND>
 __global__ __launch_bounds__(256) void leaf_score_kernel(LeafArgs a, const uint16_t* __restrict__ q,
                                                          const uint16_t* __restrict__ k,
                                                          const int32_t* __restrict__ offs,
@@ -814,7 +903,7 @@ __global__ __launch_bounds__(256) void leaf_score_kernel(LeafArgs a, const uint1
         if (valid) v = *reinterpret_cast<const uint4*>(qrow + ks * 16);
         qb[ks] = as_bf16x8(v);
       }
-      float m = -INFINITY, s = 0.f;
+      ScoreAcc st = acc_empty(KIND);
       for (int kt = 0; kt < a.C / 32; ++kt) {
         f32x16v acc;
 #pragma unroll
@@ -825,22 +914,18 @@ __global__ __launch_bounds__(256) void leaf_score_kernel(LeafArgs a, const uint1
           const bf16x8v av = as_bf16x8(*reinterpret_cast<const uint4*>(arow + ks * 16));
           acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qb[ks], acc, 0, 0, 0);
         }
-        // acc[r] is the logit of key kt*32 + 8*(r/4) + 4*half + r%4 for query `col`.
-        float tm = -INFINITY;
+        // acc[r] is the logit of key kt*32 + 8*(r/4) + 4*half + r%4 for query `col`
+        // (-inf past the end of the sequence; a tile may hold no key at all).
+        float zv[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          acc[r] = key < nrows ? acc[r] * a.qscale2 : -INFINITY;
-          tm = fmaxf(tm, acc[r]);
+          zv[r] = key < nrows ? acc[r] * a.qscale2 : -INFINITY;
         }
-        float ts = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) ts += fast_exp2(acc[r] - tm);
-        lse_merge(m, s, tm, ts);
+        acc_merge(KIND, st, acc_of(KIND, zv));
       }
-      const float m2 = __shfl_xor(m, 32), s2 = __shfl_xor(s, 32);
-      lse_merge(m, s, m2, s2);
-      u += m + fast_log2(s);
+      acc_merge(KIND, st, acc_shfl_xor(st, 32));
+      u += acc_value(KIND, st);
     }
     if (valid && half == 0) u1[(static_cast<int64_t>(bh) * a.Nq + row) * a.gK + slot] = u;
   }
@@ -857,7 +942,7 @@ struct LeafParentArgs {
 // the parent's children key blocks are staged in LDS together and each query
 // row is gathered once for all of them; every 32-key MFMA tile belongs to
 // one child, whose LSE is accumulated separately.
-template <int D>
+template <int D, int KIND>
 __global__ __launch_bounds__(256) void leaf_parent_kernel(LeafParentArgs a, const uint16_t* __restrict__ q,
                                                           const uint16_t* __restrict__ k,
                                                           const int32_t* __restrict__ a1,
@@ -909,12 +994,9 @@ __global__ __launch_bounds__(256) void leaf_parent_kernel(LeafParentArgs a, cons
         if (valid) v = *reinterpret_cast<const uint4*>(qrow + ks * 16);
         qb[ks] = as_bf16x8(v);
       }
-      float mc[4], sc[4];
+      ScoreAcc stc[4];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        mc[j] = -INFINITY;
-        sc[j] = 0.f;
-      }
+      for (int j = 0; j < 4; ++j) stc[j] = acc_empty(KIND);
 #pragma unroll
       for (int kt = 0; kt < 4; ++kt) {
         if (kt >= nkt) break;
@@ -927,26 +1009,22 @@ __global__ __launch_bounds__(256) void leaf_parent_kernel(LeafParentArgs a, cons
           const bf16x8v av = as_bf16x8(*reinterpret_cast<const uint4*>(arow + ks * 16));
           acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qb[ks], acc, 0, 0, 0);
         }
-        float tm = -INFINITY;
+        float zv[16];
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          acc[r] = key < nkeys ? acc[r] * a.qscale2 : -INFINITY;
-          tm = fmaxf(tm, acc[r]);
+          zv[r] = key < nkeys ? acc[r] * a.qscale2 : -INFINITY;
         }
-        float ts = 0.f;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) ts += fast_exp2(acc[r] - tm);
+        const ScoreAcc ts = acc_of(KIND, zv);
         const int j = kt / kt_per_child;
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj)
-          if (jj == j) lse_merge(mc[jj], sc[jj], tm, ts);
+          if (jj == j) acc_merge(KIND, stc[jj], ts);
       }
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const float m2 = __shfl_xor(mc[j], 32), s2 = __shfl_xor(sc[j], 32);
-        lse_merge(mc[j], sc[j], m2, s2);
-        uc[j] += mc[j] + fast_log2(sc[j]);
+        acc_merge(KIND, stc[j], acc_shfl_xor(stc[j], 32));
+        uc[j] += acc_value(KIND, stc[j]);
       }
     }
     if (valid && half == 0) {
@@ -1206,12 +1284,7 @@ __global__ __launch_bounds__(256) void stage1_row_kernel(SelArgs a) {
         const int nch = min(g, Mb - node * g);
         float u = 0.f;
         for (int hh = 0; hh < G; ++hh) {
-          const float* zc = s_z + lane * g * G + hh;
-          float m = -INFINITY;
-          for (int j = 0; j < nch; ++j) m = fmaxf(m, zc[j * G]);
-          float sm = 0.f;
-          for (int j = 0; j < nch; ++j) sm += fast_exp2(zc[j * G] - m);
-          u += m + fast_log2(sm);
+          u += reduce_logits(a.score_kind, s_z + lane * g * G + hh, nch, G);
         }
         key = u;
       }
@@ -1327,15 +1400,11 @@ __global__ __launch_bounds__(256) void leaf_slot_kernel(SelArgs a, const int32_t
   // LSE per head: wave w takes heads w, w + 4, ...
   const int wave = tid >> 6, lane = tid & 63;
   for (int hh = wave; hh < G; hh += 4) {
-    float m = -INFINITY;
-    for (int r = lane; r < nrows; r += 64) m = fmaxf(m, z[r * G + hh]);
+    ScoreAcc st = acc_empty(a.score_kind);
+    for (int r = lane; r < nrows; r += 64) acc_push(a.score_kind, st, z[r * G + hh]);
 #pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) m = fmaxf(m, __shfl_xor(m, o));
-    float sm = 0.f;
-    for (int r = lane; r < nrows; r += 64) sm += fast_exp2(z[r * G + hh] - m);
-#pragma unroll
-    for (int o = 32; o >= 1; o >>= 1) sm += __shfl_xor(sm, o);
-    if (lane == 0) lse_h[hh] = m + fast_log2(sm);
+    for (int o = 32; o >= 1; o >>= 1) acc_merge(a.score_kind, st, acc_shfl_xor(st, o));
+    if (lane == 0) lse_h[hh] = acc_value(a.score_kind, st);
   }
   __syncthreads();
   if (tid == 0) {
@@ -1369,6 +1438,7 @@ static SelArgs make_sel_args(const Shape& s, const Geo& geo, const void* q, cons
   a.causal = s.causal;
   a.gK = s.gK();
   a.qscale2 = kLog2e / sqrtf(static_cast<float>(s.D));
+  a.score_kind = s.score;
   return a;
 }
 
@@ -1505,14 +1575,19 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
     const size_t plds = static_cast<size_t>(128) * (s.D + 8) * 2;
     {
       ProfScope ps("leaf_score", st);
-      if (s.D == 128)
-        leaf_parent_kernel<128><<<pgrid, 256, plds, st>>>(lp, static_cast<const uint16_t*>(q),
-                                                          static_cast<const uint16_t*>(k), a1, a1cnt, co.offs,
-                                                          co.toffs, co.ncl, co.pairs, u1);
-      else
-        leaf_parent_kernel<64><<<pgrid, 256, plds, st>>>(lp, static_cast<const uint16_t*>(q),
-                                                         static_cast<const uint16_t*>(k), a1, a1cnt, co.offs,
-                                                         co.toffs, co.ncl, co.pairs, u1);
+      auto go = [&](auto kern) {
+        kern<<<pgrid, 256, plds, st>>>(lp, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), a1,
+                                       a1cnt, co.offs, co.toffs, co.ncl, co.pairs, u1);
+      };
+      if (s.D == 128) {
+        if (s.score == kScoreLse) go(leaf_parent_kernel<128, kScoreLse>);
+        else if (s.score == kScoreMean) go(leaf_parent_kernel<128, kScoreMean>);
+        else go(leaf_parent_kernel<128, kScoreMeanVar>);
+      } else {
+        if (s.score == kScoreLse) go(leaf_parent_kernel<64, kScoreLse>);
+        else if (s.score == kScoreMean) go(leaf_parent_kernel<64, kScoreMean>);
+        else go(leaf_parent_kernel<64, kScoreMeanVar>);
+      }
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   } else {
@@ -1528,10 +1603,15 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
         kern<<<lgrid, 256, llds, st>>>(la, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                                        co.offs, co.toffs, co.ncl, co.pairs, u1);
       };
-      if (s.D == 128)
-        go(leaf_score_kernel<128>);
-      else
-        go(leaf_score_kernel<64>);
+      if (s.D == 128) {
+        if (s.score == kScoreLse) go(leaf_score_kernel<128, kScoreLse>);
+        else if (s.score == kScoreMean) go(leaf_score_kernel<128, kScoreMean>);
+        else go(leaf_score_kernel<128, kScoreMeanVar>);
+      } else {
+        if (s.score == kScoreLse) go(leaf_score_kernel<64, kScoreLse>);
+        else if (s.score == kScoreMean) go(leaf_score_kernel<64, kScoreMean>);
+        else go(leaf_score_kernel<64, kScoreMeanVar>);
+      }
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }

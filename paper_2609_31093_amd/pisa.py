@@ -22,6 +22,9 @@ PISA_SCHEDULE_AUTO = 0
 PISA_SCHEDULE_TWO_STAGE = 1
 PISA_SCHEDULE_FUSED = 2
 PISA_SCHEDULE_SPLIT = 3
+PISA_SCORE_LSE = 0
+PISA_SCORE_MEAN = 1
+PISA_SCORE_MEAN_VAR = 2
 
 PISA_OK = 0
 PISA_ERR_INVALID_ARG = -1
@@ -46,17 +49,20 @@ class PisaError(RuntimeError):
 class Problem(ctypes.Structure):
     """Mirror of ``pisa_problem``."""
     _fields_ = [(n, ctypes.c_int32) for n in
-                ("B", "H", "Hkv", "Nq", "N", "d", "C", "fanout", "K", "causal", "dtype", "schedule", "Ncap")]
+                ("B", "H", "Hkv", "Nq", "N", "d", "C", "fanout", "K", "causal", "dtype", "schedule", "Ncap",
+                 "score")]
 
     def __repr__(self):
         return "Problem(" + ", ".join(f"{n}={getattr(self, n)}" for n, _ in self._fields_) + ")"
 
 
-def make_problem(B, H, Hkv, Nq, N, d, C, fanout, K, causal=1, dtype="bf16", schedule=PISA_SCHEDULE_AUTO, Ncap=0):
-    """A pisa_problem; Ncap > N reserves rows of k, v and the pyramid for a growing N."""
+def make_problem(B, H, Hkv, Nq, N, d, C, fanout, K, causal=1, dtype="bf16", schedule=PISA_SCHEDULE_AUTO, Ncap=0,
+                 score=0):
+    """A pisa_problem; Ncap > N reserves rows of k, v and the pyramid for a growing N;
+    score picks the selection's block score (PISA_SCORE_LSE / _MEAN / _MEAN_VAR)."""
     dt = {"bf16": PISA_DTYPE_BF16, "f32": PISA_DTYPE_F32,
           torch.bfloat16: PISA_DTYPE_BF16, torch.float32: PISA_DTYPE_F32}[dtype]
-    return Problem(B, H, Hkv, Nq, N, d, C, fanout, K, int(causal), dt, schedule, Ncap)
+    return Problem(B, H, Hkv, Nq, N, d, C, fanout, K, int(causal), dt, schedule, Ncap, score)
 
 
 def _load():

@@ -53,12 +53,14 @@ SHAPES = {
     "mid-rows-bf16": (1, 4, 2, 1500, 1500, 64, 32, 2, 6, 1, "bf16"),
     # few rows (split paths) with GQA, C = 128 and no causal mask
     "split-gqa-c128-noncausal": (1, 8, 2, 700, 5000, 128, 128, 2, 6, 0, "bf16"),
+    # no causal mask, so the 4-key last block is scored: key tiles with no key
+    "noncausal-c128-ragged": (1, 4, 2, 900, 900, 64, 128, 2, 4, 0, "bf16"),
 }
 
 
-def _problem(shape, schedule=0):
+def _problem(shape, schedule=0, score=0):
     B, H, Hkv, Nq, N, d, C, g, K, causal, dtype = shape
-    return pisa.make_problem(B, H, Hkv, Nq, N, d, C, g, K, causal, dtype, schedule)
+    return pisa.make_problem(B, H, Hkv, Nq, N, d, C, g, K, causal, dtype, schedule, score=score)
 
 
 def _data(shape, seed=0):
@@ -80,8 +82,8 @@ def test_pyramid_parity(name):
     assert err <= _pyr_tol(x["k"], C, g, L), err
 
 
-def _run_select(shape, schedule, x):
-    p = _problem(shape, schedule)
+def _run_select(shape, schedule, x, score=0):
+    p = _problem(shape, schedule, score)
     dtype = shape[-1]
     q, k = dev(x["q"], dtype), dev(x["k"], dtype)
     pyr = pisa.build_pyramid(p, k)
@@ -199,3 +201,28 @@ def test_deterministic_repeat():
         outs.append([t.cpu() for t in (pyr, idx, o, lse, bsa)])
     for a, b in zip(*outs):
         assert torch.equal(a, b)
+
+
+VARIANT_SHAPES = ["tiny-fp32", "gqa-ragged-bf16", "g4-gqa4-d64", "decode-row", "c128-g4-gqa", "big-budget",
+                  "noncausal-c128-ragged", "g3-noncausal"]
+
+
+@pytest.mark.parametrize("name", VARIANT_SHAPES)
+@pytest.mark.parametrize("score", [1, 2], ids=["pisa1-mean", "pisa2-mean-var"])
+@pytest.mark.parametrize("schedule", SCHEDULES, ids=["fused", "two_stage", "split"])
+def test_select_parity_score_variants(name, score, schedule):
+    """PISA-1 / PISA-2 (App. A) through every schedule, against the oracle."""
+    shape = SHAPES[name]
+    B, H, Hkv, Nq, N, d, C, g, K, causal, dtype = shape
+    if schedule == 1 and dtype != "bf16":
+        pytest.skip("two-stage schedule is bf16-only")
+    x = _data(shape, seed=7)
+    idx, sc = _run_select(shape, schedule, x, score)
+    check_selection_valid(idx, N, Nq, C, K, bool(causal))
+    rows = _rows_sample(Nq, 24, 32)
+    ora, gap = O.select(x["q"], x["k"], C, g, K, bool(causal), rows=rows, score={1: "mean", 2: "mean_var"}[score])
+    stats = compare_selection(idx[:, :, rows], ora, gap)
+    print(name, score, schedule, stats)
+    assert np.all(np.isneginf(sc) == (idx < 0))
+    assert np.all(np.isfinite(sc) | np.isinf(sc))
+

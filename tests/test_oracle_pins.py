@@ -429,3 +429,77 @@ def test_pyramid_append_in_steps_equals_one_append():
     for a, b in zip(lv, want):
         np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
 
+
+# PISA-1 / PISA-2 (App. A "First- and second-order approximations").
+def _phi(z, lam):
+    """phi(lambda) = log((1/m) sum_j exp(lambda z_j)), the block's cumulant
+    generating function, by its own formula (not through the oracle)."""
+    return float(np.log(np.mean(np.exp(lam * np.asarray(z)))))
+
+
+@pytest.mark.parametrize("seed", range(5))
+def test_score_variants_are_the_cumulant_derivatives(seed):
+    r = np.random.default_rng(seed)
+    z = r.standard_normal(r.integers(2, 70)) * r.uniform(0.2, 3.0) + r.normal() * 2
+    h = 1e-4
+    d1 = (_phi(z, h) - _phi(z, -h)) / (2 * h)                 # phi'(0) = mean
+    d2 = (_phi(z, h) - 2 * _phi(z, 0.0) + _phi(z, -h)) / h ** 2  # phi''(0) = population variance
+    assert abs(_phi(z, 0.0)) < 1e-15
+    assert abs(O.score_mean(z) - d1) < 1e-6
+    assert abs((O.score_mean_var(z) - O.score_mean(z)) - 0.5 * d2) < 1e-4
+    # LSE - log m = phi(1) >= phi'(0) (phi is convex): the truncations sit below it
+    assert O.lse(z) - math.log(z.size) >= O.score_mean(z) - 1e-12
+
+
+def test_score_variants_on_equal_logits():
+    z = np.full(13, 0.625)
+    assert O.score_mean(z) == 0.625 and O.score_mean_var(z) == 0.625
+    assert abs(O.lse(z) - (0.625 + math.log(13))) < 1e-12
+
+
+@pytest.mark.parametrize("G", [1, 3])
+def test_pisa1_scores_a_node_by_its_own_summary_logit(G):
+    """With the mean reducer and a mean-of-means pyramid, the mean of a node's
+    child logits is the node's own logit q.S/sqrt(d) (ragged nodes included),
+    so every ranked level of PISA-1 scores nodes by their own summary."""
+    N, C, g, d, K = 3000, 32, 3, 8, 6
+    qg, k = _tiny_case(70 + G, N, d, G)
+    levels = O.build_pyramid(k, C, g)
+    for t in (N - 1, 2000, 1234):
+        trace = []
+        O.select_row(qg, k, levels, t, C, g, K, True, trace=trace, score="mean")
+        n_ranked = 0
+        for lv in trace:
+            for i, u in lv["u"].items():
+                own = sum(float(levels[lv["level"] - 1][i] @ qh) / math.sqrt(d) for qh in qg)
+                assert abs(u - own) < 1e-9 * max(1.0, abs(own))
+                n_ranked += 1
+        assert n_ranked > 0
+
+
+@pytest.mark.parametrize("score", ["mean", "mean_var"])
+def test_no_intermediate_pruning_equals_flat_topk_for_variants(score):
+    """As for LSE: with M_2 <= K < M_1 the result is the forced blocks plus the
+    best eligible leaves by the variant's raw-key score (brute force)."""
+    N, C, g, d, K, G = 1024, 32, 2, 8, 16, 2
+    qg, k = _tiny_case(91, N, d, G)
+    levels = O.build_pyramid(k, C, g)
+
+    def brute(x):
+        z = x * 1.0
+        m = z.mean()
+        return m if score == "mean" else m + 0.5 * ((z - m) ** 2).mean()
+
+    for t in range(N - 1, 0, -71):
+        sel, _ = O.select_row(qg, k, levels, t, C, g, K, True, score=score)
+        c = t // C
+        elig = list(range(c + 1))
+        if len(elig) <= K:
+            assert sel == elig
+            continue
+        forced = {0, c, c - 1}
+        free = [i for i in elig if i not in forced]
+        sc = np.array([sum(brute(k[i * C:(i + 1) * C] @ qh / math.sqrt(d)) for qh in qg) for i in free])
+        order = np.lexsort((np.array(free), -sc))
+        assert sel == sorted(forced | {free[j] for j in order[:K - 3]})
+
