@@ -93,7 +93,7 @@ def committed_traffic(kernel):
     return ent["bytes_per_launch"]
 
 
-def cpu_baseline(x, w, n_rows):
+def cpu_baseline(x, w, n_rows, score="lse"):
     """The oracle, as it stands, on a bounded sample: pyramid of KV head 0 plus
     selection + attention of n_rows evenly spaced rows of head 0; extrapolated
     to the whole job (all heads, all rows) as tokens/s."""
@@ -114,7 +114,7 @@ def cpu_baseline(x, w, n_rows):
         t0 = time.perf_counter()
         for r in rows:
             t = N - Nq + r
-            sel, _ = O.select_row(x["q"][0, 0:G, r], k0, levels, t, C, g, K, bool(w["causal"]))
+            sel, _ = O.select_row(x["q"][0, 0:G, r], k0, levels, t, C, g, K, bool(w["causal"]), score=score)
             for hh in range(G):
                 O.attention_row(x["q"][0, hh, r], k0, v0, sel, t, C, bool(w["causal"]))
         t_rows = time.perf_counter() - t0
@@ -132,6 +132,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="needles-128k")
+    ap.add_argument("--score", default="lse", choices=["lse", "mean", "mean_var"],
+                    help="block score of the selection: PISA (lse), PISA-1 (mean), PISA-2 (mean_var)")
     ap.add_argument("--cpu-rows", type=int, default=12288)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bsa", action="store_true")
@@ -162,7 +164,8 @@ def main():
     x = inputs.make_inputs(w, seed=0)
     tdt = torch.bfloat16 if w["dtype"] == "bf16" else torch.float32
     q, k, v = (torch.from_numpy(x[n]).to(tdt).cuda() for n in "qkv")
-    p = pisa.make_problem(B, H, Hkv, Nq, N, d, C, g, K, w["causal"], w["dtype"])
+    score_id = {"lse": 0, "mean": 1, "mean_var": 2}[args.score]
+    p = pisa.make_problem(B, H, Hkv, Nq, N, d, C, g, K, w["causal"], w["dtype"], score=score_id)
     _, R = pisa.pisa_pyramid_layout(p)
     pyr = torch.empty((B, Hkv, R, d), dtype=torch.float32, device="cuda")
     idx = torch.empty((B, Hkv, Nq, K), dtype=torch.int32, device="cuda")
@@ -268,7 +271,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log(f"[bench] cpu baseline: oracle on {args.cpu_rows} rows")
-        cpu = cpu_baseline(x, w, args.cpu_rows)
+        cpu = cpu_baseline(x, w, args.cpu_rows, args.score)
 
     sel_ms = (split["pool"] + split["select"]) / args.steps
     res = {
@@ -285,7 +288,8 @@ def main():
         "dtype": w["dtype"],
         "data": "synthetic",
         "config": {"workload": args.workload, "B": B, "H": H, "Hkv": Hkv, "N": N, "Nq": Nq, "d": d, "C": C,
-                   "fanout": g, "K": K, "causal": bool(w["causal"]), "parallelism": "single GPU"},
+                   "fanout": g, "K": K, "causal": bool(w["causal"]), "score": args.score,
+                   "parallelism": "single GPU"},
         "split_ms": {"pool": split["pool"] / args.steps, "select": split["select"] / args.steps,
                      "attn": split["attn"] / args.steps},
         "selection_ms_incl_pool": sel_ms,
