@@ -783,6 +783,258 @@ __global__ __launch_bounds__(256) void stage1_pair_kernel(SelArgs a, int row_wor
   }
 }
 
+// ----------------------------------------------------------------------------
+// Stage 1 for fan-out 2 and K <= 16: two query rows per wavefront, lane hl of
+// a half owns candidate slot hl, with no LDS lists.
+//
+//   * Child logits: the LPE lanes of a dot group compute the dots of their
+//     own LPE slots (each lane loads 16-byte chunks sub, sub+LPE, ... of every
+//     row) and a reduce-scatter leaves slot j's logit in lane j of the group.
+//     Every valid slot, forced or not, gets both child logits: child 0 by a
+//     dot, child 1 derived from the node's own logit (a summary is the mean of
+//     its two children, so z1 = 2 z - z0), except on the row's first ranked
+//     level, where own logits are unknown and child 1 is a dot as well.
+//   * Rank: key = score (scored), +inf (forced, or every valid slot of an
+//     unranked level), -inf (empty slot); a 32-lane bitonic sort puts the
+//     survivors in lanes 0 .. min(K, #valid) - 1.
+//   * Expand: slot s of the next level is child s & 1 of survivor s >> 1; its
+//     node and its own logit come from the survivor's lanes by lane permutes.
+// ----------------------------------------------------------------------------
+
+// Broadcast lane j of each LPE-lane group to the whole group.
+template <int LPE>
+__device__ __forceinline__ int group_bcast(int v, int j, int lane) {
+  if constexpr (LPE == 4) {
+    switch (j) {
+      case 0: return dpp_i<0x00>(v);
+      case 1: return dpp_i<0x55>(v);
+      case 2: return dpp_i<0xAA>(v);
+      default: return dpp_i<0xFF>(v);
+    }
+  } else {
+    return __shfl(v, (lane & ~(LPE - 1)) | j);
+  }
+}
+
+// One reduce-scatter step over partner lane ^ M: of each pair (k, k | M) the
+// lane keeps the entry whose bit M matches its own and adds the partner's copy.
+template <int M>
+__device__ __forceinline__ void rs_step(float* w, int sub) {
+  const bool up = (sub & M) != 0;
+#pragma unroll
+  for (int k = 0; k < M; ++k) {
+    const float send = up ? w[k] : w[k | M];
+    const float mine = up ? w[k | M] : w[k];
+    w[k] = mine + xor32_f<M>(send);
+  }
+}
+
+// Lane sub of an LPE-lane group ends with the group total of w[sub].
+template <int LPE>
+__device__ __forceinline__ float reduce_scatter(float (&w)[LPE], int sub) {
+  if constexpr (LPE >= 16) rs_step<8>(w, sub);
+  if constexpr (LPE >= 8) rs_step<4>(w, sub);
+  if constexpr (LPE >= 4) rs_step<2>(w, sub);
+  rs_step<1>(w, sub);
+  return w[0];
+}
+
+// Logits of pyramid row `ri` (this lane's slot) against every head's query:
+// the group's LPE rows are loaded together, lane sub reading chunks
+// sub, sub + LPE, ... (pbase already points at chunk sub of row 0).
+template <int D, int GMAX, int LPE, int INFLIGHT>
+__device__ __forceinline__ void slot_dots(const float* __restrict__ pbase, int ri, const float (&qv)[GMAX][D / LPE],
+                                          int sub, int lane, float (&z)[GMAX]) {
+  constexpr int NCH = D / LPE / 4;
+  constexpr int UNR = INFLIGHT < LPE ? INFLIGHT : LPE;  // rows whose loads are issued together
+  float w[GMAX][LPE];
+#pragma unroll
+  for (int j0 = 0; j0 < LPE; j0 += UNR) {
+    float4 x[UNR][NCH];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int rj = group_bcast<LPE>(ri, j0 + u, lane);
+      const float* rp = pbase + static_cast<int64_t>(rj) * D;
+#pragma unroll
+      for (int i = 0; i < NCH; ++i) x[u][i] = *reinterpret_cast<const float4*>(rp + i * LPE * 4);
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+#pragma unroll
+      for (int hh = 0; hh < GMAX; ++hh) {  // heads past G have zero queries
+        float acc = 0.f;
+#pragma unroll
+        for (int i = 0; i < NCH; ++i) {
+          acc = fmaf(qv[hh][4 * i + 0], x[u][i].x, acc);
+          acc = fmaf(qv[hh][4 * i + 1], x[u][i].y, acc);
+          acc = fmaf(qv[hh][4 * i + 2], x[u][i].z, acc);
+          acc = fmaf(qv[hh][4 * i + 3], x[u][i].w, acc);
+        }
+        w[hh][j0 + u] = acc;
+      }
+    }
+  }
+#pragma unroll
+  for (int hh = 0; hh < GMAX; ++hh) z[hh] = reduce_scatter<LPE>(w[hh], sub);
+}
+
+// Score of a node from its two child logits (z1 = -inf: a single child).
+template <int KIND>
+__device__ __forceinline__ float pair_score(float z0, float z1) {
+  if constexpr (KIND == kScoreLse) {
+    const float m = fmaxf(z0, z1), n = fminf(z0, z1);
+    return m + fast_log2(1.f + fast_exp2(n - m));
+  } else {
+    const bool two = z1 != -INFINITY;
+    const float mean = two ? 0.5f * (z0 + z1) : z0;
+    if constexpr (KIND == kScoreMean) {
+      return mean;
+    } else {
+      const float h = two ? 0.5f * (z0 - z1) : 0.f;
+      return mean + 0.5f * kLn2 * (h * h);
+    }
+  }
+}
+
+// One level of the fan-out-2 walk for the two rows of a wavefront: rank the
+// slots (first K in (key desc, node asc) order survive; scored slots keyed by
+// their summed score, forced slots and every slot of an unranked level +inf,
+// empty slots -inf) and expand the survivors: slot s of the next level is
+// child s & 1 of survivor s >> 1, its own logits taken from the survivor's
+// child logits.  A half idle on this level (lev above its start) stays idle.
+template <int GMAX, int KIND>
+__device__ __forceinline__ void g2_rank_expand(const Geo& geo, int lev, int c, int causal, int K, int G, int start,
+                                               int hl, int hbase, int& node, const float (&z0)[GMAX],
+                                               const float (&z1)[GMAX], float (&zs)[GMAX]) {
+  const int lb = lev - 1;
+  const int Mb = geo.M[lb];
+  const bool valid = node >= 0;
+  const int nvalid = __builtin_popcount(static_cast<uint32_t>(__ballot(valid) >> hbase));
+  const bool ranked = nvalid > K;  // more candidates than the budget
+  const Forced fz = forced_at(geo, lev, c, causal);
+  float key = -INFINITY;
+  if (valid) {
+    if (ranked && !fz.is(node)) {
+      float u = 0.f;
+#pragma unroll
+      for (int hh = 0; hh < GMAX; ++hh) {
+        const float sc = pair_score<KIND>(z0[hh], z1[hh]);
+        u += hh < G ? sc : 0.f;
+      }
+      key = u;
+    } else {
+      key = INFINITY;
+    }
+  }
+  int pack = valid ? (node << 6) | hl : 0x7FFFFFC0 | hl;
+  sort32(key, pack, hl);
+  const int nkept = min(K, nvalid);
+
+  const int r = hl >> 1;
+  const int pr = __shfl(pack, hbase | r);
+  const int korig = pr & 63;
+  const int rmax = causal ? min(anc_at(geo, c, lb), Mb - 1) : Mb - 1;
+  const int cn = 2 * (pr >> 6) + (hl & 1);
+  const bool cvalid = r < nkept && cn <= rmax;
+#pragma unroll
+  for (int hh = 0; hh < GMAX; ++hh) {
+    const float a0 = __shfl(z0[hh], hbase | korig);
+    const float a1v = __shfl(z1[hh], hbase | korig);
+    zs[hh] = (hl & 1) ? a1v : a0;
+  }
+  if (lev <= start) node = cvalid ? cn : -1;
+}
+
+// Store a half's leaf candidate set in ascending order, -1 padded to g*K.
+__device__ __forceinline__ void g2_store_leaves(const SelArgs& a, int bh, int row, bool live, int hl, int hbase,
+                                                int node) {
+  const int nA = __builtin_popcount(static_cast<uint32_t>(__ballot(node >= 0) >> hbase));
+  float akey = node >= 0 ? -static_cast<float>(node) : -INFINITY;
+  int apack = node >= 0 ? node : 0x7FFFFFC0 | hl;
+  sort32(akey, apack, hl);
+  if (live) {
+    const int64_t orow = static_cast<int64_t>(bh) * a.Nq + row;
+    if (hl < a.gK) a.a1[orow * a.gK + hl] = hl < nA ? apack : -1;
+    if (hl == 0) a.a1cnt[orow] = nA;
+  }
+}
+
+template <int D, int GMAX, int LPE, int KIND>
+__global__ __launch_bounds__(256) void stage1_g2_kernel(SelArgs a) {
+  constexpr int DPL = D / LPE;
+  constexpr int NCH = DPL / 4;
+  const Geo& geo = a.geo;
+  const int G = a.G, K = a.K, gK = a.gK;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int half = lane >> 5, hl = lane & 31, hbase = lane & 32;
+  const int sub = hl % LPE;
+  const int row = (blockIdx.x * 4 + wave) * 2 + half;
+  const bool live = row < a.Nq;
+  const int rowc = live ? row : a.Nq - 1;
+  const int bh = blockIdx.y;
+  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+  const int t = geo.N - a.Nq + rowc;
+  const int c = t / geo.C;
+
+  float qv[GMAX][DPL];
+  {
+    const uint16_t* qb = static_cast<const uint16_t*>(a.q);
+#pragma unroll
+    for (int hh = 0; hh < GMAX; ++hh) {
+      if (hh < G) {
+        const int64_t off = ((static_cast<int64_t>(b) * a.H + h * G + hh) * a.Nq + rowc) * D + sub * 4;
+#pragma unroll
+        for (int ch = 0; ch < NCH; ++ch) {
+          float x4[4];
+          load_row_part<uint16_t, 4>(qb + off + ch * 4 * LPE, x4);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) qv[hh][ch * 4 + e] = x4[e] * a.qscale2;
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) qv[hh][e] = 0.f;
+      }
+    }
+  }
+
+  auto n_eligible = [&](int lev) { return a.causal ? min(anc_at(geo, c, lev) + 1, geo.M[lev]) : geo.M[lev]; };
+  int start = 1;  // first level holding more than K eligible nodes (1: none)
+  for (int lev = geo.L; lev >= 2; --lev) {
+    if (n_eligible(lev) > K) {
+      start = lev;
+      break;
+    }
+  }
+  const int wave_start = max(start, __shfl_xor(start, 32));
+
+  int node = -1;  // a half is idle (no valid slot) on the levels above its start
+  float zs[GMAX];
+#pragma unroll
+  for (int hh = 0; hh < GMAX; ++hh) zs[hh] = 0.f;
+
+  for (int lev = wave_start; lev >= 2; --lev) {
+    if (lev == start) node = hl < n_eligible(lev) ? hl : -1;
+    const bool fresh = lev == start;
+    const int lb = lev - 1;
+    const int Mb = geo.M[lb];
+    const bool valid = node >= 0;
+    const int nch = valid ? min(2, Mb - 2 * node) : 0;
+    const float* pbase = a.pyr + (static_cast<int64_t>(bh) * geo.R + geo.off[lb]) * D + sub * 4;
+
+    float z0[GMAX], z1[GMAX];
+    slot_dots<D, GMAX, LPE, 4>(pbase, valid ? 2 * node : 0, qv, sub, lane, z0);
+    if (__ballot(fresh && nch == 2) != 0) {
+      slot_dots<D, GMAX, LPE, 4>(pbase, nch == 2 ? 2 * node + 1 : 0, qv, sub, lane, z1);
+    }
+#pragma unroll
+    for (int hh = 0; hh < GMAX; ++hh) z1[hh] = nch < 2 ? -INFINITY : (fresh ? z1[hh] : 2.f * zs[hh] - z0[hh]);
+
+    g2_rank_expand<GMAX, KIND>(geo, lev, c, a.causal, K, G, start, hl, hbase, node, z0, z1, zs);
+  }
+  if (start == 1) node = hl < n_eligible(1) ? hl : -1;  // every eligible leaf, unranked
+  g2_store_leaves(a, bh, row, live, hl, hbase, node);
+}
+
 // Final Top-K for g*K <= 32: two rows per wavefront, one candidate per lane
 // (the candidates arrive in ascending block order).  sort32 ranks them
 // (forced and unranked rows keyed +inf); the rank of each lane's own
@@ -1543,7 +1795,29 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
       dim3 grid((s.Nq + 7) / 8, s.BH());
       const size_t lds = static_cast<size_t>(8) * words * sizeof(int);
       auto go = [&](auto kern) { kern<<<grid, 256, lds, st>>>(a, words); };
-      if (s.D == 128) {
+      auto go2 = [&](auto kern) { kern<<<grid, 256, 0, st>>>(a); };
+      auto by_kind = [&](auto k0, auto k1, auto k2) {
+        if (s.score == kScoreLse) go2(k0);
+        else if (s.score == kScoreMean) go2(k1);
+        else go2(k2);
+      };
+      if (s.g == 2 && s.G <= 4) {
+        if (s.D == 128) {
+          if (s.G == 1)
+            by_kind(stage1_g2_kernel<128, 1, 16, kScoreLse>, stage1_g2_kernel<128, 1, 16, kScoreMean>,
+                    stage1_g2_kernel<128, 1, 16, kScoreMeanVar>);
+          else
+            by_kind(stage1_g2_kernel<128, 4, 8, kScoreLse>, stage1_g2_kernel<128, 4, 8, kScoreMean>,
+                    stage1_g2_kernel<128, 4, 8, kScoreMeanVar>);
+        } else {
+          if (s.G == 1)
+            by_kind(stage1_g2_kernel<64, 1, 16, kScoreLse>, stage1_g2_kernel<64, 1, 16, kScoreMean>,
+                    stage1_g2_kernel<64, 1, 16, kScoreMeanVar>);
+          else
+            by_kind(stage1_g2_kernel<64, 4, 8, kScoreLse>, stage1_g2_kernel<64, 4, 8, kScoreMean>,
+                    stage1_g2_kernel<64, 4, 8, kScoreMeanVar>);
+        }
+      } else if (s.D == 128) {
         if (s.G == 1) go(stage1_pair_kernel<128, 1, 4>);
         else if (s.G <= 4) go(stage1_pair_kernel<128, 4, 16>);
         else go(stage1_pair_kernel<128, 16, 16>);

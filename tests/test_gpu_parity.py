@@ -55,6 +55,9 @@ SHAPES = {
     "split-gqa-c128-noncausal": (1, 8, 2, 700, 5000, 128, 128, 2, 6, 0, "bf16"),
     # no causal mask, so the 4-key last block is scored: key tiles with no key
     "noncausal-c128-ragged": (1, 4, 2, 900, 900, 64, 128, 2, 4, 0, "bf16"),
+    # fan-out 2 stage 1 with one head per KV head at d = 64, and with three heads per group
+    "mha-d64-bf16": (1, 2, 2, 3000, 3000, 64, 32, 2, 8, 1, "bf16"),
+    "gqa3-bf16": (1, 6, 2, 2500, 2500, 128, 64, 2, 8, 1, "bf16"),
 }
 
 
