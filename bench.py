@@ -35,7 +35,7 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algorithmic_work(w, pairs_scored, attn_pairs):
+def algorithmic_work(w, pairs_scored, attn_pairs, far_key_pairs=None, far_slots=None):
     """Algorithmic bytes / flops per launch of each kernel (see the design notes)."""
     B, H, Hkv, N, Nq, d, C, g, K = (w[k] for k in ("B", "H", "Hkv", "N", "Nq", "d", "C", "g", "K"))
     G = H // Hkv
@@ -61,9 +61,16 @@ def algorithmic_work(w, pairs_scored, attn_pairs):
     out["select_stage1"] = ("alu", stage1_flops)
     out["leaf_score"] = ("mfma", pairs_scored * G * C * d * 2)
     out["attn_rows"] = ("mfma", attn_pairs * 4 * d)
-    out["attn_block"] = ("mfma", attn_pairs * 4 * d)
     n_part = B * Hkv * Nq * K * G
     out["attn_combine"] = ("hbm", n_part * (2 * d + 4) + B * H * Nq * (2 * d + 4))
+    if w["causal"] and far_key_pairs is not None:
+        # block-centric kernel: the (query, key) pairs of the blocks other than the
+        # row's first, previous and own; the per-leaf-block kernel reads those
+        # slots' partials (bf16 o + fp32 log-sum) and q, and writes o and lse
+        out["attn_block"] = ("mfma", far_key_pairs * 4 * d)
+        out["attn_local"] = ("hbm", far_slots * G * (2 * d + 4) + B * H * Nq * (2 * d + 2 * d + 4))
+    else:
+        out["attn_block"] = ("mfma", attn_pairs * 4 * d)
     rows = B * Hkv * Nq
     out["final_topk"] = ("hbm", rows * (g * K * 8 + 4 + K * 4))
     out["cluster_build"] = ("hbm", rows * g * K * 4 * 3)
@@ -227,9 +234,13 @@ def main():
     cnt = torch.clamp(torch.minimum(t_pos - starts + 1, torch.full_like(starts, C)), min=0)
     cnt = torch.minimum(cnt, torch.clamp(N - starts, min=0))
     attn_pairs = int((cnt * valid).sum().item()) * (H // Hkv)
+    c_row = (t_pos // C)
+    far = valid & (idx_t != 0) & (idx_t != c_row) & (idx_t != c_row - 1)
+    far_key_pairs = int((cnt * far).sum().item()) * (H // Hkv)
+    far_slots = int(far.sum().item())
     # leaf pairs scored (upper bound): every row may score g*K candidates minus the 3 forced
     pairs_scored = B * Hkv * Nq * max(0, g * K - (3 if w["causal"] else 0))
-    work = algorithmic_work(w, pairs_scored, attn_pairs)
+    work = algorithmic_work(w, pairs_scored, attn_pairs, far_key_pairs, far_slots)
     kernels = {name: {"launches": n // args.steps if n >= args.steps else n,
                       "ms_per_step": tot / args.steps, "avg_ms": tot / max(n, 1)}
                for name, (n, tot) in kern.items()}

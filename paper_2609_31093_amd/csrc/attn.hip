@@ -374,6 +374,269 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
   }
 }
 
+// ----------------------------------------------------------------------------
+// Causal attention over the blocks that every row of a leaf block selects by
+// construction (App. B: the first block, the previous one and the row's own),
+// for all rows of that leaf block at once, merged with the partials that
+// attn_block16_kernel left for each row's other selected blocks.
+//
+// One workgroup per (batch x KV head, query leaf block c).  For each query
+// head and each of the distinct blocks {0, c-1, c}, the block is staged in
+// LDS as in attn_block16_kernel and every wavefront advances an online
+// softmax for 16 query rows on v_mfma_f32_16x16x32_bf16 (S^T = K q^T, the
+// causal mask, O^T += V^T P); a block enters a row's sum only if it is in
+// that row's index list.  The wavefront then folds in the row's partials of
+// its other slots (o normalised by its own sum, log2-sum) and writes o (bf16)
+// and lse (natural log).  The rows' shared blocks never become partials, and
+// each is read once per leaf block instead of once per row.
+// ----------------------------------------------------------------------------
+constexpr int kMergeBatch = 4;  // partials of a row requested together by attn_local_kernel
+
+template <int D, int CT>
+__global__ __launch_bounds__(256, 3) void attn_local_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
+                                                         const uint16_t* __restrict__ k,
+                                                         const uint16_t* __restrict__ v,
+                                                         const int32_t* __restrict__ idx,
+                                                         const uint16_t* __restrict__ part_o,
+                                                         const float* __restrict__ part_lse,
+                                                         uint16_t* __restrict__ o, float* __restrict__ lse) {
+  constexpr int KS = D / 32;
+  constexpr int LDK = D + 8;
+  constexpr int C = CT * 32;
+  constexpr int MT = C / 16;
+  constexpr int LDV = C + 4;
+  constexpr int DT = D / 16;
+  constexpr int QG = C / 16;             // 16-row query groups of a leaf block
+  constexpr int NPASS = (QG + 3) / 4;    // groups per wavefront
+  constexpr int DPL = D / 16;            // merge: elements per lane
+  constexpr int SROW = D + 4;            // merge: padded state row (floats)
+  extern __shared__ uint16_t lds[];
+  uint16_t* klds = lds;
+  uint16_t* vt = lds + C * LDK;
+  uint32_t* vt32 = reinterpret_cast<uint32_t*>(vt);
+
+  const int bh = blockIdx.y;
+  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+  const int tq0 = a.N - a.Nq;  // absolute position of query row 0
+  const int c = (tq0 + a.row0) / C + static_cast<int>(blockIdx.x);
+  const int p_lo = max(c * C, tq0 + a.row0), p_hi = min((c + 1) * C, tq0 + a.row0 + a.nrows);
+  if (p_lo >= p_hi) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int col = lane & 15, grp = lane >> 4;
+  int sb[3];
+  int nsb = 0;
+  sb[nsb++] = 0;
+  if (c - 1 > 0) sb[nsb++] = c - 1;
+  if (c > 0) sb[nsb++] = c;
+
+  for (int it = 0; it < NPASS * a.G; ++it) {
+    const int hh = it / NPASS, qg = (it - hh * NPASS) * 4 + wave;
+    const int p = c * C + qg * 16 + col;  // this lane's query position
+    const bool vq = qg < QG && p >= p_lo && p < p_hi;
+    const int rowq = vq ? p - tq0 : p_lo - tq0;  // a row of the tile for lanes without a query
+    const int32_t* sel = idx + (static_cast<int64_t>(bh) * a.Nq + rowq) * a.K;
+    // which shared blocks this row selected (each of the 4 lanes of a column
+    // reads a quarter of the list)
+    int has = 0;
+    for (int s = grp; s < a.K; s += 4) {
+      const int x = sel[s];
+      has |= (x == 0 ? 1 : 0) | (x == c - 1 && c - 1 > 0 ? 2 : 0) | (x == c && c > 0 ? 4 : 0);
+    }
+    has |= __shfl_xor(has, 16);
+    has |= __shfl_xor(has, 32);
+    bf16x8a qb[KS];
+    {
+      const uint16_t* qrow = q + ((static_cast<int64_t>(b) * a.H + h * a.G + hh) * a.Nq + rowq) * D + grp * 8;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) qb[ks] = u4_as_bf16x8(*reinterpret_cast<const uint4*>(qrow + ks * 32));
+    }
+    float m = -INFINITY, l = 0.f;
+    f32x4a oacc[DT];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x4a{0.f, 0.f, 0.f, 0.f};
+
+    for (int j = 0; j < nsb; ++j) {
+      const int blk = sb[j];
+      const int r0 = blk * C;
+      const int nkeys = min(C, a.N - r0);
+      __syncthreads();  // the previous block's readers are done
+      const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
+      const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
+      for (int e = threadIdx.x; e < C * (D / 8); e += 256) {
+        const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
+        uint4 kv = make_uint4(0, 0, 0, 0);
+        if (r < nkeys) kv = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
+        *reinterpret_cast<uint4*>(klds + r * LDK + c8) = kv;
+      }
+      for (int e = threadIdx.x; e < (C / 2) * (D / 8); e += 256) {
+        const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
+        uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
+        if (2 * kp < nkeys) v0 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp) * D + c8);
+        if (2 * kp + 1 < nkeys) v1 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp + 1) * D + c8);
+        const uint32_t w0[4] = {v0.x, v0.y, v0.z, v0.w};
+        const uint32_t w1[4] = {v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          vt32[(c8 + 2 * i) * (LDV / 2) + kp] = (w0[i] & 0xFFFFu) | (w1[i] << 16);
+          vt32[(c8 + 2 * i + 1) * (LDV / 2) + kp] = (w0[i] >> 16) | (w1[i] & 0xFFFF0000u);
+        }
+      }
+      __syncthreads();
+      if (qg >= QG) continue;
+      const int bit = blk == 0 ? 1 : blk == c ? 4 : 2;
+      const int kmax = (!vq || !(has & bit)) ? 0 : (a.causal ? min(nkeys, p - r0 + 1) : nkeys);
+      // S^T tiles: tile mt holds keys mt*16 + 4*grp + i of query `col`
+      f32x4a sa[MT];
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        f32x4a acc = {0.f, 0.f, 0.f, 0.f};
+        const uint16_t* arow = klds + (mt * 16 + col) * LDK + grp * 8;
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const bf16x8a av = u4_as_bf16x8(*reinterpret_cast<const uint4*>(arow + ks * 32));
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qb[ks], acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = mt * 16 + 4 * grp + i;
+          acc[i] = key < kmax ? acc[i] * a.qscale2 : -INFINITY;
+        }
+        sa[mt] = acc;
+      }
+      float bm = -INFINITY;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) bm = fmaxf(bm, fmaxf(fmaxf(sa[mt][0], sa[mt][1]), fmaxf(sa[mt][2], sa[mt][3])));
+      bm = fmaxf(bm, __shfl_xor(bm, 16));
+      bm = fmaxf(bm, __shfl_xor(bm, 32));
+      const float mn = fmaxf(m, bm);
+      const float msafe = mn == -INFINITY ? 0.f : mn;  // nothing visible yet: P = 0, the state stays empty
+      const float sc = fast_exp2(m - msafe);            // m = -inf: 0
+      l *= sc;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) oacc[dt] *= sc;
+      // P operand k = 8*grp + i: key 32 s2 + 4 grp + i (i < 4) or 32 s2 + 16 + 4 grp + i - 4
+#pragma unroll
+      for (int s2 = 0; s2 < MT / 2; ++s2) {
+        float pv[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          pv[i] = fast_exp2(sa[2 * s2][i] - msafe);
+          pv[4 + i] = fast_exp2(sa[2 * s2 + 1][i] - msafe);
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) l += pv[i];
+        uint4 u;
+        u.x = pack2_bf16(pv[0], pv[1]);
+        u.y = pack2_bf16(pv[2], pv[3]);
+        u.z = pack2_bf16(pv[4], pv[5]);
+        u.w = pack2_bf16(pv[6], pv[7]);
+        const bf16x8a pb = u4_as_bf16x8(u);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const uint16_t* vrow = vt + (dt * 16 + col) * LDV + 4 * grp + 32 * s2;
+          const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
+          const bf16x8a av = u4_as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+          oacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, pb, oacc[dt], 0, 0, 0);
+        }
+      }
+      m = mn;
+    }
+    l += __shfl_xor(l, 16);
+    l += __shfl_xor(l, 32);
+    // The wavefront's 16 states go to LDS (row-major, over the staging area
+    // once every wavefront is done with it) so that the merge reads each
+    // partial with 16 lanes x 16 bytes, like attn_combine_kernel.
+    __syncthreads();
+    if (qg >= QG) continue;
+    float* st = reinterpret_cast<float*>(lds) + wave * (16 * SROW + 32);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+      *reinterpret_cast<float4*>(st + col * SROW + dt * 16 + 4 * grp) =
+          make_float4(oacc[dt][0], oacc[dt][1], oacc[dt][2], oacc[dt][3]);
+    if (grp == 0) {
+      st[16 * SROW + col] = m;
+      st[16 * SROW + 16 + col] = l;
+    }
+    wave_sync();
+    // Merge: 16 lanes per row, four rows at a time; every row's index list
+    // and partial log-sums are requested before any partial is read.
+    const int sub = lane & 15;
+    int selA[4], selB[4];
+    float lsA[4], lsB[4];
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int pr = c * C + qg * 16 + r4 * 4 + grp;
+      const bool v4 = pr >= p_lo && pr < p_hi;
+      const int32_t* sl = idx + (static_cast<int64_t>(bh) * a.Nq + (v4 ? pr - tq0 : p_lo - tq0)) * a.K;
+      selA[r4] = (v4 && sub < a.K) ? sl[sub] : -1;
+      selB[r4] = (v4 && sub + 16 < a.K) ? sl[sub + 16] : -1;
+    }
+    auto far = [&](int x) { return x >= 0 && !(a.causal && (x == 0 || x == c || x == c - 1)); };
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int pr = c * C + qg * 16 + r4 * 4 + grp;
+      const int64_t pb = (static_cast<int64_t>(bh) * a.nrows + (pr - tq0 - a.row0)) * a.K;
+      lsA[r4] = far(selA[r4]) ? part_lse[(pb + sub) * a.G + hh] : -INFINITY;
+      lsB[r4] = far(selB[r4]) ? part_lse[(pb + sub + 16) * a.G + hh] : -INFINITY;
+    }
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int rl = r4 * 4 + grp;  // row of the wavefront's 16
+      const int pr = c * C + qg * 16 + rl;
+      const bool v4 = pr >= p_lo && pr < p_hi;
+      const int rowm = v4 ? pr - tq0 : p_lo - tq0;
+      const int64_t pb = (static_cast<int64_t>(bh) * a.nrows + (rowm - a.row0)) * a.K;
+      float mm = st[16 * SROW + rl], ll = st[16 * SROW + 16 + rl];
+      float acc[DPL];
+      {
+        const float* sr = st + rl * SROW + sub * DPL;
+#pragma unroll
+        for (int e = 0; e < DPL; e += 4) {
+          const float4 x4 = *reinterpret_cast<const float4*>(sr + e);
+          acc[e] = x4.x;
+          acc[e + 1] = x4.y;
+          acc[e + 2] = x4.z;
+          acc[e + 3] = x4.w;
+        }
+      }
+      const uint16_t* prow = part_o + (pb * a.G + hh) * D + sub * DPL;  // slot s at prow + s * G * D
+      for (int s0 = 0; s0 < a.K; s0 += kMergeBatch) {
+        float ls[kMergeBatch];
+        int off[kMergeBatch];
+#pragma unroll
+        for (int u = 0; u < kMergeBatch; ++u) {
+          const int s = s0 + u;
+          const float la = __shfl(lsA[r4], (lane & 48) | (s & 15)), lb = __shfl(lsB[r4], (lane & 48) | (s & 15));
+          ls[u] = s < a.K ? (s < 16 ? la : lb) : -INFINITY;
+          off[u] = (ls[u] != -INFINITY ? s : 0) * a.G * D;
+        }
+        float x[kMergeBatch][DPL];
+#pragma unroll
+        for (int u = 0; u < kMergeBatch; ++u) load_row_part<uint16_t, DPL>(prow + off[u], x[u]);
+#pragma unroll
+        for (int u = 0; u < kMergeBatch; ++u) {
+          if (ls[u] == -INFINITY) continue;
+          const float mn = fmaxf(mm, ls[u]);
+          const float c0 = fast_exp2(mm - mn), c1 = fast_exp2(ls[u] - mn);
+          ll = ll * c0 + c1;
+#pragma unroll
+          for (int e = 0; e < DPL; ++e) acc[e] = acc[e] * c0 + x[u][e] * c1;
+          mm = mn;
+        }
+      }
+      if (!v4) continue;
+      const int64_t orow = (static_cast<int64_t>(b) * a.H + h * a.G + hh) * a.Nq + rowm;
+      const float inv = ll > 0.f ? 1.0f / ll : 0.f;
+      float res[DPL];
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) res[e] = acc[e] * inv;
+      store_row_part<uint16_t, DPL>(o + orow * D + sub * DPL, res);
+      if (lse && sub == 0) lse[orow] = ll > 0.f ? (mm + fast_log2(ll)) * kLn2 : -INFINITY;
+    }
+  }
+}
+
 // One wavefront per (row of the chunk, query head): merge the row's K
 // partials.  16 lanes cover one partial (8 bf16 each for d = 128).
 template <int D>
@@ -669,7 +932,11 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
   hipError_t e;
   for (int row0 = 0; row0 < s.Nq; row0 += ch) {
     const int nrows = std::min(ch, s.Nq - row0);
-    ClusterArgs ca{idx, nullptr, s.K, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], kClusterAttn, row0, nrows, s.g};
+    // Causal: each row's first, previous and own block are attended per leaf
+    // block by attn_local_kernel, which also merges the other partials.
+    const bool local = s.causal != 0;
+    ClusterArgs ca{idx, nullptr, s.K, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], local ? kClusterAttnFar : kClusterAttn,
+                   row0, nrows, s.g};
     ClusterOut co{};
     if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st)) != hipSuccess) return e;
     AttnBlockArgs a{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], row0, nrows,
@@ -695,7 +962,31 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
       else
         go(attn_block16_kernel<D, 4>);
     }
-    {
+    if (local) {
+      ProfScope ps("attn_local", st);
+      const int tq0 = s.N - s.Nq;
+      const int nblk = (tq0 + row0 + nrows - 1) / s.C - (tq0 + row0) / s.C + 1;
+      dim3 grid(static_cast<unsigned>(nblk), s.BH());
+      // one key block staged, or (later) four wavefronts' 16 row states
+      const size_t lds = std::max((static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 4)) * 2,
+                                  static_cast<size_t>(4) * (16 * (D + 4) + 32) * 4);
+      const uint16_t* qq = static_cast<const uint16_t*>(q);
+      const uint16_t* kk = static_cast<const uint16_t*>(k);
+      const uint16_t* vv = static_cast<const uint16_t*>(v);
+      auto go = [&](auto kern) {
+        if (lds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        kern<<<grid, 256, lds, st>>>(a, qq, kk, vv, idx, part_o, part_lse, static_cast<uint16_t*>(o), lse);
+      };
+      if (s.C == 32)
+        go(attn_local_kernel<D, 1>);
+      else if (s.C == 64)
+        go(attn_local_kernel<D, 2>);
+      else if (s.C == 96)
+        go(attn_local_kernel<D, 3>);
+      else
+        go(attn_local_kernel<D, 4>);
+    } else {
       ProfScope ps("attn_combine", st);
       dim3 grid((nrows + 3) / 4, s.B * s.H);
       attn_combine_kernel<D><<<grid, 256, 0, st>>>(a, idx, part_o, part_lse, static_cast<uint16_t*>(o), lse);

@@ -26,6 +26,10 @@ __device__ __forceinline__ bool cluster_pair(const ClusterArgs& a, int bh, int r
   const int32_t* lst = a.list + rg * a.S;
   blk = lst[slot];
   if (blk < 0) return false;
+  if (a.mode == kClusterAttnFar) {
+    const int c = (a.N - a.Nq + a.row0 + r) / a.C;
+    return !(a.causal && (blk == 0 || blk == c || blk == c - 1));
+  }
   if (a.mode == kClusterLeaf || a.mode == kClusterLeafParent) {
     const int n = a.cnt[rg];
     if (slot >= n || n <= a.K) return false;

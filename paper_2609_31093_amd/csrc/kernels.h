@@ -39,6 +39,8 @@ constexpr int kClusterLeaf = 0;  // leaf scoring: rows with more than K candidat
 constexpr int kClusterAttn = 1;  // attention: every non-negative slot
 constexpr int kClusterLeafParent = 2;  // leaf scoring grouped by parent node: one entry per
                                        // (row, parent) at the slot of its first non-forced child
+constexpr int kClusterAttnFar = 3;     // causal attention: every non-negative slot except the row's first,
+                                       // previous and own leaf block (those are attended per leaf block)
 struct ClusterArgs {
   const int32_t* list;  // [BH, Nq, S] block per slot, -1 = none
   const int32_t* cnt;   // [BH, Nq] candidates per row (leaf mode only)
