@@ -151,6 +151,10 @@ def main():
     ap.add_argument("--decode", action="store_true",
                     help="also time the decode workload: single-token selection + attention steps against one "
                          "prebuilt 128K pyramid (extra JSON line)")
+    ap.add_argument("--quality", type=int, default=0,
+                    help="also run the block-selection quality diagnostic (Recall@K, captured mass, mass ratio "
+                         "against the full-attention reference) for PISA and flat BSA on this many evenly spaced "
+                         "rows with more than K eligible blocks (extra JSON line)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="after the run, copy a cold buffer of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -416,6 +420,44 @@ def main():
                                      "streaming_what": f"one step = pisa_pyramid_append of 1 token + pisa_select + "
                                                        f"pisa_sparse_attn_fwd, KV length growing {n0 + 1} -> {Nd} "
                                                        f"in buffers reserved for {Nd} rows"}}), flush=True)
+
+    if args.quality:
+        n_q = args.quality
+        t0_row = max(0, K * C - (N - Nq))  # first row with more than K eligible blocks
+        rows_np = np.unique(np.linspace(t0_row, Nq - 1, n_q).astype(np.int32))
+        rows_d = torch.from_numpy(rows_np).cuda()
+        nq = int(rows_d.numel())
+        idx_b = torch.empty_like(idx)
+        nb = pisa.pisa_bsa_workspace_bytes(p)
+        pisa.pisa_build_pyramid(p, k, pyr, stream)
+        pisa.pisa_select(p, q, k, pyr, idx, None, ws_sel, ws_sel_n, stream)
+        pisa.pisa_select_flat_bsa(p, q, pyr, idx_b, torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda"), nb,
+                                  stream)
+        nbq = pisa.pisa_quality_workspace_bytes(p, nq)
+        ws_q = torch.empty(max(nbq, 1), dtype=torch.uint8, device="cuda")
+        met = torch.empty((B, Hkv, nq, 3), dtype=torch.float32, device="cuda")
+        ref = torch.empty((B, Hkv, nq, K), dtype=torch.int32, device="cuda")
+        out_q = {"workload": args.workload, "rows": nq, "what": "mean over (row, KV head) of Recall@K, captured mass "
+                 "and attention mass ratio against the full-attention reference (forced blocks + highest mass)"}
+        for name, sel in (("pisa", idx), ("flat_bsa", idx_b)):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            pisa.pisa_selection_quality(p, q, k, sel, rows_d, nq, met, ref, ws_q, nbq, stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            m = met.double()
+            out_q[name] = {"recall": m[..., 0].mean().item(), "captured": m[..., 1].mean().item(),
+                           "ratio": m[..., 2].mean().item()}
+            if w.get("dist") == "needles":
+                qpos = set(inputs.needle_layout(w)["qpos"].tolist())
+                mask = torch.tensor([int(r) in qpos for r in rows_np], device="cuda")
+                if mask.any():
+                    out_q[name]["needle_rows"] = {"rows": int(mask.sum()),
+                                                  "recall": m[:, :, mask, 0].mean().item(),
+                                                  "captured": m[:, :, mask, 1].mean().item()}
+            out_q["diagnostic_ms"] = e0.elapsed_time(e1)
+        log(f"[bench] quality: {out_q}")
+        print(json.dumps({"quality": out_q}), flush=True)
 
     if args.copy_probe_mib:
         # A plain device copy of known size from a buffer evicted from the caches

@@ -181,6 +181,34 @@ int pisa_sparse_attn_fwd(const pisa_problem* p, const void* q, const void* k, co
                          const int32_t* block_idx, void* o, float* lse, void* ws,
                          size_t ws_bytes, pisa_stream_t stream);
 
+/* Block-selection quality diagnostic (Sec. 4 "Block-selection quality", eq.
+ * oracle_metrics; App. C "Block-selection diagnostic", eq. oracle_block_mass).
+ * For each (batch, KV head) and each listed query row: the full attention's
+ * log mass of every eligible leaf block, a(B) = log of the sum over B's
+ * tokens (future ones masked when causal) of exp(q.k / sqrt(d)), per query
+ * head; P(B) = mean over the KV head's query heads of each head's softmax of
+ * a over the eligible blocks.  The reference set holds the forced blocks of
+ * App. B (causal) and the eligible blocks of highest P up to K (ties to the
+ * smaller index); with at most K eligible blocks it is all of them.  For the
+ * selection in block_idx:
+ *   metrics[..., 0] = |selection & reference| / K         (Recall@K)
+ *   metrics[..., 1] = sum of P over the selection          (captured mass)
+ *   metrics[..., 2] = metrics[..., 1] / sum of P over the reference
+ *                                                          (attention mass ratio)
+ * rows: device int32 [n_rows], query-row indices; a row outside [0, Nq)
+ * gets NaN metrics and an empty reference.  block_idx: [B,Hkv,Nq,K] as
+ * pisa_select writes it (negative entries are padding; repeats count once).
+ * metrics: device float32 [B,Hkv,n_rows,3]; ref_idx: nullable device int32
+ * [B,Hkv,n_rows,K], the reference set ascending, -1 padded.  The work is dense
+ * over every visible key of every listed row (n_rows x N x d per head): meant
+ * for sampled rows.  bf16 inputs, C in {32, 64, 96, 128}, N/C <= 16384, K <= 64;
+ * otherwise PISA_ERR_UNSUPPORTED.  Workspace: pisa_quality_workspace_bytes(p,
+ * n_rows) bytes (the log masses, B*Hkv*n_rows*G*ceil(N/C) floats). */
+size_t pisa_quality_workspace_bytes(const pisa_problem* p, int32_t n_rows);
+int pisa_selection_quality(const pisa_problem* p, const void* q, const void* k, const int32_t* block_idx,
+                           const int32_t* rows, int32_t n_rows, float* metrics, int32_t* ref_idx, void* ws,
+                           size_t ws_bytes, pisa_stream_t stream);
+
 /* Per-kernel timing for benchmarks (not needed for computing anything).
  * pisa_profile_enable(1) makes every later call bracket each kernel it
  * launches with two hipEvents recorded on that call's stream (host-side

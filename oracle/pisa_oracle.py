@@ -32,6 +32,13 @@ Contents and the passage each follows:
 * ``flat_bsa_row``      -- flat block selection, Sec. 3.1 eqs.
                            (bsa_block_scores, bsa_topk), with the per-head
                            normalisation before the head sum of App. C.1.
+* ``block_log_mass``, ``selection_quality_row`` -- the block-selection
+                           diagnostic of Sec. 4 ("Block-selection quality",
+                           eq. oracle_metrics) and App. C ("Block-selection
+                           diagnostic", eq. oracle_block_mass): per-block
+                           log mass of the full attention, the head-averaged
+                           block mass P, the full-attention reference set and
+                           Recall@K / CapturedMass / MassRatio of a selection.
 
 Readings of points the paper leaves open (each also recorded in the design
 notes of the repository):
@@ -51,6 +58,10 @@ notes of the repository):
 * R8  grouped-query heads: query head h' uses KV head h' // (H / Hkv).
 * R9  outputs: selected leaf indices ascending, padded with -1 to K.
 * R10 attention with no visible token returns o = 0 and lse = -inf.
+* R15 diagnostic reference set: the forced blocks of R2 plus the eligible
+      blocks of highest grouped mass P, ties to the smaller index (R4); with
+      at most K eligible blocks it is all of them.  Recall@K divides by K as
+      printed, also for rows with fewer than K eligible blocks.
 """
 from __future__ import annotations
 
@@ -324,6 +335,69 @@ def flat_bsa_row(qg: np.ndarray, leaf_means: np.ndarray, t: int, C: int, K: int,
     return sorted(F | set(keep)), gap
 
 
+def block_log_mass(q: np.ndarray, k: np.ndarray, t: int, C: int, causal: bool) -> np.ndarray:
+    """Log mass of every eligible leaf block for one query vector (App. C,
+    eq. oracle_block_mass): a(B) = log sum over the tokens j of B (j <= t
+    when causal) of exp(q.k_j / sqrt(d)).  Returns an array over the blocks
+    0 .. |E|-1 (E = the causally available blocks, all blocks if not causal).
+    """
+    q = np.asarray(q, dtype=np.float64)
+    N, d = k.shape
+    M1 = -(-N // C)
+    nE = min(t // C + 1, M1) if causal else M1
+    a = np.empty(nE)
+    for b in range(nE):
+        hi = min((b + 1) * C, N)
+        if causal:
+            hi = min(hi, t + 1)
+        z = np.asarray(k[b * C:hi], dtype=np.float64) @ q / math.sqrt(d)
+        a[b] = lse(z)
+    return a
+
+
+def selection_quality_row(qg: np.ndarray, k: np.ndarray, sel, t: int, C: int, K: int, causal: bool):
+    """Selection quality of one (query position, KV head) against the
+    full-attention reference (Sec. 4 eq. oracle_metrics; App. C).
+
+    qg: [G, d] queries of the KV head's query heads; sel: selected leaf
+    blocks (negative entries are padding).  P(B) is, for each head, the
+    softmax of the block log masses over the eligible blocks, averaged over
+    the G heads.  The reference set holds the forced blocks (App. B) and
+    fills the remaining budget with the eligible blocks of highest P.
+
+    Returns a dict: recall = |sel & ref| / K, captured = sum of P over sel,
+    ratio = captured / (sum of P over ref), ref (ascending list), P (array
+    over the eligible blocks), gap (smallest kept minus largest dropped P
+    among the ranked blocks, +inf if nothing was ranked).
+    """
+    qg = np.asarray(qg, dtype=np.float64)
+    G = qg.shape[0]
+    P = None
+    for h in range(G):
+        a = block_log_mass(qg[h], k, t, C, causal)
+        ph = np.exp(a - lse(a))
+        P = ph if P is None else P + ph
+    P = P / G
+    nE = P.size
+    E = list(range(nE))
+    gap = POS_INF
+    if nE <= K:
+        ref = E
+    else:
+        F = forced_leaves(t, C, causal) & set(E)
+        free = [b for b in E if b not in F]
+        order = sorted(free, key=lambda b: (-P[b], b))
+        n_keep = K - len(F)
+        ref = sorted(F | set(order[:n_keep]))
+        if 0 < n_keep < len(free):
+            gap = P[order[n_keep - 1]] - P[order[n_keep]]
+    chosen = sorted({int(b) for b in sel if b >= 0})
+    captured = float(sum(P[b] for b in chosen if b < nE))
+    ref_mass = float(sum(P[b] for b in ref))
+    return {"recall": len(set(chosen) & set(ref)) / K, "captured": captured,
+            "ratio": captured / ref_mass if ref_mass > 0 else 0.0, "ref": ref, "P": P, "gap": gap}
+
+
 # ---------------------------------------------------------------------------
 # Whole-tensor drivers (loops over batch, heads and the requested rows).
 # ---------------------------------------------------------------------------
@@ -423,3 +497,30 @@ def select_flat_bsa(q, k, C, K, causal, rows=None, heads=None):
                 idx[b, hi, ri, :len(sel)] = sel
                 gap[b, hi, ri] = gp
     return idx, gap
+
+
+def selection_quality(q, k, block_idx, C, K, causal, rows, heads=None):
+    """Diagnostic for the given rows of every (batch, KV head).
+
+    block_idx: [B, Hkv, len(rows), K] selections of those rows.  Returns
+    (metrics [B, Hkv, len(rows), 3] = recall, captured, ratio;
+    ref [B, Hkv, len(rows), K] ascending, -1 padded; gap [B, Hkv, len(rows)]).
+    """
+    B, H, Nq, d = q.shape
+    _, Hkv, N, _ = k.shape
+    G = _group(H, Hkv)
+    rows = list(rows)
+    heads = list(range(Hkv)) if heads is None else list(heads)
+    met = np.zeros((B, len(heads), len(rows), 3))
+    ref = np.full((B, len(heads), len(rows), K), -1, dtype=np.int64)
+    gap = np.full((B, len(heads), len(rows)), POS_INF)
+    for b in range(B):
+        for hi, h in enumerate(heads):
+            kh = np.asarray(k[b, h], dtype=np.float64)
+            for ri, r in enumerate(rows):
+                t = N - Nq + r
+                res = selection_quality_row(q[b, h * G:(h + 1) * G, r], kh, block_idx[b, hi, ri], t, C, K, causal)
+                met[b, hi, ri] = (res["recall"], res["captured"], res["ratio"])
+                ref[b, hi, ri, :len(res["ref"])] = res["ref"]
+                gap[b, hi, ri] = res["gap"]
+    return met, ref, gap

@@ -323,6 +323,34 @@ int pisa_sparse_attn_fwd(const pisa_problem* p, const void* q, const void* k, co
       "pisa_sparse_attn_fwd");
 }
 
+size_t pisa_quality_workspace_bytes(const pisa_problem* p, int32_t n_rows) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  if (check_problem(p, &s, &g) != PISA_OK || n_rows < 1) return 0;
+  return pisa::quality_ws(s, n_rows);
+}
+
+int pisa_selection_quality(const pisa_problem* p, const void* q, const void* k, const int32_t* block_idx,
+                           const int32_t* rows, int32_t n_rows, float* metrics, int32_t* ref_idx, void* ws,
+                           size_t ws_bytes, pisa_stream_t stream) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  PISA_TRY(check_problem(p, &s, &g));
+  PISA_TRY(check_ptr(q, "q"));
+  PISA_TRY(check_ptr(k, "k"));
+  PISA_TRY(check_ptr(block_idx, "block_idx"));
+  PISA_TRY(check_ptr(rows, "rows"));
+  PISA_TRY(check_ptr(metrics, "metrics"));
+  PISA_TRY(check_ptr(ref_idx, "ref_idx", true));
+  if (n_rows < 1 || n_rows > (1 << 24)) return fail(PISA_ERR_INVALID_ARG, "n_rows %d out of [1, 2^24]", n_rows);
+  if (!pisa::quality_supported(s))
+    return fail(PISA_ERR_UNSUPPORTED, "the quality diagnostic runs on bf16 with C in {32,64,96,128}, N/C <= 16384, K <= 64");
+  PISA_TRY(check_ws(ws, ws_bytes, pisa::quality_ws(s, n_rows)));
+  return device_status(pisa::launch_quality(s, q, k, block_idx, rows, n_rows, metrics, ref_idx, ws,
+                                            static_cast<hipStream_t>(stream)),
+                       "pisa_selection_quality");
+}
+
 const char* pisa_status_string(int status) {
   switch (status) {
     case PISA_OK: return "ok";

@@ -102,6 +102,17 @@ size_t attn_ws(const Shape& s, const Geo& geo);
 hipError_t launch_attention(const Shape& s, const Geo& geo, const void* q, const void* k, const void* v,
                             const int32_t* idx, void* o, float* lse, void* ws, hipStream_t st);
 
+// Block-selection quality diagnostic (quality.hip).
+struct QualityArgs {
+  int H, Hkv, G, Nq, N, C, K, causal, M1, n_rows;
+  float qscale2;
+  int Nkv;  // rows per (batch, KV head) in k
+};
+size_t quality_ws(const Shape& s, int n_rows);
+bool quality_supported(const Shape& s);
+hipError_t launch_quality(const Shape& s, const void* q, const void* k, const int32_t* idx, const int32_t* rows,
+                          int n_rows, float* metrics, int32_t* ref, void* ws, hipStream_t st);
+
 // Flat block selection baseline.
 size_t bsa_ws(const Shape& s, const Geo& geo);
 hipError_t launch_flat_bsa(const Shape& s, const Geo& geo, const void* q, const float* pyr, int32_t* idx,

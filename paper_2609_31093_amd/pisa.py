@@ -36,6 +36,7 @@ EXPORTS = (
     "pisa_num_levels", "pisa_pyramid_layout", "pisa_pyramid_bytes",
     "pisa_select_workspace_bytes", "pisa_bsa_workspace_bytes", "pisa_attn_workspace_bytes",
     "pisa_build_pyramid", "pisa_pyramid_append", "pisa_select", "pisa_select_flat_bsa", "pisa_sparse_attn_fwd",
+    "pisa_quality_workspace_bytes", "pisa_selection_quality",
     "pisa_profile_enable", "pisa_profile_report", "pisa_status_string", "pisa_last_error",
 )
 
@@ -83,6 +84,8 @@ def _load():
         "pisa_select": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pisa_select_flat_bsa": (ctypes.c_int, [P, vp, vp, vp, vp, sz, vp]),
         "pisa_sparse_attn_fwd": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "pisa_quality_workspace_bytes": (sz, [P, i32]),
+        "pisa_selection_quality": (ctypes.c_int, [P, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp]),
         "pisa_profile_enable": (ctypes.c_int, [ctypes.c_int]),
         "pisa_profile_report": (ctypes.c_int, [ctypes.c_char_p, sz]),
         "pisa_status_string": (ctypes.c_char_p, [ctypes.c_int]),
@@ -183,6 +186,17 @@ def pisa_sparse_attn_fwd(p: Problem, q, k, v, block_idx, o, lse=None, ws=None, w
                   "pisa_sparse_attn_fwd")
 
 
+def pisa_quality_workspace_bytes(p: Problem, n_rows: int) -> int:
+    return _lib.pisa_quality_workspace_bytes(ctypes.byref(p), n_rows)
+
+
+def pisa_selection_quality(p: Problem, q, k, block_idx, rows, n_rows: int, metrics, ref_idx=None, ws=None,
+                           ws_bytes=0, stream=None) -> int:
+    return _check(_lib.pisa_selection_quality(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(block_idx), _ptr(rows), n_rows,
+                                              _ptr(metrics), _ptr(ref_idx), _ptr(ws), ws_bytes, _stream(stream)),
+                  "pisa_selection_quality")
+
+
 def pisa_profile_enable(on: bool) -> int:
     return _lib.pisa_profile_enable(1 if on else 0)
 
@@ -246,3 +260,14 @@ def sparse_attn_fwd(p: Problem, q, k, v, block_idx, stream=None):
     nb = pisa_attn_workspace_bytes(p)
     pisa_sparse_attn_fwd(p, q, k, v, block_idx, o, lse, _workspace(nb, q.device), nb, stream)
     return o, lse
+
+
+def selection_quality(p: Problem, q, k, block_idx, rows, stream=None):
+    """Allocate outputs and workspace, run pisa_selection_quality on the listed
+    rows (a device int32 tensor); returns (metrics [B,Hkv,n,3], ref [B,Hkv,n,K])."""
+    n = int(rows.numel())
+    met = torch.empty((p.B, p.Hkv, n, 3), dtype=torch.float32, device=q.device)
+    ref = torch.empty((p.B, p.Hkv, n, p.K), dtype=torch.int32, device=q.device)
+    nb = pisa_quality_workspace_bytes(p, n)
+    pisa_selection_quality(p, q, k, block_idx, rows, n, met, ref, _workspace(nb, q.device), nb, stream)
+    return met, ref

@@ -169,3 +169,22 @@ def test_capacity_layout():
     assert offs[Lp - 1] == R.value  # the root is not stored
     assert pisa.pisa_pyramid_bytes(p) == pisa.pisa_pyramid_bytes(q)
 
+
+
+def test_selection_quality_validates_before_launch():
+    p = _good()
+    lib = pisa.library()
+    n = 37
+    need = pisa.pisa_quality_workspace_bytes(p, n)
+    M1 = -(-p.N // p.C)
+    assert need == p.B * p.Hkv * n * (p.H // p.Hkv) * M1 * 4
+    assert pisa.pisa_quality_workspace_bytes(p, 0) == 0
+
+    def call(pp=p, rows=FAKE, n_rows=n, metrics=FAKE, ws=FAKE, nb=need):
+        return lib.pisa_selection_quality(ctypes.byref(pp), FAKE, FAKE, FAKE, rows, n_rows, metrics, None, ws, nb,
+                                          None)
+    assert call(rows=None) == pisa.PISA_ERR_INVALID_ARG and "rows" in pisa.pisa_last_error()
+    assert call(metrics=None) == pisa.PISA_ERR_INVALID_ARG
+    assert call(n_rows=0) == pisa.PISA_ERR_INVALID_ARG
+    assert call(nb=need - 1) == pisa.PISA_ERR_WORKSPACE
+    assert call(pp=_good(dtype="f32")) == pisa.PISA_ERR_UNSUPPORTED

@@ -503,3 +503,98 @@ def test_no_intermediate_pruning_equals_flat_topk_for_variants(score):
         order = np.lexsort((np.array(free), -sc))
         assert sel == sorted(forced | {free[j] for j in order[:K - 3]})
 
+
+
+# ------------------------------------------------ selection-quality diagnostic ---
+
+@pytest.mark.parametrize("G,causal", [(1, True), (3, True), (2, False)])
+def test_block_mass_is_dense_softmax_summed_per_block(G, causal):
+    """App. C eq. (oracle_block_mass): exp(a(B)) / sum_B' exp(a(B')) is the
+    full-attention softmax mass of B's tokens.  Checked against scipy's
+    softmax over every visible token, summed per block and averaged over the
+    group's heads; the masses sum to one."""
+    r = _rng(11)
+    N, d, C = 300, 16, 32
+    k = r.standard_normal((N, d))
+    qg = r.standard_normal((G, d))
+    t = 250
+    res = O.selection_quality_row(qg, k, [], t, C, 4, causal)
+    vis = t + 1 if causal else N
+    nE = -(-vis // C)
+    want = np.zeros(nE)
+    for h in range(G):
+        p = softmax(k[:vis] @ qg[h] / math.sqrt(d))
+        for b in range(nE):
+            want[b] += p[b * C:min((b + 1) * C, vis)].sum() / G
+    np.testing.assert_allclose(res["P"], want, rtol=1e-12, atol=1e-15)
+    assert abs(res["P"].sum() - 1.0) < 1e-12
+    # and a(B) itself is scipy's logsumexp over the block's visible logits
+    a = O.block_log_mass(qg[0], k, t, C, causal)
+    for b in range(nE):
+        z = k[b * C:min((b + 1) * C, vis)] @ qg[0] / math.sqrt(d)
+        assert abs(a[b] - logsumexp(z)) < 1e-12
+
+
+def test_quality_of_the_reference_itself():
+    """Sec. 4 eq. (oracle_metrics): a selection equal to the reference set has
+    Recall@K = 1 and MassRatio = 1; its captured mass is the reference's."""
+    r = _rng(12)
+    N, d, C, K = 2000, 16, 32, 6
+    k = r.standard_normal((N, d))
+    q = r.standard_normal((2, d))
+    for t in (700, 1500, 1999):
+        ref = O.selection_quality_row(q, k, [], t, C, K, True)
+        again = O.selection_quality_row(q, k, ref["ref"], t, C, K, True)
+        assert again["recall"] == 1.0 and abs(again["ratio"] - 1.0) < 1e-12
+        assert abs(again["captured"] - sum(ref["P"][b] for b in ref["ref"])) < 1e-12
+
+
+def test_reference_holds_forced_and_heaviest_blocks():
+    """App. C: the reference keeps the first, previous and current blocks and
+    fills the rest with the eligible blocks of highest mass.  Brute force:
+    rank the non-forced blocks by the dense per-block softmax mass."""
+    r = _rng(13)
+    N, d, C, K = 1000, 8, 20, 7
+    k = r.standard_normal((N, d))
+    q = r.standard_normal((1, d)) * 2.0
+    t = 899
+    c = t // C
+    res = O.selection_quality_row(q, k, [], t, C, K, True)
+    p = softmax(k[:t + 1] @ q[0] / math.sqrt(d))
+    mass = np.array([p[b * C:min((b + 1) * C, t + 1)].sum() for b in range(c + 1)])
+    forced = {0, c - 1, c}
+    free = [b for b in np.argsort(-mass, kind="stable") if b not in forced]
+    assert res["ref"] == sorted(forced | set(int(b) for b in free[:K - 3]))
+    # a selection missing one reference block loses exactly that block's mass
+    drop = sorted(free[:K - 3])[0]
+    partial = [b for b in res["ref"] if b != drop]
+    m = O.selection_quality_row(q, k, partial, t, C, K, True)
+    assert abs(m["recall"] - (K - 1) / K) < 1e-15
+    assert abs(m["captured"] - sum(mass[b] for b in partial)) < 1e-12
+    assert abs(m["ratio"] - sum(mass[b] for b in partial) / sum(mass[b] for b in res["ref"])) < 1e-12
+
+
+def test_planted_block_is_in_the_reference():
+    """A block whose keys all equal a large multiple of the query carries
+    nearly all the mass, so the reference (and any selection holding it)
+    captures it."""
+    r = _rng(14)
+    N, d, C, K = 1024, 16, 32, 4
+    k = r.standard_normal((N, d)) * 0.1
+    q = r.standard_normal(d)
+    q /= np.linalg.norm(q)
+    k[10 * C:11 * C] = 40.0 * q  # logit 10 per key against ~0 elsewhere
+    res = O.selection_quality_row(q[None], k, [0, 10, 30, 31], 1000, C, K, True)
+    assert 10 in res["ref"] and res["captured"] > 0.99 and res["ratio"] > 0.999
+
+
+def test_all_blocks_eligible_within_budget():
+    """With at most K eligible blocks the reference is all of them and holds
+    all the mass; Recall@K divides by K (reading R15)."""
+    r = _rng(15)
+    k = r.standard_normal((200, 8))
+    q = r.standard_normal((1, 8))
+    res = O.selection_quality_row(q, k, [0, 1, 2], 100, 32, 8, True)
+    assert res["ref"] == [0, 1, 2, 3]
+    assert abs(res["recall"] - 3 / 8) < 1e-15
+    assert abs(sum(res["P"][b] for b in res["ref"]) - 1.0) < 1e-12
