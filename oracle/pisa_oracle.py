@@ -32,6 +32,12 @@ Contents and the passage each follows:
 * ``flat_bsa_row``      -- flat block selection, Sec. 3.1 eqs.
                            (bsa_block_scores, bsa_topk), with the per-head
                            normalisation before the head sum of App. C.1.
+* ``attention_row_bwd`` -- backward of the selected sparse attention with
+                           the selection held fixed (App. B, "During
+                           backpropagation, the selected block indices are
+                           held fixed"): the gradients of eq.
+                           (selected_sparse_attention) with respect to q, k, v
+                           over the selected, visible tokens only.
 * ``block_log_mass``, ``selection_quality_row`` -- the block-selection
                            diagnostic of Sec. 4 ("Block-selection quality",
                            eq. oracle_metrics) and App. C ("Block-selection
@@ -299,6 +305,39 @@ def attention_row(q: np.ndarray, k: np.ndarray, v: np.ndarray, blocks, t: int,
     return p @ vv, row_lse
 
 
+def attention_row_bwd(q: np.ndarray, k: np.ndarray, v: np.ndarray, blocks, t: int, C: int, causal: bool,
+                      do: np.ndarray):
+    """Gradients of one query's selected attention (App. B: indices fixed).
+
+    With z_j = q.k_j / sqrt(d) over the selected visible tokens T, p = softmax(z),
+    o = sum_j p_j v_j and the output gradient do:
+        dv_j = p_j do,   dp_j = do.v_j,   D = do.o,   ds_j = p_j (dp_j - D),
+        dq = sum_j ds_j k_j / sqrt(d),   dk_j = ds_j q / sqrt(d).
+    Returns (dq [d], tokens [|T|], dk [|T|, d], dv [|T|, d]): the per-token
+    contributions, to be summed over every query row and head that reaches
+    the token.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    do = np.asarray(do, dtype=np.float64)
+    N, d = k.shape
+    tokens = sorted({j for i in blocks if i >= 0
+                     for j in range(i * C, min((i + 1) * C, N))
+                     if not causal or j <= t})
+    if not tokens:
+        return np.zeros(d), [], np.zeros((0, d)), np.zeros((0, d))
+    kk = np.asarray(k[tokens], dtype=np.float64)
+    vv = np.asarray(v[tokens], dtype=np.float64)
+    z = kk @ q / math.sqrt(d)
+    p = np.exp(z - lse(z))
+    o = p @ vv
+    dv = p[:, None] * do[None, :]
+    dp = vv @ do
+    ds = p * (dp - float(do @ o))
+    dq = ds @ kk / math.sqrt(d)
+    dk = ds[:, None] * q[None, :] / math.sqrt(d)
+    return dq, tokens, dk, dv
+
+
 def flat_bsa_row(qg: np.ndarray, leaf_means: np.ndarray, t: int, C: int, K: int,
                  causal: bool):
     """Flat (single-level) block selection for one position and KV head.
@@ -524,3 +563,30 @@ def selection_quality(q, k, block_idx, C, K, causal, rows, heads=None):
                 ref[b, hi, ri, :len(res["ref"])] = res["ref"]
                 gap[b, hi, ri] = res["gap"]
     return met, ref, gap
+
+
+def sparse_attention_bwd(q, k, v, block_idx, do, C, causal):
+    """Gradients of the selected attention for every row and head (indices
+    fixed): q, do [B, H, Nq, d]; k, v [B, Hkv, N, d]; block_idx [B, Hkv, Nq, K].
+    Returns (dq [B, H, Nq, d], dk [B, Hkv, N, d], dv [B, Hkv, N, d]), float64;
+    dk and dv sum the contributions of every query head of the KV group."""
+    B, H, Nq, d = q.shape
+    _, Hkv, N, _ = k.shape
+    G = _group(H, Hkv)
+    dq = np.zeros((B, H, Nq, d))
+    dk = np.zeros((B, Hkv, N, d))
+    dv = np.zeros((B, Hkv, N, d))
+    for b in range(B):
+        for hq in range(H):
+            hk = hq // G
+            kh = np.asarray(k[b, hk], dtype=np.float64)
+            vh = np.asarray(v[b, hk], dtype=np.float64)
+            for r in range(Nq):
+                t = N - Nq + r
+                g_q, tok, g_k, g_v = attention_row_bwd(q[b, hq, r], kh, vh, block_idx[b, hk, r], t, C, causal,
+                                                       do[b, hq, r])
+                dq[b, hq, r] = g_q
+                if tok:
+                    dk[b, hk, tok] += g_k
+                    dv[b, hk, tok] += g_v
+    return dq, dk, dv

@@ -598,3 +598,94 @@ def test_all_blocks_eligible_within_budget():
     assert res["ref"] == [0, 1, 2, 3]
     assert abs(res["recall"] - 3 / 8) < 1e-15
     assert abs(sum(res["P"][b] for b in res["ref"]) - 1.0) < 1e-12
+
+
+# -------------------------------------------------- backward, indices fixed ---
+
+def _masked_dense_grads(q, k, v, idx, do, C, causal):
+    """torch float64 autograd through dense attention with a block mask built
+    from the selected indices (the library's own softmax and matmul)."""
+    B, H, Nq, d = q.shape
+    Hkv, N = k.shape[1], k.shape[2]
+    G = H // Hkv
+    qt = torch.tensor(q, dtype=torch.float64, requires_grad=True)
+    kt = torch.tensor(k, dtype=torch.float64, requires_grad=True)
+    vt = torch.tensor(v, dtype=torch.float64, requires_grad=True)
+    mask = torch.zeros((B, Hkv, Nq, N), dtype=torch.bool)
+    for b in range(B):
+        for h in range(Hkv):
+            for r in range(Nq):
+                t = N - Nq + r
+                for blk in idx[b, h, r]:
+                    if blk < 0:
+                        continue
+                    hi = min((blk + 1) * C, N)
+                    if causal:
+                        hi = min(hi, t + 1)
+                    mask[b, h, r, blk * C:hi] = True
+    kx = kt.repeat_interleave(G, dim=1)
+    vx = vt.repeat_interleave(G, dim=1)
+    z = qt @ kx.transpose(-1, -2) / math.sqrt(d)
+    z = z.masked_fill(~mask.repeat_interleave(G, dim=1), float("-inf"))
+    o = torch.softmax(z, dim=-1) @ vx
+    (o * torch.tensor(do, dtype=torch.float64)).sum().backward()
+    return qt.grad.numpy(), kt.grad.numpy(), vt.grad.numpy()
+
+
+@pytest.mark.parametrize("G,causal", [(1, True), (2, True), (3, False)])
+def test_backward_equals_autograd_of_block_masked_attention(G, causal):
+    """App. B (indices held fixed): the oracle's gradients equal torch's
+    autograd of dense attention restricted to the selected tokens."""
+    r = _rng(21)
+    B, Hkv, Nq, N, d, C, K = 1, 2, 70, 200, 16, 16, 4
+    H = Hkv * G
+    q = r.standard_normal((B, H, Nq, d))
+    k = r.standard_normal((B, Hkv, N, d))
+    v = r.standard_normal((B, Hkv, N, d))
+    do = r.standard_normal((B, H, Nq, d))
+    M1 = -(-N // C)
+    idx = np.full((B, Hkv, Nq, K), -1)
+    for h in range(Hkv):
+        for row in range(Nq):
+            t = N - Nq + row
+            top = t // C if causal else M1 - 1
+            pick = sorted(r.choice(top + 1, size=min(K, top + 1), replace=False))
+            idx[0, h, row, :len(pick)] = pick
+    got = O.sparse_attention_bwd(q, k, v, idx, do, C, causal)
+    want = _masked_dense_grads(q, k, v, idx, do, C, causal)
+    for g_, w_ in zip(got, want):
+        np.testing.assert_allclose(g_, w_, rtol=1e-10, atol=1e-12)
+
+
+def test_backward_matches_finite_differences():
+    """The gradient of L = sum(do * o) by central differences of the oracle's
+    own forward (attention_row), one coordinate of q, k and v at a time."""
+    r = _rng(22)
+    N, d, C, t = 40, 6, 8, 33
+    q = r.standard_normal(d)
+    k = r.standard_normal((N, d))
+    v = r.standard_normal((N, d))
+    do = r.standard_normal(d)
+    blocks = [0, 2, 3, 4]
+
+    def loss(qq, kk, vv):
+        return float(O.attention_row(qq, kk, vv, blocks, t, C, True)[0] @ do)
+
+    dq, tok, dk, dv = O.attention_row_bwd(q, k, v, blocks, t, C, True, do)
+    eps = 1e-6
+    for i in range(d):
+        e = np.zeros(d)
+        e[i] = eps
+        assert abs((loss(q + e, k, v) - loss(q - e, k, v)) / (2 * eps) - dq[i]) < 1e-7
+    for j, tj in enumerate(tok[::5]):
+        for i in (0, d - 1):
+            kp, km = k.copy(), k.copy()
+            kp[tj, i] += eps
+            km[tj, i] -= eps
+            assert abs((loss(q, kp, v) - loss(q, km, v)) / (2 * eps) - dk[tok.index(tj), i]) < 1e-7
+            vp, vm = v.copy(), v.copy()
+            vp[tj, i] += eps
+            vm[tj, i] -= eps
+            assert abs((loss(q, k, vp) - loss(q, k, vm)) / (2 * eps) - dv[tok.index(tj), i]) < 1e-7
+    # a token outside the selection (block 1) and a future token get no gradient
+    assert 9 not in tok and 35 not in tok
