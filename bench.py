@@ -151,6 +151,8 @@ def main():
     ap.add_argument("--decode", action="store_true",
                     help="also time the decode workload: single-token selection + attention steps against one "
                          "prebuilt 128K pyramid (extra JSON line)")
+    ap.add_argument("--backward", action="store_true",
+                    help="also time pisa_sparse_attn_bwd (indices fixed) on the workload's selection (extra JSON line)")
     ap.add_argument("--quality", type=int, default=0,
                     help="also run the block-selection quality diagnostic (Recall@K, captured mass, mass ratio "
                          "against the full-attention reference) for PISA and flat BSA on this many evenly spaced "
@@ -420,6 +422,47 @@ def main():
                                      "streaming_what": f"one step = pisa_pyramid_append of 1 token + pisa_select + "
                                                        f"pisa_sparse_attn_fwd, KV length growing {n0 + 1} -> {Nd} "
                                                        f"in buffers reserved for {Nd} rows"}}), flush=True)
+
+    if args.backward:
+        pisa.pisa_build_pyramid(p, k, pyr, stream)
+        pisa.pisa_select(p, q, k, pyr, idx, None, ws_sel, ws_sel_n, stream)
+        pisa.pisa_sparse_attn_fwd(p, q, k, v, idx, o, lse, ws_att, ws_att_n, stream)
+        gen = torch.Generator(device="cuda").manual_seed(1)
+        d_o = torch.randn(q.shape, device="cuda", generator=gen).to(tdt)
+        dq_, dk_, dv_ = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+        nbb = pisa.pisa_attn_bwd_workspace_bytes(p)
+        ws_b = torch.empty(max(nbb, 1), dtype=torch.uint8, device="cuda")
+
+        def bwd():
+            pisa.pisa_sparse_attn_bwd(p, q, k, v, idx, o, lse, d_o, dq_, dk_, dv_, ws_b, nbb, stream)
+        bwd()
+        torch.cuda.synchronize()
+        nrep = 5
+        pisa.pisa_profile_enable(True)
+        pisa.pisa_profile_report()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(nrep):
+            bwd()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        kb = pisa.pisa_profile_report()
+        pisa.pisa_profile_enable(False)
+        bwd_ms = e0.elapsed_time(e1) / nrep
+        # algorithmic work: per visible (query, key) pair S, dP, dq, dk, dv = 10 d flops
+        bflops = attn_pairs * 10 * d
+        blk = kb.get("attn_bwd_block")
+        out_b = {"workload": args.workload, "ms": bwd_ms, "tokens_per_s": B * Nq / (bwd_ms / 1e3),
+                 "kernels": {n: {"launches": c // nrep, "ms": t / nrep} for n, (c, t) in kb.items()},
+                 "algorithmic_tflop": bflops / 1e12,
+                 "what": "pisa_sparse_attn_bwd: dq, dk, dv with the selection held fixed (inputs resident)"}
+        if blk:
+            blk_s = blk[1] / blk[0] / 1e3
+            out_b["roofline"] = {"kernel": "attn_bwd_block", "bound": "mfma", "achieved": bflops / blk_s / 1e12,
+                                 "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                                 "frac": bflops / blk_s / 1e12 / MFMA_BF16_PEAK_TFLOPS}
+        log(f"[bench] backward: {bwd_ms:.3f} ms")
+        print(json.dumps({"backward": out_b}), flush=True)
 
     if args.quality:
         n_q = args.quality

@@ -181,6 +181,25 @@ int pisa_sparse_attn_fwd(const pisa_problem* p, const void* q, const void* k, co
                          const int32_t* block_idx, void* o, float* lse, void* ws,
                          size_t ws_bytes, pisa_stream_t stream);
 
+/* Backward of the selected sparse attention with the block indices held
+ * fixed (App. B: during backpropagation gradients flow through the attention
+ * over the selected entries, not through the selection).  For every row and
+ * query head, with z = q.k / sqrt(d) over the selected visible tokens,
+ * p = exp(z - lse) and D = d_o . o:
+ *   dv_j += p_j d_o,  ds_j = p_j (d_o . v_j - D),  dq = sum_j ds_j k_j / sqrt(d),
+ *   dk_j += ds_j q / sqrt(d)
+ * (dk, dv summed over every row and query head that reaches token j).
+ * o and lse are the forward's outputs (pisa_sparse_attn_fwd on the same
+ * block_idx); d_o has o's layout.  Writes dq [B,H,Nq,d] and dk, dv in k's
+ * layout [B,Hkv,N,d] (row stride Ncap; every stored row is written, rows no
+ * query reaches get 0), all in the problem dtype; sums run in fp32.  bf16
+ * with d in {64,128} and C in {32,64,96,128}, else PISA_ERR_UNSUPPORTED.
+ * Workspace: pisa_attn_bwd_workspace_bytes(p). */
+size_t pisa_attn_bwd_workspace_bytes(const pisa_problem* p);
+int pisa_sparse_attn_bwd(const pisa_problem* p, const void* q, const void* k, const void* v,
+                         const int32_t* block_idx, const void* o, const float* lse, const void* d_o, void* dq,
+                         void* dk, void* dv, void* ws, size_t ws_bytes, pisa_stream_t stream);
+
 /* Block-selection quality diagnostic (Sec. 4 "Block-selection quality", eq.
  * oracle_metrics; App. C "Block-selection diagnostic", eq. oracle_block_mass).
  * For each (batch, KV head) and each listed query row: the full attention's

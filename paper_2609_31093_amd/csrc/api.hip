@@ -323,6 +323,37 @@ int pisa_sparse_attn_fwd(const pisa_problem* p, const void* q, const void* k, co
       "pisa_sparse_attn_fwd");
 }
 
+size_t pisa_attn_bwd_workspace_bytes(const pisa_problem* p) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  if (check_problem(p, &s, &g) != PISA_OK || !pisa::attn_bwd_supported(s)) return 0;
+  return pisa::attn_bwd_ws(s, g);
+}
+
+int pisa_sparse_attn_bwd(const pisa_problem* p, const void* q, const void* k, const void* v,
+                         const int32_t* block_idx, const void* o, const float* lse, const void* d_o, void* dq,
+                         void* dk, void* dv, void* ws, size_t ws_bytes, pisa_stream_t stream) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  PISA_TRY(check_problem(p, &s, &g));
+  PISA_TRY(check_ptr(q, "q"));
+  PISA_TRY(check_ptr(k, "k"));
+  PISA_TRY(check_ptr(v, "v"));
+  PISA_TRY(check_ptr(block_idx, "block_idx"));
+  PISA_TRY(check_ptr(o, "o"));
+  PISA_TRY(check_ptr(lse, "lse"));
+  PISA_TRY(check_ptr(d_o, "d_o"));
+  PISA_TRY(check_ptr(dq, "dq"));
+  PISA_TRY(check_ptr(dk, "dk"));
+  PISA_TRY(check_ptr(dv, "dv"));
+  if (!pisa::attn_bwd_supported(s))
+    return fail(PISA_ERR_UNSUPPORTED, "the attention backward runs on bf16 with d in {64,128} and C in {32,64,96,128}");
+  PISA_TRY(check_ws(ws, ws_bytes, pisa::attn_bwd_ws(s, g)));
+  return device_status(pisa::launch_attention_bwd(s, g, q, k, v, block_idx, o, lse, d_o, dq, dk, dv, ws,
+                                                  static_cast<hipStream_t>(stream)),
+                       "pisa_sparse_attn_bwd");
+}
+
 size_t pisa_quality_workspace_bytes(const pisa_problem* p, int32_t n_rows) {
   pisa::Shape s{};
   pisa::Geo g{};

@@ -169,11 +169,15 @@ int64_t cluster_max_tiles(int BH, int M1, int64_t max_pairs) {
   return (max_pairs + kClusterTile - 1) / kClusterTile + static_cast<int64_t>(BH) * M1;
 }
 
+int64_t cluster_max_chunks(int BH, int M1, int64_t max_pairs, int tile) {
+  return (max_pairs + tile - 1) / tile + static_cast<int64_t>(BH) * M1;
+}
+
 static size_t al(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
-hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* out, hipStream_t st) {
+hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* out, hipStream_t st, int tile) {
   // the rows read are [row0, row0 + nrows) of [0, Nq): refuse anything else
-  if (a.row0 < 0 || a.nrows < 1 || a.row0 + a.nrows > a.Nq || a.M1 < 1 ||
+  if (a.row0 < 0 || a.nrows < 1 || a.row0 + a.nrows > a.Nq || a.M1 < 1 || tile < 1 ||
       (a.mode == kClusterLeafParent && a.g < 2))
     return hipErrorInvalidValue;
   const int64_t ncl = static_cast<int64_t>(BH) * a.M1;
@@ -192,7 +196,7 @@ hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* ou
   dim3 grid((a.nrows + kClusterRows - 1) / kClusterRows, BH);
   const size_t lds = static_cast<size_t>(a.M1) * 4;
   cluster_hist_kernel<<<grid, kClusterThreads, lds, st>>>(a, hist);
-  cluster_scan_kernel<<<1, 1024, 0, st>>>(hist, offs, cursor, toffs, ncl, kClusterTile);
+  cluster_scan_kernel<<<1, 1024, 0, st>>>(hist, offs, cursor, toffs, ncl, tile);
   cluster_scatter_kernel<<<grid, kClusterThreads, lds, st>>>(a, cursor, pairs);
   return hipGetLastError();
 }

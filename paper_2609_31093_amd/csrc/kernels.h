@@ -73,7 +73,25 @@ __device__ __forceinline__ bool cluster_tile(const int32_t* __restrict__ offs, c
   end = min(offs[cl + 1], beg + kClusterTile);
   return true;
 }
-hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* out, hipStream_t st);
+// Chunk w of the cluster list when the consumer takes up to `tile` pairs per
+// workgroup (the tile offsets of launch_cluster(..., tile)).
+__device__ __forceinline__ bool cluster_chunk(const int32_t* __restrict__ offs, const int32_t* __restrict__ toffs,
+                                              int64_t ncl, int64_t w, int tile, int64_t& cl, int& beg, int& end) {
+  if (w >= toffs[ncl]) return false;
+  int64_t lo = 0, hi = ncl - 1;
+  while (lo < hi) {
+    const int64_t mid = (lo + hi + 1) >> 1;
+    if (toffs[mid] <= w) lo = mid; else hi = mid - 1;
+  }
+  cl = lo;
+  beg = offs[cl] + static_cast<int>(w - toffs[cl]) * tile;
+  end = min(offs[cl + 1], beg + tile);
+  return true;
+}
+// Groups the pairs by block; toffs counts `tile`-pair chunks per cluster.
+hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* out, hipStream_t st,
+                          int tile = kClusterTile);
+int64_t cluster_max_chunks(int BH, int M1, int64_t max_pairs, int tile);
 
 hipError_t launch_build_pyramid(const Geo& geo, int BH, int D, bool bf16, const void* k, float* pyr,
                                 hipStream_t st);
@@ -96,6 +114,13 @@ size_t select_two_stage_ws(const Shape& s, const Geo& geo);
 hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q, const void* k,
                                    const float* pyr, int32_t* idx, float* score, void* ws,
                                    hipStream_t st);
+
+// Backward of the sparse attention with the selection held fixed (attn_bwd.hip).
+size_t attn_bwd_ws(const Shape& s, const Geo& geo);
+bool attn_bwd_supported(const Shape& s);
+hipError_t launch_attention_bwd(const Shape& s, const Geo& geo, const void* q, const void* k, const void* v,
+                                const int32_t* idx, const void* o, const float* lse, const void* d_o, void* dq,
+                                void* dk, void* dv, void* ws, hipStream_t st);
 
 // Sparse attention.
 size_t attn_ws(const Shape& s, const Geo& geo);

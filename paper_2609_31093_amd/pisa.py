@@ -36,6 +36,7 @@ EXPORTS = (
     "pisa_num_levels", "pisa_pyramid_layout", "pisa_pyramid_bytes",
     "pisa_select_workspace_bytes", "pisa_bsa_workspace_bytes", "pisa_attn_workspace_bytes",
     "pisa_build_pyramid", "pisa_pyramid_append", "pisa_select", "pisa_select_flat_bsa", "pisa_sparse_attn_fwd",
+    "pisa_attn_bwd_workspace_bytes", "pisa_sparse_attn_bwd",
     "pisa_quality_workspace_bytes", "pisa_selection_quality",
     "pisa_profile_enable", "pisa_profile_report", "pisa_status_string", "pisa_last_error",
 )
@@ -84,6 +85,8 @@ def _load():
         "pisa_select": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pisa_select_flat_bsa": (ctypes.c_int, [P, vp, vp, vp, vp, sz, vp]),
         "pisa_sparse_attn_fwd": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "pisa_attn_bwd_workspace_bytes": (sz, [P]),
+        "pisa_sparse_attn_bwd": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pisa_quality_workspace_bytes": (sz, [P, i32]),
         "pisa_selection_quality": (ctypes.c_int, [P, vp, vp, vp, vp, i32, vp, vp, vp, sz, vp]),
         "pisa_profile_enable": (ctypes.c_int, [ctypes.c_int]),
@@ -186,6 +189,17 @@ def pisa_sparse_attn_fwd(p: Problem, q, k, v, block_idx, o, lse=None, ws=None, w
                   "pisa_sparse_attn_fwd")
 
 
+def pisa_attn_bwd_workspace_bytes(p: Problem) -> int:
+    return _lib.pisa_attn_bwd_workspace_bytes(ctypes.byref(p))
+
+
+def pisa_sparse_attn_bwd(p: Problem, q, k, v, block_idx, o, lse, d_o, dq, dk, dv, ws=None, ws_bytes=0,
+                         stream=None) -> int:
+    return _check(_lib.pisa_sparse_attn_bwd(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(v), _ptr(block_idx), _ptr(o),
+                                            _ptr(lse), _ptr(d_o), _ptr(dq), _ptr(dk), _ptr(dv), _ptr(ws), ws_bytes,
+                                            _stream(stream)), "pisa_sparse_attn_bwd")
+
+
 def pisa_quality_workspace_bytes(p: Problem, n_rows: int) -> int:
     return _lib.pisa_quality_workspace_bytes(ctypes.byref(p), n_rows)
 
@@ -271,3 +285,13 @@ def selection_quality(p: Problem, q, k, block_idx, rows, stream=None):
     nb = pisa_quality_workspace_bytes(p, n)
     pisa_selection_quality(p, q, k, block_idx, rows, n, met, ref, _workspace(nb, q.device), nb, stream)
     return met, ref
+
+
+def sparse_attn_bwd(p: Problem, q, k, v, block_idx, o, lse, d_o, stream=None):
+    """Allocate gradients and workspace, run pisa_sparse_attn_bwd; returns (dq, dk, dv)."""
+    dq = torch.empty_like(q)
+    dk = torch.empty_like(k)
+    dv = torch.empty_like(v)
+    nb = pisa_attn_bwd_workspace_bytes(p)
+    pisa_sparse_attn_bwd(p, q, k, v, block_idx, o, lse, d_o, dq, dk, dv, _workspace(nb, q.device), nb, stream)
+    return dq, dk, dv

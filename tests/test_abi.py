@@ -188,3 +188,22 @@ def test_selection_quality_validates_before_launch():
     assert call(n_rows=0) == pisa.PISA_ERR_INVALID_ARG
     assert call(nb=need - 1) == pisa.PISA_ERR_WORKSPACE
     assert call(pp=_good(dtype="f32")) == pisa.PISA_ERR_UNSUPPORTED
+
+
+def test_attention_backward_validates_before_launch():
+    p = _good()
+    lib = pisa.library()
+    need = pisa.pisa_attn_bwd_workspace_bytes(p)
+    assert need > 0
+    args = [FAKE] * 10
+
+    def call(pp=p, args=args, ws=FAKE, nb=need):
+        return lib.pisa_sparse_attn_bwd(ctypes.byref(pp), *args, ws, nb, None)
+    for i, name in enumerate(["q", "k", "v", "block_idx", "o", "lse", "d_o", "dq", "dk", "dv"]):
+        bad = list(args)
+        bad[i] = None
+        assert call(args=bad) == pisa.PISA_ERR_INVALID_ARG, name
+        assert name in pisa.pisa_last_error()
+    assert call(nb=need - 1) == pisa.PISA_ERR_WORKSPACE
+    assert call(pp=_good(dtype="f32")) == pisa.PISA_ERR_UNSUPPORTED
+    assert pisa.pisa_attn_bwd_workspace_bytes(_good(dtype="f32")) == 0
