@@ -336,8 +336,8 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
                 float d0 = 0.f;
 #pragma unroll
                 for (int e = 0; e < DPL; ++e) d0 = fmaf(qv[hh][e], x[u][e], d0);
-                d0 = sum16(d0);
-                if (sub == 0 && p < npairs) zbuf[p * G + hh] = ld[u] ? d0 : -INFINITY;
+                d0 = rowsum16_to15(d0);  // DPP row reduction: the total lands in the group's lane 15
+                if (sub == 15 && p < npairs) zbuf[p * G + hh] = ld[u] ? d0 : -INFINITY;
               }
             }
           }
