@@ -842,7 +842,7 @@ __device__ __forceinline__ float reduce_scatter(float (&w)[LPE], int sub) {
 // Logits of pyramid row `ri` (this lane's slot) against every head's query:
 // the group's LPE rows are loaded together, lane sub reading chunks
 // sub, sub + LPE, ... (pbase already points at chunk sub of row 0).
-template <int D, int GMAX, int LPE, int INFLIGHT>
+template <int D, int GMAX, int LPE, int INFLIGHT, int RS = D>
 __device__ __forceinline__ void slot_dots(const float* __restrict__ pbase, int ri, const float (&qv)[GMAX][D / LPE],
                                           int sub, int lane, float (&z)[GMAX]) {
   constexpr int NCH = D / LPE / 4;
@@ -854,7 +854,7 @@ __device__ __forceinline__ void slot_dots(const float* __restrict__ pbase, int r
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
       const int rj = group_bcast<LPE>(ri, j0 + u, lane);
-      const float* rp = pbase + static_cast<int64_t>(rj) * D;
+      const float* rp = pbase + static_cast<int64_t>(rj) * RS;
 #pragma unroll
       for (int i = 0; i < NCH; ++i) x[u][i] = *reinterpret_cast<const float4*>(rp + i * LPE * 4);
     }
@@ -959,16 +959,21 @@ __device__ __forceinline__ void g2_store_leaves(const SelArgs& a, int bh, int ro
   }
 }
 
-template <int D, int GMAX, int LPE, int KIND>
-__global__ __launch_bounds__(256) void stage1_g2_kernel(SelArgs a) {
+// Stage-1 coarse levels kept in LDS by a workgroup (fp32 rows padded to
+// D + 4 floats): the budget in floats.
+constexpr int kStageFloats = 16384;  // 64 KiB: two workgroups of 8 wavefronts per CU
+
+template <int D, int GMAX, int LPE, int KIND, int NWAVE, bool STAGE>
+__global__ __launch_bounds__(NWAVE * 64) void stage1_g2_kernel(SelArgs a) {
   constexpr int DPL = D / LPE;
   constexpr int NCH = DPL / 4;
+  constexpr int SROW = D + 4;
   const Geo& geo = a.geo;
   const int G = a.G, K = a.K, gK = a.gK;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, hl = lane & 31, hbase = lane & 32;
   const int sub = hl % LPE;
-  const int row = (blockIdx.x * 4 + wave) * 2 + half;
+  const int row = (blockIdx.x * NWAVE + wave) * 2 + half;
   const bool live = row < a.Nq;
   const int rowc = live ? row : a.Nq - 1;
   const int bh = blockIdx.y;
@@ -1007,6 +1012,55 @@ __global__ __launch_bounds__(256) void stage1_g2_kernel(SelArgs a) {
   }
   const int wave_start = max(start, __shfl_xor(start, 32));
 
+  // Coarse levels in LDS: every level read by the workgroup's rows, from the
+  // coarsest down, whose eligible prefix (for the last row, plus one row for
+  // the second child of the last eligible node) still fits the budget; each
+  // row then reads them from LDS instead of through the L1 data path.
+  extern __shared__ float stg[];
+  int stage_lo = 1 << 30, stage_hi = -1;  // staged levels [stage_lo, stage_hi]
+  auto stage_rows = [&](int cl, int lb) {
+    const int e = a.causal ? anc_at(geo, cl, lb) + 2 : geo.M[lb];
+    return min(e, geo.M[lb]);
+  };
+  int c_last = c;
+  if constexpr (STAGE) {
+    const int last = min(static_cast<int>(blockIdx.x + 1) * NWAVE * 2, a.Nq) - 1;
+    c_last = (geo.N - a.Nq + last) / geo.C;
+    int tstart = 1;
+    for (int lev = geo.L; lev >= 2; --lev) {
+      if ((a.causal ? min(anc_at(geo, c_last, lev) + 1, geo.M[lev]) : geo.M[lev]) > K) {
+        tstart = lev;
+        break;
+      }
+    }
+    int used = 0;
+    for (int lb = tstart - 1; lb >= 1; --lb) {
+      const int need = stage_rows(c_last, lb) * SROW;
+      if (used + need > kStageFloats) break;
+      if (stage_hi < 0) stage_hi = lb;
+      stage_lo = lb;
+      used += need;
+    }
+    int off = 0;
+    for (int lb = stage_hi; lb >= stage_lo && stage_hi >= 0; --lb) {
+      const int nr = stage_rows(c_last, lb);
+      const float* src = a.pyr + (static_cast<int64_t>(bh) * geo.R + geo.off[lb]) * D;
+      for (int e = threadIdx.x; e < nr * (D / 4); e += NWAVE * 64) {
+        const int r = e / (D / 4), c4 = (e - r * (D / 4)) * 4;
+        *reinterpret_cast<float4*>(stg + off + r * SROW + c4) =
+            *reinterpret_cast<const float4*>(src + static_cast<int64_t>(r) * D + c4);
+      }
+      off += nr * SROW;
+    }
+    __syncthreads();
+  }
+  // LDS offset of staged level lb (levels stacked from stage_hi down)
+  auto stage_off = [&](int lb) {
+    int off = 0;
+    for (int l = stage_hi; l > lb; --l) off += stage_rows(c_last, l) * SROW;
+    return off;
+  };
+
   int node = -1;  // a half is idle (no valid slot) on the levels above its start
   float zs[GMAX];
 #pragma unroll
@@ -1019,12 +1073,16 @@ __global__ __launch_bounds__(256) void stage1_g2_kernel(SelArgs a) {
     const int Mb = geo.M[lb];
     const bool valid = node >= 0;
     const int nch = valid ? min(2, Mb - 2 * node) : 0;
-    const float* pbase = a.pyr + (static_cast<int64_t>(bh) * geo.R + geo.off[lb]) * D + sub * 4;
-
     float z0[GMAX], z1[GMAX];
-    slot_dots<D, GMAX, LPE, 4>(pbase, valid ? 2 * node : 0, qv, sub, lane, z0);
-    if (__ballot(fresh && nch == 2) != 0) {
-      slot_dots<D, GMAX, LPE, 4>(pbase, nch == 2 ? 2 * node + 1 : 0, qv, sub, lane, z1);
+    const bool two = __ballot(fresh && nch == 2) != 0;
+    if (STAGE && lb >= stage_lo && lb <= stage_hi) {
+      const float* sbase = stg + stage_off(lb) + sub * 4;
+      slot_dots<D, GMAX, LPE, 4, SROW>(sbase, valid ? 2 * node : 0, qv, sub, lane, z0);
+      if (two) slot_dots<D, GMAX, LPE, 4, SROW>(sbase, nch == 2 ? 2 * node + 1 : 0, qv, sub, lane, z1);
+    } else {
+      const float* pbase = a.pyr + (static_cast<int64_t>(bh) * geo.R + geo.off[lb]) * D + sub * 4;
+      slot_dots<D, GMAX, LPE, 4>(pbase, valid ? 2 * node : 0, qv, sub, lane, z0);
+      if (two) slot_dots<D, GMAX, LPE, 4>(pbase, nch == 2 ? 2 * node + 1 : 0, qv, sub, lane, z1);
     }
 #pragma unroll
     for (int hh = 0; hh < GMAX; ++hh) z1[hh] = nch < 2 ? -INFINITY : (fresh ? z1[hh] : 2.f * zs[hh] - z0[hh]);
@@ -1795,7 +1853,22 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
       dim3 grid((s.Nq + 7) / 8, s.BH());
       const size_t lds = static_cast<size_t>(8) * words * sizeof(int);
       auto go = [&](auto kern) { kern<<<grid, 256, lds, st>>>(a, words); };
-      auto go2 = [&](auto kern) { kern<<<grid, 256, 0, st>>>(a); };
+      // One head per KV head: 16 rows per workgroup with the coarse levels
+      // staged in LDS.  Several heads: 8 rows per workgroup (the query
+      // registers of four heads leave no room for the staged variant).
+      dim3 grid2((s.Nq + 15) / 16, s.BH());
+      const size_t slds = static_cast<size_t>(kStageFloats) * 4;
+      auto go2 = [&](auto kern) {
+        (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                  static_cast<int>(slds));
+        kern<<<grid2, 512, slds, st>>>(a);
+      };
+      auto go4 = [&](auto kern) { kern<<<grid, 256, 0, st>>>(a); };
+      auto by_kind4 = [&](auto k0, auto k1, auto k2) {
+        if (s.score == kScoreLse) go4(k0);
+        else if (s.score == kScoreMean) go4(k1);
+        else go4(k2);
+      };
       auto by_kind = [&](auto k0, auto k1, auto k2) {
         if (s.score == kScoreLse) go2(k0);
         else if (s.score == kScoreMean) go2(k1);
@@ -1804,18 +1877,18 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
       if (s.g == 2 && s.G <= 4) {
         if (s.D == 128) {
           if (s.G == 1)
-            by_kind(stage1_g2_kernel<128, 1, 16, kScoreLse>, stage1_g2_kernel<128, 1, 16, kScoreMean>,
-                    stage1_g2_kernel<128, 1, 16, kScoreMeanVar>);
+            by_kind(stage1_g2_kernel<128, 1, 16, kScoreLse, 8, true>, stage1_g2_kernel<128, 1, 16, kScoreMean, 8, true>,
+                    stage1_g2_kernel<128, 1, 16, kScoreMeanVar, 8, true>);
           else
-            by_kind(stage1_g2_kernel<128, 4, 8, kScoreLse>, stage1_g2_kernel<128, 4, 8, kScoreMean>,
-                    stage1_g2_kernel<128, 4, 8, kScoreMeanVar>);
+            by_kind4(stage1_g2_kernel<128, 4, 8, kScoreLse, 4, false>, stage1_g2_kernel<128, 4, 8, kScoreMean, 4, false>,
+                     stage1_g2_kernel<128, 4, 8, kScoreMeanVar, 4, false>);
         } else {
           if (s.G == 1)
-            by_kind(stage1_g2_kernel<64, 1, 16, kScoreLse>, stage1_g2_kernel<64, 1, 16, kScoreMean>,
-                    stage1_g2_kernel<64, 1, 16, kScoreMeanVar>);
+            by_kind(stage1_g2_kernel<64, 1, 16, kScoreLse, 8, true>, stage1_g2_kernel<64, 1, 16, kScoreMean, 8, true>,
+                    stage1_g2_kernel<64, 1, 16, kScoreMeanVar, 8, true>);
           else
-            by_kind(stage1_g2_kernel<64, 4, 8, kScoreLse>, stage1_g2_kernel<64, 4, 8, kScoreMean>,
-                    stage1_g2_kernel<64, 4, 8, kScoreMeanVar>);
+            by_kind4(stage1_g2_kernel<64, 4, 8, kScoreLse, 4, false>, stage1_g2_kernel<64, 4, 8, kScoreMean, 4, false>,
+                     stage1_g2_kernel<64, 4, 8, kScoreMeanVar, 4, false>);
         }
       } else if (s.D == 128) {
         if (s.G == 1) go(stage1_pair_kernel<128, 1, 4>);
