@@ -209,10 +209,12 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
   constexpr int MT = C / 16;       // 16-key tiles of S
   constexpr int LDV = C + 4;       // padded V^T row
   constexpr int DT = D / 16;       // 16-row d tiles of O
+  constexpr int TBS = D + 8;       // padded row of the partial transposition buffer
   extern __shared__ uint16_t lds[];
   uint16_t* klds = lds;
   uint16_t* vt = lds + C * LDK;
   uint32_t* vt32 = reinterpret_cast<uint32_t*>(vt);
+  uint16_t* tbuf = vt + D * LDV;   // [4 wavefronts][16][TBS]
 
   int64_t cl;
   int beg, end;
@@ -359,17 +361,29 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
       l += __shfl_xor(l, 32);
       const float inv = l > 0.f ? 1.0f / l : 0.f;
       const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + slot) * a.G + hh;
-      if (valid) {
-        // oacc[dt][i] = O[d = dt*16 + 4*grp + i][query col]
+      // oacc[dt][i] = O[d = dt*16 + 4*grp + i][query col]: the tile's 16
+      // partial rows go through LDS so that each store writes whole rows
+      // (16 lanes x 16 bytes per row, four rows per instruction).
+      uint16_t* tb = tbuf + wave * (16 * TBS);
 #pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          uint2 w;
-          w.x = pack2_bf16(oacc[dt][0] * inv, oacc[dt][1] * inv);
-          w.y = pack2_bf16(oacc[dt][2] * inv, oacc[dt][3] * inv);
-          *reinterpret_cast<uint2*>(part_o + pidx * D + dt * 16 + 4 * grp) = w;
-        }
-        if (grp == 0) part_lse[pidx] = l > 0.f ? m + fast_log2(l) : -INFINITY;
+      for (int dt = 0; dt < DT; ++dt) {
+        uint2 w;
+        w.x = pack2_bf16(oacc[dt][0] * inv, oacc[dt][1] * inv);
+        w.y = pack2_bf16(oacc[dt][2] * inv, oacc[dt][3] * inv);
+        *reinterpret_cast<uint2*>(tb + col * TBS + dt * 16 + 4 * grp) = w;
       }
+      if (valid && grp == 0) part_lse[pidx] = l > 0.f ? m + fast_log2(l) : -INFINITY;
+      wave_sync();
+#pragma unroll
+      for (int j = 0; j < 16 * D / 8 / 64; ++j) {
+        const int e = j * 64 + lane;           // 16-byte chunk of the tile
+        const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
+        const int64_t pr_idx = __shfl(pidx, r);  // lane r (grp 0) holds column r's pair
+        const bool pv_ok = __shfl(static_cast<int>(valid), r) != 0;
+        const uint4 u = *reinterpret_cast<const uint4*>(tb + r * TBS + c8);
+        if (pv_ok) *reinterpret_cast<uint4*>(part_o + pr_idx * D + c8) = u;
+      }
+      wave_sync();
     }
   }
 }
@@ -944,7 +958,8 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
     {
       ProfScope ps("attn_block", st);
       dim3 grid(static_cast<unsigned>(cluster_max_tiles(s.BH(), geo.M[1], static_cast<int64_t>(s.BH()) * nrows * s.K)));
-      const size_t lds = (static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 4)) * 2;
+      const size_t lds =
+          (static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 4) + 4 * 16 * static_cast<size_t>(D + 8)) * 2;
       const uint16_t* qq = static_cast<const uint16_t*>(q);
       const uint16_t* kk = static_cast<const uint16_t*>(k);
       const uint16_t* vv = static_cast<const uint16_t*>(v);
