@@ -60,7 +60,8 @@ __device__ __forceinline__ void store_bf16_part(uint16_t* p, const float (&x)[DP
 __host__ __device__ constexpr bool bwd_kt(int C, int D) { return C <= 96 || D <= 64; }
 __host__ __device__ constexpr size_t bwd_lds_elems(int C, int D) {
   return 2 * static_cast<size_t>(C) * (D + 8) + (bwd_kt(C, D) ? static_cast<size_t>(D) * (C + 4) : 0) +
-         2 * static_cast<size_t>(C) * (kBwdCols + 8) + 2 * static_cast<size_t>(kBwdCols) * (D + 8);
+         2 * static_cast<size_t>(C) * (kBwdCols + 8) + 2 * static_cast<size_t>(kBwdCols) * (D + 8) +
+         4 * 16 * static_cast<size_t>(D + 8);
 }
 
 // stat[(b*H + h)*Nq + row] = (lse * log2(e), do . o): 16 lanes per (row, head).
@@ -108,6 +109,7 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
   uint16_t* st = pt + C * LPC;                          // [C][LPC] dS^T
   uint16_t* qr = st + C * LPC;                          // [64][LQC] q of the group's columns
   uint16_t* dr = qr + kBwdCols * LQC;                   // [64][LQC] do of the group's columns
+  uint16_t* tb = dr + kBwdCols * LQC + (threadIdx.x >> 6) * 16 * LQC;  // [16][LQC] this wavefront's dq rows
 
   int64_t cl;
   int beg, end;
@@ -238,15 +240,28 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
         qacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(u4_bf16x8b2(ak), sb, qacc[dt], 0, 0, 0);
       }
     }
-    if (pr >= 0) {
+    {
+      // the 16 dq partial rows of this wavefront through LDS, stored as whole
+      // rows (16 lanes x 16 bytes per row)
       const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + slot) * a.G + hh;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         uint2 w;
         w.x = pack2_bf16(qacc[dt][0] * a.rscale, qacc[dt][1] * a.rscale);
         w.y = pack2_bf16(qacc[dt][2] * a.rscale, qacc[dt][3] * a.rscale);
-        *reinterpret_cast<uint2*>(part_dq + pidx * D + dt * 16 + 4 * grp) = w;
+        *reinterpret_cast<uint2*>(tb + col * LQC + dt * 16 + 4 * grp) = w;
       }
+      wave_sync();
+#pragma unroll
+      for (int u = 0; u < 16 * D / 8 / 64; ++u) {
+        const int e = u * 64 + lane;
+        const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
+        const int64_t px = __shfl(pidx, r);  // lanes 0-15 hold columns 0-15
+        const bool ok = __shfl(pr, r) >= 0;
+        const uint4 x = *reinterpret_cast<const uint4*>(tb + r * LQC + c8);
+        if (ok) *reinterpret_cast<uint4*>(part_dq + px * D + c8) = x;
+      }
+      wave_sync();
     }
     // P^T and dS^T of the group, one row per key
 #pragma unroll
