@@ -194,6 +194,8 @@ struct AttnBlockArgs {
 
 __device__ __forceinline__ bf16x8a u4_as_bf16x8(uint4 r) { return __builtin_bit_cast(bf16x8a, r); }
 
+constexpr int kAttnChunk = 1024;  // pairs of one selected-block cluster per workgroup (key block staged once)
+
 template <int D, int CT>
 __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
                                                            const uint16_t* __restrict__ k,
@@ -217,8 +219,8 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
   uint16_t* tbuf = vt + D * LDV;   // [4 wavefronts][16][TBS]
 
   int64_t cl;
-  int beg, end;
-  if (!cluster_tile(offs, toffs, ncl, blockIdx.x, cl, beg, end)) return;
+  int cbeg, cend;
+  if (!cluster_chunk(offs, toffs, ncl, blockIdx.x, kAttnChunk, cl, cbeg, cend)) return;
   const int bh = static_cast<int>(cl / a.M1);
   const int blk = static_cast<int>(cl - static_cast<int64_t>(bh) * a.M1);
   const int b = bh / a.Hkv, h = bh - b * a.Hkv;
@@ -229,11 +231,38 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
   const int wave = threadIdx.x >> 6;
   const int col = lane & 15;   // query column
   const int grp = lane >> 4;   // 0..3: k slice of the operands, row group of the results
-  // This wavefront's 16-pair tiles are wave, wave + 4, ... (at most 4 of a
-  // 256-pair tile); iteration it covers tile it / G and query head it % G.
-  // The pair words of all of them are read up front, and the query operand
-  // of the next iteration is gathered while the current one computes.
+
+  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
+  const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
+  for (int e = threadIdx.x; e < C * (D / 8); e += 256) {
+    const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
+    uint4 kv = make_uint4(0, 0, 0, 0);
+    if (r < nkeys) kv = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
+    *reinterpret_cast<uint4*>(klds + r * LDK + c8) = kv;
+  }
+  for (int e = threadIdx.x; e < (C / 2) * (D / 8); e += 256) {
+    const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
+    uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
+    if (2 * kp < nkeys) v0 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp) * D + c8);
+    if (2 * kp + 1 < nkeys) v1 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp + 1) * D + c8);
+    const uint32_t w0[4] = {v0.x, v0.y, v0.z, v0.w};
+    const uint32_t w1[4] = {v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      vt32[(c8 + 2 * i) * (LDV / 2) + kp] = (w0[i] & 0xFFFFu) | (w1[i] << 16);
+      vt32[(c8 + 2 * i + 1) * (LDV / 2) + kp] = (w0[i] >> 16) | (w1[i] & 0xFFFF0000u);
+    }
+  }
+  __syncthreads();
+
+  // The chunk's pairs in 256-pair tiles.  This wavefront's 16-pair tiles of
+  // a tile are wave, wave + 4, ... (at most 4); iteration it covers tile
+  // it / G and query head it % G.  The pair words of all of them are read up
+  // front, and the query operand of the next iteration is gathered while the
+  // current one computes.
   static_assert(kClusterTile == 256, "four 16-pair tiles per wavefront");
+  for (int beg = cbeg; beg < cend; beg += kClusterTile) {
+  const int end = min(cend, beg + kClusterTile);
   const int ntile = (end - beg + 15) / 16;
   const int nmine = ntile > wave ? (ntile - wave + 3) / 4 : 0;
   const int nit = nmine * a.G;
@@ -258,29 +287,6 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
   };
   bf16x8a qn[KS];
   if (nit > 0) gather(0, qn);
-
-  const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
-  const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
-  for (int e = threadIdx.x; e < C * (D / 8); e += 256) {
-    const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
-    uint4 kv = make_uint4(0, 0, 0, 0);
-    if (r < nkeys) kv = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
-    *reinterpret_cast<uint4*>(klds + r * LDK + c8) = kv;
-  }
-  for (int e = threadIdx.x; e < (C / 2) * (D / 8); e += 256) {
-    const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
-    uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
-    if (2 * kp < nkeys) v0 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp) * D + c8);
-    if (2 * kp + 1 < nkeys) v1 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp + 1) * D + c8);
-    const uint32_t w0[4] = {v0.x, v0.y, v0.z, v0.w};
-    const uint32_t w1[4] = {v1.x, v1.y, v1.z, v1.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      vt32[(c8 + 2 * i) * (LDV / 2) + kp] = (w0[i] & 0xFFFFu) | (w1[i] << 16);
-      vt32[(c8 + 2 * i + 1) * (LDV / 2) + kp] = (w0[i] >> 16) | (w1[i] & 0xFFFF0000u);
-    }
-  }
-  __syncthreads();
 
   for (int it = 0; it < nit; ++it) {
     bf16x8a qb[KS];
@@ -385,6 +391,7 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
       }
       wave_sync();
     }
+  }
   }
 }
 
@@ -952,12 +959,13 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
     ClusterArgs ca{idx, nullptr, s.K, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], local ? kClusterAttnFar : kClusterAttn,
                    row0, nrows, s.g};
     ClusterOut co{};
-    if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st)) != hipSuccess) return e;
+    if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st, kAttnChunk)) != hipSuccess) return e;
     AttnBlockArgs a{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], row0, nrows,
                     kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv};
     {
       ProfScope ps("attn_block", st);
-      dim3 grid(static_cast<unsigned>(cluster_max_tiles(s.BH(), geo.M[1], static_cast<int64_t>(s.BH()) * nrows * s.K)));
+      dim3 grid(static_cast<unsigned>(
+          cluster_max_chunks(s.BH(), geo.M[1], static_cast<int64_t>(s.BH()) * nrows * s.K, kAttnChunk)));
       const size_t lds =
           (static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 4) + 4 * 16 * static_cast<size_t>(D + 8)) * 2;
       const uint16_t* qq = static_cast<const uint16_t*>(q);
