@@ -1247,8 +1247,10 @@ struct LeafParentArgs {
   int Nkv;  // rows per (batch, KV head) in k
 };
 
+constexpr int kLeafChunk = 1024;  // (row, parent) entries per workgroup of leaf_parent_kernel
+
 // Leaf scoring grouped by parent node (g*C <= 128 keys): one workgroup per
-// tile of up to kClusterTile (row, first-child slot) entries of one parent;
+// chunk of up to kLeafChunk (row, first-child slot) entries of one parent;
 // the parent's children key blocks are staged in LDS together and each query
 // row is gathered once for all of them; every 32-key MFMA tile belongs to
 // one child, whose LSE is accumulated separately.
@@ -1266,7 +1268,7 @@ __global__ __launch_bounds__(256) void leaf_parent_kernel(LeafParentArgs a, cons
   extern __shared__ uint16_t klds[];
   int64_t cl;
   int beg, end;
-  if (!cluster_tile(offs, toffs, ncl, blockIdx.x, cl, beg, end)) return;
+  if (!cluster_chunk(offs, toffs, ncl, blockIdx.x, kLeafChunk, cl, beg, end)) return;
   const int bh = static_cast<int>(cl / a.M2);
   const int par = static_cast<int>(cl - static_cast<int64_t>(bh) * a.M2);
   const int b = bh / a.Hkv, h = bh - b * a.Hkv;
@@ -1914,11 +1916,12 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
   ClusterArgs ca{a1, a1cnt, s.gK(), s.Nq, s.N, s.C, s.K, s.causal, by_parent ? M2 : geo.M[1],
                  by_parent ? kClusterLeafParent : kClusterLeaf, 0, s.Nq, s.g};
   ClusterOut co{};
-  if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st)) != hipSuccess) return e;
+  if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st, by_parent ? kLeafChunk : kClusterTile)) != hipSuccess)
+    return e;
   if (by_parent) {
     LeafParentArgs lp{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.g, geo.M[1], M2, s.gK(), s.K, s.causal,
                       kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv};
-    dim3 pgrid(static_cast<unsigned>(cluster_max_tiles(s.BH(), M2, rows * s.gK())));
+    dim3 pgrid(static_cast<unsigned>(cluster_max_chunks(s.BH(), M2, rows * s.gK(), kLeafChunk)));
     const size_t plds = static_cast<size_t>(128) * (s.D + 8) * 2;
     {
       ProfScope ps("leaf_score", st);
