@@ -228,6 +228,60 @@ __device__ __forceinline__ float reduce_logits(int kind, const float* z, int n, 
   return mean + 0.5f * kLn2 * (m2 / static_cast<float>(n));
 }
 
+// Rank order (key desc, pack asc) as one ascending 64-bit integer: the high
+// word maps the float key to an unsigned value that decreases as the key
+// grows (total order, -inf last), the low word is the non-negative pack.
+__device__ __forceinline__ uint32_t desc_bits(float key) {
+  const uint32_t u = __float_as_uint(key + 0.0f);  // -0 ranks as +0
+  const uint32_t m = static_cast<uint32_t>(static_cast<int32_t>(u) >> 31);
+  return u ^ (~m & 0x7FFFFFFFu);
+}
+__device__ __forceinline__ float desc_bits_inv(uint32_t d) {
+  const uint32_t m = static_cast<uint32_t>(static_cast<int32_t>(d) >> 31);
+  return __uint_as_float(d ^ (~m & 0x7FFFFFFFu));
+}
+
+// Bitonic sort of 128 (key, pack) entries held two per lane (entry lane and
+// lane + 64) into rank order (key desc, pack asc); packs are non-negative.
+__device__ __forceinline__ void sort128(uint32_t (&hi)[2], uint32_t (&lo)[2], int lane) {
+#pragma unroll
+  for (int k2 = 2; k2 <= 128; k2 <<= 1) {
+#pragma unroll
+    for (int j = k2 >> 1; j >= 1; j >>= 1) {
+      if (j == 64) {  // the two entries of a lane: the lower index keeps the smaller
+        const uint64_t x = (static_cast<uint64_t>(hi[0]) << 32) | lo[0];
+        const uint64_t y = (static_cast<uint64_t>(hi[1]) << 32) | lo[1];
+        const bool sw = y < x;
+        const uint32_t h0 = sw ? hi[1] : hi[0], l0 = sw ? lo[1] : lo[0];
+        hi[1] = sw ? hi[0] : hi[1];
+        lo[1] = sw ? lo[0] : lo[1];
+        hi[0] = h0;
+        lo[0] = l0;
+        continue;
+      }
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const int e = lane + 64 * s;
+        uint32_t ohi, olo;
+        switch (j) {
+          case 1: ohi = xor32_i<1>(hi[s]); olo = xor32_i<1>(lo[s]); break;
+          case 2: ohi = xor32_i<2>(hi[s]); olo = xor32_i<2>(lo[s]); break;
+          case 4: ohi = xor32_i<4>(hi[s]); olo = xor32_i<4>(lo[s]); break;
+          case 8: ohi = xor32_i<8>(hi[s]); olo = xor32_i<8>(lo[s]); break;
+          case 16: ohi = xor32_i<16>(hi[s]); olo = xor32_i<16>(lo[s]); break;
+          default: ohi = __shfl_xor(static_cast<int>(hi[s]), 32); olo = __shfl_xor(static_cast<int>(lo[s]), 32); break;
+        }
+        const uint64_t mine = (static_cast<uint64_t>(hi[s]) << 32) | lo[s];
+        const uint64_t other = (static_cast<uint64_t>(ohi) << 32) | olo;
+        const bool want_small = ((e & k2) == 0) == ((e & j) == 0);
+        const bool take = (other < mine) == want_small;
+        hi[s] = take ? ohi : hi[s];
+        lo[s] = take ? olo : lo[s];
+      }
+    }
+  }
+}
+
 template <typename T, int D, int TEAM, int GMAX, bool FUSED>
 __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
   constexpr int DPL = D / 16;
@@ -254,9 +308,13 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
   float* score = reinterpret_cast<float*>(L + 2 * gK);
   int* flag = L + 3 * gK;
   int* misc = L + 4 * gK;
+  // Per-candidate strides padded by one word so that lanes owning
+  // consecutive candidates hit different LDS banks.
+  const int CS = g * G + 1;           // zbuf stride per candidate
+  const int SS = G + 1;               // zself stride per candidate
   float* zbuf = reinterpret_cast<float*>(L + 4 * gK + 8);
-  float* zself = zbuf + gK * g * G;   // logit of each candidate (per head), NaN if unknown
-  float* zself2 = zself + gK * G;
+  float* zself = zbuf + gK * CS;      // logit of each candidate (per head), NaN if unknown
+  float* zself2 = zself + gK * SS;
 
   const int row = blockIdx.x * ROWS + team;
   if (row >= a.Nq) return;  // the whole team leaves together
@@ -316,7 +374,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
               const int ci = p / g, j = p - ci * g;
               const int node = cand[ci];
               const int nch = min(g, Mb - node * g);
-              const bool derived = j == nch - 1 && !__builtin_isnan(zself[ci * G]);
+              const bool derived = j == nch - 1 && !__builtin_isnan(zself[ci * SS]);
               r = node * g + j;
               ld[u] = j < nch && !fz.is(node) && !derived;
             }
@@ -337,7 +395,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
 #pragma unroll
                 for (int e = 0; e < DPL; ++e) d0 = fmaf(qv[hh][e], x[u][e], d0);
                 d0 = rowsum16_to15(d0);  // DPP row reduction: the total lands in the group's lane 15
-                if (sub == 15 && p < npairs) zbuf[p * G + hh] = ld[u] ? d0 : -INFINITY;
+                if (sub == 15 && p < npairs) zbuf[(p / g) * CS + (p % g) * G + hh] = ld[u] ? d0 : -INFINITY;
               }
             }
           }
@@ -348,13 +406,13 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
           float u = 0.f;
           if (!fz.is(node)) {
             const int nch = min(g, Mb - node * g);
-            const bool has_self = !__builtin_isnan(zself[ci * G]);
+            const bool has_self = !__builtin_isnan(zself[ci * SS]);
             for (int hh = 0; hh < G; ++hh) {
-              float* zc = zbuf + ci * g * G + hh;
+              float* zc = zbuf + ci * CS + hh;
               if (has_self) {
                 float others = 0.f;
                 for (int j = 0; j < nch - 1; ++j) others += zc[j * G];
-                zc[(nch - 1) * G] = static_cast<float>(nch) * zself[ci * G + hh] - others;
+                zc[(nch - 1) * G] = static_cast<float>(nch) * zself[ci * SS + hh] - others;
               }
               u += reduce_logits(a.score_kind, zc, nch, G);
             }
@@ -404,7 +462,33 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
       team_sync<TEAM>();
       // Rank the non-forced candidates; keep forced + the best K - |F|.
       const int keepn = a.K - fz.count();
-      for (int ci = tid; ci < nA; ci += TEAM) {
+      bool sorted = false;
+      if constexpr (TEAM == 64) {
+        if (nA <= 128) {  // one wavefront, two candidates per lane: a bitonic rank sort
+          // Forced candidates sort first (key word 0), then score descending,
+          // ties by candidate index (candidates are ascending node ids), then
+          // the empty slots.
+          uint32_t hi[2], lo[2];
+          int nforced = 0;
+#pragma unroll
+          for (int s2 = 0; s2 < 2; ++s2) {
+            const int ci = lane + 64 * s2;
+            const bool v = ci < nA;
+            const bool f = v && fz.is(cand[ci]);
+            hi[s2] = !v ? 0xFFFFFFFFu : (f ? 0u : desc_bits(score[ci]));
+            lo[s2] = static_cast<uint32_t>(ci);
+            nforced += __popcll(__ballot(f));
+          }
+          sort128(hi, lo, lane);
+#pragma unroll
+          for (int s2 = 0; s2 < 2; ++s2) {
+            const int r = lane + 64 * s2;  // rank among all candidates
+            if (static_cast<int>(lo[s2]) < nA) flag[lo[s2]] = (r < nforced || r - nforced < keepn) ? 1 : 0;
+          }
+          sorted = true;
+        }
+      }
+      for (int ci = tid; !sorted && ci < nA; ci += TEAM) {
         const int node = cand[ci];
         int keep = 1;
         if (!fz.is(node)) {
@@ -447,7 +531,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
           for (int j = 0; j < n; ++j) {
             cand2[pos + j] = c0 + j;
             for (int hh = 0; hh < G; ++hh)
-              zself2[(pos + j) * G + hh] = known ? zbuf[(ci * g + j) * G + hh] : __builtin_nanf("");
+              zself2[(pos + j) * SS + hh] = known ? zbuf[ci * CS + j * G + hh] : __builtin_nanf("");
           }
           pos += n;
         }
@@ -455,7 +539,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
       team_sync<TEAM>();
       for (int ci = tid; ci < total; ci += TEAM) {
         cand[ci] = cand2[ci];
-        for (int hh = 0; hh < G; ++hh) zself[ci * G + hh] = zself2[ci * G + hh];
+        for (int hh = 0; hh < G; ++hh) zself[ci * SS + hh] = zself2[ci * SS + hh];
       }
       nA = total;
       team_sync<TEAM>();
@@ -508,19 +592,6 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
 // staging list.  The leaf candidate set is sorted ascending before it is
 // stored.
 // ----------------------------------------------------------------------------
-
-// Rank order (key desc, pack asc) as one ascending 64-bit integer: the high
-// word maps the float key to an unsigned value that decreases as the key
-// grows (total order, -inf last), the low word is the non-negative pack.
-__device__ __forceinline__ uint32_t desc_bits(float key) {
-  const uint32_t u = __float_as_uint(key + 0.0f);  // -0 ranks as +0
-  const uint32_t m = static_cast<uint32_t>(static_cast<int32_t>(u) >> 31);
-  return u ^ (~m & 0x7FFFFFFFu);
-}
-__device__ __forceinline__ float desc_bits_inv(uint32_t d) {
-  const uint32_t m = static_cast<uint32_t>(static_cast<int32_t>(d) >> 31);
-  return __uint_as_float(d ^ (~m & 0x7FFFFFFFu));
-}
 
 // One compare-exchange stage of the bitonic network, without branches: the
 // lane keeps the smaller of (itself, partner) where the stage wants the
@@ -1732,7 +1803,7 @@ __global__ __launch_bounds__(256) void leaf_slot_kernel(SelArgs a, const int32_t
 
 static int sel_lds_words(const Shape& s) {
   const int gK = s.gK();
-  int w = 4 * gK + 8 + gK * s.g * s.G + 2 * gK * s.G;
+  int w = 4 * gK + 8 + gK * (s.g * s.G + 1) + 2 * gK * (s.G + 1);
   return (w + 3) & ~3;
 }
 
