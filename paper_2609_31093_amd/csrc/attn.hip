@@ -195,9 +195,10 @@ struct AttnBlockArgs {
 __device__ __forceinline__ bf16x8a u4_as_bf16x8(uint4 r) { return __builtin_bit_cast(bf16x8a, r); }
 
 constexpr int kAttnChunk = 1024;  // pairs of one selected-block cluster per workgroup (key block staged once)
+constexpr int kAttnBlockWaves = 8;  // wavefronts per workgroup for blocks of up to 64 keys
 
-template <int D, int CT>
-__global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
+template <int D, int CT, int NW>
+__global__ __launch_bounds__(NW * 64, (CT >= 4 ? 2 : NW == 8 ? 4 : 3)) void attn_block16_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
                                                            const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ v,
                                                            const int32_t* __restrict__ offs,
@@ -216,7 +217,8 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
   uint16_t* klds = lds;
   uint16_t* vt = lds + C * LDK;
   uint32_t* vt32 = reinterpret_cast<uint32_t*>(vt);
-  uint16_t* tbuf = vt + D * LDV;   // [4 wavefronts][16][TBS]
+  uint16_t* tbuf = vt + D * LDV;   // [NW wavefronts][16][TBS]
+  constexpr int NT = 16 / NW;      // 16-pair tiles of a 256-pair tile per wavefront
 
   int64_t cl;
   int cbeg, cend;
@@ -234,13 +236,13 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
 
   const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
   const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
-  for (int e = threadIdx.x; e < C * (D / 8); e += 256) {
+  for (int e = threadIdx.x; e < C * (D / 8); e += NW * 64) {
     const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
     uint4 kv = make_uint4(0, 0, 0, 0);
     if (r < nkeys) kv = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
     *reinterpret_cast<uint4*>(klds + r * LDK + c8) = kv;
   }
-  for (int e = threadIdx.x; e < (C / 2) * (D / 8); e += 256) {
+  for (int e = threadIdx.x; e < (C / 2) * (D / 8); e += NW * 64) {
     const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
     uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
     if (2 * kp < nkeys) v0 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp) * D + c8);
@@ -256,23 +258,28 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
   __syncthreads();
 
   // The chunk's pairs in 256-pair tiles.  This wavefront's 16-pair tiles of
-  // a tile are wave, wave + 4, ... (at most 4); iteration it covers tile
+  // a tile are wave, wave + NW, ... (at most NT); iteration it covers tile
   // it / G and query head it % G.  The pair words of all of them are read up
   // front, and the query operand of the next iteration is gathered while the
   // current one computes.
-  static_assert(kClusterTile == 256, "four 16-pair tiles per wavefront");
+  static_assert(kClusterTile == 256 && NT * NW == 16, "sixteen 16-pair tiles per 256-pair tile");
   for (int beg = cbeg; beg < cend; beg += kClusterTile) {
   const int end = min(cend, beg + kClusterTile);
   const int ntile = (end - beg + 15) / 16;
-  const int nmine = ntile > wave ? (ntile - wave + 3) / 4 : 0;
+  const int nmine = ntile > wave ? (ntile - wave + NW - 1) / NW : 0;
   const int nit = nmine * a.G;
-  int prw[4];
+  int prw[NT];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int p = beg + (wave + 4 * j) * 16 + col;
+  for (int j = 0; j < NT; ++j) {
+    const int p = beg + (wave + NW * j) * 16 + col;
     prw[j] = (j < nmine && p < end) ? pairs[p] : -1;
   }
-  auto pair_of = [&](int j) { return j == 0 ? prw[0] : j == 1 ? prw[1] : j == 2 ? prw[2] : prw[3]; };
+  auto pair_of = [&](int j) {
+    int r = prw[0];
+#pragma unroll
+    for (int jj = 1; jj < NT; ++jj) r = j == jj ? prw[jj] : r;
+    return r;
+  };
   auto gather = [&](int it, bf16x8a (&dst)[KS]) {
     const int j = it / a.G, hh = it - j * a.G;
     const int pr = pair_of(j);
@@ -301,7 +308,10 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
     const int t = a.N - a.Nq + row;
     const int kmax = a.causal ? min(nkeys, t - r0 + 1) : nkeys;
     {
-      // S^T tile mt holds keys mt*16 + 4*grp + i (i = 0..3) of query `col`.
+      // S^T tile mt holds raw logits (unscaled) of keys mt*16 + 4*grp + i
+      // (i = 0..3) of query `col`; keys at or past the query's causal limit
+      // become -inf, a test made only when some pair of the tile needs it.
+      const bool masked = __ballot(kmax < C) != 0;
       auto s_tile = [&](int mt) {
         f32x4a acc = {0.f, 0.f, 0.f, 0.f};
         const uint16_t* arow = klds + (mt * 16 + col) * LDK + grp * 8;
@@ -310,41 +320,51 @@ __global__ __launch_bounds__(256) void attn_block16_kernel(AttnBlockArgs a, cons
           const bf16x8a av = u4_as_bf16x8(*reinterpret_cast<const uint4*>(arow + ks * 32));
           acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av, qb[ks], acc, 0, 0, 0);
         }
+        if (masked) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int key = mt * 16 + 4 * grp + i;
-          acc[i] = key < kmax ? acc[i] * a.qscale2 : -INFINITY;
+          for (int i = 0; i < 4; ++i) acc[i] = mt * 16 + 4 * grp + i < kmax ? acc[i] : -INFINITY;
         }
         return acc;
       };
-      // pass A: the block-local maximum of the query's logits
+      // The block-local maximum m (scaled, log2 units), then P = 2^(S*scale
+      // - m) per 32-key step and O^T += V^T P.  Blocks of up to 64 keys keep
+      // their S tiles in registers; larger ones recompute them in the second
+      // pass.  The P operand k = 8*grp + i holds key 32s + 4*grp + i (i < 4)
+      // or 32s + 16 + 4*grp + (i - 4) (i >= 4); the V^T operand reads the
+      // same keys.
+      constexpr bool kKeepS = MT <= 4;
+      f32x4a st[kKeepS ? MT : 1];
       float m = -INFINITY;
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
         const f32x4a sa = s_tile(mt);
+        if constexpr (kKeepS) st[mt] = sa;
         m = fmaxf(m, fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])));
       }
       m = fmaxf(m, __shfl_xor(m, 16));
       m = fmaxf(m, __shfl_xor(m, 32));
-      const float msafe = (m == -INFINITY) ? 0.f : m;
-      // keep pass A's tiles from being reused (recomputing S is cheaper than
-      // holding it in registers)
-      asm volatile("" ::: "memory");
-      // pass B: P = 2^(S - m) per 32-key step and O^T += V^T P.  The P operand
-      // k = 8*grp + i holds key 32s + 4*grp + i (i < 4) or 32s + 16 + 4*grp +
-      // (i - 4) (i >= 4); the V^T operand reads the same keys.
+      const float msafe = (m == -INFINITY) ? 0.f : m * a.qscale2;
+      m = msafe;
+      if constexpr (!kKeepS) asm volatile("" ::: "memory");  // recompute rather than hold the tiles
       f32x4a oacc[DT];
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x4a{0.f, 0.f, 0.f, 0.f};
       float l = 0.f;
 #pragma unroll
       for (int s2 = 0; s2 < MT / 2; ++s2) {
-        const f32x4a sa = s_tile(2 * s2), sb = s_tile(2 * s2 + 1);
+        f32x4a sa, sb;
+        if constexpr (kKeepS) {
+          sa = st[2 * s2];
+          sb = st[2 * s2 + 1];
+        } else {
+          sa = s_tile(2 * s2);
+          sb = s_tile(2 * s2 + 1);
+        }
         float pv[8];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          pv[i] = fast_exp2(sa[i] - msafe);
-          pv[4 + i] = fast_exp2(sb[i] - msafe);
+          pv[i] = fast_exp2(fmaf(sa[i], a.qscale2, -msafe));
+          pv[4 + i] = fast_exp2(fmaf(sb[i], a.qscale2, -msafe));
         }
 #pragma unroll
         for (int i = 0; i < 8; ++i) l += pv[i];
@@ -966,24 +986,26 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
       ProfScope ps("attn_block", st);
       dim3 grid(static_cast<unsigned>(
           cluster_max_chunks(s.BH(), geo.M[1], static_cast<int64_t>(s.BH()) * nrows * s.K, kAttnChunk)));
-      const size_t lds =
-          (static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 4) + 4 * 16 * static_cast<size_t>(D + 8)) * 2;
       const uint16_t* qq = static_cast<const uint16_t*>(q);
       const uint16_t* kk = static_cast<const uint16_t*>(k);
       const uint16_t* vv = static_cast<const uint16_t*>(v);
-      auto go = [&](auto kern) {
+      // Blocks of up to 64 keys: eight wavefronts share the staged block
+      // (two workgroups, 16 wavefronts per CU); larger blocks: four.
+      auto go = [&](auto kern, int nw) {
+        const size_t lds = (static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 4) +
+                            static_cast<size_t>(nw) * 16 * (D + 8)) * 2;
         if (lds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-        kern<<<grid, 256, lds, st>>>(a, qq, kk, vv, co.offs, co.toffs, co.ncl, co.pairs, part_o, part_lse);
+        kern<<<grid, nw * 64, lds, st>>>(a, qq, kk, vv, co.offs, co.toffs, co.ncl, co.pairs, part_o, part_lse);
       };
       if (s.C == 32)
-        go(attn_block16_kernel<D, 1>);
+        go(attn_block16_kernel<D, 1, kAttnBlockWaves>, kAttnBlockWaves);
       else if (s.C == 64)
-        go(attn_block16_kernel<D, 2>);
+        go(attn_block16_kernel<D, 2, kAttnBlockWaves>, kAttnBlockWaves);
       else if (s.C == 96)
-        go(attn_block16_kernel<D, 3>);
+        go(attn_block16_kernel<D, 3, 4>, 4);
       else
-        go(attn_block16_kernel<D, 4>);
+        go(attn_block16_kernel<D, 4, 4>, 4);
     }
     if (local) {
       ProfScope ps("attn_local", st);

@@ -78,6 +78,10 @@ __global__ __launch_bounds__(kClusterThreads) void cluster_hist_kernel(ClusterAr
 
 // Exclusive scans of the n counts into offs[0..n] (pair offsets, also copied
 // to cursor) and of their tile counts ceil(count / tile) into toffs[0..n].
+// Each thread owns a contiguous run of the counts; runs of up to kScanRun
+// are read into registers with independent loads.
+constexpr int kScanRun = 32;
+
 __global__ __launch_bounds__(1024) void cluster_scan_kernel(const int32_t* __restrict__ hist,
                                                             int32_t* __restrict__ offs,
                                                             int32_t* __restrict__ cursor,
@@ -85,12 +89,25 @@ __global__ __launch_bounds__(1024) void cluster_scan_kernel(const int32_t* __res
   __shared__ int wsum[16], wtile[16];
   const int tid = threadIdx.x;
   const int64_t per = (n + 1023) / 1024;
-  const int64_t i0 = tid * per, i1 = min(n, i0 + per);
+  const int64_t i0 = min(n, tid * per), i1 = min(n, i0 + per);
+  const int cnt = static_cast<int>(i1 - i0);
+  const bool inreg = per <= kScanRun;
+  int v[kScanRun];
   int local = 0, ltile = 0;
-  for (int64_t i = i0; i < i1; ++i) {
-    const int c = hist[i];
-    local += c;
-    ltile += (c + tile - 1) / tile;
+  if (inreg) {
+#pragma unroll
+    for (int j = 0; j < kScanRun; ++j) v[j] = j < cnt ? hist[i0 + j] : 0;
+#pragma unroll
+    for (int j = 0; j < kScanRun; ++j) {
+      local += v[j];
+      ltile += (v[j] + tile - 1) / tile;
+    }
+  } else {
+    for (int64_t i = i0; i < i1; ++i) {
+      const int c = hist[i];
+      local += c;
+      ltile += (c + tile - 1) / tile;
+    }
   }
   const int lane = tid & 63, w = tid >> 6;
   int x = local, y = ltile;
@@ -115,13 +132,26 @@ __global__ __launch_bounds__(1024) void cluster_scan_kernel(const int32_t* __res
     ttot += wtile[i];
   }
   int run = pre + x - local, trun = tpre + y - ltile;
-  for (int64_t i = i0; i < i1; ++i) {
-    const int c = hist[i];
-    offs[i] = run;
-    cursor[i] = run;
-    toffs[i] = trun;
-    run += c;
-    trun += (c + tile - 1) / tile;
+  if (inreg) {
+#pragma unroll
+    for (int j = 0; j < kScanRun; ++j) {
+      if (j < cnt) {
+        offs[i0 + j] = run;
+        cursor[i0 + j] = run;
+        toffs[i0 + j] = trun;
+      }
+      run += v[j];
+      trun += (v[j] + tile - 1) / tile;
+    }
+  } else {
+    for (int64_t i = i0; i < i1; ++i) {
+      const int c = hist[i];
+      offs[i] = run;
+      cursor[i] = run;
+      toffs[i] = trun;
+      run += c;
+      trun += (c + tile - 1) / tile;
+    }
   }
   if (tid == 0) {
     offs[n] = tot;
