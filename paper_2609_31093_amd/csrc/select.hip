@@ -1393,10 +1393,15 @@ __global__ __launch_bounds__(256) void leaf_parent_kernel(LeafParentArgs a, cons
           acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qb[ks], acc, 0, 0, 0);
         }
         float zv[16];
+        if (kt * 32 + 32 <= nkeys) {  // a full tile: no key past the parent's end
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          zv[r] = key < nkeys ? acc[r] * a.qscale2 : -INFINITY;
+          for (int r = 0; r < 16; ++r) zv[r] = acc[r] * a.qscale2;
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+            zv[r] = key < nkeys ? acc[r] * a.qscale2 : -INFINITY;
+          }
         }
         const ScoreAcc ts = acc_of(KIND, zv);
         const int j = kt / kt_per_child;
