@@ -195,10 +195,10 @@ struct AttnBlockArgs {
 __device__ __forceinline__ bf16x8a u4_as_bf16x8(uint4 r) { return __builtin_bit_cast(bf16x8a, r); }
 
 constexpr int kAttnChunk = 1024;  // pairs of one selected-block cluster per workgroup (key block staged once)
-constexpr int kAttnBlockWaves = 8;  // wavefronts per workgroup for blocks of up to 64 keys
+constexpr int kAttnBlockWaves = 8;  // wavefronts per workgroup of attn_block16_kernel
 
 template <int D, int CT, int NW>
-__global__ __launch_bounds__(NW * 64, (CT >= 4 ? 2 : NW == 8 ? 4 : 3)) void attn_block16_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
+__global__ __launch_bounds__(NW * 64, (CT >= 3 ? 1 : NW == 8 ? 4 : 3)) void attn_block16_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
                                                            const uint16_t* __restrict__ k,
                                                            const uint16_t* __restrict__ v,
                                                            const int32_t* __restrict__ offs,
@@ -275,10 +275,14 @@ __global__ __launch_bounds__(NW * 64, (CT >= 4 ? 2 : NW == 8 ? 4 : 3)) void attn
     prw[j] = (j < nmine && p < end) ? pairs[p] : -1;
   }
   auto pair_of = [&](int j) {
-    int r = prw[0];
+    if constexpr (NT == 4) {
+      return j == 0 ? prw[0] : j == 1 ? prw[1] : j == 2 ? prw[2] : prw[3];
+    } else {
+      int r = prw[0];
 #pragma unroll
-    for (int jj = 1; jj < NT; ++jj) r = j == jj ? prw[jj] : r;
-    return r;
+      for (int jj = 1; jj < NT; ++jj) r = j == jj ? prw[jj] : r;
+      return r;
+    }
   };
   auto gather = [&](int it, bf16x8a (&dst)[KS]) {
     const int j = it / a.G, hh = it - j * a.G;
@@ -308,10 +312,15 @@ __global__ __launch_bounds__(NW * 64, (CT >= 4 ? 2 : NW == 8 ? 4 : 3)) void attn
     const int t = a.N - a.Nq + row;
     const int kmax = a.causal ? min(nkeys, t - r0 + 1) : nkeys;
     {
-      // S^T tile mt holds raw logits (unscaled) of keys mt*16 + 4*grp + i
-      // (i = 0..3) of query `col`; keys at or past the query's causal limit
-      // become -inf, a test made only when some pair of the tile needs it.
-      const bool masked = __ballot(kmax < C) != 0;
+      // S^T tile mt holds the logits of keys mt*16 + 4*grp + i (i = 0..3) of
+      // query `col`; keys at or past the query's causal limit become -inf.
+      // Blocks of up to 64 keys keep their S tiles in registers (raw logits;
+      // the causal mask applied only when some pair of the tile needs it, the
+      // scale folded into the exponent); larger blocks recompute the scaled,
+      // masked tiles in the second pass.
+      constexpr bool kKeepS = MT <= 4;
+      const bool masked = !kKeepS || __ballot(kmax < C) != 0;
+      const float sscale = kKeepS ? 1.f : a.qscale2;
       auto s_tile = [&](int mt) {
         f32x4a acc = {0.f, 0.f, 0.f, 0.f};
         const uint16_t* arow = klds + (mt * 16 + col) * LDK + grp * 8;
@@ -322,17 +331,14 @@ __global__ __launch_bounds__(NW * 64, (CT >= 4 ? 2 : NW == 8 ? 4 : 3)) void attn
         }
         if (masked) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) acc[i] = mt * 16 + 4 * grp + i < kmax ? acc[i] : -INFINITY;
+          for (int i = 0; i < 4; ++i) acc[i] = mt * 16 + 4 * grp + i < kmax ? acc[i] * sscale : -INFINITY;
         }
         return acc;
       };
-      // The block-local maximum m (scaled, log2 units), then P = 2^(S*scale
-      // - m) per 32-key step and O^T += V^T P.  Blocks of up to 64 keys keep
-      // their S tiles in registers; larger ones recompute them in the second
-      // pass.  The P operand k = 8*grp + i holds key 32s + 4*grp + i (i < 4)
-      // or 32s + 16 + 4*grp + (i - 4) (i >= 4); the V^T operand reads the
-      // same keys.
-      constexpr bool kKeepS = MT <= 4;
+      // The block-local maximum m (scaled, log2 units), then P = 2^(S - m)
+      // per 32-key step and O^T += V^T P.  The P operand k = 8*grp + i holds
+      // key 32s + 4*grp + i (i < 4) or 32s + 16 + 4*grp + (i - 4) (i >= 4);
+      // the V^T operand reads the same keys.
       f32x4a st[kKeepS ? MT : 1];
       float m = -INFINITY;
 #pragma unroll
@@ -343,9 +349,10 @@ __global__ __launch_bounds__(NW * 64, (CT >= 4 ? 2 : NW == 8 ? 4 : 3)) void attn
       }
       m = fmaxf(m, __shfl_xor(m, 16));
       m = fmaxf(m, __shfl_xor(m, 32));
-      const float msafe = (m == -INFINITY) ? 0.f : m * a.qscale2;
+      const float msafe = (m == -INFINITY) ? 0.f : (kKeepS ? m * a.qscale2 : m);
       m = msafe;
       if constexpr (!kKeepS) asm volatile("" ::: "memory");  // recompute rather than hold the tiles
+      const float pscale = kKeepS ? a.qscale2 : 1.f;
       f32x4a oacc[DT];
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) oacc[dt] = f32x4a{0.f, 0.f, 0.f, 0.f};
@@ -363,8 +370,8 @@ __global__ __launch_bounds__(NW * 64, (CT >= 4 ? 2 : NW == 8 ? 4 : 3)) void attn
         float pv[8];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          pv[i] = fast_exp2(fmaf(sa[i], a.qscale2, -msafe));
-          pv[4 + i] = fast_exp2(fmaf(sb[i], a.qscale2, -msafe));
+          pv[i] = fast_exp2(fmaf(sa[i], pscale, -msafe));
+          pv[4 + i] = fast_exp2(fmaf(sb[i], pscale, -msafe));
         }
 #pragma unroll
         for (int i = 0; i < 8; ++i) l += pv[i];
@@ -989,8 +996,8 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
       const uint16_t* qq = static_cast<const uint16_t*>(q);
       const uint16_t* kk = static_cast<const uint16_t*>(k);
       const uint16_t* vv = static_cast<const uint16_t*>(v);
-      // Blocks of up to 64 keys: eight wavefronts share the staged block
-      // (two workgroups, 16 wavefronts per CU); larger blocks: four.
+      // Eight wavefronts share the staged block: with blocks of up to 64 keys
+      // two workgroups (16 wavefronts) fit a CU, with larger blocks one.
       auto go = [&](auto kern, int nw) {
         const size_t lds = (static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 4) +
                             static_cast<size_t>(nw) * 16 * (D + 8)) * 2;
@@ -1003,9 +1010,9 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
       else if (s.C == 64)
         go(attn_block16_kernel<D, 2, kAttnBlockWaves>, kAttnBlockWaves);
       else if (s.C == 96)
-        go(attn_block16_kernel<D, 3, 4>, 4);
+        go(attn_block16_kernel<D, 3, kAttnBlockWaves>, kAttnBlockWaves);
       else
-        go(attn_block16_kernel<D, 4, 4>, 4);
+        go(attn_block16_kernel<D, 4, kAttnBlockWaves>, kAttnBlockWaves);
     }
     if (local) {
       ProfScope ps("attn_local", st);

@@ -580,6 +580,226 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
 }
 
 // ----------------------------------------------------------------------------
+// Stage 1 on the matrix cores (bf16 queries, fan-out 2 or 4, at most 16 heads
+// per KV head, 32 < g*K <= 128): one wavefront per query row.
+//
+// Each ranked level scores its candidates' children as one product per
+// 16-child tile on v_mfma_f32_16x16x32_bf16: A = 16 child summary rows (lane
+// l: child row l%16, dims 8*(l/16)..+7 of each 32-dim step), B = the group's
+// query heads as columns (lane l: head l%16, zero past G).  The fp32
+// summaries enter as a bf16 pair hi + lo (hi = the rounded value, lo = the
+// rounded remainder: about 16 mantissa bits) with two products per step; the
+// bf16 queries are exact.  In the result lane l holds tile rows 4*(l/16)+i
+// (i = 0..3) of head l%16, i.e. all children of 4/g candidates, so each
+// lane reduces its candidates' children to per-head scores in registers and
+// a 16-lane row sum adds the heads.  Ranking is the 128-entry register
+// bitonic sort of the wavefront; expansion and the stored leaf candidate set
+// are as in select_kernel.
+// ----------------------------------------------------------------------------
+
+typedef __bf16 bf16x8m __attribute__((ext_vector_type(8)));
+typedef float f32x4m __attribute__((ext_vector_type(4)));
+
+// Score of the first n of a lane's child logits (n >= 1).
+template <int KIND, int NC>
+__device__ __forceinline__ float lane_children_score(const float (&z)[NC], int n) {
+  if constexpr (KIND == kScoreLse) {
+    float m = z[0];
+#pragma unroll
+    for (int i = 1; i < NC; ++i) m = i < n ? fmaxf(m, z[i]) : m;
+    float sm = 0.f;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) sm += i < n ? fast_exp2(z[i] - m) : 0.f;
+    return m + fast_log2(sm);
+  } else {
+    float sum = 0.f;
+#pragma unroll
+    for (int i = 0; i < NC; ++i) sum += i < n ? z[i] : 0.f;
+    const float mean = sum / static_cast<float>(n);
+    if constexpr (KIND == kScoreMean) {
+      return mean;
+    } else {
+      float m2 = 0.f;
+#pragma unroll
+      for (int i = 0; i < NC; ++i) {
+        const float dv = z[i] - mean;
+        m2 += i < n ? dv * dv : 0.f;
+      }
+      return mean + 0.5f * kLn2 * (m2 / static_cast<float>(n));
+    }
+  }
+}
+
+constexpr int kMfmaSelRows = 4;  // rows (wavefronts) per workgroup
+
+template <int D, int GC, int KIND>
+__global__ __launch_bounds__(kMfmaSelRows * 64) void stage1_mfma_kernel(SelArgs a, const uint16_t* __restrict__ hilo) {
+  constexpr int KS = D / 32;      // 32-dim steps
+  constexpr int CPL = 4 / GC;     // candidates per lane in the result layout
+  constexpr int CPT = 16 / GC;    // candidates per 16-row tile
+  __shared__ int s_cand[kMfmaSelRows][128];
+  __shared__ int s_cand2[kMfmaSelRows][128];
+  __shared__ int s_flag[kMfmaSelRows][128];
+  __shared__ float s_score[kMfmaSelRows][128];
+  const Geo& geo = a.geo;
+  const int G = a.G, K = a.K, gK = a.gK;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int row = blockIdx.x * kMfmaSelRows + wave;
+  if (row >= a.Nq) return;  // the whole wavefront leaves; only wavefront-level syncs follow
+  int* cand = s_cand[wave];
+  int* cand2 = s_cand2[wave];
+  int* flag = s_flag[wave];
+  float* score = s_score[wave];
+  const int bh = blockIdx.y;
+  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+  const int t = geo.N - a.Nq + row;
+  const int c = t / geo.C;
+  const int col = lane & 15, quad = lane >> 4;
+
+  bf16x8m qB[KS];
+  {
+    const bool hv = col < G;
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) +
+                           ((static_cast<int64_t>(b) * a.H + h * G + (hv ? col : 0)) * a.Nq + row) * D + 8 * quad;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      uint4 u = make_uint4(0, 0, 0, 0);
+      if (hv) u = *reinterpret_cast<const uint4*>(qrow + ks * 32);
+      qB[ks] = __builtin_bit_cast(bf16x8m, u);
+    }
+  }
+
+  if (lane == 0) cand[0] = 0;
+  int nA = 1;
+  wave_sync();
+  for (int lev = geo.L; lev >= 2; --lev) {
+    const Forced fz = forced_at(geo, lev, c, a.causal);
+    const bool ranked = nA > K;
+    if (ranked) {
+      const int Mb = geo.M[lev - 1];
+      const uint16_t* pb = hilo + (static_cast<int64_t>(bh) * geo.R + geo.off[lev - 1]) * (2 * D) + 16 * quad;
+      const int ntile = (nA * GC + 15) / 16;
+      for (int tile = 0; tile < ntile; ++tile) {
+        // A operand: tile row r = (candidate r / GC, child r % GC)
+        const int r = tile * 16 + col;
+        const int ci = r / GC, j = r % GC;
+        bool ok = false;
+        int crow = 0;
+        if (ci < nA) {
+          const int node = cand[ci];
+          crow = node * GC + j;
+          ok = crow < Mb && !fz.is(node);
+        }
+        const uint16_t* ar = pb + static_cast<int64_t>(ok ? crow : 0) * (2 * D);
+        uint4 hi[KS], lo[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          hi[ks] = make_uint4(0, 0, 0, 0);
+          lo[ks] = make_uint4(0, 0, 0, 0);
+          if (ok) {
+            hi[ks] = *reinterpret_cast<const uint4*>(ar + ks * 64);
+            lo[ks] = *reinterpret_cast<const uint4*>(ar + ks * 64 + 8);
+          }
+        }
+        f32x4m acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8m, hi[ks]), qB[ks], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8m, lo[ks]), qB[ks], acc, 0, 0, 0);
+        }
+        // This lane: tile rows 4*quad + i of head col; candidate(s) tile*CPT + CPL*quad + k.
+#pragma unroll
+        for (int k2 = 0; k2 < CPL; ++k2) {
+          const int cj = tile * CPT + CPL * quad + k2;
+          float z[GC];
+#pragma unroll
+          for (int i = 0; i < GC; ++i) z[i] = acc[k2 * GC + i] * a.qscale2;
+          int n = 1;
+          if (cj < nA) n = max(1, min(GC, Mb - cand[cj] * GC));
+          float u = col < G ? lane_children_score<KIND, GC>(z, n) : 0.f;
+          u = rowsum16_to15(u);
+          if (col == 15 && cj < nA) score[cj] = u;
+        }
+      }
+      wave_sync();
+      // Forced candidates first (key word 0), then score descending, ties by
+      // candidate index (candidates are ascending node ids), then empty slots.
+      const int keepn = K - fz.count();
+      uint32_t khi[2], klo[2];
+      int nforced = 0;
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int ci = lane + 64 * s2;
+        const bool v = ci < nA;
+        const bool f = v && fz.is(cand[ci]);
+        khi[s2] = !v ? 0xFFFFFFFFu : (f ? 0u : desc_bits(score[ci]));
+        klo[s2] = static_cast<uint32_t>(ci);
+        nforced += __popcll(__ballot(f));
+      }
+      sort128(khi, klo, lane);
+#pragma unroll
+      for (int s2 = 0; s2 < 2; ++s2) {
+        const int rk = lane + 64 * s2;
+        if (static_cast<int>(klo[s2]) < nA) flag[klo[s2]] = (rk < nforced || rk - nforced < keepn) ? 1 : 0;
+      }
+    } else {
+      for (int ci = lane; ci < nA; ci += 64) flag[ci] = 1;
+    }
+    wave_sync();
+    // Expand kept nodes to their eligible children at level lev-1.
+    const int Mb = geo.M[lev - 1];
+    const int rmax = a.causal ? min(anc_at(geo, c, lev - 1), Mb - 1) : Mb - 1;
+    const int i0 = lane * 2, i1 = min(nA, i0 + 2);
+    int mine = 0;
+    for (int ci = i0; ci < i1; ++ci) {
+      if (flag[ci]) {
+        const int c0 = cand[ci] * GC;
+        mine += max(0, min(c0 + GC - 1, rmax) - c0 + 1);
+      }
+    }
+    int total;
+    int pos = team_scan<64>(mine, nullptr, total);
+    for (int ci = i0; ci < i1; ++ci) {
+      if (flag[ci]) {
+        const int c0 = cand[ci] * GC;
+        const int n = max(0, min(c0 + GC - 1, rmax) - c0 + 1);
+        for (int jj = 0; jj < n; ++jj) cand2[pos + jj] = c0 + jj;
+        pos += n;
+      }
+    }
+    wave_sync();
+    for (int ci = lane; ci < total; ci += 64) cand[ci] = cand2[ci];
+    nA = total;
+    wave_sync();
+  }
+
+  const int64_t orow = static_cast<int64_t>(bh) * a.Nq + row;
+  for (int ci = lane; ci < gK; ci += 64) a.a1[orow * gK + ci] = ci < nA ? cand[ci] : -1;
+  if (lane == 0) a.a1cnt[orow] = nA;
+}
+
+// Summaries as bf16 pairs for stage1_mfma_kernel: each group of 8 fp32
+// values becomes 8 rounded values (hi) followed by 8 rounded remainders (lo).
+__global__ __launch_bounds__(256) void pyr_hilo_kernel(const float* __restrict__ pyr, uint16_t* __restrict__ hilo,
+                                                       int64_t ngroups) {
+  const int64_t i = blockIdx.x * 256LL + threadIdx.x;
+  if (i >= ngroups) return;
+  const float4 x0 = reinterpret_cast<const float4*>(pyr)[2 * i];
+  const float4 x1 = reinterpret_cast<const float4*>(pyr)[2 * i + 1];
+  const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+  uint32_t hw[4], lw[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    hw[e] = pack2_bf16(x[2 * e], x[2 * e + 1]);
+    const float h0 = __uint_as_float(hw[e] << 16), h1 = __uint_as_float(hw[e] & 0xFFFF0000u);
+    lw[e] = pack2_bf16(x[2 * e] - h0, x[2 * e + 1] - h1);
+  }
+  uint4* out = reinterpret_cast<uint4*>(hilo) + 2 * i;
+  out[0] = make_uint4(hw[0], hw[1], hw[2], hw[3]);
+  out[1] = make_uint4(lw[0], lw[1], lw[2], lw[3]);
+}
+
+// ----------------------------------------------------------------------------
 // Stage 1 for g*K <= 32: two query rows per wavefront, one candidate per lane.
 //
 // Lanes 0-31 own row 2w and lanes 32-63 row 2w+1 (lane hl of a half holds
@@ -1877,8 +2097,16 @@ hipError_t launch_select_fused(const Shape& s, const Geo& geo, const void* q, co
 static size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 struct TwoStageWs {
-  size_t a1, a1cnt, u1, cl, total;
+  size_t a1, a1cnt, u1, cl, hilo, total;
 };
+
+// Stage 1 on the matrix cores: bf16 queries, fan-out 2 or 4, up to 16 heads
+// per KV head, candidate sets wider than one wavefront half (g*K > 32) and
+// within the 128-entry rank sort.
+static bool stage1_mfma_ok(const Shape& s) {
+  return s.bf16 && (s.g == 2 || s.g == 4) && s.G <= 16 && s.gK() > 32 && s.gK() <= 128 &&
+         (s.D == 64 || s.D == 128);
+}
 
 static TwoStageWs two_stage_layout(const Shape& s, const Geo& geo) {
   const size_t rows = static_cast<size_t>(s.BH()) * s.Nq;
@@ -1888,6 +2116,8 @@ static TwoStageWs two_stage_layout(const Shape& s, const Geo& geo) {
   w.a1cnt = o;  o += align256(rows * 4);
   w.u1 = o;     o += align256(rows * s.gK() * 4);
   w.cl = o;     o += align256(cluster_ws(s.BH(), geo.M[1], static_cast<int64_t>(rows) * s.gK()));
+  w.hilo = o;
+  if (stage1_mfma_ok(s)) o += align256(static_cast<size_t>(s.BH()) * geo.R * s.D * 4);  // bf16 hi + lo per value
   w.total = o;
   return w;
 }
@@ -1976,6 +2206,31 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
         if (s.G == 1) go(stage1_pair_kernel<64, 1, 4>);
         else if (s.G <= 4) go(stage1_pair_kernel<64, 4, 16>);
         else go(stage1_pair_kernel<64, 16, 16>);
+      }
+    } else if (stage1_mfma_ok(s)) {
+      uint16_t* hilo = reinterpret_cast<uint16_t*>(base + w.hilo);
+      const int64_t ngroups = static_cast<int64_t>(s.BH()) * geo.R * s.D / 8;
+      pyr_hilo_kernel<<<static_cast<unsigned>((ngroups + 255) / 256), 256, 0, st>>>(pyr, hilo, ngroups);
+      dim3 grid((s.Nq + kMfmaSelRows - 1) / kMfmaSelRows, s.BH());
+      auto go = [&](auto k0, auto k1, auto k2) {
+        if (s.score == kScoreLse) k0<<<grid, kMfmaSelRows * 64, 0, st>>>(a, hilo);
+        else if (s.score == kScoreMean) k1<<<grid, kMfmaSelRows * 64, 0, st>>>(a, hilo);
+        else k2<<<grid, kMfmaSelRows * 64, 0, st>>>(a, hilo);
+      };
+      if (s.D == 128) {
+        if (s.g == 4)
+          go(stage1_mfma_kernel<128, 4, kScoreLse>, stage1_mfma_kernel<128, 4, kScoreMean>,
+             stage1_mfma_kernel<128, 4, kScoreMeanVar>);
+        else
+          go(stage1_mfma_kernel<128, 2, kScoreLse>, stage1_mfma_kernel<128, 2, kScoreMean>,
+             stage1_mfma_kernel<128, 2, kScoreMeanVar>);
+      } else {
+        if (s.g == 4)
+          go(stage1_mfma_kernel<64, 4, kScoreLse>, stage1_mfma_kernel<64, 4, kScoreMean>,
+             stage1_mfma_kernel<64, 4, kScoreMeanVar>);
+        else
+          go(stage1_mfma_kernel<64, 2, kScoreLse>, stage1_mfma_kernel<64, 2, kScoreMean>,
+             stage1_mfma_kernel<64, 2, kScoreMeanVar>);
       }
     } else {
       launch_sel_d<uint16_t, 64, false>(s, a, st);

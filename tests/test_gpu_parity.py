@@ -58,6 +58,11 @@ SHAPES = {
     # fan-out 2 stage 1 with one head per KV head at d = 64, and with three heads per group
     "mha-d64-bf16": (1, 2, 2, 3000, 3000, 64, 32, 2, 8, 1, "bf16"),
     "gqa3-bf16": (1, 6, 2, 2500, 2500, 128, 64, 2, 8, 1, "bf16"),
+    # g*K > 32: stage 1 on the matrix cores (fan-out 4 and 2, one to four heads per KV head)
+    "wide-g4-gqa4": (1, 8, 2, 4000, 4000, 128, 32, 4, 12, 1, "bf16"),
+    "wide-g2-d64": (1, 2, 2, 5000, 5000, 64, 32, 2, 24, 1, "bf16"),
+    "wide-g4-k32": (1, 4, 2, 9000, 9000, 128, 32, 4, 32, 1, "bf16"),
+    "wide-g4-noncausal-suffix": (1, 4, 1, 1500, 3000, 128, 32, 4, 10, 0, "bf16"),
 }
 
 
@@ -207,7 +212,7 @@ def test_deterministic_repeat():
 
 
 VARIANT_SHAPES = ["tiny-fp32", "gqa-ragged-bf16", "g4-gqa4-d64", "decode-row", "c128-g4-gqa", "big-budget",
-                  "noncausal-c128-ragged", "g3-noncausal"]
+                  "noncausal-c128-ragged", "g3-noncausal", "wide-g4-gqa4", "wide-g2-d64"]
 
 
 @pytest.mark.parametrize("name", VARIANT_SHAPES)
