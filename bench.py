@@ -58,7 +58,10 @@ def algorithmic_work(w, pairs_scored, attn_pairs, far_key_pairs=None, far_slots=
         if M[lv - 1] > K:      # this level can hold more than K candidates
             ranked += 1
     stage1_flops = B * Hkv * Nq * G * ranked * g * K * g * 2 * d
-    out["select_stage1"] = ("alu", stage1_flops)
+    # bf16 candidate sets wider than 32 with fan-out 2 or 4 are scored on the
+    # matrix cores (stage1_mfma_kernel); the others on the fp32 vector ALUs
+    on_mfma = w["dtype"] == "bf16" and g in (2, 4) and 32 < g * K <= 128 and G <= 16 and d in (64, 128)
+    out["select_stage1"] = ("mfma" if on_mfma else "alu", stage1_flops)
     out["leaf_score"] = ("mfma", pairs_scored * G * C * d * 2)
     out["attn_rows"] = ("mfma", attn_pairs * 4 * d)
     n_part = B * Hkv * Nq * K * G
