@@ -588,6 +588,23 @@ def test_planted_block_is_in_the_reference():
     assert 10 in res["ref"] and res["captured"] > 0.99 and res["ratio"] > 0.999
 
 
+def test_reference_ties_prefer_smaller_block_index():
+    """Reading R15: blocks of exactly equal mass enter the reference in
+    ascending index order.  Three copies of one heavy key block compete for
+    two free slots (no causal policy, so nothing is forced)."""
+    r = _rng(16)
+    N, d, C, K = 256, 8, 32, 2
+    k = r.standard_normal((N, d)) * 0.1
+    q = r.standard_normal(d)
+    heavy = 3.0 * q + 0.1 * r.standard_normal((C, d))
+    for blk in (6, 1, 4):
+        k[blk * C:(blk + 1) * C] = heavy
+    res = O.selection_quality_row(q[None], k, [4, 6], N - 1, C, K, False)
+    assert res["P"][1] == res["P"][4] == res["P"][6] and res["gap"] == 0.0
+    assert res["ref"] == [1, 4]
+    assert abs(res["recall"] - 0.5) < 1e-15
+
+
 def test_all_blocks_eligible_within_budget():
     """With at most K eligible blocks the reference is all of them and holds
     all the mass; Recall@K divides by K (reading R15)."""
