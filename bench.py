@@ -58,9 +58,11 @@ def algorithmic_work(w, pairs_scored, attn_pairs, far_key_pairs=None, far_slots=
         if M[lv - 1] > K:      # this level can hold more than K candidates
             ranked += 1
     stage1_flops = B * Hkv * Nq * G * ranked * g * K * g * 2 * d
-    # bf16 candidate sets wider than 32 with fan-out 2 or 4 are scored on the
-    # matrix cores (stage1_mfma_kernel); the others on the fp32 vector ALUs
-    on_mfma = w["dtype"] == "bf16" and g in (2, 4) and 32 < g * K <= 128 and G <= 16 and d in (64, 128)
+    # bf16 with fan-out 2 or 4 and candidate sets wider than 32 or 8+ heads per
+    # KV head is scored on the matrix cores (stage1_mfma_kernel); the others on
+    # the fp32 vector ALUs
+    on_mfma = (w["dtype"] == "bf16" and g in (2, 4) and g * K <= 128 and G <= 16 and d in (64, 128)
+               and (g * K > 32 or G >= 8))
     out["select_stage1"] = ("mfma" if on_mfma else "alu", stage1_flops)
     out["leaf_score"] = ("mfma", pairs_scored * G * C * d * 2)
     out["attn_rows"] = ("mfma", attn_pairs * 4 * d)
@@ -514,9 +516,14 @@ def main():
         evict.fill_(1.0)
         dst = torch.empty_like(src)
         torch.cuda.synchronize()
+        ce0, ce1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        ce0.record()
         dst.copy_(src)
+        ce1.record()
         torch.cuda.synchronize()
-        log(f"[bench] copy probe: {n} bytes read, {n} bytes written")
+        cms = ce0.elapsed_time(ce1)
+        log(f"[bench] copy probe: {n} bytes read, {n} bytes written in {cms:.3f} ms "
+            f"({2 * n / cms / 1e6:.0f} GB/s read + write)")
 
 
 if __name__ == "__main__":

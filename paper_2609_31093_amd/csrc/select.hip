@@ -581,7 +581,8 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
 
 // ----------------------------------------------------------------------------
 // Stage 1 on the matrix cores (bf16 queries, fan-out 2 or 4, at most 16 heads
-// per KV head, 32 < g*K <= 128): one wavefront per query row.
+// per KV head, g*K <= 128; used for g*K > 32 or 8+ heads per KV head): one
+// wavefront per query row.
 //
 // Each ranked level scores its candidates' children as one product per
 // 16-child tile on v_mfma_f32_16x16x32_bf16: A = 16 child summary rows (lane
@@ -2101,10 +2102,11 @@ struct TwoStageWs {
 };
 
 // Stage 1 on the matrix cores: bf16 queries, fan-out 2 or 4, up to 16 heads
-// per KV head, candidate sets wider than one wavefront half (g*K > 32) and
-// within the 128-entry rank sort.
+// per KV head, within the 128-entry rank sort, and either candidate sets
+// wider than one wavefront half (g*K > 32) or groups of 8 or more heads
+// (enough columns of the 16-wide tile do work to beat the vector ALUs).
 static bool stage1_mfma_ok(const Shape& s) {
-  return s.bf16 && (s.g == 2 || s.g == 4) && s.G <= 16 && s.gK() > 32 && s.gK() <= 128 &&
+  return s.bf16 && (s.g == 2 || s.g == 4) && s.G <= 16 && (s.gK() > 32 || s.G >= 8) && s.gK() <= 128 &&
          (s.D == 64 || s.D == 128);
 }
 
@@ -2152,7 +2154,7 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
   SelArgs a = make_sel_args(s, geo, q, k, pyr);
   a.a1 = a1;
   a.a1cnt = a1cnt;
-  const bool narrow = s.gK() <= 32;
+  const bool narrow = s.gK() <= 32 && !stage1_mfma_ok(s);
   {
     ProfScope ps("select_stage1", st);
     if (narrow) {

@@ -23,6 +23,9 @@ rows, d = head dim, C = leaf block size, g = fan-out, K = block budget):
                    the sequence (rho = 0.999) per (head, dim); v i.i.d. N(0,1).
 * ``decode-128k``  bf16, B=1, H=Hkv=8, N=131072, Nq=1, d=128, C=64, g=2,
                    K=16; k, v i.i.d. N(0,1); 64 single-token query steps.
+* ``paper-sel-128k`` bf16, B=1, H=32, Hkv=2, N=131072, d=64, C=64, g=2, K=8
+                   (the paper's block-selection benchmark shape); q, k, v
+                   i.i.d. N(0,1).
 
 Every (batch, head) slice of every tensor comes from its own stream
 ``np.random.default_rng(SeedSequence([seed, cfg_id, tensor_id, b, h]))`` in
@@ -47,6 +50,10 @@ WORKLOADS = {
                      causal=1, dtype="bf16", dist="ar1"),
     "decode-128k": dict(cfg_id=5, B=1, H=8, Hkv=8, N=131072, Nq=1, d=128, C=64, g=2, K=16,
                         causal=1, dtype="bf16", dist="iid", steps=64),
+    # the shape of the paper's block-selection latency benchmark (App. B):
+    # 32 query heads on 2 KV heads, d = 64, C = 64, K = 8, g = 2, random bf16 q and k
+    "paper-sel-128k": dict(cfg_id=6, B=1, H=32, Hkv=2, N=131072, Nq=None, d=64, C=64, g=2, K=8,
+                           causal=1, dtype="bf16", dist="iid"),
 }
 
 _Q, _K, _V, _AUX = 0, 1, 2, 3

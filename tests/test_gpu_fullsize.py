@@ -67,7 +67,7 @@ def _run(w, x):
     return pyr, idx, o, lse, bsa
 
 
-@pytest.mark.parametrize("name", ["gqa-32k", "needles-128k", "ar1-512k"])
+@pytest.mark.parametrize("name", ["gqa-32k", "needles-128k", "ar1-512k", "paper-sel-128k"])
 def test_fullsize_workload(name):
     w = inputs.workload(name)
     B, H, Hkv, N, Nq, d, C, g, K = (w[k] for k in ("B", "H", "Hkv", "N", "Nq", "d", "C", "g", "K"))

@@ -63,6 +63,9 @@ SHAPES = {
     "wide-g2-d64": (1, 2, 2, 5000, 5000, 64, 32, 2, 24, 1, "bf16"),
     "wide-g4-k32": (1, 4, 2, 9000, 9000, 128, 32, 4, 32, 1, "bf16"),
     "wide-g4-noncausal-suffix": (1, 4, 1, 1500, 3000, 128, 32, 4, 10, 0, "bf16"),
+    # sixteen and eight query heads per KV head (the paper's benchmark grouping)
+    "gqa16-d64-k8": (1, 32, 2, 3000, 3000, 64, 64, 2, 8, 1, "bf16"),
+    "gqa8-g4-c32": (1, 16, 2, 4000, 4000, 128, 32, 4, 6, 1, "bf16"),
 }
 
 
@@ -212,7 +215,7 @@ def test_deterministic_repeat():
 
 
 VARIANT_SHAPES = ["tiny-fp32", "gqa-ragged-bf16", "g4-gqa4-d64", "decode-row", "c128-g4-gqa", "big-budget",
-                  "noncausal-c128-ragged", "g3-noncausal", "wide-g4-gqa4", "wide-g2-d64"]
+                  "noncausal-c128-ragged", "g3-noncausal", "wide-g4-gqa4", "wide-g2-d64", "gqa16-d64-k8"]
 
 
 @pytest.mark.parametrize("name", VARIANT_SHAPES)
