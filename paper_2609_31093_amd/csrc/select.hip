@@ -580,6 +580,61 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
 }
 
 // ----------------------------------------------------------------------------
+// Stage 1 for g*K <= 32: two query rows per wavefront, one candidate per lane.
+//
+// Lanes 0-31 own row 2w and lanes 32-63 row 2w+1 (lane hl of a half holds
+// candidate hl).  Per ranked level: the candidates needing child logits build
+// a compact load list (a candidate whose own logit is known loads one child
+// fewer, see select_kernel), the lane groups of each half (4, 8 or 16 lanes
+// per dot) compute the listed dots, each lane turns its children's logits
+// into its LSE score, and a 32-lane bitonic sort on (score desc, node asc) with forced nodes keyed
+// +inf ranks the half: the first K survive.  Survivors expand through an LDS
+// staging list.  The leaf candidate set is sorted ascending before it is
+// stored.
+// ----------------------------------------------------------------------------
+
+// One compare-exchange stage of the bitonic network, without branches: the
+// lane keeps the smaller of (itself, partner) where the stage wants the
+// smaller, else the larger.
+template <int K2, int J>
+__device__ __forceinline__ void sort32_step(uint32_t& hi, uint32_t& lo, int hl) {
+  const uint32_t ohi = static_cast<uint32_t>(xor32_i<J>(static_cast<int>(hi)));
+  const uint32_t olo = static_cast<uint32_t>(xor32_i<J>(static_cast<int>(lo)));
+  const uint64_t mine = (static_cast<uint64_t>(hi) << 32) | lo;
+  const uint64_t other = (static_cast<uint64_t>(ohi) << 32) | olo;
+  const bool want_small = ((hl & K2) == 0) == ((hl & J) == 0);
+  const bool take = (other < mine) == want_small;
+  hi = take ? ohi : hi;
+  lo = take ? olo : lo;
+}
+
+// Bitonic sort of the 32 lanes of each wavefront half into rank order
+// (key desc, pack asc); packs are non-negative.
+__device__ __forceinline__ void sort32(float& key, int& pack, int hl) {
+  uint32_t hi = desc_bits(key), lo = static_cast<uint32_t>(pack);
+  sort32_step<2, 1>(hi, lo, hl);
+  sort32_step<4, 2>(hi, lo, hl);
+  sort32_step<4, 1>(hi, lo, hl);
+  sort32_step<8, 4>(hi, lo, hl);
+  sort32_step<8, 2>(hi, lo, hl);
+  sort32_step<8, 1>(hi, lo, hl);
+  sort32_step<16, 8>(hi, lo, hl);
+  sort32_step<16, 4>(hi, lo, hl);
+  sort32_step<16, 2>(hi, lo, hl);
+  sort32_step<16, 1>(hi, lo, hl);
+  sort32_step<32, 16>(hi, lo, hl);
+  sort32_step<32, 8>(hi, lo, hl);
+  sort32_step<32, 4>(hi, lo, hl);
+  sort32_step<32, 2>(hi, lo, hl);
+  sort32_step<32, 1>(hi, lo, hl);
+  key = desc_bits_inv(hi);
+  pack = static_cast<int>(lo);
+}
+
+// Inclusive prefix sum over the 32 lanes of a wavefront half.
+__device__ __forceinline__ int scan32(int v, int) { return scan32_incl(v); }
+
+// ----------------------------------------------------------------------------
 // Stage 1 on the matrix cores (bf16 queries, fan-out 2 or 4, at most 16 heads
 // per KV head, g*K <= 128; used for g*K > 32 or 8+ heads per KV head): one
 // wavefront per query row.
@@ -723,25 +778,35 @@ __global__ __launch_bounds__(kMfmaSelRows * 64) void stage1_mfma_kernel(SelArgs 
         }
       }
       wave_sync();
-      // Forced candidates first (key word 0), then score descending, ties by
-      // candidate index (candidates are ascending node ids), then empty slots.
+      // Forced candidates first, then score descending, ties by candidate
+      // index (candidates are ascending node ids), then empty slots.
       const int keepn = K - fz.count();
-      uint32_t khi[2], klo[2];
-      int nforced = 0;
+      if (nA <= 32) {  // one 32-lane sort (the upper half sorts nothing of use)
+        const bool v = lane < nA;
+        const bool f = v && fz.is(cand[lane]);
+        float key = !v ? -INFINITY : (f ? INFINITY : score[lane]);
+        int pack = lane;
+        const int nforced = __popcll(__ballot(f));
+        sort32(key, pack, lane & 31);
+        if (lane < nA) flag[pack] = (lane < nforced || lane - nforced < keepn) ? 1 : 0;
+      } else {  // two candidates per lane: the 128-entry sort (forced keyed below every score)
+        uint32_t khi[2], klo[2];
+        int nforced = 0;
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        const int ci = lane + 64 * s2;
-        const bool v = ci < nA;
-        const bool f = v && fz.is(cand[ci]);
-        khi[s2] = !v ? 0xFFFFFFFFu : (f ? 0u : desc_bits(score[ci]));
-        klo[s2] = static_cast<uint32_t>(ci);
-        nforced += __popcll(__ballot(f));
-      }
-      sort128(khi, klo, lane);
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const int ci = lane + 64 * s2;
+          const bool v = ci < nA;
+          const bool f = v && fz.is(cand[ci]);
+          khi[s2] = !v ? 0xFFFFFFFFu : (f ? 0u : desc_bits(score[ci]));
+          klo[s2] = static_cast<uint32_t>(ci);
+          nforced += __popcll(__ballot(f));
+        }
+        sort128(khi, klo, lane);
 #pragma unroll
-      for (int s2 = 0; s2 < 2; ++s2) {
-        const int rk = lane + 64 * s2;
-        if (static_cast<int>(klo[s2]) < nA) flag[klo[s2]] = (rk < nforced || rk - nforced < keepn) ? 1 : 0;
+        for (int s2 = 0; s2 < 2; ++s2) {
+          const int rk = lane + 64 * s2;
+          if (static_cast<int>(klo[s2]) < nA) flag[klo[s2]] = (rk < nforced || rk - nforced < keepn) ? 1 : 0;
+        }
       }
     } else {
       for (int ci = lane; ci < nA; ci += 64) flag[ci] = 1;
@@ -800,60 +865,6 @@ __global__ __launch_bounds__(256) void pyr_hilo_kernel(const float* __restrict__
   out[1] = make_uint4(lw[0], lw[1], lw[2], lw[3]);
 }
 
-// ----------------------------------------------------------------------------
-// Stage 1 for g*K <= 32: two query rows per wavefront, one candidate per lane.
-//
-// Lanes 0-31 own row 2w and lanes 32-63 row 2w+1 (lane hl of a half holds
-// candidate hl).  Per ranked level: the candidates needing child logits build
-// a compact load list (a candidate whose own logit is known loads one child
-// fewer, see select_kernel), the lane groups of each half (4, 8 or 16 lanes
-// per dot) compute the listed dots, each lane turns its children's logits
-// into its LSE score, and a 32-lane bitonic sort on (score desc, node asc) with forced nodes keyed
-// +inf ranks the half: the first K survive.  Survivors expand through an LDS
-// staging list.  The leaf candidate set is sorted ascending before it is
-// stored.
-// ----------------------------------------------------------------------------
-
-// One compare-exchange stage of the bitonic network, without branches: the
-// lane keeps the smaller of (itself, partner) where the stage wants the
-// smaller, else the larger.
-template <int K2, int J>
-__device__ __forceinline__ void sort32_step(uint32_t& hi, uint32_t& lo, int hl) {
-  const uint32_t ohi = static_cast<uint32_t>(xor32_i<J>(static_cast<int>(hi)));
-  const uint32_t olo = static_cast<uint32_t>(xor32_i<J>(static_cast<int>(lo)));
-  const uint64_t mine = (static_cast<uint64_t>(hi) << 32) | lo;
-  const uint64_t other = (static_cast<uint64_t>(ohi) << 32) | olo;
-  const bool want_small = ((hl & K2) == 0) == ((hl & J) == 0);
-  const bool take = (other < mine) == want_small;
-  hi = take ? ohi : hi;
-  lo = take ? olo : lo;
-}
-
-// Bitonic sort of the 32 lanes of each wavefront half into rank order
-// (key desc, pack asc); packs are non-negative.
-__device__ __forceinline__ void sort32(float& key, int& pack, int hl) {
-  uint32_t hi = desc_bits(key), lo = static_cast<uint32_t>(pack);
-  sort32_step<2, 1>(hi, lo, hl);
-  sort32_step<4, 2>(hi, lo, hl);
-  sort32_step<4, 1>(hi, lo, hl);
-  sort32_step<8, 4>(hi, lo, hl);
-  sort32_step<8, 2>(hi, lo, hl);
-  sort32_step<8, 1>(hi, lo, hl);
-  sort32_step<16, 8>(hi, lo, hl);
-  sort32_step<16, 4>(hi, lo, hl);
-  sort32_step<16, 2>(hi, lo, hl);
-  sort32_step<16, 1>(hi, lo, hl);
-  sort32_step<32, 16>(hi, lo, hl);
-  sort32_step<32, 8>(hi, lo, hl);
-  sort32_step<32, 4>(hi, lo, hl);
-  sort32_step<32, 2>(hi, lo, hl);
-  sort32_step<32, 1>(hi, lo, hl);
-  key = desc_bits_inv(hi);
-  pack = static_cast<int>(lo);
-}
-
-// Inclusive prefix sum over the 32 lanes of a wavefront half.
-__device__ __forceinline__ int scan32(int v, int) { return scan32_incl(v); }
 
 // Total of a 32-lane half from an inclusive scan.
 __device__ __forceinline__ int half_total(int incl, int lane) {
