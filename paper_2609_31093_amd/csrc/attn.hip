@@ -649,14 +649,17 @@ __global__ __launch_bounds__(256, 3) void attn_local_kernel(AttnBlockArgs a, con
         }
       }
       const uint16_t* prow = part_o + (pb * a.G + hh) * D + sub * DPL;  // slot s at prow + s * G * D
-      for (int s0 = 0; s0 < a.K; s0 += kMergeBatch) {
+      // Slots 0..31 (lane sub holds the words of slots sub and sub + 16);
+      // attn_combine_kernel<D, true> takes in any further slots afterwards.
+      const int k32 = min(a.K, 32);
+      for (int s0 = 0; s0 < k32; s0 += kMergeBatch) {
         float ls[kMergeBatch];
         int off[kMergeBatch];
 #pragma unroll
         for (int u = 0; u < kMergeBatch; ++u) {
           const int s = s0 + u;
           const float la = __shfl(lsA[r4], (lane & 48) | (s & 15)), lb = __shfl(lsB[r4], (lane & 48) | (s & 15));
-          ls[u] = s < a.K ? (s < 16 ? la : lb) : -INFINITY;
+          ls[u] = s < k32 ? (s < 16 ? la : lb) : -INFINITY;
           off[u] = (ls[u] != -INFINITY ? s : 0) * a.G * D;
         }
         float x[kMergeBatch][DPL];
@@ -686,8 +689,12 @@ __global__ __launch_bounds__(256, 3) void attn_local_kernel(AttnBlockArgs a, con
 }
 
 // One wavefront per (row of the chunk, query head): merge the row's K
-// partials.  16 lanes cover one partial (8 bf16 each for d = 128).
-template <int D>
+// partials.  16 lanes cover one partial (8 bf16 each for d = 128).  TAIL:
+// causal budgets above 32, after attn_local_kernel has merged slots 0..31
+// into o and lse: the row's state restarts from (o, lse) and takes in the
+// partials of its other slots (not its first, previous or own block, which
+// never have partials).
+template <int D, bool TAIL>
 __global__ __launch_bounds__(256) void attn_combine_kernel(AttnBlockArgs a, const int32_t* __restrict__ idx,
                                                            const uint16_t* __restrict__ part_o,
                                                            const float* __restrict__ part_lse,
@@ -704,11 +711,27 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnBlockArgs a, cons
   const int bh = b * a.Hkv + hk;
   const int row = a.row0 + rr;
   const int32_t* sel = idx + (static_cast<int64_t>(bh) * a.Nq + row) * a.K;
+  const int64_t orow = (static_cast<int64_t>(b) * a.H + hq) * a.Nq + row;
   float m = -INFINITY, s = 0.f, acc[DPL];
 #pragma unroll
   for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
-  for (int slot = grp; slot < a.K; slot += 4) {
-    if (sel[slot] < 0) continue;
+  int slot0 = 0;
+  const int c = (a.N - a.Nq + row) / a.C;
+  if constexpr (TAIL) {
+    slot0 = 32;
+    if (grp == 0) {
+      const float l0 = lse[orow];
+      if (l0 != -INFINITY) {
+        m = l0 * kLog2e;
+        s = 1.f;
+        load_row_part<uint16_t, DPL>(o + orow * D + sub * DPL, acc);
+      }
+    }
+  }
+  for (int slot = slot0 + grp; slot < a.K; slot += 4) {
+    const int blk = sel[slot];
+    if (blk < 0) continue;
+    if (TAIL && (blk == 0 || blk == c || blk == c - 1)) continue;
     const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + slot) * a.G + hh;
     const float ls = part_lse[pidx];
     if (ls == -INFINITY) continue;
@@ -730,7 +753,6 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnBlockArgs a, cons
     merge_state<DPL>(m, s, acc, m2, s2, o2);
   }
   if (grp == 0) {
-    const int64_t orow = (static_cast<int64_t>(b) * a.H + hq) * a.Nq + row;
     float res[DPL];
     const float inv = s > 0.f ? 1.0f / s : 0.f;
 #pragma unroll
@@ -899,7 +921,7 @@ static bool use_split_path(const Shape& s, const Geo& geo) {
 }
 
 struct AttnWs {
-  size_t part_o, part_lse, cl, total;
+  size_t part_o, part_lse, cl, row_lse, total;
 };
 
 static AttnWs attn_layout(const Shape& s, const Geo& geo) {
@@ -911,6 +933,10 @@ static AttnWs attn_layout(const Shape& s, const Geo& geo) {
   w.part_o = o;   o += al(np * s.G * s.D * 2);
   w.part_lse = o; o += al(np * s.G * 4);
   w.cl = o;       o += al(cluster_ws(s.BH(), geo.M[1], static_cast<int64_t>(np)));
+  // causal budgets above 32: the rows' log-sums between the per-leaf-block
+  // merge and the tail merge, for callers that pass no lse
+  w.row_lse = o;
+  if (s.causal && s.K > 32) o += al(static_cast<size_t>(s.B) * s.H * s.Nq * 4);
   w.total = o;
   return w;
 }
@@ -964,7 +990,7 @@ static hipError_t launch_split_path(const Shape& s, const void* q, const void* k
   {
     ProfScope ps("attn_combine", st);
     dim3 grid((s.Nq + 3) / 4, s.B * s.H);
-    attn_combine_kernel<D><<<grid, 256, 0, st>>>(a, idx, part_o, part_lse, static_cast<uint16_t*>(o), lse);
+    attn_combine_kernel<D, false><<<grid, 256, 0, st>>>(a, idx, part_o, part_lse, static_cast<uint16_t*>(o), lse);
   }
   return hipGetLastError();
 }
@@ -976,6 +1002,7 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
   char* base = static_cast<char*>(ws);
   uint16_t* part_o = reinterpret_cast<uint16_t*>(base + w.part_o);
   float* part_lse = reinterpret_cast<float*>(base + w.part_lse);
+  if (!lse && s.causal && s.K > 32) lse = reinterpret_cast<float*>(base + w.row_lse);
   const int ch = attn_chunk_rows(s);
   hipError_t e;
   for (int row0 = 0; row0 < s.Nq; row0 += ch) {
@@ -1038,10 +1065,15 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
         go(attn_local_kernel<D, 3>);
       else
         go(attn_local_kernel<D, 4>);
+      if (s.K > 32) {  // attn_local_kernel merges the first 32 slots
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        dim3 tgrid((nrows + 3) / 4, s.B * s.H);
+        attn_combine_kernel<D, true><<<tgrid, 256, 0, st>>>(a, idx, part_o, part_lse, static_cast<uint16_t*>(o), lse);
+      }
     } else {
       ProfScope ps("attn_combine", st);
       dim3 grid((nrows + 3) / 4, s.B * s.H);
-      attn_combine_kernel<D><<<grid, 256, 0, st>>>(a, idx, part_o, part_lse, static_cast<uint16_t*>(o), lse);
+      attn_combine_kernel<D, false><<<grid, 256, 0, st>>>(a, idx, part_o, part_lse, static_cast<uint16_t*>(o), lse);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }

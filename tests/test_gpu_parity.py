@@ -66,6 +66,9 @@ SHAPES = {
     # sixteen and eight query heads per KV head (the paper's benchmark grouping)
     "gqa16-d64-k8": (1, 32, 2, 3000, 3000, 64, 64, 2, 8, 1, "bf16"),
     "gqa8-g4-c32": (1, 16, 2, 4000, 4000, 128, 32, 4, 6, 1, "bf16"),
+    # causal budgets above 32 on the block attention path (slots 32.. merged after the per-leaf-block kernel)
+    "k40-causal-block": (1, 4, 2, 5000, 5000, 64, 32, 2, 40, 1, "bf16"),
+    "k48-causal-block-d128": (1, 2, 1, 6000, 6000, 128, 64, 2, 48, 1, "bf16"),
 }
 
 
