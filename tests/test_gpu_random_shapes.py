@@ -171,3 +171,23 @@ def test_random_shape_quality(i):
     assert not ((got_ref != want_ref).any(-1) & decisive).any()
     np.testing.assert_array_equal(np.rint(got_met[..., 0] * K)[decisive], np.rint(want_met[..., 0] * K)[decisive])
     np.testing.assert_allclose(got_met[..., 1:], want_met[..., 1:], atol=1e-4, rtol=0)
+
+
+BSA_SHAPES = [s for s in _shapes(10, 31) if s[8] <= 32]
+
+
+@pytest.mark.parametrize("i", range(len(BSA_SHAPES)), ids=[f"rf{i}" for i in range(len(BSA_SHAPES))])
+def test_random_shape_flat_bsa(i):
+    """Flat block selection (the baseline) against its oracle on sampled rows."""
+    B, H, Hkv, Nq, N, d, C, g, K, causal, dtype = BSA_SHAPES[i]
+    print("shape", BSA_SHAPES[i], flush=True)
+    x = inputs.random_qkv(B, H, Hkv, Nq, N, d, dtype, seed=600 + i)
+    p = pisa.make_problem(B, H, Hkv, Nq, N, d, C, g, K, causal, dtype)
+    q, k = dev(x["q"], dtype), dev(x["k"], dtype)
+    idx = pisa.select_flat_bsa(p, q, pisa.build_pyramid(p, k))
+    torch.cuda.synchronize()
+    idx_np = idx.cpu().numpy()
+    check_selection_valid(idx_np, N, Nq, C, K, bool(causal))
+    rows = _rows(Nq, 70 + i)
+    ora, gap = O.select_flat_bsa(x["q"], x["k"], C, K, bool(causal), rows=rows)
+    print(compare_selection(idx_np[:, :, rows], ora, gap))
