@@ -168,8 +168,9 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(AttnArgs a) {
 // ----------------------------------------------------------------------------
 // Block-centric attention for many rows (bf16).
 //
-// attn_block16_kernel: one workgroup per tile of up to kClusterTile (row,
-// slot) pairs of one (batch x KV head, key block) cluster.  The block's C
+// attn_block16_kernel: one workgroup per chunk of up to kAttnChunk (row,
+// slot) pairs of one (batch x KV head, key block) cluster, taken as
+// kClusterTile-pair tiles.  The block's C
 // keys are staged in LDS row-major and its values transposed (V^T, two keys
 // per 32-bit word, so that the PV product reads contiguous 8-byte runs);
 // the pairs are processed 16 per wavefront tile on v_mfma_f32_16x16x32_bf16
@@ -178,8 +179,9 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(AttnArgs a) {
 // M, queries along N), the causal mask, the block-local max, P = 2^(S - m)
 // in bf16, then O^T = V^T P with the key order of P's operand reproduced in
 // the V^T reads.  Each pair leaves a partial: o normalised by its own sum
-// (bf16) and its log2-sum (fp32).  attn_combine_kernel merges the K
-// partials of each (row, head) with the usual log-sum-exp weights.
+// (bf16) and its log2-sum (fp32).  attn_local_kernel (causal) or
+// attn_combine_kernel merges the partials of each (row, head) with the usual
+// log-sum-exp weights.
 // ----------------------------------------------------------------------------
 
 typedef __bf16 bf16x8a __attribute__((ext_vector_type(8)));

@@ -195,10 +195,6 @@ size_t cluster_ws(int BH, int M1, int64_t max_pairs) {
   return 4 * ((ncl + 1) * 4 + 256) + static_cast<size_t>(max_pairs) * 4 + 256;
 }
 
-int64_t cluster_max_tiles(int BH, int M1, int64_t max_pairs) {
-  return (max_pairs + kClusterTile - 1) / kClusterTile + static_cast<int64_t>(BH) * M1;
-}
-
 int64_t cluster_max_chunks(int BH, int M1, int64_t max_pairs, int tile) {
   return (max_pairs + tile - 1) / tile + static_cast<int64_t>(BH) * M1;
 }

@@ -48,33 +48,18 @@ struct ClusterArgs {
   int row0, nrows;      // rows [row0, row0 + nrows) of every (batch, KV head)
   int g;                // fan-out (parent mode)
 };
-constexpr int kClusterTile = 256;  // pairs per workgroup tile of a cluster consumer
+constexpr int kClusterTile = 256;  // pairs per inner tile of the block attention's workgroup chunks
 struct ClusterOut {
   const int32_t* offs;   // [BH*M1 + 1] cluster start offsets into pairs
-  const int32_t* toffs;  // [BH*M1 + 1] first tile of each cluster (kClusterTile pairs per tile)
+  const int32_t* toffs;  // [BH*M1 + 1] first chunk of each cluster (the `tile` of launch_cluster pairs per chunk)
   const int32_t* pairs;  // (row - row0) << 8 | slot, grouped by (bh, block)
   int64_t ncl;           // BH*M1
 };
 size_t cluster_ws(int BH, int M1, int64_t max_pairs);
-int64_t cluster_max_tiles(int BH, int M1, int64_t max_pairs);
 
-// Tile w of the cluster list: its cluster (largest cl with toffs[cl] <= w)
-// and pair range; false when w is past the last tile.
-__device__ __forceinline__ bool cluster_tile(const int32_t* __restrict__ offs, const int32_t* __restrict__ toffs,
-                                             int64_t ncl, int64_t w, int64_t& cl, int& beg, int& end) {
-  if (w >= toffs[ncl]) return false;
-  int64_t lo = 0, hi = ncl - 1;
-  while (lo < hi) {
-    const int64_t mid = (lo + hi + 1) >> 1;
-    if (toffs[mid] <= w) lo = mid; else hi = mid - 1;
-  }
-  cl = lo;
-  beg = offs[cl] + static_cast<int>(w - toffs[cl]) * kClusterTile;
-  end = min(offs[cl + 1], beg + kClusterTile);
-  return true;
-}
 // Chunk w of the cluster list when the consumer takes up to `tile` pairs per
-// workgroup (the tile offsets of launch_cluster(..., tile)).
+// workgroup (the tile offsets of launch_cluster(..., tile)): its cluster (the
+// largest cl with toffs[cl] <= w) and pair range; false past the last chunk.
 __device__ __forceinline__ bool cluster_chunk(const int32_t* __restrict__ offs, const int32_t* __restrict__ toffs,
                                               int64_t ncl, int64_t w, int tile, int64_t& cl, int& beg, int& end) {
   if (w >= toffs[ncl]) return false;
@@ -89,8 +74,7 @@ __device__ __forceinline__ bool cluster_chunk(const int32_t* __restrict__ offs, 
   return true;
 }
 // Groups the pairs by block; toffs counts `tile`-pair chunks per cluster.
-hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* out, hipStream_t st,
-                          int tile = kClusterTile);
+hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* out, hipStream_t st, int tile);
 int64_t cluster_max_chunks(int BH, int M1, int64_t max_pairs, int tile);
 
 hipError_t launch_build_pyramid(const Geo& geo, int BH, int D, bool bf16, const void* k, float* pyr,

@@ -1457,16 +1457,18 @@ __device__ __forceinline__ bf16x8v as_bf16x8(uint4 r) {
   return __builtin_bit_cast(bf16x8v, r);
 }
 
+constexpr int kLeafChunk = 1024;  // pairs (or (row, parent) entries) per workgroup of the leaf scorers
+
 struct LeafArgs {
   int H, Hkv, G, Nq, N, C, M1, gK;
   float qscale2;
   int Nkv;  // rows per (batch, KV head) in k
 };
 
-// One workgroup per tile of up to kClusterTile pairs of one (batch x KV head,
-// leaf block) cluster: the C x D key block is staged in LDS (rows padded by
-// 16 B against bank conflicts) and the tile's (query, slot) pairs are scored
-// against it, 32 pairs per wavefront MFMA tile.
+// One workgroup per chunk of up to kLeafChunk pairs of one (batch x KV head,
+// leaf block) cluster: the C x D key block is staged in LDS once (rows padded
+// by 16 B against bank conflicts) and the chunk's (query, slot) pairs are
+// scored against it, 32 pairs per wavefront MFMA tile.
 template <int D, int KIND>
 __global__ __launch_bounds__(256) void leaf_score_kernel(LeafArgs a, const uint16_t* __restrict__ q,
                                                          const uint16_t* __restrict__ k,
@@ -1479,7 +1481,7 @@ __global__ __launch_bounds__(256) void leaf_score_kernel(LeafArgs a, const uint1
   extern __shared__ uint16_t klds[];
   int64_t cl;
   int beg, end;
-  if (!cluster_tile(offs, toffs, ncl, blockIdx.x, cl, beg, end)) return;
+  if (!cluster_chunk(offs, toffs, ncl, blockIdx.x, kLeafChunk, cl, beg, end)) return;
   const int bh = static_cast<int>(cl / a.M1);
   const int blk = static_cast<int>(cl - static_cast<int64_t>(bh) * a.M1);
   const int b = bh / a.Hkv, h = bh - b * a.Hkv;
@@ -1530,10 +1532,15 @@ __global__ __launch_bounds__(256) void leaf_score_kernel(LeafArgs a, const uint1
         // acc[r] is the logit of key kt*32 + 8*(r/4) + 4*half + r%4 for query `col`
         // (-inf past the end of the sequence; a tile may hold no key at all).
         float zv[16];
+        if (kt * 32 + 32 <= nrows) {  // a full tile: no key past the end of the sequence
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-          zv[r] = key < nrows ? acc[r] * a.qscale2 : -INFINITY;
+          for (int r = 0; r < 16; ++r) zv[r] = acc[r] * a.qscale2;
+        } else {
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
+            zv[r] = key < nrows ? acc[r] * a.qscale2 : -INFINITY;
+          }
         }
         acc_merge(KIND, st, acc_of(KIND, zv));
       }
@@ -1550,7 +1557,6 @@ struct LeafParentArgs {
   int Nkv;  // rows per (batch, KV head) in k
 };
 
-constexpr int kLeafChunk = 1024;  // (row, parent) entries per workgroup of leaf_parent_kernel
 
 // Leaf scoring grouped by parent node (g*C <= 128 keys): one workgroup per
 // chunk of up to kLeafChunk (row, first-child slot) entries of one parent;
@@ -2260,8 +2266,7 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
   ClusterArgs ca{a1, a1cnt, s.gK(), s.Nq, s.N, s.C, s.K, s.causal, by_parent ? M2 : geo.M[1],
                  by_parent ? kClusterLeafParent : kClusterLeaf, 0, s.Nq, s.g};
   ClusterOut co{};
-  if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st, by_parent ? kLeafChunk : kClusterTile)) != hipSuccess)
-    return e;
+  if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st, kLeafChunk)) != hipSuccess) return e;
   if (by_parent) {
     LeafParentArgs lp{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.g, geo.M[1], M2, s.gK(), s.K, s.causal,
                       kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv};
@@ -2287,7 +2292,7 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
   } else {
     // Stage 2: leaf scoring against each key block once per cluster.
     LeafArgs la{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, geo.M[1], s.gK(), kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv};
-    dim3 lgrid(static_cast<unsigned>(cluster_max_tiles(s.BH(), geo.M[1], rows * s.gK())));
+    dim3 lgrid(static_cast<unsigned>(cluster_max_chunks(s.BH(), geo.M[1], rows * s.gK(), kLeafChunk)));
     const size_t llds = static_cast<size_t>(s.C) * (s.D + 8) * 2;
     {
       ProfScope ps("leaf_score", st);
