@@ -1709,15 +1709,37 @@ __global__ __launch_bounds__(256) void final_topk_kernel(TopkArgs a, const int32
   }
   wave_sync();
   const int keepn = a.K - nF;
-  for (int i = lane; i < n; i += 64) {
-    const int node = nodes[i];
-    int kp = 1;
-    if (ranked && !forced(node)) {
-      int rank = 0;
-      for (int j = 0; j < n; ++j) rank += (!forced(nodes[j]) && ranks_before(us[j], nodes[j], us[i], node)) ? 1 : 0;
-      kp = rank < keepn;
+  if (ranked && n <= 128) {
+    // Up to 128 candidates: the 128-entry register sort, forced candidates
+    // keyed below every score, ties by candidate index (ascending nodes).
+    uint32_t khi[2], klo[2];
+    int nforced = 0;
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      const int ci = lane + 64 * s2;
+      const bool v = ci < n;
+      const bool f = v && forced(nodes[ci]);
+      khi[s2] = !v ? 0xFFFFFFFFu : (f ? 0u : desc_bits(us[ci]));
+      klo[s2] = static_cast<uint32_t>(ci);
+      nforced += __popcll(__ballot(f));
     }
-    keep[i] = kp;
+    sort128(khi, klo, lane);
+#pragma unroll
+    for (int s2 = 0; s2 < 2; ++s2) {
+      const int rk = lane + 64 * s2;
+      if (static_cast<int>(klo[s2]) < n) keep[klo[s2]] = (rk < nforced || rk - nforced < keepn) ? 1 : 0;
+    }
+  } else {
+    for (int i = lane; i < n; i += 64) {
+      const int node = nodes[i];
+      int kp = 1;
+      if (ranked && !forced(node)) {
+        int rank = 0;
+        for (int j = 0; j < n; ++j) rank += (!forced(nodes[j]) && ranks_before(us[j], nodes[j], us[i], node)) ? 1 : 0;
+        kp = rank < keepn;
+      }
+      keep[i] = kp;
+    }
   }
   wave_sync();
   // Compact in order (candidates are ascending).
