@@ -442,8 +442,9 @@ __global__ __launch_bounds__(NW * 64, (CT >= 3 ? 1 : NW == 8 ? 4 : 3)) void attn
 // ----------------------------------------------------------------------------
 constexpr int kMergeBatch = 4;  // partials of a row requested together by attn_local_kernel
 
-template <int D, int CT>
-__global__ __launch_bounds__(256, 3) void attn_local_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
+// NWL wavefronts per workgroup, each owning 16-row query groups NWL apart.
+template <int D, int CT, int NWL>
+__global__ __launch_bounds__(NWL * 64, NWL == 8 ? 2 : 3) void attn_local_kernel(AttnBlockArgs a, const uint16_t* __restrict__ q,
                                                          const uint16_t* __restrict__ k,
                                                          const uint16_t* __restrict__ v,
                                                          const int32_t* __restrict__ idx,
@@ -457,7 +458,7 @@ __global__ __launch_bounds__(256, 3) void attn_local_kernel(AttnBlockArgs a, con
   constexpr int LDV = C + 4;
   constexpr int DT = D / 16;
   constexpr int QG = C / 16;             // 16-row query groups of a leaf block
-  constexpr int NPASS = (QG + 3) / 4;    // groups per wavefront
+  constexpr int NPASS = (QG + NWL - 1) / NWL;  // groups per wavefront
   constexpr int DPL = D / 16;            // merge: elements per lane
   constexpr int SROW = D + 4;            // merge: padded state row (floats)
   extern __shared__ uint16_t lds[];
@@ -480,7 +481,7 @@ __global__ __launch_bounds__(256, 3) void attn_local_kernel(AttnBlockArgs a, con
   if (c > 0) sb[nsb++] = c;
 
   for (int it = 0; it < NPASS * a.G; ++it) {
-    const int hh = it / NPASS, qg = (it - hh * NPASS) * 4 + wave;
+    const int hh = it / NPASS, qg = (it - hh * NPASS) * NWL + wave;
     const int p = c * C + qg * 16 + col;  // this lane's query position
     const bool vq = qg < QG && p >= p_lo && p < p_hi;
     const int rowq = vq ? p - tq0 : p_lo - tq0;  // a row of the tile for lanes without a query
@@ -512,13 +513,13 @@ __global__ __launch_bounds__(256, 3) void attn_local_kernel(AttnBlockArgs a, con
       __syncthreads();  // the previous block's readers are done
       const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
       const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
-      for (int e = threadIdx.x; e < C * (D / 8); e += 256) {
+      for (int e = threadIdx.x; e < C * (D / 8); e += NWL * 64) {
         const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
         uint4 kv = make_uint4(0, 0, 0, 0);
         if (r < nkeys) kv = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
         *reinterpret_cast<uint4*>(klds + r * LDK + c8) = kv;
       }
-      for (int e = threadIdx.x; e < (C / 2) * (D / 8); e += 256) {
+      for (int e = threadIdx.x; e < (C / 2) * (D / 8); e += NWL * 64) {
         const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
         uint4 v0 = make_uint4(0, 0, 0, 0), v1 = make_uint4(0, 0, 0, 0);
         if (2 * kp < nkeys) v0 = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp) * D + c8);
@@ -1048,25 +1049,28 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
       const int tq0 = s.N - s.Nq;
       const int nblk = (tq0 + row0 + nrows - 1) / s.C - (tq0 + row0) / s.C + 1;
       dim3 grid(static_cast<unsigned>(nblk), s.BH());
-      // one key block staged, or (later) four wavefronts' 16 row states
+      // one key block staged, or (later) the wavefronts' 16 row states; blocks
+      // of 128 keys give every one of eight wavefronts one 16-row group, so
+      // that each shared block is staged once per query head
+      const int nwl = s.C == 128 ? 8 : 4;
       const size_t lds = std::max((static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 4)) * 2,
-                                  static_cast<size_t>(4) * (16 * (D + 4) + 32) * 4);
+                                  static_cast<size_t>(nwl) * (16 * (D + 4) + 32) * 4);
       const uint16_t* qq = static_cast<const uint16_t*>(q);
       const uint16_t* kk = static_cast<const uint16_t*>(k);
       const uint16_t* vv = static_cast<const uint16_t*>(v);
       auto go = [&](auto kern) {
         if (lds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
-        kern<<<grid, 256, lds, st>>>(a, qq, kk, vv, idx, part_o, part_lse, static_cast<uint16_t*>(o), lse);
+        kern<<<grid, nwl * 64, lds, st>>>(a, qq, kk, vv, idx, part_o, part_lse, static_cast<uint16_t*>(o), lse);
       };
       if (s.C == 32)
-        go(attn_local_kernel<D, 1>);
+        go(attn_local_kernel<D, 1, 4>);
       else if (s.C == 64)
-        go(attn_local_kernel<D, 2>);
+        go(attn_local_kernel<D, 2, 4>);
       else if (s.C == 96)
-        go(attn_local_kernel<D, 3>);
+        go(attn_local_kernel<D, 3, 4>);
       else
-        go(attn_local_kernel<D, 4>);
+        go(attn_local_kernel<D, 4, 8>);
       if (s.K > 32) {  // attn_local_kernel merges the first 32 slots
         if ((e = hipGetLastError()) != hipSuccess) return e;
         dim3 tgrid((nrows + 3) / 4, s.B * s.H);
