@@ -197,6 +197,28 @@ __device__ __forceinline__ ScoreAcc acc_of(int kind, const float (&v)[NV]) {
   return ScoreAcc{n, mean, m2};
 }
 
+// The score state of NV raw logits (unscaled, -inf = no key) times a
+// positive scale: for the LSE the scale enters the exponent's FMA, since the
+// maximum of the raw logits scales to the maximum of the scaled ones.
+template <int KIND, int NV>
+__device__ __forceinline__ ScoreAcc acc_of_scaled(float (&v)[NV], float scale) {
+  if constexpr (KIND == kScoreLse) {
+    float m = v[0];
+#pragma unroll
+    for (int i = 1; i < NV; ++i) m = fmaxf(m, v[i]);
+    if (m == -INFINITY) return ScoreAcc{-INFINITY, 0.f, 0.f};
+    const float ms = m * scale;
+    float sm = 0.f;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) sm += fast_exp2(fmaf(v[i], scale, -ms));
+    return ScoreAcc{ms, sm, 0.f};
+  } else {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) v[i] *= scale;
+    return acc_of(KIND, v);
+  }
+}
+
 __device__ __forceinline__ ScoreAcc acc_shfl_xor(const ScoreAcc& a, int mask) {
   return ScoreAcc{__shfl_xor(a.x, mask), __shfl_xor(a.y, mask), __shfl_xor(a.z, mask)};
 }
@@ -1532,17 +1554,16 @@ __global__ __launch_bounds__(256) void leaf_score_kernel(LeafArgs a, const uint1
         // acc[r] is the logit of key kt*32 + 8*(r/4) + 4*half + r%4 for query `col`
         // (-inf past the end of the sequence; a tile may hold no key at all).
         float zv[16];
-        if (kt * 32 + 32 <= nrows) {  // a full tile: no key past the end of the sequence
 #pragma unroll
-          for (int r = 0; r < 16; ++r) zv[r] = acc[r] * a.qscale2;
-        } else {
+        for (int r = 0; r < 16; ++r) zv[r] = acc[r];
+        if (kt * 32 + 32 > nrows) {  // a partial tile: keys past the end of the sequence drop out
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-            zv[r] = key < nrows ? acc[r] * a.qscale2 : -INFINITY;
+            zv[r] = key < nrows ? zv[r] : -INFINITY;
           }
         }
-        acc_merge(KIND, st, acc_of(KIND, zv));
+        acc_merge(KIND, st, acc_of_scaled<KIND, 16>(zv, a.qscale2));
       }
       acc_merge(KIND, st, acc_shfl_xor(st, 32));
       u += acc_value(KIND, st);
@@ -1631,17 +1652,16 @@ __global__ __launch_bounds__(256) void leaf_parent_kernel(LeafParentArgs a, cons
           acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, qb[ks], acc, 0, 0, 0);
         }
         float zv[16];
-        if (kt * 32 + 32 <= nkeys) {  // a full tile: no key past the parent's end
 #pragma unroll
-          for (int r = 0; r < 16; ++r) zv[r] = acc[r] * a.qscale2;
-        } else {
+        for (int r = 0; r < 16; ++r) zv[r] = acc[r];
+        if (kt * 32 + 32 > nkeys) {  // a partial tile: keys past the parent's end drop out
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-            zv[r] = key < nkeys ? acc[r] * a.qscale2 : -INFINITY;
+            zv[r] = key < nkeys ? zv[r] : -INFINITY;
           }
         }
-        const ScoreAcc ts = acc_of(KIND, zv);
+        const ScoreAcc ts = acc_of_scaled<KIND, 16>(zv, a.qscale2);
         const int j = kt / kt_per_child;
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj)
