@@ -272,6 +272,38 @@ def main():
         roof["frac"] = roof["achieved"] / roof["peak"]
         roof["traffic"] = committed_traffic(dom)
 
+    # Every timed kernel against its own roofline (same definitions as above).
+    def roof_of(name):
+        if name not in work:
+            return None
+        bound, amount = work[name]
+        avg_s = kernels[name]["avg_ms"] / 1e3
+        if bound == "hbm":
+            ach, peak, unit = amount / avg_s / 1e9, HBM_PEAK_GBS, "GB/s"
+        elif bound == "mfma":
+            ach, peak, unit = amount / avg_s / 1e12, MFMA_BF16_PEAK_TFLOPS, "TFLOP/s"
+        else:
+            ach, peak, unit = amount / avg_s / 1e12, VALU_F32_PEAK_TFLOPS, "TFLOP/s"
+        return {"bound": bound, "achieved": ach, "peak": peak, "unit": unit, "frac": ach / peak}
+
+    per_kernel = {name: r for name in kernels if (r := roof_of(name)) is not None}
+    # The metric's two fractions: selection's compulsory bytes (q and k read,
+    # the fp32 pyramid written and read back, the indices written) over the
+    # selection time (pooling included) against HBM peak; the attention's exact
+    # causal flops (4d per visible (query, key) pair) over its time against the
+    # bf16 MFMA peak.
+    es = 2 if w["dtype"] == "bf16" else 4
+    _, R_rows = pisa.pisa_pyramid_layout(p)
+    sel_bytes = (B * H * Nq * d * es + B * Hkv * N * d * es + 2 * B * Hkv * R_rows * d * 4 + B * Hkv * Nq * K * 4)
+    sel_s = (split["pool"] + split["select"]) / args.steps / 1e3
+    attn_s = split["attn"] / args.steps / 1e3
+    fractions = {
+        "selection_hbm": {"bytes": sel_bytes, "achieved_GBps": sel_bytes / sel_s / 1e9,
+                          "frac": sel_bytes / sel_s / 1e9 / HBM_PEAK_GBS},
+        "attention_mfma": {"flops": attn_pairs * 4 * d, "achieved_TFLOPs": attn_pairs * 4 * d / attn_s / 1e12,
+                           "frac": attn_pairs * 4 * d / attn_s / 1e12 / MFMA_BF16_PEAK_TFLOPS},
+    }
+
     bsa_ms = None
     if not args.no_bsa:
         log("[bench] flat-BSA baseline")
@@ -319,6 +351,8 @@ def main():
         "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": cpu,
+        "fractions": fractions,
+        "per_kernel_roofline": per_kernel,
     }
     print(json.dumps(res), flush=True)
 

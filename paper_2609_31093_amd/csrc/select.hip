@@ -670,9 +670,9 @@ __device__ __forceinline__ int scan32(int v, int) { return scan32_incl(v); }
 // bf16 queries are exact.  In the result lane l holds tile rows 4*(l/16)+i
 // (i = 0..3) of head l%16, i.e. all children of 4/g candidates, so each
 // lane reduces its candidates' children to per-head scores in registers and
-// a 16-lane row sum adds the heads.  Ranking is the 128-entry register
-// bitonic sort of the wavefront; expansion and the stored leaf candidate set
-// are as in select_kernel.
+// a 16-lane row sum adds the heads.  Ranking is a 32-lane bitonic sort for
+// up to 32 candidates, else the 128-entry register sort of the wavefront;
+// expansion and the stored leaf candidate set are as in select_kernel.
 // ----------------------------------------------------------------------------
 
 typedef __bf16 bf16x8m __attribute__((ext_vector_type(8)));
