@@ -429,6 +429,35 @@ def main():
                 if rep == 1:
                     lat.append(e0.elapsed_time(e1) * 1e3)
         lat.sort()
+        # The same step captured once into a HIP graph and replayed per token,
+        # the query copied into the captured buffer before each replay.
+        q_static = qsteps[0].clone()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            sst = torch.cuda.current_stream()
+            pisa.pisa_select(pd, q_static, kd, pyr_d, idx_d, None, ws_d, nsd, sst)
+            pisa.pisa_sparse_attn_fwd(pd, q_static, kd, vd, idx_d, o_d, lse_d, ws_d, nad, sst)
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            gst = torch.cuda.current_stream()
+            pisa.pisa_select(pd, q_static, kd, pyr_d, idx_d, None, ws_d, nsd, gst)
+            pisa.pisa_sparse_attn_fwd(pd, q_static, kd, vd, idx_d, o_d, lse_d, ws_d, nad, gst)
+        torch.cuda.synchronize()
+        lat_g = []
+        for rep in range(2):
+            for qd in qsteps:
+                q_static.copy_(qd)
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+                graph.replay()
+                e1.record(stream)
+                torch.cuda.synchronize()
+                if rep == 1:
+                    lat_g.append(e0.elapsed_time(e1) * 1e3)
+        lat_g.sort()
         # Streaming decode: the cache grows by one token per step in place
         # (k, v and pyramid reserve Nd rows); a step appends the token to the
         # pyramid, then selects and attends at the new length.
@@ -456,6 +485,10 @@ def main():
                                      "median_us": lat[len(lat) // 2], "p90_us": lat[int(0.9 * len(lat))],
                                      "what": "one step = pisa_select + pisa_sparse_attn_fwd for 8 heads x 1 token "
                                              "at KV length 131072, pyramid prebuilt",
+                                     "graph_median_us": lat_g[len(lat_g) // 2],
+                                     "graph_p90_us": lat_g[int(0.9 * len(lat_g))],
+                                     "graph_what": "the same step captured once into a HIP graph and replayed per "
+                                                   "token (query copied into the captured buffer before each replay)",
                                      "streaming_median_us": lat_s[len(lat_s) // 2],
                                      "streaming_p90_us": lat_s[int(0.9 * len(lat_s))],
                                      "streaming_what": f"one step = pisa_pyramid_append of 1 token + pisa_select + "
