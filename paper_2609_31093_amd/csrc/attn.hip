@@ -979,8 +979,8 @@ static hipError_t launch_split_path(const Shape& s, const void* q, const void* k
     dim3 grid(s.K, static_cast<unsigned>(static_cast<int64_t>(s.BH()) * s.Nq));
     auto go = [&](auto kern, int gmax) {
       const size_t lds = static_cast<size_t>(2) * s.C * D * 2 + (static_cast<size_t>(s.C) * gmax + 256 + 2 * gmax) * 4;
-      if (lds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+      if (lds > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
       kern<<<grid, 256, lds, st>>>(a, qq, kk, vv, idx, part_o, part_lse);
     };
     if (s.G == 1)
@@ -1031,8 +1031,8 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
       auto go = [&](auto kern, int nw) {
         const size_t lds = (static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 4) +
                             static_cast<size_t>(nw) * 16 * (D + 8)) * 2;
-        if (lds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        if (lds > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
         kern<<<grid, nw * 64, lds, st>>>(a, qq, kk, vv, co.offs, co.toffs, co.ncl, co.pairs, part_o, part_lse);
       };
       if (s.C == 32)
@@ -1059,8 +1059,8 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
       const uint16_t* kk = static_cast<const uint16_t*>(k);
       const uint16_t* vv = static_cast<const uint16_t*>(v);
       auto go = [&](auto kern) {
-        if (lds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+        if (lds > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                   hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
         kern<<<grid, nwl * 64, lds, st>>>(a, qq, kk, vv, idx, part_o, part_lse, static_cast<uint16_t*>(o), lse);
       };
       if (s.C == 32)

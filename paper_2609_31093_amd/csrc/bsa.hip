@@ -455,8 +455,8 @@ hipError_t launch_flat_bsa(const Shape& s, const Geo& geo, const void* q, const 
     const size_t hred = static_cast<size_t>(64) * 16 * 4 * 2 * 4;
     const size_t lds = std::max(chunk, std::max(merge, s.G > 1 ? hred : size_t(0)));
     auto go = [&](auto kern) {
-      if (lds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
+      if (lds > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
       kern<<<grid, 256, lds, st>>>(a);
     };
     if (s.D == 128) {

@@ -2339,8 +2339,8 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
     {
       ProfScope ps("leaf_score", st);
       auto go = [&](auto kern) {
-        if (llds > 65536) hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                              hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(llds));
+        if (llds > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                    hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(llds));
         kern<<<lgrid, 256, llds, st>>>(la, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
                                        co.offs, co.toffs, co.ncl, co.pairs, u1);
       };
@@ -2411,8 +2411,8 @@ hipError_t launch_select_split(const Shape& s, const Geo& geo, const void* q, co
         using T = decltype(tag);
         auto run = [&](auto kern) {
           if (lds > 60000)  // beyond the default dynamic limit once the static arrays are added
-            hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                static_cast<int>(lds));
+            (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds));
           kern<<<grid, 256, lds, st>>>(a);
         };
         if (s.D == 128) {
