@@ -191,3 +191,57 @@ def test_random_shape_flat_bsa(i):
     rows = _rows(Nq, 70 + i)
     ora, gap = O.select_flat_bsa(x["q"], x["k"], C, K, bool(causal), rows=rows)
     print(compare_selection(idx_np[:, :, rows], ora, gap))
+
+
+def _edge_shapes(n=16, seed=77):
+    """Small and degenerate shapes: a handful of blocks (N from below one
+    block to a few), single query rows, budgets at or above the block count."""
+    r = np.random.default_rng(seed)
+    out = []
+    while len(out) < n:
+        d = int(r.choice([64, 128]))
+        C = int(r.choice([32, 64, 128]))
+        g = int(r.choice([2, 3, 4]))
+        G = int(r.choice([1, 2, 4, 8, 16]))
+        Hkv = int(r.choice([1, 2]))
+        causal = int(r.choice([0, 1]))
+        N = int(r.integers(1, 6 * C + 1))
+        M1 = -(-N // C)
+        kmax = min(128 // g, 2048 // (g * g * G), M1 + 2)
+        K = int(r.integers(3, max(4, kmax + 1)))
+        if g * K > 128 or g * g * K * G > 2048:
+            continue
+        Nq = int(r.choice([1, 2, N])) if N > 2 else N
+        Nq = min(Nq, N)
+        dtype = "bf16" if r.random() < 0.75 else "f32"
+        out.append((1, G * Hkv, Hkv, Nq, N, d, C, g, K, causal, dtype))
+    return out
+
+
+EDGE_SHAPES = _edge_shapes()
+
+
+@pytest.mark.parametrize("i", range(len(EDGE_SHAPES)), ids=[f"re{i}" for i in range(len(EDGE_SHAPES))])
+def test_edge_shape_parity(i):
+    B, H, Hkv, Nq, N, d, C, g, K, causal, dtype = EDGE_SHAPES[i]
+    print("shape", EDGE_SHAPES[i], flush=True)
+    x = inputs.random_qkv(B, H, Hkv, Nq, N, d, dtype, seed=700 + i)
+    p = pisa.make_problem(B, H, Hkv, Nq, N, d, C, g, K, causal, dtype)
+    q, k, v = dev(x["q"], dtype), dev(x["k"], dtype), dev(x["v"], dtype)
+    pyr = pisa.build_pyramid(p, k)
+    idx = pisa.select(p, q, k, pyr)
+    o, lse = pisa.sparse_attn_fwd(p, q, k, v, idx)
+    bsa = pisa.select_flat_bsa(p, q, pyr) if K <= 32 or dtype == "f32" or N // C < 16384 else None
+    torch.cuda.synchronize()
+    idx_np = idx.cpu().numpy()
+    check_selection_valid(idx_np, N, Nq, C, K, bool(causal))
+    rows = np.arange(Nq)
+    ora, gap = O.select(x["q"], x["k"], C, g, K, bool(causal), rows=rows)
+    compare_selection(idx_np, ora, gap)
+    want_o, want_lse = O.sparse_attention(x["q"], x["k"], x["v"], idx_np, C, bool(causal), rows=rows)
+    tol = 2e-2 if dtype == "bf16" else 1e-4
+    assert np.abs(o.float().cpu().numpy() - want_o).max() <= tol
+    assert np.abs(lse.cpu().numpy() - want_lse).max() <= 1e-3
+    if bsa is not None:
+        ora_b, gap_b = O.select_flat_bsa(x["q"], x["k"], C, K, bool(causal), rows=rows)
+        compare_selection(bsa.cpu().numpy(), ora_b, gap_b)
