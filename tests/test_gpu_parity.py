@@ -69,6 +69,9 @@ SHAPES = {
     # causal budgets above 32 on the block attention path (slots 32.. merged after the per-leaf-block kernel)
     "k40-causal-block": (1, 4, 2, 5000, 5000, 64, 32, 2, 40, 1, "bf16"),
     "k48-causal-block-d128": (1, 2, 1, 6000, 6000, 128, 64, 2, 48, 1, "bf16"),
+    # leaf blocks above 128 keys (query-centric attention; the general leaf scorer with > 64 KiB of LDS)
+    "c256-two-stage": (1, 4, 2, 3000, 6000, 128, 256, 2, 6, 1, "bf16"),
+    "c160-g3-noncausal": (1, 2, 1, 2500, 2500, 64, 160, 3, 5, 0, "bf16"),
 }
 
 
