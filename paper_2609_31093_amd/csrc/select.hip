@@ -866,6 +866,256 @@ __global__ __launch_bounds__(kMfmaSelRows * 64) void stage1_mfma_kernel(SelArgs 
   if (lane == 0) a.a1cnt[orow] = nA;
 }
 
+// Stage 1 on the matrix cores for kUnionRows consecutive query rows per
+// wavefront (G = 1, 2 or 4 heads per KV head, so that the rows' heads fill at
+// most the 16 columns of a tile): each ranked level scores the union of the
+// rows' candidate sets once, column r*G + h of the tile being head h of row
+// r, so that rows whose candidates coincide (neighbouring queries mostly
+// select the same nodes) share every summary load; each row then ranks its
+// own candidates with the union's scores.  The union is built through a
+// bitmap over the level's nodes, so it comes out ascending, and a node's
+// place in it is the population count below its bit.  Products, scores,
+// ranking and expansion are otherwise those of stage1_mfma_kernel.
+constexpr int kUnionRows = 4;   // query rows per wavefront
+constexpr int kUnionWaves = 4;  // wavefronts per workgroup
+
+// LDS words of one wavefront of stage1_union_kernel.
+__host__ __device__ constexpr int union_wave_words(int bm_words) {
+  return kUnionRows * 128 * 3 + kUnionRows * 128 + kUnionRows * 128 * kUnionRows + 2 * (bm_words + 1);
+}
+
+template <int D, int GC, int KIND>
+__global__ __launch_bounds__(kUnionWaves * 64) void stage1_union_kernel(SelArgs a, const uint16_t* __restrict__ hilo,
+                                                                       int bm_words) {
+  constexpr int KS = D / 32;
+  constexpr int CPL = 4 / GC;   // union candidates per lane in the result layout
+  constexpr int CPT = 16 / GC;  // union candidates per 16-row tile
+  constexpr int R = kUnionRows;
+  constexpr int UMAX = R * 128;
+  extern __shared__ int lds_u[];
+  const Geo& geo = a.geo;
+  const int G = a.G, K = a.K, gK = a.gK;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int row0 = (blockIdx.x * kUnionWaves + wave) * R;
+  if (row0 >= a.Nq) return;  // the whole wavefront leaves; only wavefront-level syncs follow
+  int* L = lds_u + wave * union_wave_words(bm_words);
+  int* cand = L;                     // [R][128]
+  int* cand2 = cand + R * 128;       // [R][128]
+  int* flag = cand2 + R * 128;       // [R][128]
+  int* U = flag + R * 128;           // [UMAX] union, ascending
+  float* us = reinterpret_cast<float*>(U + UMAX);  // [UMAX][R] scores of the union for each row
+  uint32_t* bm = reinterpret_cast<uint32_t*>(us + UMAX * R);  // [bm_words + 1]
+  int* pre = reinterpret_cast<int*>(bm + bm_words + 1);       // [bm_words + 1]
+  const int bh = blockIdx.y;
+  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+  const int col = lane & 15, quad = lane >> 4;
+  const int crow_r = col / G, chh = col - crow_r * G;  // this lane's column: row crow_r, head chh
+  const bool cvalid = col < R * G && row0 + crow_r < a.Nq;
+
+  bf16x8m qB[KS];
+  {
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) +
+                           ((static_cast<int64_t>(b) * a.H + h * G + (cvalid ? chh : 0)) * a.Nq +
+                            (cvalid ? row0 + crow_r : 0)) * D + 8 * quad;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      uint4 u = make_uint4(0, 0, 0, 0);
+      if (cvalid) u = *reinterpret_cast<const uint4*>(qrow + ks * 32);
+      qB[ks] = __builtin_bit_cast(bf16x8m, u);
+    }
+  }
+
+  int nAr[R], cr[R];
+  bool rv[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    rv[r] = row0 + r < a.Nq;
+    nAr[r] = 1;
+    cr[r] = (geo.N - a.Nq + row0 + r) / geo.C;
+    if (lane == 0) cand[r * 128] = 0;
+  }
+  wave_sync();
+  for (int lev = geo.L; lev >= 2; --lev) {
+    const int Mb = geo.M[lev - 1];
+    bool rk[R];
+    bool any = false;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      rk[r] = rv[r] && nAr[r] > K;
+      any = any || rk[r];
+    }
+    if (any) {
+      // 1) the union of the ranked rows' candidates
+      const int nw = (geo.M[lev] + 31) / 32;
+      for (int w = lane; w < nw; w += 64) bm[w] = 0u;
+      wave_sync();
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (!rk[r]) continue;
+        for (int ci = lane; ci < nAr[r]; ci += 64) {
+          const int node = cand[r * 128 + ci];
+          atomicOr(&bm[node >> 5], 1u << (node & 31));
+        }
+      }
+      wave_sync();
+      const int wpl = (nw + 63) / 64;
+      const int w0 = min(nw, lane * wpl), w1 = min(nw, w0 + wpl);
+      int mine = 0;
+      for (int w = w0; w < w1; ++w) mine += __popc(bm[w]);
+      int nU;
+      int pos = team_scan<64>(mine, nullptr, nU);
+      for (int w = w0; w < w1; ++w) {
+        pre[w] = pos;
+        uint32_t bits = bm[w];
+        while (bits) {
+          U[pos++] = w * 32 + __ffs(bits) - 1;
+          bits &= bits - 1;
+        }
+      }
+      wave_sync();
+      // 2) the union's child logits, tile by tile, every row's heads as columns
+      const uint16_t* pb = hilo + (static_cast<int64_t>(bh) * geo.R + geo.off[lev - 1]) * (2 * D) + 16 * quad;
+      const int ntile = (nU * GC + 15) / 16;
+      for (int tile = 0; tile < ntile; ++tile) {
+        const int rr = tile * 16 + col;
+        const int ui = rr / GC, j = rr % GC;
+        bool ok = false;
+        int crow = 0;
+        if (ui < nU) {
+          crow = U[ui] * GC + j;
+          ok = crow < Mb;
+        }
+        const uint16_t* ar = pb + static_cast<int64_t>(ok ? crow : 0) * (2 * D);
+        uint4 hi[KS], lo[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          hi[ks] = make_uint4(0, 0, 0, 0);
+          lo[ks] = make_uint4(0, 0, 0, 0);
+          if (ok) {
+            hi[ks] = *reinterpret_cast<const uint4*>(ar + ks * 64);
+            lo[ks] = *reinterpret_cast<const uint4*>(ar + ks * 64 + 8);
+          }
+        }
+        f32x4m acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8m, hi[ks]), qB[ks], acc, 0, 0, 0);
+          acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8m, lo[ks]), qB[ks], acc, 0, 0, 0);
+        }
+#pragma unroll
+        for (int k2 = 0; k2 < CPL; ++k2) {
+          const int cj = tile * CPT + CPL * quad + k2;
+          float z[GC];
+#pragma unroll
+          for (int i = 0; i < GC; ++i) z[i] = acc[k2 * GC + i] * a.qscale2;
+          int n = 1;
+          if (cj < nU) n = max(1, min(GC, Mb - U[cj] * GC));
+          float u = cvalid ? lane_children_score<KIND, GC>(z, n) : 0.f;
+          // the G heads of a row sit in G neighbouring lanes of the 16-lane row
+          for (int o = 1; o < G; o <<= 1) u += __shfl_xor(u, o);
+          if (cvalid && chh == 0 && cj < nU) us[cj * R + crow_r] = u;
+        }
+      }
+      wave_sync();
+      // 3) each ranked row ranks its own candidates with the union's scores:
+      // forced first, then score descending, ties by candidate index
+      // (ascending nodes), then empty slots
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        if (!rk[r]) continue;
+        const Forced fz = forced_at(geo, lev, cr[r], a.causal);
+        const int keepn = K - fz.count();
+        const int nA = nAr[r];
+        const int* cr_ = cand + r * 128;
+        auto score_of = [&](int node) {
+          const int w = node >> 5;
+          const int ui = pre[w] + __popc(bm[w] & ((1u << (node & 31)) - 1u));
+          return us[ui * R + r];
+        };
+        int* fl = flag + r * 128;
+        if (nA <= 32) {
+          const bool v = lane < nA;
+          const int node = v ? cr_[lane] : 0;
+          const bool f = v && fz.is(node);
+          float key = !v ? -INFINITY : (f ? INFINITY : score_of(node));
+          int pack = lane;
+          const int nforced = __popcll(__ballot(f));
+          sort32(key, pack, lane & 31);
+          if (lane < nA) fl[pack] = (lane < nforced || lane - nforced < keepn) ? 1 : 0;
+        } else {
+          uint32_t khi[2], klo[2];
+          int nforced = 0;
+#pragma unroll
+          for (int s2 = 0; s2 < 2; ++s2) {
+            const int ci = lane + 64 * s2;
+            const bool v = ci < nA;
+            const int node = v ? cr_[ci] : 0;
+            const bool f = v && fz.is(node);
+            khi[s2] = !v ? 0xFFFFFFFFu : (f ? 0u : desc_bits(score_of(node)));
+            klo[s2] = static_cast<uint32_t>(ci);
+            nforced += __popcll(__ballot(f));
+          }
+          sort128(khi, klo, lane);
+#pragma unroll
+          for (int s2 = 0; s2 < 2; ++s2) {
+            const int rk2 = lane + 64 * s2;
+            if (static_cast<int>(klo[s2]) < nA) fl[klo[s2]] = (rk2 < nforced || rk2 - nforced < keepn) ? 1 : 0;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (rv[r] && !rk[r])
+        for (int ci = lane; ci < nAr[r]; ci += 64) flag[r * 128 + ci] = 1;
+    }
+    wave_sync();
+    // 4) each row expands its kept nodes to their eligible children
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (!rv[r]) continue;
+      const int rmax = a.causal ? min(anc_at(geo, cr[r], lev - 1), Mb - 1) : Mb - 1;
+      const int* cr_ = cand + r * 128;
+      const int* fl = flag + r * 128;
+      int* c2 = cand2 + r * 128;
+      const int i0 = lane * 2, i1 = min(nAr[r], i0 + 2);
+      int mine = 0;
+      for (int ci = i0; ci < i1; ++ci) {
+        if (fl[ci]) {
+          const int c0 = cr_[ci] * GC;
+          mine += max(0, min(c0 + GC - 1, rmax) - c0 + 1);
+        }
+      }
+      int total;
+      int pos = team_scan<64>(mine, nullptr, total);
+      for (int ci = i0; ci < i1; ++ci) {
+        if (fl[ci]) {
+          const int c0 = cr_[ci] * GC;
+          const int n = max(0, min(c0 + GC - 1, rmax) - c0 + 1);
+          for (int jj = 0; jj < n; ++jj) c2[pos + jj] = c0 + jj;
+          pos += n;
+        }
+      }
+      nAr[r] = total;
+    }
+    wave_sync();
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      if (!rv[r]) continue;
+      for (int ci = lane; ci < nAr[r]; ci += 64) cand[r * 128 + ci] = cand2[r * 128 + ci];
+    }
+    wave_sync();
+  }
+
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    if (!rv[r]) continue;
+    const int64_t orow = static_cast<int64_t>(bh) * a.Nq + row0 + r;
+    for (int ci = lane; ci < gK; ci += 64) a.a1[orow * gK + ci] = ci < nAr[r] ? cand[r * 128 + ci] : -1;
+    if (lane == 0) a.a1cnt[orow] = nAr[r];
+  }
+}
+
 // Summaries as bf16 pairs for stage1_mfma_kernel: each group of 8 fp32
 // values becomes 8 rounded values (hi) followed by 8 rounded remainders (lo).
 __global__ __launch_bounds__(256) void pyr_hilo_kernel(const float* __restrict__ pyr, uint16_t* __restrict__ hilo,
@@ -2278,7 +2528,38 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
         else if (s.score == kScoreMean) k1<<<grid, kMfmaSelRows * 64, 0, st>>>(a, hilo);
         else k2<<<grid, kMfmaSelRows * 64, 0, st>>>(a, hilo);
       };
-      if (s.D == 128) {
+      // 1, 2 or 4 heads per KV head: kUnionRows rows per wavefront share the
+      // union of their candidates (their heads fill at most 16 columns)
+      const int bm_words = (geo.L >= 2 ? (geo.M[2] + 31) / 32 : 1);
+      dim3 ugrid((s.Nq + kUnionRows * kUnionWaves - 1) / (kUnionRows * kUnionWaves), s.BH());
+      const size_t ulds = static_cast<size_t>(kUnionWaves) * union_wave_words(bm_words) * 4;
+      auto gu = [&](auto k0, auto k1, auto k2) {
+        auto run = [&](auto kern) {
+          if (ulds > 65536)
+            (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                      hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(ulds));
+          kern<<<ugrid, kUnionWaves * 64, ulds, st>>>(a, hilo, bm_words);
+        };
+        if (s.score == kScoreLse) run(k0);
+        else if (s.score == kScoreMean) run(k1);
+        else run(k2);
+      };
+      const bool union_rows = s.G == 1 || s.G == 2 || s.G == 4;
+      if (union_rows && s.D == 128) {
+        if (s.g == 4)
+          gu(stage1_union_kernel<128, 4, kScoreLse>, stage1_union_kernel<128, 4, kScoreMean>,
+             stage1_union_kernel<128, 4, kScoreMeanVar>);
+        else
+          gu(stage1_union_kernel<128, 2, kScoreLse>, stage1_union_kernel<128, 2, kScoreMean>,
+             stage1_union_kernel<128, 2, kScoreMeanVar>);
+      } else if (union_rows) {
+        if (s.g == 4)
+          gu(stage1_union_kernel<64, 4, kScoreLse>, stage1_union_kernel<64, 4, kScoreMean>,
+             stage1_union_kernel<64, 4, kScoreMeanVar>);
+        else
+          gu(stage1_union_kernel<64, 2, kScoreLse>, stage1_union_kernel<64, 2, kScoreMean>,
+             stage1_union_kernel<64, 2, kScoreMeanVar>);
+      } else if (s.D == 128) {
         if (s.g == 4)
           go(stage1_mfma_kernel<128, 4, kScoreLse>, stage1_mfma_kernel<128, 4, kScoreMean>,
              stage1_mfma_kernel<128, 4, kScoreMeanVar>);
