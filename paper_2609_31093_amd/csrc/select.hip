@@ -653,6 +653,34 @@ __device__ __forceinline__ void sort32(float& key, int& pack, int hl) {
   pack = static_cast<int>(lo);
 }
 
+// The best 16 of each wavefront half (key desc, pack asc) in its lanes 0-15,
+// in no particular order, when only that set matters: the network's last
+// merge stops after its first step (each 16-lane run is sorted, in opposite
+// directions, and lane i keeps the better of i and i ^ 16); `full` finishes
+// the sort (rank order in every lane), as sort32.
+__device__ __forceinline__ void sort32_top16(float& key, int& pack, int hl, bool full) {
+  uint32_t hi = desc_bits(key), lo = static_cast<uint32_t>(pack);
+  sort32_step<2, 1>(hi, lo, hl);
+  sort32_step<4, 2>(hi, lo, hl);
+  sort32_step<4, 1>(hi, lo, hl);
+  sort32_step<8, 4>(hi, lo, hl);
+  sort32_step<8, 2>(hi, lo, hl);
+  sort32_step<8, 1>(hi, lo, hl);
+  sort32_step<16, 8>(hi, lo, hl);
+  sort32_step<16, 4>(hi, lo, hl);
+  sort32_step<16, 2>(hi, lo, hl);
+  sort32_step<16, 1>(hi, lo, hl);
+  sort32_step<32, 16>(hi, lo, hl);
+  if (full) {
+    sort32_step<32, 8>(hi, lo, hl);
+    sort32_step<32, 4>(hi, lo, hl);
+    sort32_step<32, 2>(hi, lo, hl);
+    sort32_step<32, 1>(hi, lo, hl);
+  }
+  key = desc_bits_inv(hi);
+  pack = static_cast<int>(lo);
+}
+
 // Inclusive prefix sum over the 32 lanes of a wavefront half.
 __device__ __forceinline__ int scan32(int v, int) { return scan32_incl(v); }
 
@@ -1502,15 +1530,18 @@ __device__ __forceinline__ void g2_rank_expand(const Geo& geo, int lev, int c, i
     }
   }
   int pack = valid ? (node << 6) | hl : 0x7FFFFFC0 | hl;
-  sort32(key, pack, hl);
-  const int nkept = min(K, nvalid);
+  // With K = 16 only the set of the best 16 matters (a survivor's place
+  // among the next level's slots does not), so the sort stops early; the
+  // survivors then sit in lanes 0-15 in any order, empty slots among them.
+  sort32_top16(key, pack, hl, K != 16);
+  const int nkept = K == 16 ? 16 : min(K, nvalid);
 
   const int r = hl >> 1;
   const int pr = __shfl(pack, hbase | r);
   const int korig = pr & 63;
   const int rmax = causal ? min(anc_at(geo, c, lb), Mb - 1) : Mb - 1;
   const int cn = 2 * (pr >> 6) + (hl & 1);
-  const bool cvalid = r < nkept && cn <= rmax;
+  const bool cvalid = r < nkept && pr < 0x7FFFFFC0 && cn <= rmax;
 #pragma unroll
   for (int hh = 0; hh < GMAX; ++hh) {
     const float a0 = __shfl(z0[hh], hbase | korig);
@@ -1699,8 +1730,9 @@ __global__ __launch_bounds__(256) void final_topk_pair_kernel(TopkArgsP a, const
   if (valid) key = (ranked && !isf) ? u_raw : INFINITY;
   const float own = key;
   int pack = valid ? (node << 6) | hl : 0x7FFFFFC0 | hl;
-  sort32(key, pack, hl);
-  // lane p of the sorted half holds rank p; send it back to the source lane
+  // lane p of the sorted half holds rank p (with K = 16 only the best 16 are
+  // separated from the rest); send it back to the source lane
+  sort32_top16(key, pack, hl, a.K != 16);
   s_rank[wave][(lane & 32) + (pack & 63)] = hl;
   wave_sync();
   const bool kept = valid && s_rank[wave][lane] < a.K;
