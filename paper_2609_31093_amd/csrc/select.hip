@@ -615,16 +615,32 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
 // stored.
 // ----------------------------------------------------------------------------
 
+// The lanes of a wavefront whose entry e (= lane & 31 for the 32-lane
+// sorts) keeps the smaller of itself and its partner in the bitonic step
+// (K2, J), as a lane mask known at compile time.
+template <int K2, int J>
+constexpr uint64_t sort32_want_small() {
+  uint64_t m = 0;
+  for (int l = 0; l < 64; ++l) {
+    const int e = l & 31;
+    if (((e & K2) == 0) == ((e & J) == 0)) m |= uint64_t(1) << l;
+  }
+  return m;
+}
+
 // One compare-exchange stage of the bitonic network, without branches: the
 // lane keeps the smaller of (itself, partner) where the stage wants the
-// smaller, else the larger.
+// smaller, else the larger.  hl = lane & 31 (the stage's direction comes
+// from a constant lane mask).
 template <int K2, int J>
 __device__ __forceinline__ void sort32_step(uint32_t& hi, uint32_t& lo, int hl) {
+  (void)hl;
   const uint32_t ohi = static_cast<uint32_t>(xor32_i<J>(static_cast<int>(hi)));
   const uint32_t olo = static_cast<uint32_t>(xor32_i<J>(static_cast<int>(lo)));
   const uint64_t mine = (static_cast<uint64_t>(hi) << 32) | lo;
   const uint64_t other = (static_cast<uint64_t>(ohi) << 32) | olo;
-  const bool want_small = ((hl & K2) == 0) == ((hl & J) == 0);
+  constexpr uint64_t kWant = sort32_want_small<K2, J>();
+  const bool want_small = __builtin_amdgcn_inverse_ballot_w64(kWant);
   const bool take = (other < mine) == want_small;
   hi = take ? ohi : hi;
   lo = take ? olo : lo;
