@@ -265,43 +265,65 @@ __device__ __forceinline__ float desc_bits_inv(uint32_t d) {
 
 // Bitonic sort of 128 (key, pack) entries held two per lane (entry lane and
 // lane + 64) into rank order (key desc, pack asc); packs are non-negative.
-__device__ __forceinline__ void sort128(uint32_t (&hi)[2], uint32_t (&lo)[2], int lane) {
-#pragma unroll
-  for (int k2 = 2; k2 <= 128; k2 <<= 1) {
-#pragma unroll
-    for (int j = k2 >> 1; j >= 1; j >>= 1) {
-      if (j == 64) {  // the two entries of a lane: the lower index keeps the smaller
-        const uint64_t x = (static_cast<uint64_t>(hi[0]) << 32) | lo[0];
-        const uint64_t y = (static_cast<uint64_t>(hi[1]) << 32) | lo[1];
-        const bool sw = y < x;
-        const uint32_t h0 = sw ? hi[1] : hi[0], l0 = sw ? lo[1] : lo[0];
-        hi[1] = sw ? hi[0] : hi[1];
-        lo[1] = sw ? lo[0] : lo[1];
-        hi[0] = h0;
-        lo[0] = l0;
-        continue;
-      }
-#pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        const int e = lane + 64 * s;
-        uint32_t ohi, olo;
-        switch (j) {
-          case 1: ohi = xor32_i<1>(hi[s]); olo = xor32_i<1>(lo[s]); break;
-          case 2: ohi = xor32_i<2>(hi[s]); olo = xor32_i<2>(lo[s]); break;
-          case 4: ohi = xor32_i<4>(hi[s]); olo = xor32_i<4>(lo[s]); break;
-          case 8: ohi = xor32_i<8>(hi[s]); olo = xor32_i<8>(lo[s]); break;
-          case 16: ohi = xor32_i<16>(hi[s]); olo = xor32_i<16>(lo[s]); break;
-          default: ohi = __shfl_xor(static_cast<int>(hi[s]), 32); olo = __shfl_xor(static_cast<int>(lo[s]), 32); break;
-        }
-        const uint64_t mine = (static_cast<uint64_t>(hi[s]) << 32) | lo[s];
-        const uint64_t other = (static_cast<uint64_t>(ohi) << 32) | olo;
-        const bool want_small = ((e & k2) == 0) == ((e & j) == 0);
-        const bool take = (other < mine) == want_small;
-        hi[s] = take ? ohi : hi[s];
-        lo[s] = take ? olo : lo[s];
-      }
-    }
+// Step (K2, J) of entry e keeps the smaller of e and e ^ J where
+// (e & K2 == 0) == (e & J == 0); that direction is a lane mask per entry
+// half, known at compile time.
+template <int K2, int J, int S>
+constexpr uint64_t sort128_want_small() {
+  uint64_t m = 0;
+  for (int l = 0; l < 64; ++l) {
+    const int e = l + 64 * S;
+    if (((e & K2) == 0) == ((e & J) == 0)) m |= uint64_t(1) << l;
   }
+  return m;
+}
+
+template <int K2, int J, int S>
+__device__ __forceinline__ void sort128_half_step(uint32_t& hi, uint32_t& lo) {
+  uint32_t ohi, olo;
+  if constexpr (J < 32) {
+    ohi = static_cast<uint32_t>(xor32_i<J>(static_cast<int>(hi)));
+    olo = static_cast<uint32_t>(xor32_i<J>(static_cast<int>(lo)));
+  } else {
+    ohi = static_cast<uint32_t>(__shfl_xor(static_cast<int>(hi), 32));
+    olo = static_cast<uint32_t>(__shfl_xor(static_cast<int>(lo), 32));
+  }
+  const uint64_t mine = (static_cast<uint64_t>(hi) << 32) | lo;
+  const uint64_t other = (static_cast<uint64_t>(ohi) << 32) | olo;
+  constexpr uint64_t kWant = sort128_want_small<K2, J, S>();
+  const bool take = (other < mine) == __builtin_amdgcn_inverse_ballot_w64(kWant);
+  hi = take ? ohi : hi;
+  lo = take ? olo : lo;
+}
+
+// The steps J = J0, J0 / 2, ..., 1 of stage K2.
+template <int K2, int J>
+__device__ __forceinline__ void sort128_stage(uint32_t (&hi)[2], uint32_t (&lo)[2]) {
+  if constexpr (J == 64) {  // the two entries of a lane: the lower index keeps the smaller
+    const uint64_t x = (static_cast<uint64_t>(hi[0]) << 32) | lo[0];
+    const uint64_t y = (static_cast<uint64_t>(hi[1]) << 32) | lo[1];
+    const bool sw = y < x;
+    const uint32_t h0 = sw ? hi[1] : hi[0], l0 = sw ? lo[1] : lo[0];
+    hi[1] = sw ? hi[0] : hi[1];
+    lo[1] = sw ? lo[0] : lo[1];
+    hi[0] = h0;
+    lo[0] = l0;
+  } else {
+    sort128_half_step<K2, J, 0>(hi[0], lo[0]);
+    sort128_half_step<K2, J, 1>(hi[1], lo[1]);
+  }
+  if constexpr (J > 1) sort128_stage<K2, J / 2>(hi, lo);
+}
+
+__device__ __forceinline__ void sort128(uint32_t (&hi)[2], uint32_t (&lo)[2], int lane) {
+  (void)lane;
+  sort128_stage<2, 1>(hi, lo);
+  sort128_stage<4, 2>(hi, lo);
+  sort128_stage<8, 4>(hi, lo);
+  sort128_stage<16, 8>(hi, lo);
+  sort128_stage<32, 16>(hi, lo);
+  sort128_stage<64, 32>(hi, lo);
+  sort128_stage<128, 64>(hi, lo);
 }
 
 template <typename T, int D, int TEAM, int GMAX, bool FUSED>
