@@ -139,6 +139,37 @@ __global__ __launch_bounds__(256) void pool_top_kernel(float* __restrict__ pyr, 
   }
 }
 
+// The same levels with the level below first_level read into LDS once (every
+// load in flight together) and each coarser level computed from LDS, so that
+// the level-by-level chain does not wait on global memory; used when the two
+// largest levels fit the dynamic LDS.  Same arithmetic, same results.
+__global__ __launch_bounds__(1024) void pool_top_lds_kernel(float* __restrict__ pyr, Geo geo, int first_level, int D) {
+  extern __shared__ float lds[];
+  const int bh = blockIdx.x;
+  float* pb = pyr + static_cast<int64_t>(bh) * geo.R * D;
+  float* src = lds;
+  float* dst = lds + static_cast<int64_t>(geo.M[first_level - 1]) * D;
+  {
+    const int n4 = geo.M[first_level - 1] * D / 4;
+    const float4* g4 = reinterpret_cast<const float4*>(pb + static_cast<int64_t>(geo.off[first_level - 1]) * D);
+    for (int e = threadIdx.x; e < n4; e += blockDim.x) reinterpret_cast<float4*>(src)[e] = g4[e];
+  }
+  __syncthreads();
+  for (int lv = first_level; lv <= geo.Lstore; ++lv) {
+    const int n = geo.M[lv] * D;
+    for (int e = threadIdx.x; e < n; e += blockDim.x) {
+      const int node = e / D, col = e - node * D;
+      const float mval = node_mean(geo, lv, node, col, [&](int ch, int cc) { return src[ch * D + cc]; });
+      dst[e] = mval;
+      pb[(geo.off[lv] + node) * D + col] = mval;
+    }
+    __syncthreads();
+    float* t = src;
+    src = dst;
+    dst = t;
+  }
+}
+
 // Decode-cache update (App. B): one workgroup per (batch, KV head).  The
 // leaf blocks from c_first (the block holding row n_old) to the end are
 // recomputed, then level by level the nodes from the ancestor of c_first to
@@ -269,6 +300,8 @@ hipError_t launch_pyramid_append(const Geo& geo, const Geo& geo_old, int BH, int
   return hipGetLastError();
 }
 
+constexpr size_t kPoolTopLds = 160 * 1024;  // dynamic LDS of one workgroup on a CDNA4 CU
+
 // s = number of coarser levels computed inside pool_leaf_kernel: the largest
 // s with g^s <= 16.
 static int pool_s_levels(int g) {
@@ -303,7 +336,20 @@ hipError_t launch_build_pyramid(const Geo& geo, int BH, int D, bool bf16, const 
   if (e != hipSuccess) return e;
   if (geo.Lstore >= s + 2) {
     ProfScope ps("pool_top", st);
-    pool_top_kernel<<<BH, 256, 0, st>>>(pyr, geo, s + 2, D);
+    // levels s+1 (read) and s+2 (the largest computed) in LDS, the coarser
+    // ones reuse the two buffers
+    const size_t tlds = static_cast<size_t>(geo.M[s + 1] + geo.M[s + 2]) * D * sizeof(float);
+    bool fits = tlds <= kPoolTopLds;
+    if (fits && tlds > 65536) {
+      fits = hipFuncSetAttribute(reinterpret_cast<const void*>(pool_top_lds_kernel),
+                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(tlds)) == hipSuccess;
+      if (!fits) (void)hipGetLastError();  // the refusal is not the caller's error
+    }
+    if (fits) {
+      pool_top_lds_kernel<<<BH, 1024, tlds, st>>>(pyr, geo, s + 2, D);
+    } else {
+      pool_top_kernel<<<BH, 256, 0, st>>>(pyr, geo, s + 2, D);
+    }
     e = hipGetLastError();
   }
   return e;
