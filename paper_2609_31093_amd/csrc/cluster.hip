@@ -159,6 +159,80 @@ __global__ __launch_bounds__(1024) void cluster_scan_kernel(const int32_t* __res
   }
 }
 
+// The same scans with the counts staged through LDS (n <= kScanLdsMax): the
+// counts are read and the offsets written with coalesced accesses, and each
+// thread's run is read from LDS (one pad word per 16 keeps the runs on
+// distinct banks) instead of as strided global loads.
+constexpr int kScanLdsMax = 17408;
+__host__ __device__ __forceinline__ int scan_pad(int i) { return i + (i >> 4); }
+
+__global__ __launch_bounds__(1024) void cluster_scan_lds_kernel(const int32_t* __restrict__ hist,
+                                                                int32_t* __restrict__ offs,
+                                                                int32_t* __restrict__ cursor,
+                                                                int32_t* __restrict__ toffs, int n, int tile) {
+  extern __shared__ int32_t sh[];
+  __shared__ int wsum[16], wtile[16];
+  int32_t* ho = sh;                       // counts, then offsets (padded)
+  int32_t* ht = sh + scan_pad(n) + 1;     // tile offsets (padded)
+  const int tid = threadIdx.x;
+  for (int e = tid; e < n; e += 1024) ho[scan_pad(e)] = hist[e];
+  __syncthreads();
+  const int per = (n + 1023) / 1024;
+  const int i0 = min(n, tid * per), i1 = min(n, i0 + per);
+  const int cnt = i1 - i0;
+  int v[kScanRun];
+  int local = 0, ltile = 0;
+#pragma unroll
+  for (int j = 0; j < kScanRun; ++j) {
+    v[j] = j < cnt ? ho[scan_pad(i0 + j)] : 0;
+    local += v[j];
+    ltile += (v[j] + tile - 1) / tile;
+  }
+  const int lane = tid & 63, w = tid >> 6;
+  int x = local, y = ltile;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int xs = __shfl_up(x, o), ys = __shfl_up(y, o);
+    if (lane >= o) {
+      x += xs;
+      y += ys;
+    }
+  }
+  if (lane == 63) {
+    wsum[w] = x;
+    wtile[w] = y;
+  }
+  __syncthreads();
+  int pre = 0, tot = 0, tpre = 0, ttot = 0;
+  for (int i = 0; i < 16; ++i) {
+    pre += (i < w) ? wsum[i] : 0;
+    tot += wsum[i];
+    tpre += (i < w) ? wtile[i] : 0;
+    ttot += wtile[i];
+  }
+  int run = pre + x - local, trun = tpre + y - ltile;
+#pragma unroll
+  for (int j = 0; j < kScanRun; ++j) {
+    if (j < cnt) {
+      ho[scan_pad(i0 + j)] = run;
+      ht[scan_pad(i0 + j)] = trun;
+    }
+    run += v[j];
+    trun += (v[j] + tile - 1) / tile;
+  }
+  __syncthreads();
+  for (int e = tid; e < n; e += 1024) {
+    const int o = ho[scan_pad(e)];
+    offs[e] = o;
+    cursor[e] = o;
+    toffs[e] = ht[scan_pad(e)];
+  }
+  if (tid == 0) {
+    offs[n] = tot;
+    toffs[n] = ttot;
+  }
+}
+
 __global__ __launch_bounds__(kClusterThreads) void cluster_scatter_kernel(ClusterArgs a, int32_t* __restrict__ cursor,
                                                                           int32_t* __restrict__ pairs) {
   extern __shared__ int32_t h[];
@@ -222,7 +296,15 @@ hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* ou
   dim3 grid((a.nrows + kClusterRows - 1) / kClusterRows, BH);
   const size_t lds = static_cast<size_t>(a.M1) * 4;
   cluster_hist_kernel<<<grid, kClusterThreads, lds, st>>>(a, hist);
-  cluster_scan_kernel<<<1, 1024, 0, st>>>(hist, offs, cursor, toffs, ncl, tile);
+  if (ncl <= kScanLdsMax) {
+    const size_t slds = 2 * (static_cast<size_t>(scan_pad(static_cast<int>(ncl))) + 1) * sizeof(int32_t);
+    if (slds > 65536)
+      (void)hipFuncSetAttribute(reinterpret_cast<const void*>(cluster_scan_lds_kernel),
+                                hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(slds));
+    cluster_scan_lds_kernel<<<1, 1024, slds, st>>>(hist, offs, cursor, toffs, static_cast<int>(ncl), tile);
+  } else {
+    cluster_scan_kernel<<<1, 1024, 0, st>>>(hist, offs, cursor, toffs, ncl, tile);
+  }
   cluster_scatter_kernel<<<grid, kClusterThreads, lds, st>>>(a, cursor, pairs);
   return hipGetLastError();
 }
