@@ -1482,9 +1482,11 @@ __device__ __forceinline__ float reduce_scatter(float (&w)[LPE], int sub) {
 
 // Logits of pyramid row `ri` (this lane's slot) against every head's query:
 // the group's LPE rows are loaded together, lane sub reading chunks
-// sub, sub + LPE, ... (pbase already points at chunk sub of row 0).
+// sub, sub + LPE, ... of each.  `base` (row 0 of the level, the same for the
+// whole wavefront) plus a 32-bit byte offset per row keeps the address
+// arithmetic to one instruction per row.
 template <int D, int GMAX, int LPE, int INFLIGHT, int RS = D>
-__device__ __forceinline__ void slot_dots(const float* __restrict__ pbase, int ri, const float (&qv)[GMAX][D / LPE],
+__device__ __forceinline__ void slot_dots(const float* __restrict__ base, int ri, const float (&qv)[GMAX][D / LPE],
                                           int sub, int lane, float (&z)[GMAX]) {
   constexpr int NCH = D / LPE / 4;
   constexpr int UNR = INFLIGHT < LPE ? INFLIGHT : LPE;  // rows whose loads are issued together
@@ -1495,9 +1497,10 @@ __device__ __forceinline__ void slot_dots(const float* __restrict__ pbase, int r
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
       const int rj = group_bcast<LPE>(ri, j0 + u, lane);
-      const float* rp = pbase + static_cast<int64_t>(rj) * RS;
+      const uint32_t boff = (__umul24(static_cast<uint32_t>(rj), RS) + static_cast<uint32_t>(sub) * 4u) * 4u;
+      const char* rp = reinterpret_cast<const char*>(base) + boff;
 #pragma unroll
-      for (int i = 0; i < NCH; ++i) x[u][i] = *reinterpret_cast<const float4*>(rp + i * LPE * 4);
+      for (int i = 0; i < NCH; ++i) x[u][i] = *reinterpret_cast<const float4*>(rp + i * LPE * 16);
     }
 #pragma unroll
     for (int u = 0; u < UNR; ++u) {
@@ -1654,7 +1657,9 @@ __global__ __launch_bounds__(NWAVE * 64) void stage1_g2_kernel(SelArgs a) {
       break;
     }
   }
-  const int wave_start = max(start, __shfl_xor(start, 32));
+  // the same in every lane; readfirstlane lets the compiler keep the level
+  // loop, and every per-level address, in scalar registers
+  const int wave_start = __builtin_amdgcn_readfirstlane(max(start, __shfl_xor(start, 32)));
 
   // Coarse levels in LDS: every level read by the workgroup's rows, from the
   // coarsest down, whose eligible prefix (for the last row, plus one row for
@@ -1720,11 +1725,11 @@ __global__ __launch_bounds__(NWAVE * 64) void stage1_g2_kernel(SelArgs a) {
     float z0[GMAX], z1[GMAX];
     const bool two = __ballot(fresh && nch == 2) != 0;
     if (STAGE && lb >= stage_lo && lb <= stage_hi) {
-      const float* sbase = stg + stage_off(lb) + sub * 4;
+      const float* sbase = stg + stage_off(lb);
       slot_dots<D, GMAX, LPE, 4, SROW>(sbase, valid ? 2 * node : 0, qv, sub, lane, z0);
       if (two) slot_dots<D, GMAX, LPE, 4, SROW>(sbase, nch == 2 ? 2 * node + 1 : 0, qv, sub, lane, z1);
     } else {
-      const float* pbase = a.pyr + (static_cast<int64_t>(bh) * geo.R + geo.off[lb]) * D + sub * 4;
+      const float* pbase = a.pyr + (static_cast<int64_t>(bh) * geo.R + geo.off[lb]) * D;
       slot_dots<D, GMAX, LPE, 4>(pbase, valid ? 2 * node : 0, qv, sub, lane, z0);
       if (two) slot_dots<D, GMAX, LPE, 4>(pbase, nch == 2 ? 2 * node + 1 : 0, qv, sub, lane, z1);
     }

@@ -99,6 +99,29 @@ def test_pyramid_parity(name):
     assert err <= _pyr_tol(x["k"], C, g, L), err
 
 
+# Long sequences whose top pyramid levels do (g = 4, 4096 leaves: 160 KiB) or
+# do not (g = 2, 4096 leaves: 192 KiB) fit the LDS of the top-level pooling
+# workgroup, so that both of its variants are compared with the oracle.
+LARGE_PYRAMIDS = {
+    "top-levels-in-lds-g4": (1, 1, 1, 16, 524288, 128, 128, 4, 8, 1, "bf16"),
+    "top-levels-global-g2": (1, 1, 1, 16, 262144, 128, 64, 2, 8, 1, "bf16"),
+}
+
+
+@pytest.mark.parametrize("name", list(LARGE_PYRAMIDS))
+def test_pyramid_parity_large(name):
+    shape = LARGE_PYRAMIDS[name]
+    B, H, Hkv, Nq, N, d, C, g, K, causal, dtype = shape
+    x = _data(shape)
+    p = _problem(shape)
+    pyr = pisa.build_pyramid(p, dev(x["k"], dtype))
+    torch.cuda.synchronize()
+    want = O.pyramid(x["k"], C, g)
+    L = len(O.level_sizes(N, C, g))
+    err = np.abs(pyr.cpu().numpy() - want).max()
+    assert err <= _pyr_tol(x["k"], C, g, L), err
+
+
 def _run_select(shape, schedule, x, score=0):
     p = _problem(shape, schedule, score)
     dtype = shape[-1]
