@@ -1910,7 +1910,7 @@ struct LeafParentArgs {
 // row is gathered once for all of them; every 32-key MFMA tile belongs to
 // one child, whose LSE is accumulated separately.
 template <int D, int KIND>
-__global__ __launch_bounds__(256) void leaf_parent_kernel(LeafParentArgs a, const uint16_t* __restrict__ q,
+__global__ __launch_bounds__(256, KIND == kScoreLse ? 5 : 1) void leaf_parent_kernel(LeafParentArgs a, const uint16_t* __restrict__ q,
                                                           const uint16_t* __restrict__ k,
                                                           const int32_t* __restrict__ a1,
                                                           const int32_t* __restrict__ a1cnt,
@@ -1980,10 +1980,15 @@ __global__ __launch_bounds__(256) void leaf_parent_kernel(LeafParentArgs a, cons
 #pragma unroll
         for (int r = 0; r < 16; ++r) zv[r] = acc[r];
         if (kt * 32 + 32 > nkeys) {  // a partial tile: keys past the parent's end drop out
+          // (for the LSE reducer the limit is re-read here so that its per-lane
+          // compares are not hoisted out of the loop and held in scalar
+          // registers throughout, which spilled them)
+          int nk = nkeys;
+          if constexpr (KIND == kScoreLse) asm volatile("" : "+s"(nk));
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-            zv[r] = key < nkeys ? zv[r] : -INFINITY;
+            zv[r] = key < nk ? zv[r] : -INFINITY;
           }
         }
         const ScoreAcc ts = acc_of_scaled<KIND, 16>(zv, a.qscale2);
