@@ -166,7 +166,7 @@ def main():
                     help="after the run, copy a cold buffer of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one MI355X: this build has no multi-GPU path "
+        print("bench.py measures one MI355X: the library has no multi-GPU path "
               "(the hot path shards by KV head with no exchange); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
