@@ -280,6 +280,193 @@ def select_row(qg: np.ndarray, k: np.ndarray, levels: list[np.ndarray], t: int,
     return I, min_gap
 
 
+def candidate_score(qg: np.ndarray, k: np.ndarray, levels: list[np.ndarray], lv: int, i: int,
+                    C: int, g: int, score: str = "lse") -> float:
+    """Grouped score u of node i at level lv >= 1 for the query heads qg [G, d]
+    (Sec. 3.2 eq. direct_child_lse, summed over heads by Sec. 3.3 eq.
+    kernel_grouped_score): the sum over the heads of the reducer of the
+    children's scaled logits -- the summaries of level lv-1 for lv >= 2, the
+    raw keys of leaf block i for lv = 1.  Same per-candidate arithmetic as
+    ``select_row`` (so equal inputs give bit-equal scores)."""
+    qg = np.asarray(qg, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    N, d = k.shape
+    scale = 1.0 / math.sqrt(d)
+    if lv >= 2:
+        below = levels[lv - 2]
+        x = below[list(range(i * g, min((i + 1) * g, below.shape[0])))]
+    else:
+        x = k[i * C:min((i + 1) * C, N)]
+    reduce = SCORES[score]
+    return sum(reduce(x @ qh * scale) for qh in qg)
+
+
+def _kept_set_ok(kept, u: dict, tol: float, strict_ties: bool) -> bool:
+    """A kept subset of the scored candidates is admissible when no dropped
+    candidate beats a kept one by more than tol; with strict_ties a kept and a
+    dropped candidate of exactly equal score must follow the tie rule R4
+    (the smaller index is kept)."""
+    kept = set(kept)
+    ks = [u[i] for i in kept]
+    ds = [u[j] for j in u if j not in kept]
+    if not ks or not ds:
+        return True
+    if min(ks) < max(ds) - tol:
+        return False
+    if strict_ties:
+        for i in kept:
+            for j in u:
+                if j not in kept and u[j] == u[i] and j < i:
+                    return False
+    return True
+
+
+def selection_admissible(qg: np.ndarray, k: np.ndarray, levels: list[np.ndarray], t: int, C: int, g: int,
+                         K: int, causal: bool, chosen, tol: float = 1e-3, score: str = "lse",
+                         strict_ties: bool = True, budget: int = 4000) -> dict:
+    """Is the leaf set ``chosen`` a possible outcome of the coarse-to-fine
+    selection of ``select_row`` when every ranking may be decided by scores
+    that differ from the exact ones by rounding (a kept candidate may score up
+    to ``tol`` below a dropped one)?
+
+    A selector that computes every score within tol/2 of the exact value and
+    otherwise follows Sec. 3.2 eq. hierarchical_topk (with the App. B forced
+    set and eligibility) produces an admissible set; on rows whose exact
+    margins all exceed tol the only admissible set is ``select_row``'s.
+
+    The replay walks the levels from the root.  At each level the kept set
+    must contain the ancestors of every chosen leaf (a leaf is a candidate only
+    below kept ancestors), keep the forced nodes, and be admissible in the
+    sense of ``_kept_set_ok``; the remaining slots may be filled by any
+    admissible choice, which changes the next level's candidates, so the
+    choices are searched depth first (exact ranking first, then the other
+    admissible fills of the tie band).  At the leaf level the kept set is
+    ``chosen`` itself.
+
+    Returns a dict: ``ok`` (True / False, or None when ``budget`` level visits
+    did not settle it), ``leaf_ranked`` (whether the accepted path ranked the
+    leaf level, i.e. whether the chosen blocks carry scores), ``leaf_u`` (the
+    exact leaf scores of the accepted path's scored candidates), ``visits``.
+    """
+    qg = np.asarray(qg, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    N, d = k.shape
+    M = [lv.shape[0] for lv in levels]
+    L = len(M)
+    f_leaf = forced_leaves(t, C, causal)
+    chosen = {int(j) for j in chosen if j >= 0}
+
+    def span(lv: int) -> int:
+        return C * g ** (lv - 1)
+
+    def eligible(lv: int, i: int) -> bool:
+        return i < M[lv - 1] and (not causal or i * span(lv) <= t)
+
+    def children(lv: int, i: int) -> range:
+        return range(i * g, min((i + 1) * g, M[lv - 2]))
+
+    need = {lv: {j // g ** (lv - 1) for j in chosen} for lv in range(1, L + 1)}
+    state = {"visits": 0, "leaf_ranked": False, "leaf_u": {}}
+    dead: set = set()
+
+    class _Budget(Exception):
+        pass
+
+    def fills(free, u, n_keep, must):
+        """Admissible kept sets of size n_keep that contain ``must``, the exact
+        ranking's first."""
+        if n_keep == 0:
+            if not must:
+                yield set()
+            return
+        ranked = sorted(free, key=lambda i: (-u[i], i))
+        hi, lo = u[ranked[n_keep - 1]], u[ranked[n_keep]]
+        sure = [i for i in ranked if u[i] > hi + tol]
+        band = [i for i in ranked if lo - tol <= u[i] <= hi + tol]
+        if not must <= set(sure) | set(band):
+            return
+        fixed = set(sure) | (must & set(band))
+        rest = [i for i in band if i not in fixed]
+        r = n_keep - len(fixed)
+        if r < 0 or r > len(rest):
+            return
+        from itertools import combinations
+        for extra in combinations(rest, r):
+            S = fixed | set(extra)
+            if _kept_set_ok(S, u, tol, strict_ties):
+                yield S
+
+    def visit(lv: int, A: list) -> bool:
+        state["visits"] += 1
+        if state["visits"] > budget:
+            raise _Budget()
+        key = (lv, tuple(sorted(A)))
+        if key in dead:
+            return False
+        A_set = set(A)
+        if not need[lv] <= A_set:
+            dead.add(key)
+            return False
+        F = {j // g ** (lv - 1) for j in f_leaf} & A_set
+        if len(A) <= K:
+            options = [A_set]
+            u = {}
+        else:
+            free = [i for i in A if i not in F]
+            u = {i: candidate_score(qg, k, levels, lv, i, C, g, score) for i in free}
+            n_keep = K - len(F)
+            if lv == 1:
+                S = chosen - F
+                ok_leaf = (F <= chosen and len(S) == n_keep and S <= set(free)
+                           and _kept_set_ok(S, u, tol, strict_ties))
+                options = [chosen] if ok_leaf else []
+            else:
+                options = (F | S for S in fills(free, u, n_keep, need[lv] - F))
+        for I in options:
+            if lv == 1:
+                if set(I) == chosen:
+                    state["leaf_ranked"] = len(A) > K
+                    state["leaf_u"] = dict(u)
+                    return True
+                continue
+            nxt = [r for i in sorted(I) for r in children(lv, i) if eligible(lv - 1, r)]
+            if visit(lv - 1, nxt):
+                return True
+        dead.add(key)
+        return False
+
+    try:
+        ok = visit(L, [0])
+    except _Budget:
+        ok = None
+    return {"ok": ok, "leaf_ranked": state["leaf_ranked"], "leaf_u": state["leaf_u"], "visits": state["visits"]}
+
+
+def flat_bsa_admissible(qg: np.ndarray, leaf_means: np.ndarray, t: int, C: int, K: int, causal: bool,
+                        chosen, tol: float = 1e-3, strict_ties: bool = True) -> bool:
+    """Is ``chosen`` a possible flat-BSA selection (``flat_bsa_row``) under
+    rounding of the scores by up to tol (log units of the summed per-head
+    probabilities)?  The forced blocks must be kept and no dropped eligible
+    block may beat a kept one by more than tol."""
+    qg = np.asarray(qg, dtype=np.float64)
+    S1 = np.asarray(leaf_means, dtype=np.float64)
+    M1, d = S1.shape
+    c = t // C
+    E = [i for i in range(M1) if not causal or i <= c]
+    chosen = {int(j) for j in chosen if j >= 0}
+    if len(E) <= K:
+        return chosen == set(E)
+    F = forced_leaves(t, C, causal) & set(E)
+    free = [i for i in E if i not in F]
+    z = qg @ S1[free].T / math.sqrt(d)
+    p = np.zeros(len(free))
+    for zh in z:
+        p += np.exp(zh - lse(zh))
+    u = dict(zip(free, np.log(p)))
+    S = chosen - F
+    return F <= chosen and len(S) == K - len(F) and S <= set(free) and _kept_set_ok(S, u, tol, strict_ties)
+
+
 def attention_row(q: np.ndarray, k: np.ndarray, v: np.ndarray, blocks, t: int,
                   C: int, causal: bool):
     """Attention of one query over the tokens of the selected leaf blocks.
