@@ -2530,8 +2530,8 @@ static hipError_t launch_final_topk(const Shape& s, const int32_t* a1, const int
   return hipGetLastError();
 }
 
-hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q, const void* k,
-                                   const float* pyr, int32_t* idx, float* score, void* ws, hipStream_t st) {
+static hipError_t launch_two_stage_heads(const Shape& s, const Geo& geo, const void* q, const void* k,
+                                        const float* pyr, int32_t* idx, float* score, void* ws, hipStream_t st) {
   const TwoStageWs w = two_stage_layout(s, geo);
   char* base = static_cast<char*>(ws);
   int32_t* a1 = reinterpret_cast<int32_t*>(base + w.a1);
@@ -2719,6 +2719,40 @@ hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q
   }
 
   return launch_final_topk(s, a1, a1cnt, u1, idx, score, st);
+}
+
+// The cluster builder counts and places (row, slot) pairs with 32-bit
+// offsets, so one pass may hold at most kMaxPairsPerPass pairs: larger
+// problems run as passes over consecutive (batch, KV head) slices, each a
+// problem of its own (B = 1, the slice's heads) with the same workspace
+// layout, shrunk.  One slice holds Nq * g * K < 2^23 * 2^8 pairs, so every
+// problem the ABI accepts splits.
+constexpr int64_t kMaxPairsPerPass = (int64_t(1) << 31) - 1;
+
+static int two_stage_heads_per_pass(const Shape& s) {
+  const int64_t per_bh = static_cast<int64_t>(s.Nq) * s.gK();
+  return static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(s.BH(), kMaxPairsPerPass / per_bh)));
+}
+
+hipError_t launch_select_two_stage(const Shape& s, const Geo& geo, const void* q, const void* k,
+                                   const float* pyr, int32_t* idx, float* score, void* ws, hipStream_t st) {
+  const int per = two_stage_heads_per_pass(s);
+  if (per >= s.BH()) return launch_two_stage_heads(s, geo, q, k, pyr, idx, score, ws, st);
+  for (int bh0 = 0; bh0 < s.BH(); bh0 += per) {
+    Shape sub = s;
+    sub.B = 1;
+    sub.Hkv = std::min(per, s.BH() - bh0);
+    sub.H = sub.Hkv * s.G;
+    const int64_t qoff = static_cast<int64_t>(bh0) * s.G * s.Nq * s.D;  // bf16 elements
+    const int64_t koff = static_cast<int64_t>(bh0) * s.Nkv * s.D;
+    const int64_t poff = static_cast<int64_t>(bh0) * geo.R * s.D;
+    const int64_t ioff = static_cast<int64_t>(bh0) * s.Nq * s.K;
+    const hipError_t e = launch_two_stage_heads(
+        sub, geo, static_cast<const uint16_t*>(q) + qoff, static_cast<const uint16_t*>(k) + koff, pyr + poff,
+        idx + ioff, score ? score + ioff : nullptr, ws, st);
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 // Split schedule: stage 1 with a workgroup per row, every scored leaf
