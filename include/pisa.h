@@ -175,8 +175,13 @@ int pisa_select_flat_bsa(const pisa_problem* p, const void* q, const float* pyra
 /* Selected sparse attention (Sec. 3.1 eq. selected_sparse_attention): for
  * every query row and head, softmax over the tokens of its KV head's selected
  * blocks (future tokens masked when causal, App. B) applied to the original
- * values.  Negative indices are padding.  Writes o (problem dtype) and lse
- * (nullable); a row with no visible token gets o = 0 and lse = -inf. */
+ * values.  block_idx entries outside [0, ceil(N/C)) -- negative ones and
+ * ones past the last leaf block -- are padding and contribute nothing; in
+ * causal mode a block that starts after the query contributes nothing either
+ * (all of its tokens are masked).  The entries of a row need not be sorted
+ * but must be distinct (pisa_select writes them so): a block listed twice is
+ * attended twice.  Writes o (problem dtype) and lse (nullable); a row with no
+ * visible token gets o = 0 and lse = -inf. */
 int pisa_sparse_attn_fwd(const pisa_problem* p, const void* q, const void* k, const void* v,
                          const int32_t* block_idx, void* o, float* lse, void* ws,
                          size_t ws_bytes, pisa_stream_t stream);

@@ -33,9 +33,9 @@ Contents and the passage each follows:
                            (bsa_block_scores, bsa_topk), with the per-head
                            normalisation before the head sum of App. C.1.
 * ``attention_row_bwd`` -- backward of the selected sparse attention with
-                           the selection held fixed (App. B, "During
-                           backpropagation, the selected block indices are
-                           held fixed"): the gradients of eq.
+                           the selection held fixed (App. B: the backward
+                           pass treats the chosen block indices as
+                           constants): the gradients of eq.
                            (selected_sparse_attention) with respect to q, k, v
                            over the selected, visible tokens only.
 * ``block_log_mass``, ``selection_quality_row`` -- the block-selection
@@ -479,7 +479,7 @@ def attention_row(q: np.ndarray, k: np.ndarray, v: np.ndarray, blocks, t: int,
     """
     q = np.asarray(q, dtype=np.float64)
     N, d = k.shape
-    tokens = sorted({j for i in blocks if i >= 0
+    tokens = sorted({j for i in map(int, blocks) if i >= 0
                      for j in range(i * C, min((i + 1) * C, N))
                      if not causal or j <= t})
     if not tokens:
@@ -507,7 +507,7 @@ def attention_row_bwd(q: np.ndarray, k: np.ndarray, v: np.ndarray, blocks, t: in
     q = np.asarray(q, dtype=np.float64)
     do = np.asarray(do, dtype=np.float64)
     N, d = k.shape
-    tokens = sorted({j for i in blocks if i >= 0
+    tokens = sorted({j for i in map(int, blocks) if i >= 0
                      for j in range(i * C, min((i + 1) * C, N))
                      if not causal or j <= t})
     if not tokens:

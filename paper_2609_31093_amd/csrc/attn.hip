@@ -105,10 +105,11 @@ __global__ __launch_bounds__(256) void attn_rows_kernel(AttnArgs a) {
   for (int e = 0; e < DPL; ++e) o[e] = 0.f;
 
   const int total = a.K * a.C;
+  const int nblk = (a.N + a.C - 1) / a.C;
   for (int i = grp; i < total; i += NGRP) {
     const int slot = i / a.C;
     const int blk = sel[slot];
-    if (blk < 0) continue;
+    if (blk < 0 || blk >= nblk) continue;  // padding
     const int tok = blk * a.C + (i - slot * a.C);
     if (tok >= a.N || (a.causal && tok > t)) continue;
     float x[DPL], y[DPL];
@@ -623,7 +624,7 @@ __global__ __launch_bounds__(NWL * 64, NWL == 8 ? 2 : 3) void attn_local_kernel(
       selA[r4] = (v4 && sub < a.K) ? sl[sub] : -1;
       selB[r4] = (v4 && sub + 16 < a.K) ? sl[sub + 16] : -1;
     }
-    auto far = [&](int x) { return x >= 0 && !(a.causal && (x == 0 || x == c || x == c - 1)); };
+    auto far = [&](int x) { return x >= 0 && x < a.M1 && !(a.causal && (x == 0 || x == c || x == c - 1)); };
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
       const int pr = c * C + qg * 16 + r4 * 4 + grp;
@@ -733,7 +734,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnBlockArgs a, cons
   }
   for (int slot = slot0 + grp; slot < a.K; slot += 4) {
     const int blk = sel[slot];
-    if (blk < 0) continue;
+    if (blk < 0 || blk >= a.M1) continue;  // padding (no partial was written)
     if (TAIL && (blk == 0 || blk == c || blk == c - 1)) continue;
     const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + slot) * a.G + hh;
     const float ls = part_lse[pidx];
@@ -793,7 +794,7 @@ __global__ __launch_bounds__(256) void attn_slot_kernel(AttnBlockArgs a, const u
   const int bh = blockIdx.y / a.nrows;
   const int row = a.row0 + rr;
   const int blk = idx[(static_cast<int64_t>(bh) * a.Nq + row) * a.K + slot];
-  if (blk < 0) return;  // the combine skips empty slots
+  if (blk < 0 || blk >= a.M1) return;  // padding: the combine skips these slots
   const int b = bh / a.Hkv, h = bh - b * a.Hkv;
   const int G = a.G;
   const int t = a.N - a.Nq + row;
@@ -969,7 +970,7 @@ static hipError_t launch_split_path(const Shape& s, const void* q, const void* k
   char* base = static_cast<char*>(ws);
   uint16_t* part_o = reinterpret_cast<uint16_t*>(base + w.part_o);
   float* part_lse = reinterpret_cast<float*>(base + w.part_lse);
-  AttnBlockArgs a{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, 0, 0, s.Nq,
+  AttnBlockArgs a{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, (s.N + s.C - 1) / s.C, 0, s.Nq,
                   kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv};
   const uint16_t* qq = static_cast<const uint16_t*>(q);
   const uint16_t* kk = static_cast<const uint16_t*>(k);

@@ -341,7 +341,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnBwdArgs a, const i
 #pragma unroll
   for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
   for (int s = 0; s < a.K; ++s) {
-    if (sel[s] < 0) continue;
+    if (sel[s] < 0 || sel[s] >= a.M1) continue;  // padding: no partial was written
     const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + s) * a.G + hh;
     float x[DPL];
     load_row_part<uint16_t, DPL>(part_dq + pidx * D + sub * DPL, x);

@@ -26,6 +26,9 @@ __device__ __forceinline__ bool cluster_pair(const ClusterArgs& a, int bh, int r
   const int32_t* lst = a.list + rg * a.S;
   blk = lst[slot];
   if (blk < 0) return false;
+  // attention lists come from the caller: entries past the last leaf block
+  // are padding, like negative ones (the bins cover blocks 0 .. M1-1 only)
+  if ((a.mode == kClusterAttn || a.mode == kClusterAttnFar) && blk >= a.M1) return false;
   if (a.mode == kClusterAttnFar) {
     const int c = (a.N - a.Nq + a.row0 + r) / a.C;
     return !(a.causal && (blk == 0 || blk == c || blk == c - 1));

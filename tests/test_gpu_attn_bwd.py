@@ -122,3 +122,29 @@ def test_attention_backward_needles_128k():
     want, got = np.array(want), np.array(got)
     # the same bound as the other shapes: 2% of the sampled rows' largest magnitude
     assert np.abs(got - want).max() <= REL * np.abs(want).max()
+
+
+def test_backward_out_of_range_indices_are_padding():
+    """Entries at or past ceil(N/C) add nothing to any gradient."""
+    B, H, Hkv, Nq, N, d, C, K, causal = SHAPES["gqa2-c64"]
+    seed = 9
+    x = inputs.random_qkv(B, H, Hkv, Nq, N, d, "bf16", seed=seed)
+    do_np = inputs.round_to_bf16(np.random.default_rng(seed + 100).standard_normal((B, H, Nq, d)).astype(np.float32))
+    q, k, v = (torch.from_numpy(x[n]).to(torch.bfloat16).cuda() for n in "qkv")
+    d_o = torch.from_numpy(do_np).to(torch.bfloat16).cuda()
+    p = pisa.make_problem(B, H, Hkv, Nq, N, d, C, 2, K, causal, "bf16")
+    idx = pisa.select(p, q, k, pisa.build_pyramid(p, k))
+    torch.cuda.synchronize()
+    M1 = -(-N // C)
+    planted = idx.cpu().numpy()
+    planted[..., ::2, -1] = M1 + 3
+    planted[..., 1::2, -1] = (1 << 30) - 1
+    pidx = torch.from_numpy(planted).cuda()
+    o, lse = pisa.sparse_attn_fwd(p, q, k, v, pidx)
+    dq, dk, dv = pisa.sparse_attn_bwd(p, q, k, v, pidx, o, lse, d_o)
+    torch.cuda.synchronize()
+    want = O.sparse_attention_bwd(x["q"], x["k"], x["v"], planted, do_np, C, bool(causal))
+    for label, g, w in zip(("dq", "dk", "dv"), (dq, dk, dv), want):
+        scale = float(np.abs(w).max())
+        err = float(np.abs(g.float().cpu().numpy() - w).max())
+        assert err <= REL * scale, (label, err, scale)

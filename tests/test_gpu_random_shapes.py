@@ -2,7 +2,8 @@
 dim 64 / 128, leaf blocks of 32-128 keys, fan-out 2-4, 1-16 query heads per KV
 head, budgets up to g*K = 128, causal or not, suffix query rows), through the
 automatic schedule: indices against the oracle on sampled rows (decisive rows
-identical), every row a valid selection, and attention on the GPU's own
+identical, near-tie rows admissible), block scores against the oracle's,
+every row a valid selection, and attention on the GPU's own
 indices within the bf16 / fp32 bounds of the other parity tests."""
 import numpy as np
 import pytest
@@ -10,7 +11,7 @@ import torch
 
 import oracle as O
 from paper_2609_31093_amd import inputs
-from tests.helpers import check_selection_valid, compare_selection, dev
+from tests.helpers import check_flat_bsa_rows, check_selection_rows, check_selection_valid, dev
 
 pytestmark = pytest.mark.gpu
 
@@ -64,12 +65,14 @@ def test_random_shape_parity(i):
     pyr = pisa.build_pyramid(p, k)
     idx = pisa.select(p, q, k, pyr)
     o, lse = pisa.sparse_attn_fwd(p, q, k, v, idx)
+    idx2, sc = pisa.select(p, q, k, pyr, with_score=True)
     torch.cuda.synchronize()
     idx_np = idx.cpu().numpy()
+    assert np.array_equal(idx_np, idx2.cpu().numpy())
     check_selection_valid(idx_np, N, Nq, C, K, bool(causal))
     rows = _rows(Nq, i)
-    ora, gap = O.select(x["q"], x["k"], C, g, K, bool(causal), rows=rows)
-    print(compare_selection(idx_np[:, :, rows], ora, gap))
+    print(check_selection_rows(x["q"], x["k"], C, g, K, bool(causal), idx_np[:, :, rows], rows,
+                               gpu_score=sc.cpu().numpy()[:, :, rows]))
     want_o, want_lse = O.sparse_attention(x["q"], x["k"], x["v"], idx_np[:, :, rows], C, bool(causal), rows=rows)
     tol = 2e-2 if dtype == "bf16" else 1e-4
     assert np.abs(o.float().cpu().numpy()[:, :, rows] - want_o).max() <= tol
@@ -112,13 +115,13 @@ def test_random_shape_schedules(i, schedule):
     x = inputs.random_qkv(B, H, Hkv, Nq, N, d, dtype, seed=200 + i)
     p = pisa.make_problem(B, H, Hkv, Nq, N, d, C, g, K, causal, dtype, schedule)
     q, k = dev(x["q"], dtype), dev(x["k"], dtype)
-    idx = pisa.select(p, q, k, pisa.build_pyramid(p, k))
+    idx, sc = pisa.select(p, q, k, pisa.build_pyramid(p, k), with_score=True)
     torch.cuda.synchronize()
     idx_np = idx.cpu().numpy()
     check_selection_valid(idx_np, N, Nq, C, K, bool(causal))
     rows = _rows(Nq, 50 + i)
-    ora, gap = O.select(x["q"], x["k"], C, g, K, bool(causal), rows=rows)
-    print(compare_selection(idx_np[:, :, rows], ora, gap))
+    print(check_selection_rows(x["q"], x["k"], C, g, K, bool(causal), idx_np[:, :, rows], rows,
+                               gpu_score=sc.cpu().numpy()[:, :, rows]))
 
 
 BWD_SHAPES = _bf16_shapes(6, 11, 2400, 48, nqmax=1200, work=6e8)
@@ -189,8 +192,7 @@ def test_random_shape_flat_bsa(i):
     idx_np = idx.cpu().numpy()
     check_selection_valid(idx_np, N, Nq, C, K, bool(causal))
     rows = _rows(Nq, 70 + i)
-    ora, gap = O.select_flat_bsa(x["q"], x["k"], C, K, bool(causal), rows=rows)
-    print(compare_selection(idx_np[:, :, rows], ora, gap))
+    print(check_flat_bsa_rows(x["q"], x["k"], C, K, bool(causal), idx_np[:, :, rows], rows))
 
 
 def _edge_shapes(n=16, seed=77):
@@ -236,12 +238,10 @@ def test_edge_shape_parity(i):
     idx_np = idx.cpu().numpy()
     check_selection_valid(idx_np, N, Nq, C, K, bool(causal))
     rows = np.arange(Nq)
-    ora, gap = O.select(x["q"], x["k"], C, g, K, bool(causal), rows=rows)
-    compare_selection(idx_np, ora, gap)
+    check_selection_rows(x["q"], x["k"], C, g, K, bool(causal), idx_np, rows)
     want_o, want_lse = O.sparse_attention(x["q"], x["k"], x["v"], idx_np, C, bool(causal), rows=rows)
     tol = 2e-2 if dtype == "bf16" else 1e-4
     assert np.abs(o.float().cpu().numpy() - want_o).max() <= tol
     assert np.abs(lse.cpu().numpy() - want_lse).max() <= 1e-3
     if bsa is not None:
-        ora_b, gap_b = O.select_flat_bsa(x["q"], x["k"], C, K, bool(causal), rows=rows)
-        compare_selection(bsa.cpu().numpy(), ora_b, gap_b)
+        check_flat_bsa_rows(x["q"], x["k"], C, K, bool(causal), bsa.cpu().numpy(), rows)

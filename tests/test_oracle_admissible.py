@@ -219,3 +219,48 @@ def test_flat_bsa_admissible():
             wrong = sorted((set(sel) - {free_kept[0]}) | {others[0]})
             assert not O.flat_bsa_admissible(qg, S1, t, C, K, True, wrong, tol=0.0)
     assert near > 0
+
+
+def test_row_checker_accepts_the_oracle_and_rejects_planted_errors():
+    """The GPU tests' row checker (tests/helpers.py), fed the oracle's own
+    selections and scores, accepts them; a changed decisive row, a wrong block
+    score and a finite score on a forced block are each rejected."""
+    from tests.helpers import check_selection_rows
+
+    B, H, Hkv, N, d, C, g, K = 1, 4, 2, 640, 8, 8, 2, 6
+    r = np.random.default_rng(4)
+    q = r.standard_normal((B, H, N, d))
+    k = r.standard_normal((B, Hkv, N, d))
+    rows = np.array([5, 100, 333, 639])
+    idx, gap = O.select(q, k, C, g, K, True, rows=rows)
+    sc = np.full(idx.shape, -np.inf)
+    for h in range(Hkv):
+        lv = O.build_pyramid(k[0, h], C, g)
+        for ri, row in enumerate(rows):
+            trace = []
+            sel, _ = O.select_row(q[0, 2 * h:2 * h + 2, row], k[0, h], lv, row, C, g, K, True, trace=trace)
+            leaf = trace[-1]
+            f = O.forced_leaves(row, C, True)
+            for pos, j in enumerate(sel):
+                sc[0, h, ri, pos] = leaf["u"][j] if (len(leaf["A"]) > K and j not in f) else np.inf
+    st = check_selection_rows(q, k, C, g, K, True, idx, rows, gpu_score=sc)
+    assert st["rows"] == 8 and st["scored_blocks"] > 0
+    ri = int(np.argmax(np.where(np.isfinite(gap[0, 0]), gap[0, 0], -1.0)))   # a ranked decisive row of head 0
+    assert gap[0, 0, ri] > 1e-3 and rows[ri] > K * C
+    bad = idx.copy()
+    c = rows[ri] // C
+    free_pos = [pos for pos, j in enumerate(bad[0, 0, ri]) if j not in (0, c - 1, c)]
+    others = [j for j in range(c + 1) if j not in bad[0, 0, ri]]
+    bad[0, 0, ri, free_pos[0]] = others[0]
+    bad[0, 0, ri] = np.sort(bad[0, 0, ri])
+    with pytest.raises(AssertionError):
+        check_selection_rows(q, k, C, g, K, True, bad, rows, gpu_score=None)
+    wrong = sc.copy()
+    wrong[0, 0, ri, free_pos[0]] += 2e-3
+    with pytest.raises(AssertionError):
+        check_selection_rows(q, k, C, g, K, True, idx, rows, gpu_score=wrong)
+    wrong = sc.copy()
+    fpos = list(idx[0, 0, ri]).index(0)
+    wrong[0, 0, ri, fpos] = 1.0
+    with pytest.raises(AssertionError):
+        check_selection_rows(q, k, C, g, K, True, idx, rows, gpu_score=wrong)

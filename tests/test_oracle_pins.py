@@ -706,3 +706,18 @@ def test_backward_matches_finite_differences():
             assert abs((loss(q, k, vp) - loss(q, k, vm)) / (2 * eps) - dv[tok.index(tj), i]) < 1e-7
     # a token outside the selection (block 1) and a future token get no gradient
     assert 9 not in tok and 35 not in tok
+
+
+def test_attention_ignores_blocks_past_the_end():
+    """Blocks at or past ceil(N/C) hold no tokens, whatever the index type
+    (int32 arrays included: block * C must not wrap)."""
+    r = _rng(41)
+    N, C, d = 300, 16, 8
+    q, k, v = r.standard_normal(d), r.standard_normal((N, d)), r.standard_normal((N, d))
+    base = np.array([0, 3, 7, 18], dtype=np.int32)
+    want = O.attention_row(q, k, v, base, N - 1, C, True)
+    for extra in (19, 25, (1 << 30) - 1, (1 << 31) - 1):
+        got = O.attention_row(q, k, v, np.append(base, np.int32(extra)), N - 1, C, True)
+        assert np.array_equal(got[0], want[0]) and got[1] == want[1], extra
+        gb = O.attention_row_bwd(q, k, v, np.append(base, np.int32(extra)), N - 1, C, True, r.standard_normal(d))
+        assert all(0 <= j < N for j in gb[1])
