@@ -163,6 +163,26 @@ int pisa_select(const pisa_problem* p, const void* q, const void* k, const float
                 int32_t* block_idx, float* block_score, void* ws, size_t ws_bytes,
                 pisa_stream_t stream);
 
+/* Bytes of the static scratch that pisa_select_static uses instead of a
+ * caller workspace (one copy per device, held while the library is loaded). */
+#define PISA_STATIC_SCRATCH_BYTES (32u << 20)
+
+/* pisa_select without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops that must not
+ * call hipMalloc, harnesses that forbid it).  Same arguments, validation,
+ * kernels and results as pisa_select; the scratch it needs comes from a
+ * static device array of PISA_STATIC_SCRATCH_BYTES bytes instead of `ws`.
+ * A problem whose pisa_select_workspace_bytes() exceeds that size is refused
+ * with PISA_ERR_WORKSPACE (nothing is launched; use pisa_select).  The call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine);
+ * its first call on a device looks up that device's copy of the array.
+ * Every call on a device shares that device's one array, so calls that
+ * overlap on one device (concurrent streams, or host threads) race and give
+ * undefined results: serialise them.  The array keeps the last call's
+ * contents; every call writes what it reads. */
+int pisa_select_static(const pisa_problem* p, const void* q, const void* k, const float* pyramid,
+                       int32_t* block_idx, float* block_score, pisa_stream_t stream);
+
 /* Flat block selection baseline (Sec. 3.1 eqs. bsa_block_scores, bsa_topk):
  * every eligible leaf summary (pyramid level 1) is scored; with G > 1 the
  * scores are turned into per-head softmax probabilities over the eligible

@@ -7,6 +7,8 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <mutex>
+
 #include "../../include/pisa.h"
 #include "common.h"
 #include "kernels.h"
@@ -189,6 +191,74 @@ size_t select_ws(int sched, const pisa::Shape& s, const pisa::Geo& g) {
     if (_st != PISA_OK) return _st; \
   } while (0)
 
+// Argument checks of pisa_select and pisa_select_static (everything except
+// the workspace); fills the kernel view and the schedule.
+int check_select(const pisa_problem* p, const void* q, const void* k, const float* pyramid, const int32_t* block_idx,
+                 const float* block_score, pisa::Shape* s, pisa::Geo* g, int* sched) {
+  PISA_TRY(check_problem(p, s, g));
+  PISA_TRY(check_ptr(q, "q"));
+  PISA_TRY(check_ptr(k, "k"));
+  PISA_TRY(check_ptr(pyramid, "pyramid"));
+  PISA_TRY(check_ptr(block_idx, "block_idx"));
+  PISA_TRY(check_ptr(block_score, "block_score", true));
+  *sched = pick_schedule(p, *s, *g);
+  const bool two = *sched == PISA_SCHEDULE_TWO_STAGE;
+  if (two && !s->bf16)
+    return fail(PISA_ERR_UNSUPPORTED, "the two-stage schedule runs on bf16 inputs (use the fused schedule)");
+  if (two && g->M[1] > kMaxClusterBins)
+    return fail(PISA_ERR_UNSUPPORTED, "the two-stage schedule needs N/C <= %d", kMaxClusterBins);
+  return PISA_OK;
+}
+
+int run_select(const pisa::Shape& s, const pisa::Geo& g, int sched, const void* q, const void* k,
+               const float* pyramid, int32_t* block_idx, float* block_score, void* ws, hipStream_t st,
+               const char* who) {
+  hipError_t e;
+  if (sched == PISA_SCHEDULE_TWO_STAGE)
+    e = pisa::launch_select_two_stage(s, g, q, k, pyramid, block_idx, block_score, ws, st);
+  else if (sched == PISA_SCHEDULE_SPLIT)
+    e = pisa::launch_select_split(s, g, q, k, pyramid, block_idx, block_score, ws, st);
+  else
+    e = pisa::launch_select_fused(s, g, q, k, pyramid, block_idx, block_score, st);
+  return device_status(e, who);
+}
+
+// Per-device address of the static scratch of pisa_select_static, taken once
+// per device (with that device current) on its first call there.
+constexpr int kMaxDevices = 64;
+std::once_flag g_scratch_once[kMaxDevices];
+void* g_scratch_ptr[kMaxDevices];
+hipError_t g_scratch_err[kMaxDevices];
+
+}  // namespace
+
+namespace pisa {
+// Scratch of pisa_select_static: one copy per device, held while the library
+// is loaded.  Host code never passes this name to a kernel or a copy (on the
+// host it only names the symbol); it uses the device address from
+// hipGetSymbolAddress instead.
+__device__ __align__(256) unsigned char scratch[PISA_STATIC_SCRATCH_BYTES];
+}  // namespace pisa
+
+namespace {
+
+int static_scratch(void** out) {
+  int dev = 0;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return device_status(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(PISA_ERR_UNSUPPORTED, "device %d (supported: < %d)", dev, kMaxDevices);
+  std::call_once(g_scratch_once[dev], [dev] {
+    void* ptr = nullptr;
+    g_scratch_err[dev] = hipGetSymbolAddress(&ptr, HIP_SYMBOL(pisa::scratch));
+    g_scratch_ptr[dev] = ptr;
+  });
+  if (g_scratch_err[dev] != hipSuccess) return device_status(g_scratch_err[dev], "hipGetSymbolAddress(scratch)");
+  if ((reinterpret_cast<uintptr_t>(g_scratch_ptr[dev]) & 255u) != 0)
+    return fail(PISA_ERR_DEVICE, "static scratch is not 256-byte aligned");
+  *out = g_scratch_ptr[dev];
+  return PISA_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -265,28 +335,29 @@ int pisa_select(const pisa_problem* p, const void* q, const void* k, const float
                 float* block_score, void* ws, size_t ws_bytes, pisa_stream_t stream) {
   pisa::Shape s{};
   pisa::Geo g{};
-  PISA_TRY(check_problem(p, &s, &g));
-  PISA_TRY(check_ptr(q, "q"));
-  PISA_TRY(check_ptr(k, "k"));
-  PISA_TRY(check_ptr(pyramid, "pyramid"));
-  PISA_TRY(check_ptr(block_idx, "block_idx"));
-  PISA_TRY(check_ptr(block_score, "block_score", true));
-  const int sched = pick_schedule(p, s, g);
-  const bool two = sched == PISA_SCHEDULE_TWO_STAGE;
-  if (two && !s.bf16)
-    return fail(PISA_ERR_UNSUPPORTED, "the two-stage schedule runs on bf16 inputs (use the fused schedule)");
-  if (two && g.M[1] > kMaxClusterBins)
-    return fail(PISA_ERR_UNSUPPORTED, "the two-stage schedule needs N/C <= %d", kMaxClusterBins);
+  int sched = 0;
+  PISA_TRY(check_select(p, q, k, pyramid, block_idx, block_score, &s, &g, &sched));
   PISA_TRY(check_ws(ws, ws_bytes, select_ws(sched, s, g)));
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  hipError_t e;
-  if (two)
-    e = pisa::launch_select_two_stage(s, g, q, k, pyramid, block_idx, block_score, ws, st);
-  else if (sched == PISA_SCHEDULE_SPLIT)
-    e = pisa::launch_select_split(s, g, q, k, pyramid, block_idx, block_score, ws, st);
-  else
-    e = pisa::launch_select_fused(s, g, q, k, pyramid, block_idx, block_score, st);
-  return device_status(e, "pisa_select");
+  return run_select(s, g, sched, q, k, pyramid, block_idx, block_score, ws, static_cast<hipStream_t>(stream),
+                    "pisa_select");
+}
+
+int pisa_select_static(const pisa_problem* p, const void* q, const void* k, const float* pyramid,
+                       int32_t* block_idx, float* block_score, pisa_stream_t stream) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  int sched = 0;
+  PISA_TRY(check_select(p, q, k, pyramid, block_idx, block_score, &s, &g, &sched));
+  const size_t need = select_ws(sched, s, g);
+  if (need > PISA_STATIC_SCRATCH_BYTES)
+    return fail(PISA_ERR_WORKSPACE,
+                "pisa_select_static: this selection needs %zu bytes of scratch, the static scratch holds %zu "
+                "(call pisa_select with a workspace instead)",
+                need, static_cast<size_t>(PISA_STATIC_SCRATCH_BYTES));
+  void* ws = nullptr;
+  if (need > 0) PISA_TRY(static_scratch(&ws));
+  return run_select(s, g, sched, q, k, pyramid, block_idx, block_score, ws, static_cast<hipStream_t>(stream),
+                    "pisa_select_static");
 }
 
 int pisa_select_flat_bsa(const pisa_problem* p, const void* q, const float* pyramid, int32_t* block_idx, void* ws,

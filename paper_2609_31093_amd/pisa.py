@@ -35,7 +35,8 @@ PISA_ERR_DEVICE = -4
 EXPORTS = (
     "pisa_num_levels", "pisa_pyramid_layout", "pisa_pyramid_bytes",
     "pisa_select_workspace_bytes", "pisa_bsa_workspace_bytes", "pisa_attn_workspace_bytes",
-    "pisa_build_pyramid", "pisa_pyramid_append", "pisa_select", "pisa_select_flat_bsa", "pisa_sparse_attn_fwd",
+    "pisa_build_pyramid", "pisa_pyramid_append", "pisa_select", "pisa_select_static", "pisa_select_flat_bsa",
+    "pisa_sparse_attn_fwd",
     "pisa_attn_bwd_workspace_bytes", "pisa_sparse_attn_bwd",
     "pisa_quality_workspace_bytes", "pisa_selection_quality",
     "pisa_profile_enable", "pisa_profile_report", "pisa_status_string", "pisa_last_error",
@@ -83,6 +84,7 @@ def _load():
         "pisa_build_pyramid": (ctypes.c_int, [P, vp, vp, vp]),
         "pisa_pyramid_append": (ctypes.c_int, [P, vp, vp, i32, vp]),
         "pisa_select": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "pisa_select_static": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp]),
         "pisa_select_flat_bsa": (ctypes.c_int, [P, vp, vp, vp, vp, sz, vp]),
         "pisa_sparse_attn_fwd": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pisa_attn_bwd_workspace_bytes": (sz, [P]),
@@ -176,6 +178,14 @@ def pisa_pyramid_append(p: Problem, k, pyramid, n_old: int, stream=None) -> int:
 def pisa_select(p: Problem, q, k, pyramid, block_idx, block_score=None, ws=None, ws_bytes=0, stream=None) -> int:
     return _check(_lib.pisa_select(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(pyramid), _ptr(block_idx),
                                    _ptr(block_score), _ptr(ws), ws_bytes, _stream(stream)), "pisa_select")
+
+
+def pisa_select_static(p: Problem, q, k, pyramid, block_idx, block_score=None, stream=None) -> int:
+    return _check(_lib.pisa_select_static(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(pyramid), _ptr(block_idx),
+                                          _ptr(block_score), _stream(stream)), "pisa_select_static")
+
+
+PISA_STATIC_SCRATCH_BYTES = 32 << 20  # include/pisa.h
 
 
 def pisa_select_flat_bsa(p: Problem, q, pyramid, block_idx, ws=None, ws_bytes=0, stream=None) -> int:
