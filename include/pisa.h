@@ -149,6 +149,34 @@ int pisa_build_pyramid(const pisa_problem* p, const void* k, float* pyramid, pis
 int pisa_pyramid_append(const pisa_problem* p, const void* k, float* pyramid, int32_t n_old,
                         pisa_stream_t stream);
 
+/* Capacity rule of the decode cache (App. B "Decode cache": when the cache
+ * needs room, each level's capacity grows by a fixed fraction, so a level is
+ * re-laid a constant number of times per doubling of the length and the
+ * copying through length N stays within O((N/C) d log N) per KV head).
+ * Returns the capacity (in tokens) for a cache that reserves `cap` tokens and
+ * must hold `need`: cap when need <= cap, otherwise the smallest multiple of
+ * C that is >= need and >= cap + cap/2 (the fraction is 1/2), clamped to the
+ * largest supported capacity (65535 leaf blocks); a negative status if need
+ * itself exceeds it or an argument is invalid (cap >= 0, need >= 1, C >= 1).
+ * Host only. */
+int32_t pisa_cache_capacity(int32_t cap, int32_t need, int32_t C);
+
+/* Decode cache growth (App. B "Decode cache"): re-lays a cache of p->N tokens
+ * held in buffers reserved for p->Ncap tokens (0 means N) into caller-
+ * allocated buffers reserved for new_cap >= max(N, Ncap) tokens.  Per (batch,
+ * KV head), the rows of every stored level of pyr_old (the layout of
+ * pisa_pyramid_layout for Ncap) move to that level's offset in pyr_new (the
+ * layout for new_cap), and, when the four key/value pointers are non-NULL,
+ * the first N rows of k_old, v_old [B,Hkv,Ncap,d] go to k_new, v_new
+ * [B,Hkv,new_cap,d].  Afterwards pyr_new equals pisa_build_pyramid of the
+ * problem with Ncap = new_cap bit for bit, and pisa_pyramid_append continues
+ * from it with that Ncap.  Rows past N in the new buffers are not written.
+ * The key/value pointers are all NULL (pyramid only) or all non-NULL; old and
+ * new buffers must not overlap (PISA_ERR_INVALID_ARG otherwise).  One launch,
+ * no workspace, no allocation. */
+int pisa_cache_grow(const pisa_problem* p, int32_t new_cap, const float* pyr_old, float* pyr_new, const void* k_old,
+                    void* k_new, const void* v_old, void* v_new, pisa_stream_t stream);
+
 /* Pyramid Top-K selection (Sec. 3.2 eqs. hierarchical_topk and
  * direct_child_lse; grouped heads Sec. 3.3 eq. kernel_grouped_score; causal
  * policy App. B).  From the root, each level keeps all candidates when there

@@ -7,6 +7,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <mutex>
 
 #include "../../include/pisa.h"
@@ -27,9 +28,8 @@ int fail(int status, const char* fmt, ...) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-// Level sizes of the hierarchy (Sec. 3.2 eq. key_hierarchy).  Returns L or a
-// negative status.
-// Level sizes of an N-token hierarchy (M[1..L]); returns L or a negative status.
+// Level sizes M[1..L] of an N-token hierarchy (Sec. 3.2 eq. key_hierarchy);
+// returns L or a negative status.
 int level_sizes(int64_t N, int32_t C, int32_t g, int32_t* M) {
   int64_t m = (N + C - 1) / C;
   int L = 1;
@@ -80,6 +80,9 @@ int compute_geo(int32_t N, int32_t C, int32_t g, pisa::Geo* geo, int32_t cap = 0
   return L;
 }
 
+// Leaf blocks of the capacity (Ncap tokens) a problem may reserve.
+constexpr int32_t kMaxLeafBlocks = 65535;
+
 // Full validation of a problem; fills the kernel view on success.
 int check_problem(const pisa_problem* p, pisa::Shape* s, pisa::Geo* geo) {
   if (!p) return fail(PISA_ERR_INVALID_ARG, "problem is NULL");
@@ -121,8 +124,8 @@ int check_problem(const pisa_problem* p, pisa::Shape* s, pisa::Geo* geo) {
   pisa::Geo g{};
   const int L = compute_geo(p->N, p->C, p->fanout, &g, p->Ncap);
   if (L < 0) return fail(L, "hierarchy too deep");
-  if ((static_cast<int64_t>(g.Nkv) + p->C - 1) / p->C > 65535)
-    return fail(PISA_ERR_UNSUPPORTED, "more than 65535 leaf blocks");
+  if ((static_cast<int64_t>(g.Nkv) + p->C - 1) / p->C > kMaxLeafBlocks)
+    return fail(PISA_ERR_UNSUPPORTED, "more than %d leaf blocks", kMaxLeafBlocks);
   if (s) {
     s->B = p->B;
     s->H = p->H;
@@ -329,6 +332,77 @@ int pisa_pyramid_append(const pisa_problem* p, const void* k, float* pyramid, in
   return device_status(pisa::launch_pyramid_append(g, g_old, s.BH(), s.D, s.bf16, k, pyramid, n_old,
                                                    static_cast<hipStream_t>(stream)),
                        "pisa_pyramid_append");
+}
+
+int32_t pisa_cache_capacity(int32_t cap, int32_t need, int32_t C) {
+  if (cap < 0 || need < 1 || C < 1) return fail(PISA_ERR_INVALID_ARG, "need cap >= 0, need >= 1, C >= 1");
+  if (need <= cap) return cap;
+  const int64_t grown = std::max<int64_t>(need, static_cast<int64_t>(cap) + (static_cast<int64_t>(cap) + 1) / 2);
+  const int64_t rounded = (grown + C - 1) / C * C;
+  const int64_t limit = static_cast<int64_t>(kMaxLeafBlocks) * C;
+  if (rounded <= limit && rounded <= INT32_MAX) return static_cast<int32_t>(rounded);
+  if (need <= limit && need <= INT32_MAX) return static_cast<int32_t>(std::min<int64_t>(limit, INT32_MAX));
+  return fail(PISA_ERR_UNSUPPORTED, "a cache of %d tokens exceeds %d leaf blocks of %d", need, kMaxLeafBlocks, C);
+}
+
+int pisa_cache_grow(const pisa_problem* p, int32_t new_cap, const float* pyr_old, float* pyr_new, const void* k_old,
+                    void* k_new, const void* v_old, void* v_new, pisa_stream_t stream) {
+  pisa::Shape s{};
+  pisa::Geo g{};
+  PISA_TRY(check_problem(p, &s, &g));
+  if (new_cap < g.Nkv)
+    return fail(PISA_ERR_INVALID_ARG, "new_cap (%d) is below the current capacity (%d)", new_cap, g.Nkv);
+  pisa_problem pn = *p;
+  pn.Ncap = new_cap;
+  pisa::Geo gn{};
+  PISA_TRY(check_problem(&pn, nullptr, &gn));
+  PISA_TRY(check_ptr(pyr_old, "pyr_old"));
+  PISA_TRY(check_ptr(pyr_new, "pyr_new"));
+  const bool kv = k_old || k_new || v_old || v_new;
+  if (kv) {
+    PISA_TRY(check_ptr(k_old, "k_old"));
+    PISA_TRY(check_ptr(k_new, "k_new"));
+    PISA_TRY(check_ptr(v_old, "v_old"));
+    PISA_TRY(check_ptr(v_new, "v_new"));
+  }
+  const int64_t BH = s.BH();
+  const size_t esz = s.bf16 ? 2 : 4;
+  auto overlap = [](const void* a, size_t na, const void* b, size_t nb) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return x < y + nb && y < x + na;
+  };
+  const size_t pyr_old_bytes = static_cast<size_t>(BH) * g.R * s.D * 4;
+  const size_t pyr_new_bytes = static_cast<size_t>(BH) * gn.R * s.D * 4;
+  if (overlap(pyr_old, pyr_old_bytes, pyr_new, pyr_new_bytes))
+    return fail(PISA_ERR_INVALID_ARG, "pyr_old and pyr_new overlap");
+  if (kv) {
+    const size_t kv_old_bytes = static_cast<size_t>(BH) * g.Nkv * s.D * esz;
+    const size_t kv_new_bytes = static_cast<size_t>(BH) * gn.Nkv * s.D * esz;
+    if (overlap(k_old, kv_old_bytes, k_new, kv_new_bytes) || overlap(v_old, kv_old_bytes, v_new, kv_new_bytes) ||
+        overlap(k_new, kv_new_bytes, v_new, kv_new_bytes) || overlap(k_old, kv_old_bytes, v_new, kv_new_bytes) ||
+        overlap(v_old, kv_old_bytes, k_new, kv_new_bytes))
+      return fail(PISA_ERR_INVALID_ARG, "old and new key/value buffers overlap");
+  }
+  // 16-byte units: a summary row is D floats (16 or 32 units), a key row D
+  // elements of esz bytes (8/16 units in bf16, 16/32 in fp32)
+  const int64_t pu = s.D / 4, ku = s.D * static_cast<int64_t>(esz) / 16;
+  pisa::GrowArgs a{};
+  int64_t end = 0;
+  for (int l = 1; l <= g.Lstore; ++l) {
+    end += static_cast<int64_t>(g.M[l]) * pu;
+    a.lev_end[l - 1] = end;
+    a.off_old[l - 1] = g.off[l] * pu;
+    a.off_new[l - 1] = gn.off[l] * pu;
+  }
+  a.pyr_units = end;
+  a.kv_units = kv ? static_cast<int64_t>(s.N) * ku : 0;
+  a.pyr_old_stride = g.R * pu;
+  a.pyr_new_stride = gn.R * pu;
+  a.kv_old_stride = static_cast<int64_t>(g.Nkv) * ku;
+  a.kv_new_stride = static_cast<int64_t>(gn.Nkv) * ku;
+  return device_status(pisa::launch_cache_grow(a, static_cast<int>(BH), pyr_old, pyr_new, k_old, k_new, v_old, v_new,
+                                               static_cast<hipStream_t>(stream)),
+                       "pisa_cache_grow");
 }
 
 int pisa_select(const pisa_problem* p, const void* q, const void* k, const float* pyramid, int32_t* block_idx,

@@ -84,6 +84,21 @@ hipError_t launch_build_pyramid(const Geo& geo, int BH, int D, bool bf16, const 
 hipError_t launch_pyramid_append(const Geo& geo, const Geo& geo_old, int BH, int D, bool bf16, const void* k,
                                  float* pyr, int n_old, hipStream_t st);
 
+// Decode-cache growth: the stored levels' rows and the first N rows of k and
+// v moved into a layout for a larger capacity.  All counts and offsets are in
+// 16-byte units; lev_end[l] is the end of stored level l+1 within a head's
+// stream (levels in order), off_old/off_new that level's first unit in the
+// old / new pyramid of one head.  kv_units = 0 copies no keys or values.
+struct GrowArgs {
+  int64_t pyr_units, kv_units;
+  int64_t pyr_old_stride, pyr_new_stride;  // units per head
+  int64_t kv_old_stride, kv_new_stride;    // units per head
+  int64_t lev_end[kMaxLevels];
+  int64_t off_old[kMaxLevels], off_new[kMaxLevels];
+};
+hipError_t launch_cache_grow(const GrowArgs& a, int BH, const float* pyr_old, float* pyr_new, const void* k_old,
+                             void* k_new, const void* v_old, void* v_new, hipStream_t st);
+
 // Fused single-stage selector (all levels, raw leaf keys scored per query).
 hipError_t launch_select_fused(const Shape& s, const Geo& geo, const void* q, const void* k,
                                const float* pyr, int32_t* idx, float* score, hipStream_t st);

@@ -300,6 +300,46 @@ hipError_t launch_pyramid_append(const Geo& geo, const Geo& geo_old, int BH, int
   return hipGetLastError();
 }
 
+// Decode-cache capacity growth (App. B): per (batch, KV head) one stream of
+// 16-byte units -- the rows of every stored level, moved from that level's
+// offset in the old layout to its offset in the new one, then the first N
+// rows of k and of v -- copied with coalesced vector loads and stores.
+__global__ __launch_bounds__(256) void cache_grow_kernel(GrowArgs a, const uint4* __restrict__ pyr_old,
+                                                         uint4* __restrict__ pyr_new, const uint4* __restrict__ k_old,
+                                                         uint4* __restrict__ k_new, const uint4* __restrict__ v_old,
+                                                         uint4* __restrict__ v_new) {
+  const int64_t bh = blockIdx.y;
+  const int64_t total = a.pyr_units + 2 * a.kv_units;
+  for (int64_t e = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; e < total;
+       e += static_cast<int64_t>(gridDim.x) * 256) {
+    if (e < a.pyr_units) {
+      int l = 0;
+      while (e >= a.lev_end[l]) ++l;
+      const int64_t local = e - (l > 0 ? a.lev_end[l - 1] : 0);
+      pyr_new[bh * a.pyr_new_stride + a.off_new[l] + local] = pyr_old[bh * a.pyr_old_stride + a.off_old[l] + local];
+    } else if (e < a.pyr_units + a.kv_units) {
+      const int64_t local = e - a.pyr_units;
+      k_new[bh * a.kv_new_stride + local] = k_old[bh * a.kv_old_stride + local];
+    } else {
+      const int64_t local = e - a.pyr_units - a.kv_units;
+      v_new[bh * a.kv_new_stride + local] = v_old[bh * a.kv_old_stride + local];
+    }
+  }
+}
+
+hipError_t launch_cache_grow(const GrowArgs& a, int BH, const float* pyr_old, float* pyr_new, const void* k_old,
+                             void* k_new, const void* v_old, void* v_new, hipStream_t st) {
+  const int64_t total = a.pyr_units + 2 * a.kv_units;
+  // enough workgroups for ~4 units per thread, at most 65535 per head
+  const int64_t per_head = (total + 1023) / 1024;
+  dim3 grid(static_cast<unsigned>(per_head < 1 ? 1 : (per_head > 65535 ? 65535 : per_head)), BH);
+  ProfScope ps("cache_grow", st);
+  cache_grow_kernel<<<grid, 256, 0, st>>>(a, reinterpret_cast<const uint4*>(pyr_old), reinterpret_cast<uint4*>(pyr_new),
+                                          static_cast<const uint4*>(k_old), static_cast<uint4*>(k_new),
+                                          static_cast<const uint4*>(v_old), static_cast<uint4*>(v_new));
+  return hipGetLastError();
+}
+
 constexpr size_t kPoolTopLds = 160 * 1024;  // dynamic LDS of one workgroup on a CDNA4 CU
 
 // s = number of coarser levels computed inside pool_leaf_kernel: the largest

@@ -35,7 +35,7 @@ PISA_ERR_DEVICE = -4
 EXPORTS = (
     "pisa_num_levels", "pisa_pyramid_layout", "pisa_pyramid_bytes",
     "pisa_select_workspace_bytes", "pisa_bsa_workspace_bytes", "pisa_attn_workspace_bytes",
-    "pisa_build_pyramid", "pisa_pyramid_append", "pisa_select", "pisa_select_static", "pisa_select_flat_bsa",
+    "pisa_build_pyramid", "pisa_pyramid_append", "pisa_cache_capacity", "pisa_cache_grow", "pisa_select", "pisa_select_static", "pisa_select_flat_bsa",
     "pisa_sparse_attn_fwd",
     "pisa_attn_bwd_workspace_bytes", "pisa_sparse_attn_bwd",
     "pisa_quality_workspace_bytes", "pisa_selection_quality",
@@ -83,6 +83,8 @@ def _load():
         "pisa_attn_workspace_bytes": (sz, [P]),
         "pisa_build_pyramid": (ctypes.c_int, [P, vp, vp, vp]),
         "pisa_pyramid_append": (ctypes.c_int, [P, vp, vp, i32, vp]),
+        "pisa_cache_capacity": (ctypes.c_int32, [i32, i32, i32]),
+        "pisa_cache_grow": (ctypes.c_int, [P, i32, vp, vp, vp, vp, vp, vp, vp]),
         "pisa_select": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pisa_select_static": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp]),
         "pisa_select_flat_bsa": (ctypes.c_int, [P, vp, vp, vp, vp, sz, vp]),
@@ -175,6 +177,17 @@ def pisa_pyramid_append(p: Problem, k, pyramid, n_old: int, stream=None) -> int:
                   "pisa_pyramid_append")
 
 
+def pisa_cache_capacity(cap: int, need: int, C: int) -> int:
+    r = _lib.pisa_cache_capacity(cap, need, C)
+    return _check(r, "pisa_cache_capacity") if r < 0 else r
+
+
+def pisa_cache_grow(p: Problem, new_cap: int, pyr_old, pyr_new, k_old=None, k_new=None, v_old=None, v_new=None,
+                    stream=None) -> int:
+    return _check(_lib.pisa_cache_grow(ctypes.byref(p), new_cap, _ptr(pyr_old), _ptr(pyr_new), _ptr(k_old), _ptr(k_new),
+                                       _ptr(v_old), _ptr(v_new), _stream(stream)), "pisa_cache_grow")
+
+
 def pisa_select(p: Problem, q, k, pyramid, block_idx, block_score=None, ws=None, ws_bytes=0, stream=None) -> int:
     return _check(_lib.pisa_select(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(pyramid), _ptr(block_idx),
                                    _ptr(block_score), _ptr(ws), ws_bytes, _stream(stream)), "pisa_select")
@@ -259,6 +272,22 @@ def build_pyramid(p: Problem, k, stream=None):
     pyr = torch.empty((p.B, p.Hkv, R, p.d), dtype=torch.float32, device=k.device)
     pisa_build_pyramid(p, k, pyr, stream)
     return pyr
+
+
+def grow_cache(p: Problem, new_cap: int, pyramid, k=None, v=None, stream=None):
+    """Allocate buffers for new_cap tokens and move the cache of problem p into
+    them with pisa_cache_grow.  Returns (problem with Ncap = new_cap, pyramid,
+    k, v); k and v are None when not given."""
+    pn = Problem(*[getattr(p, n) for n, _ in Problem._fields_])
+    pn.Ncap = new_cap
+    _, R = pisa_pyramid_layout(pn)
+    pyr = torch.empty((p.B, p.Hkv, R, p.d), dtype=torch.float32, device=pyramid.device)
+    kn = vn = None
+    if k is not None:
+        kn = torch.empty((p.B, p.Hkv, new_cap, p.d), dtype=k.dtype, device=k.device)
+        vn = torch.empty((p.B, p.Hkv, new_cap, p.d), dtype=v.dtype, device=v.device)
+    pisa_cache_grow(p, new_cap, pyramid, pyr, k, kn, v, vn, stream)
+    return pn, pyr, kn, vn
 
 
 def select(p: Problem, q, k, pyramid, with_score=False, stream=None):

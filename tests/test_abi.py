@@ -2,6 +2,7 @@
 symbol the header declares, computes the hierarchy geometry, and rejects bad
 arguments (exact status, non-empty detail) before anything is launched."""
 import ctypes
+import math
 import os
 import re
 import subprocess
@@ -207,3 +208,63 @@ def test_attention_backward_validates_before_launch():
     assert call(nb=need - 1) == pisa.PISA_ERR_WORKSPACE
     assert call(pp=_good(dtype="f32")) == pisa.PISA_ERR_UNSUPPORTED
     assert pisa.pisa_attn_bwd_workspace_bytes(_good(dtype="f32")) == 0
+
+
+# Decode cache capacity (App. B "Decode cache": each level grows by a fixed
+# fraction when more room is needed).
+@pytest.mark.parametrize("C", [32, 64, 128])
+def test_cache_capacity_rule(C):
+    assert pisa.pisa_cache_capacity(1000, 1000, C) == 1000      # fits: unchanged
+    assert pisa.pisa_cache_capacity(1000, 10, C) == 1000
+    for cap, need in [(0, 1), (0, 777), (512, 513), (768, 769), (4096, 9000), (1000, 1001)]:
+        got = pisa.pisa_cache_capacity(cap, need, C)
+        assert got % C == 0 and got >= need and got >= cap + (cap + 1) // 2, (cap, need, got)
+        assert got - C < max(need, cap + (cap + 1) // 2), (cap, need, got)   # the smallest such multiple
+
+
+def test_cache_capacity_grows_geometrically():
+    """Streaming one token at a time from 1000 to 2^21 tokens: each growth
+    multiplies the capacity by at least 3/2, so there are O(log N) of them
+    (about 1.7 per doubling) and the rows copied over all growths stay below
+    three times the final length (a geometric series)."""
+    C, cap, n = 64, 1024, 1000
+    growths, copied = 0, 0
+    while n < (1 << 21):
+        n += 1
+        if n > cap:
+            new = pisa.pisa_cache_capacity(cap, n, C)
+            assert new >= 1.5 * cap
+            copied += n - 1           # the rows that move
+            cap = new
+            growths += 1
+    assert growths <= math.ceil(math.log((1 << 21) / 1024, 1.5)) + 1
+    assert copied < 3 * (1 << 21)
+
+
+def test_cache_capacity_limits():
+    C = 64
+    top = 65535 * C
+    assert pisa.pisa_cache_capacity(top - 10, top - 5, C) == top          # clamped, still holds need
+    assert pisa.pisa_cache_capacity(50000 * C, 50000 * C + 1, C) == top     # 3/2 would pass the limit
+    lib = pisa.library()
+    assert lib.pisa_cache_capacity(top, top + 1, C) == pisa.PISA_ERR_UNSUPPORTED
+    assert lib.pisa_cache_capacity(-1, 5, C) == pisa.PISA_ERR_INVALID_ARG
+    assert lib.pisa_cache_capacity(5, 0, C) == pisa.PISA_ERR_INVALID_ARG
+    with pytest.raises(pisa.PisaError):
+        pisa.pisa_cache_capacity(top, top + 1, C)
+
+
+def test_cache_grow_validates_before_launch():
+    p = _good(N=1000, Ncap=1024, C=64)
+    lib = pisa.library()
+    big = FAKE * 64
+
+    def call(new_cap=1536, po=FAKE, pn=big, ko=None, kn=None, vo=None, vn=None, pp=p):
+        return lib.pisa_cache_grow(ctypes.byref(pp), new_cap, po, pn, ko, kn, vo, vn, None)
+    assert call(new_cap=1000) == pisa.PISA_ERR_INVALID_ARG and "capacity" in pisa.pisa_last_error()
+    assert call(new_cap=65536 * 64) == pisa.PISA_ERR_UNSUPPORTED
+    assert call(pn=FAKE + 4096) == pisa.PISA_ERR_INVALID_ARG and "overlap" in pisa.pisa_last_error()
+    assert call(po=None) == pisa.PISA_ERR_INVALID_ARG
+    assert call(ko=big * 2) == pisa.PISA_ERR_INVALID_ARG            # keys without the other three pointers
+    assert call(ko=big * 2, kn=big * 3, vo=big * 4, vn=big * 3 + 4096) == pisa.PISA_ERR_INVALID_ARG  # k_new, v_new overlap
+    assert call(pp=_good(d=96)) == pisa.PISA_ERR_UNSUPPORTED

@@ -88,6 +88,17 @@ def _run_guarded(p, q, k, v, schedules, with_bwd, with_quality):
     pisa.pisa_pyramid_append(p, k, pyr2.ptr(), n_old)
     pyr2.check("pisa_pyramid_append")
     assert torch.equal(pyr2.t, ref_pyr)
+    # decode-cache growth into buffers for 1.5x the tokens (pyramid, k and v)
+    new_cap = pisa.pisa_cache_capacity(N, N + 1, p.C)
+    pn = pisa.make_problem(B, H, Hkv, Nq, N, d, p.C, p.fanout, K, p.causal, tdt, Ncap=new_cap)
+    _, Rn = pisa.pisa_pyramid_layout(pn)
+    gp = _out((B, Hkv, Rn, d), torch.float32)
+    gk = _out((B, Hkv, new_cap, d), tdt)
+    gv = _out((B, Hkv, new_cap, d), tdt)
+    pisa.pisa_cache_grow(p, new_cap, pyr.ptr(), gp.ptr(), k, gk.ptr(), v, gv.ptr())
+    for buf, what in ((gp, "pyramid"), (gk, "k"), (gv, "v")):
+        buf.check(f"pisa_cache_grow {what}")
+    assert torch.equal(gk.t[:, :, :N], k) and torch.equal(gv.t[:, :, :N], v)
     # selection, every requested schedule, with block scores
     idx_ref = None
     for sched in schedules:
