@@ -29,6 +29,7 @@ METRIC = "PISA select+attn tokens/s at N=128K; % HBM peak (select), % MFMA peak 
 HBM_PEAK_GBS = 8000.0
 MFMA_BF16_PEAK_TFLOPS = 2500.0
 VALU_F32_PEAK_TFLOPS = 78.6   # 256 CU x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz (no packed FP32)
+VALU_F32_PACKED_PEAK_TFLOPS = 157.3  # MI355X published fp32 vector peak (packed FMA)
 
 
 def log(*a):
@@ -82,6 +83,47 @@ def algorithmic_work(w, pairs_scored, attn_pairs, far_key_pairs=None, far_slots=
     return out
 
 
+def attention_sharing(idx, w):
+    """Block sharing of the block-centric attention, from a selection
+    (counted on the GPU, outside any timed region): (query head, row, block)
+    triples attended divided by the K/V block stagings the kernels make.  A far
+    block (not the row's first, previous or own) is staged once per workgroup
+    chunk of up to 1024 (row, slot) pairs of its cluster and serves every query
+    head of the pair; causal rows' first, previous and own blocks are staged by
+    the per-leaf-block kernel once per (query leaf block, query head, pass of
+    its row groups).  None where another attention path runs."""
+    import torch
+
+    B, H, Hkv, N, Nq, C, K = (w[k] for k in ("B", "H", "Hkv", "N", "Nq", "C", "K"))
+    G = H // Hkv
+    M1 = -(-N // C)
+    if w["dtype"] != "bf16" or B * Hkv * Nq < 4096 or M1 > 16384 or C > 128:
+        return None
+    it = idx.long()
+    t_pos = torch.arange(N - Nq, N, device=idx.device).view(1, 1, Nq, 1)
+    c_row = t_pos // C
+    valid = (it >= 0) & (it < M1)
+    forced = (it == 0) | (it == c_row) | (it == c_row - 1) if w["causal"] else torch.zeros_like(valid)
+    far = valid & ~forced
+    bh = torch.arange(B * Hkv, device=idx.device).view(B, Hkv, 1, 1)
+    cl = (bh * M1 + it)[far]
+    counts = torch.bincount(cl, minlength=B * Hkv * M1)
+    far_loads = int(((counts + 1023) // 1024).sum().item())
+    far_triples = int(far.sum().item()) * G
+    local_loads = local_triples = 0
+    if w["causal"]:
+        nwl = 8 if C == 128 else 4
+        npass = -(-(C // 16) // nwl)
+        cs = torch.unique(c_row.flatten())
+        nsb = 1 + (cs - 1 > 0).long() + (cs > 0).long()
+        local_loads = B * Hkv * int(nsb.sum().item()) * npass * G
+        local_triples = int((valid & forced).sum().item()) * G
+    return {"factor": (far_triples + local_triples) / max(1, far_loads + local_loads),
+            "far": far_triples / max(1, far_loads), "local": local_triples / max(1, local_loads) if local_loads else None,
+            "triples": far_triples + local_triples, "block_stagings": far_loads + local_loads,
+            "what": "(query head, row, block) triples attended / K-V block stagings into LDS by the attention kernels"}
+
+
 def committed_traffic(kernel):
     """HBM bytes per launch of `kernel` from the committed counter summary
     (profiles/traffic.json), or None when absent or when the kernel's source
@@ -105,37 +147,99 @@ def committed_traffic(kernel):
     return ent["bytes_per_launch"]
 
 
-def cpu_baseline(x, w, n_rows, score="lse"):
-    """The oracle, as it stands, on a bounded sample: pyramid of KV head 0 plus
-    selection + attention of n_rows evenly spaced rows of head 0; extrapolated
-    to the whole job (all heads, all rows) as tokens/s."""
+# The CPU baseline runs the oracle in worker processes forked before anything
+# touches the GPU; they read the inputs from this module-level slot.
+_CPU_CTX = {}
+
+
+def _oracle_task(task):
+    """One (KV head, chunk of rows) of the CPU baseline: the oracle's selection
+    of each row plus the attention of its G query heads (the head's pyramid is
+    built once per worker and timed separately)."""
     import numpy as np
     from threadpoolctl import threadpool_limits
 
     import oracle as O
 
-    N, Nq, d, C, g, K, H, Hkv = (w[k] for k in ("N", "Nq", "d", "C", "g", "K", "H", "Hkv"))
+    h, rows = task
+    x, w, score = _CPU_CTX["x"], _CPU_CTX["w"], _CPU_CTX["score"]
+    N, Nq, C, g, K, H, Hkv = (w[k] for k in ("N", "Nq", "C", "g", "K", "H", "Hkv"))
     G = H // Hkv
+    causal = bool(w["causal"])
+    cache = _CPU_CTX.setdefault("pyramids", {})
+    t_pyr = None
     with threadpool_limits(1):
-        k0 = x["k"][0, 0].astype(np.float64)
-        v0 = x["v"][0, 0]
-        t0 = time.perf_counter()
-        levels = O.build_pyramid(k0, C, g)
-        t_pyr = time.perf_counter() - t0
-        rows = np.unique(np.linspace(0, Nq - 1, n_rows).astype(int))
+        kh = x["k"][0, h].astype(np.float64)
+        if h not in cache:
+            t0 = time.perf_counter()
+            cache[h] = O.build_pyramid(kh, C, g)
+            t_pyr = time.perf_counter() - t0
+        levels = cache[h]
+        vh = x["v"][0, h]
         t0 = time.perf_counter()
         for r in rows:
             t = N - Nq + r
-            sel, _ = O.select_row(x["q"][0, 0:G, r], k0, levels, t, C, g, K, bool(w["causal"]), score=score)
-            for hh in range(G):
-                O.attention_row(x["q"][0, hh, r], k0, v0, sel, t, C, bool(w["causal"]))
+            sel, _ = O.select_row(x["q"][0, h * G:(h + 1) * G, r], kh, levels, t, C, g, K, causal, score=score)
+            for hh in range(h * G, (h + 1) * G):
+                O.attention_row(x["q"][0, hh, r], kh, vh, sel, t, C, causal)
         t_rows = time.perf_counter() - t0
-    per_row = t_rows / len(rows)              # one (row, KV head) incl. its G heads' attention
-    total = w["B"] * Hkv * (t_pyr + Nq * per_row)
-    return {"value": w["B"] * Nq / total, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"pyramid of 1 KV head + selection and attention of {len(rows)} evenly spaced rows "
-                      f"of that head ({t_pyr + t_rows:.1f} s), extrapolated to {w['B'] * Hkv} KV heads x "
-                      f"{Nq} rows; float64 numpy, 1 thread"}
+    return h, t_pyr, t_rows, len(rows)
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(x, w, n_rows, score="lse"):
+    """The oracle, as it stands, on a bounded sample of the workload, on the
+    host's cores: n_rows rows spread evenly over every KV head, in worker
+    processes (one per core of this process's CPU share, at most 16), each
+    building its heads' pyramids once.  Extrapolated to the whole job (every
+    row of every KV head) as tokens/s: the measured CPU seconds per pyramid and
+    per row, divided by the measured parallel speed-up of the sample.  Must run
+    before the GPU is initialised (the workers are forked)."""
+    import multiprocessing as mp
+
+    import numpy as np
+
+    N, Nq, Hkv = w["N"], w["Nq"], w["Hkv"]
+    per_head = max(1, n_rows // (w["B"] * Hkv))
+    rows = np.unique(np.linspace(0, Nq - 1, per_head).astype(int))
+    n_workers = max(1, min(16, len(os.sched_getaffinity(0))))
+    # about one task per worker, each on one KV head (one pyramid build each)
+    per = max(1, -(-n_workers // Hkv))
+    chunk = max(1, -(-len(rows) // per))
+    tasks = [(h, rows[i:i + chunk].tolist()) for h in range(Hkv) for i in range(0, len(rows), chunk)]
+    n_workers = min(n_workers, len(tasks))
+    _CPU_CTX.update(x=x, w=w, score=score)
+    ctx = mp.get_context("fork")
+    t0 = time.perf_counter()
+    with ctx.Pool(n_workers) as pool:
+        out = pool.map(_oracle_task, tasks, chunksize=1)
+    wall = time.perf_counter() - t0
+    _CPU_CTX.clear()
+    pyr_times = [tp for _, tp, _, _ in out if tp is not None]
+    t_rows = sum(tr for _, _, tr, _ in out)
+    n_done = sum(n for _, _, _, n in out)
+    busy = sum(pyr_times) + t_rows
+    speedup = busy / wall
+    per_row = t_rows / n_done
+    t_pyr = sum(pyr_times) / len(pyr_times)
+    total_cpu = w["B"] * Hkv * (t_pyr + Nq * per_row)
+    return {"value": w["B"] * Nq / (total_cpu / speedup), "unit": "tokens/s", "cores": n_workers, "kind": "oracle",
+            "cpu_model": _cpu_model(), "host_logical_cpus": os.cpu_count(),
+            "sample": f"{n_done} rows ({len(rows)} evenly spaced rows of each of {Hkv} KV heads, each with its "
+                      f"{w['H'] // Hkv} query heads' attention) and {len(pyr_times)} pyramid builds: "
+                      f"{busy:.1f} CPU-s in {wall:.1f} s wall on {n_workers} worker processes (speed-up "
+                      f"{speedup:.1f}); extrapolated to {w['B'] * Hkv} KV heads x {Nq} rows; float64 numpy, "
+                      f"1 thread per worker"}
 
 
 def main():
@@ -146,7 +250,8 @@ def main():
     ap.add_argument("--workload", default="needles-128k")
     ap.add_argument("--score", default="lse", choices=["lse", "mean", "mean_var"],
                     help="block score of the selection: PISA (lse), PISA-1 (mean), PISA-2 (mean_var)")
-    ap.add_argument("--cpu-rows", type=int, default=12288)
+    ap.add_argument("--cpu-rows", type=int, default=8192,
+                    help="rows (over all KV heads) of the CPU oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bsa", action="store_true")
     ap.add_argument("--sweep", default="",
@@ -173,13 +278,22 @@ def main():
     import numpy as np
     import torch
 
-    from paper_2609_31093_amd import inputs, pisa
+    from paper_2609_31093_amd import inputs
 
-    torch.cuda.set_device(0)
     w = inputs.workload(args.workload)
     B, H, Hkv, N, Nq, d, C, g, K = (w[k] for k in ("B", "H", "Hkv", "N", "Nq", "d", "C", "g", "K"))
     log(f"[bench] generating {args.workload} inputs")
     x = inputs.make_inputs(w, seed=0)
+    cpu = None
+    if not args.no_cpu_baseline:
+        # before anything touches the GPU: the oracle's workers are forked
+        log(f"[bench] cpu baseline: oracle on {args.cpu_rows} rows over every KV head")
+        cpu = cpu_baseline(x, w, args.cpu_rows, args.score)
+        log(f"[bench] cpu baseline: {cpu['value']:.1f} tokens/s on {cpu['cores']} cores")
+
+    from paper_2609_31093_amd import pisa
+
+    torch.cuda.set_device(0)
     tdt = torch.bfloat16 if w["dtype"] == "bf16" else torch.float32
     q, k, v = (torch.from_numpy(x[n]).to(tdt).cuda() for n in "qkv")
     score_id = {"lse": 0, "mean": 1, "mean_var": 2}[args.score]
@@ -195,47 +309,61 @@ def main():
     ws_att = torch.empty(max(ws_att_n, 1), dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
 
-    ev = {n: (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for n in ("pool", "select", "attn")}
-
-    def step(timed=False):
-        if timed:
-            ev["pool"][0].record(stream)
+    def step(evs=None):
+        if evs:
+            evs[0].record(stream)
         pisa.pisa_build_pyramid(p, k, pyr, stream)
-        if timed:
-            ev["pool"][1].record(stream)
-            ev["select"][0].record(stream)
+        if evs:
+            evs[1].record(stream)
         pisa.pisa_select(p, q, k, pyr, idx, None, ws_sel, ws_sel_n, stream)
-        if timed:
-            ev["select"][1].record(stream)
-            ev["attn"][0].record(stream)
+        if evs:
+            evs[2].record(stream)
         pisa.pisa_sparse_attn_fwd(p, q, k, v, idx, o, lse, ws_att, ws_att_n, stream)
-        if timed:
-            ev["attn"][1].record(stream)
+        if evs:
+            evs[3].record(stream)
 
     log(f"[bench] warmup {args.warmup}")
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
 
+    # Timed region: exactly `steps` back-to-back steps between two
+    # synchronisations; hipEvents on the launch stream (phase boundaries here,
+    # every kernel inside the library) are read afterwards.
     log(f"[bench] timing {args.steps} steps")
+    phase = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     pisa.pisa_profile_enable(True)
     pisa.pisa_profile_report()  # clear
-    split = {n: 0.0 for n in ev}
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step(timed=True)
-        torch.cuda.synchronize()   # per-step sync so the phase events can be read
-        for n, (a, b) in ev.items():
-            split[n] += a.elapsed_time(b)
+    for i in range(args.steps):
+        step(phase[i])
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     kern = pisa.pisa_profile_report()
     pisa.pisa_profile_enable(False)
+    split = {"pool": sum(e[0].elapsed_time(e[1]) for e in phase),
+             "select": sum(e[1].elapsed_time(e[2]) for e in phase),
+             "attn": sum(e[2].elapsed_time(e[3]) for e in phase)}
+    warm_steps = sorted(e[0].elapsed_time(e[3]) for e in phase)
     ms_per_step = (t1 - t0) * 1e3 / args.steps
     tokens_per_s = B * Nq / (ms_per_step / 1e3)
     log(f"[bench] {ms_per_step:.3f} ms/step, {tokens_per_s / 1e6:.2f} M tokens/s")
+
+    # Cold caches: before each of a few further steps, a 512 MiB write evicts
+    # the 256 MB MALL and the L2s; each step timed on its own.
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    cold = []
+    for i in range(5):
+        flush.fill_(i)
+        c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        c0.record(stream)
+        step()
+        c1.record(stream)
+        torch.cuda.synchronize()
+        cold.append(c0.elapsed_time(c1))
+    cold.sort()
+    del flush
 
     # Algorithmic work of this workload (counted from the outputs, outside the timed region).
     idx_t = idx.long()
@@ -268,7 +396,10 @@ def main():
                     "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s"}
         else:
             roof = {"kernel": dom, "bound": "alu", "achieved": amount / avg_s / 1e12,
-                    "peak": VALU_F32_PEAK_TFLOPS, "unit": "TFLOP/s"}
+                    "peak": VALU_F32_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "peak_note": "fp32 VALU without packed instructions (packed FP32 is disabled in every build)",
+                    "published_peak": VALU_F32_PACKED_PEAK_TFLOPS,
+                    "frac_of_published_peak": amount / avg_s / 1e12 / VALU_F32_PACKED_PEAK_TFLOPS}
         roof["frac"] = roof["achieved"] / roof["peak"]
         roof["traffic"] = committed_traffic(dom)
 
@@ -322,11 +453,6 @@ def main():
         torch.cuda.synchronize()
         bsa_ms = e0.elapsed_time(e1) / nrep
 
-    cpu = None
-    if not args.no_cpu_baseline:
-        log(f"[bench] cpu baseline: oracle on {args.cpu_rows} rows")
-        cpu = cpu_baseline(x, w, args.cpu_rows, args.score)
-
     sel_ms = (split["pool"] + split["select"]) / args.steps
     res = {
         "metric": METRIC,
@@ -346,12 +472,17 @@ def main():
                    "parallelism": "single GPU"},
         "split_ms": {"pool": split["pool"] / args.steps, "select": split["select"] / args.steps,
                      "attn": split["attn"] / args.steps},
+        "step_ms": {"warm_median": warm_steps[len(warm_steps) // 2], "warm_mean": sum(warm_steps) / len(warm_steps),
+                    "cold_median": cold[len(cold) // 2], "cold_steps": len(cold),
+                    "what": "hipEvents around single steps: warm = the timed steps, cold = further steps each "
+                            "after a 512 MiB write that evicts the MALL and L2"},
         "selection_ms_incl_pool": sel_ms,
         "flat_bsa_selection_ms_incl_pool": bsa_ms,
         "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": cpu,
         "fractions": fractions,
+        "attention_sharing": attention_sharing(idx, w),
         "per_kernel_roofline": per_kernel,
     }
     print(json.dumps(res), flush=True)
@@ -481,6 +612,68 @@ def main():
                 if rep == 1:
                     lat_s.append(e0.elapsed_time(e1) * 1e3)
         lat_s.sort()
+        # Streaming across a capacity growth: 1024 tokens from 512 below a full
+        # cache of cap0 rows.  At token cap0 + 1 the caller allocates buffers
+        # for pisa_cache_capacity(cap0, cap0 + 1, C) tokens (outside the
+        # events) and pisa_cache_grow moves pyramid, k and v into them; that
+        # step's time includes the move.
+        cap0 = Nd - 1024
+        n_start = cap0 - 512
+        kg = kd[:, :, :cap0].clone()
+        vg = vd[:, :, :cap0].clone()
+        cap_g = cap0
+        pg = pisa.make_problem(Bd, Hd, Hkvd, 1, n_start, dd, Cd, gd, Kd, 1, "bf16", Ncap=cap_g)
+        pyr_g = pisa.build_pyramid(pg, kg)
+        torch.cuda.synchronize()
+        lat_grow, grow_us, grow_step = [], None, None
+        for i in range(1024):
+            n = n_start + i
+            pre = None
+            if n + 1 > cap_g:
+                new_cap = pisa.pisa_cache_capacity(cap_g, n + 1, Cd)
+                p_cur = pisa.make_problem(Bd, Hd, Hkvd, 1, n, dd, Cd, gd, Kd, 1, "bf16", Ncap=cap_g)
+                p_nxt = pisa.make_problem(Bd, Hd, Hkvd, 1, n, dd, Cd, gd, Kd, 1, "bf16", Ncap=new_cap)
+                _, R_n = pisa.pisa_pyramid_layout(p_nxt)
+                pyr_n = torch.empty((Bd, Hkvd, R_n, dd), dtype=torch.float32, device="cuda")
+                k_n = torch.empty((Bd, Hkvd, new_cap, dd), dtype=torch.bfloat16, device="cuda")
+                v_n = torch.empty_like(k_n)
+                torch.cuda.synchronize()
+                pre = (p_cur, new_cap, pyr_n, k_n, v_n)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            eg = torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            if pre is not None:
+                p_cur, new_cap, pyr_n, k_n, v_n = pre
+                pisa.pisa_cache_grow(p_cur, new_cap, pyr_g, pyr_n, kg, k_n, vg, v_n, stream)
+                eg.record(stream)
+                pyr_g, kg, vg, cap_g = pyr_n, k_n, v_n, new_cap
+            # the new token's key and value (the caller's write), then the step
+            kg[:, :, n].copy_(kd[:, :, n])
+            vg[:, :, n].copy_(vd[:, :, n])
+            ps_ = pisa.make_problem(Bd, Hd, Hkvd, 1, n + 1, dd, Cd, gd, Kd, 1, "bf16", Ncap=cap_g)
+            pisa.pisa_pyramid_append(ps_, kg, pyr_g, n, stream)
+            qd = qsteps[i % len(qsteps)]
+            pisa.pisa_select(ps_, qd, kg, pyr_g, idx_d, None, ws_d, nsd, stream)
+            pisa.pisa_sparse_attn_fwd(ps_, qd, kg, vg, idx_d, o_d, lse_d, ws_d, nad, stream)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            lat_grow.append(e0.elapsed_time(e1) * 1e3)
+            if pre is not None:
+                grow_us = e0.elapsed_time(eg) * 1e3
+                grow_step = i
+        med_grow = sorted(lat_grow)[len(lat_grow) // 2]
+        per_doubling = math.log(2) / math.log(1.5)   # growths per doubling of the length
+        growth_stream = {
+            "tokens": len(lat_grow), "start": n_start + 1, "capacity_before": cap0, "capacity_after": cap_g,
+            "grow_us": grow_us, "growth_step_us": lat_grow[grow_step] if grow_step is not None else None,
+            "median_step_us": med_grow, "mean_step_us": sum(lat_grow) / len(lat_grow),
+            "amortised_growth_us_per_token": per_doubling * grow_us / (cap0 / 2) if grow_us else None,
+            "amortised_step_us": med_grow + (per_doubling * grow_us / (cap0 / 2) if grow_us else 0.0),
+            "what": "one step = the token's k/v row written + pisa_pyramid_append + pisa_select + "
+                    "pisa_sparse_attn_fwd; at the capacity the step also runs pisa_cache_grow (pyramid, k and v "
+                    "of 8 KV heads moved to buffers for 3/2 the tokens; buffer allocation not timed).  Amortised: "
+                    "the median step plus the move's time spread over the tokens of a doubling of the length "
+                    "(log 2 / log 1.5 moves per doubling, each at most this one's size)"}
         print(json.dumps({"decode": {"workload": "decode-128k", "steps": len(lat),
                                      "median_us": lat[len(lat) // 2], "p90_us": lat[int(0.9 * len(lat))],
                                      "what": "one step = pisa_select + pisa_sparse_attn_fwd for 8 heads x 1 token "
@@ -493,7 +686,8 @@ def main():
                                      "streaming_p90_us": lat_s[int(0.9 * len(lat_s))],
                                      "streaming_what": f"one step = pisa_pyramid_append of 1 token + pisa_select + "
                                                        f"pisa_sparse_attn_fwd, KV length growing {n0 + 1} -> {Nd} "
-                                                       f"in buffers reserved for {Nd} rows"}}), flush=True)
+                                                       f"in buffers reserved for {Nd} rows",
+                                     "growth": growth_stream}}), flush=True)
 
     if args.backward:
         pisa.pisa_build_pyramid(p, k, pyr, stream)
