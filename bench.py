@@ -253,6 +253,8 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=8192,
                     help="rows (over all KV heads) of the CPU oracle's timed sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold-steps", type=int, default=5,
+                    help="further steps timed one by one after a cache-evicting write (0: none)")
     ap.add_argument("--no-bsa", action="store_true")
     ap.add_argument("--sweep", default="",
                     help="comma-separated N values: time PISA selection and flat-BSA selection "
@@ -354,7 +356,7 @@ def main():
     # the 256 MB MALL and the L2s; each step timed on its own.
     flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
     cold = []
-    for i in range(5):
+    for i in range(args.cold_steps):
         flush.fill_(i)
         c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         c0.record(stream)
@@ -364,6 +366,7 @@ def main():
         cold.append(c0.elapsed_time(c1))
     cold.sort()
     del flush
+    cold_median = cold[len(cold) // 2] if cold else None
 
     # Algorithmic work of this workload (counted from the outputs, outside the timed region).
     idx_t = idx.long()
@@ -473,7 +476,7 @@ def main():
         "split_ms": {"pool": split["pool"] / args.steps, "select": split["select"] / args.steps,
                      "attn": split["attn"] / args.steps},
         "step_ms": {"warm_median": warm_steps[len(warm_steps) // 2], "warm_mean": sum(warm_steps) / len(warm_steps),
-                    "cold_median": cold[len(cold) // 2], "cold_steps": len(cold),
+                    "cold_median": cold_median, "cold_steps": len(cold),
                     "what": "hipEvents around single steps: warm = the timed steps, cold = further steps each "
                             "after a 512 MiB write that evicts the MALL and L2"},
         "selection_ms_incl_pool": sel_ms,

@@ -311,3 +311,27 @@ def test_attention_out_of_range_indices_are_padding(name):
     tol = 2e-2 if dtype == "bf16" else 1e-4
     assert np.abs(o.float().cpu().numpy()[:, :, rows] - want_o).max() <= tol
     assert np.abs(lse.cpu().numpy()[:, :, rows] - want_lse).max() <= 1e-3
+
+
+@pytest.mark.parametrize("G", [1, 4])
+def test_flat_bsa_all_scores_tied(G):
+    """Every key equal: every block scores the same, so each row keeps its
+    forced blocks plus the smallest eligible ones (reading R4).  More tied
+    blocks rank at the cut than the fast threshold method collects, so its
+    exact fallback runs (single head, more than 8 chunks of 64 blocks)."""
+    B, Hkv, Nq, N, d, C, K = 1, 2, 600, 40000, 64, 32, 16
+    H = G * Hkv
+    x = inputs.random_qkv(B, H, Hkv, Nq, N, d, "bf16", seed=21)
+    x["k"][:] = x["k"][:, :, :1, :]
+    p = pisa.make_problem(B, H, Hkv, Nq, N, d, C, 2, K, 1, "bf16")
+    q, k = dev(x["q"], "bf16"), dev(x["k"], "bf16")
+    idx = pisa.select_flat_bsa(p, q, pisa.build_pyramid(p, k))
+    torch.cuda.synchronize()
+    idx = idx.cpu().numpy()
+    check_selection_valid(idx, N, Nq, C, K, True)
+    rows = _rows_sample(Nq, 8, 16)
+    print(check_flat_bsa_rows(x["q"], x["k"], C, K, True, idx[:, :, rows], rows))
+    for r in rows:
+        c = (N - Nq + r) // C
+        want = sorted({0, c - 1, c} | set(range(1, K - 2)))   # K - 3 unforced: blocks 1 .. K - 3
+        assert list(idx[0, 0, r]) == want, (r, idx[0, 0, r])
