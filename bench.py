@@ -9,8 +9,10 @@ to stderr.
 
 Also reported: the per-kernel time split (hipEvents recorded by the library
 on the launch stream during the timed steps), the flat-BSA selection
-baseline, the roofline of the dominant kernel and the CPU oracle timed on a
-bounded sample of the same workload (cpu_baseline).
+baseline, the roofline of the dominant kernel, the metric's two fractions
+against the published peaks and against attainable peaks measured on the
+device after the timed region (probes), and the CPU oracle timed on a bounded
+sample of the same workload (cpu_baseline).
 """
 from __future__ import annotations
 
@@ -242,6 +244,60 @@ def cpu_baseline(x, w, n_rows, score="lse"):
                       f"1 thread per worker"}
 
 
+def probe_peaks():
+    """Attainable peaks measured on this device, beside the published ones.
+    HBM: the better of a plain 1 GiB device copy of a cache-evicted buffer
+    (bytes read + written over its time) and a 2 GiB fp32 sum (bytes read);
+    bf16 matrix cores: a 16384 x 16384 x 8192 bf16 GEMM of the vendor library
+    (torch.matmul -> hipBLASLt).  Best of a few runs each."""
+    import torch
+
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def best_of(fn, reps):
+        best = float("inf")
+        for _ in range(reps):
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1))
+        return best
+
+    n = 1 << 30
+    src = torch.ones(n // 2, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    evict = torch.empty(1 << 29, dtype=torch.float16, device="cuda")
+
+    def copy():
+        dst.copy_(src)
+
+    copy_ms = float("inf")
+    for _ in range(3):
+        evict.fill_(1.0)
+        copy_ms = min(copy_ms, best_of(copy, 1))
+    del src, dst
+    big = torch.ones(1 << 29, dtype=torch.float32, device="cuda")
+    sum_ms = float("inf")
+    for _ in range(3):
+        evict.fill_(1.0)
+        sum_ms = min(sum_ms, best_of(lambda: big.sum(), 1))
+    del big, evict
+    m, kk = 16384, 8192
+    a = torch.randn((m, kk), device="cuda").to(torch.bfloat16)
+    b = torch.randn((kk, m), device="cuda").to(torch.bfloat16)
+    best_of(lambda: torch.matmul(a, b), 2)
+    mm_ms = best_of(lambda: torch.matmul(a, b), 5)
+    del a, b
+    torch.cuda.empty_cache()
+    copy_gbs, sum_gbs = 2 * n / copy_ms / 1e6, 4 * (1 << 29) / sum_ms / 1e6
+    return {"hbm_copy_GBps": copy_gbs, "hbm_read_sum_GBps": sum_gbs, "hbm_probe_GBps": max(copy_gbs, sum_gbs),
+            "mfma_bf16_gemm_TFLOPs": 2 * m * m * kk / mm_ms / 1e9,
+            "what": "attainable peaks on this device: a 1 GiB device copy (read + written bytes) and a 2 GiB fp32 "
+                    "sum of cache-evicted buffers, a 16384 x 16384 x 8192 bf16 GEMM (torch.matmul); the "
+                    "fractions' frac_of_probe divide by hbm_probe_GBps and mfma_bf16_gemm_TFLOPs"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -438,6 +494,11 @@ def main():
                            "frac": attn_pairs * 4 * d / attn_s / 1e12 / MFMA_BF16_PEAK_TFLOPS},
     }
 
+    probes = probe_peaks()
+    fractions["selection_hbm"]["frac_of_probe"] = fractions["selection_hbm"]["achieved_GBps"] / probes["hbm_probe_GBps"]
+    fractions["attention_mfma"]["frac_of_probe"] = (fractions["attention_mfma"]["achieved_TFLOPs"] /
+                                                    probes["mfma_bf16_gemm_TFLOPs"])
+
     bsa_ms = None
     if not args.no_bsa:
         log("[bench] flat-BSA baseline")
@@ -485,6 +546,7 @@ def main():
         "roofline": roof,
         "cpu_baseline": cpu,
         "fractions": fractions,
+        "probes": probes,
         "attention_sharing": attention_sharing(idx, w),
         "per_kernel_roofline": per_kernel,
     }
