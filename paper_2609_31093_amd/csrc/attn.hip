@@ -936,7 +936,7 @@ static AttnWs attn_layout(const Shape& s, const Geo& geo) {
   auto al = [](size_t x) { return (x + 255) & ~static_cast<size_t>(255); };
   w.part_o = o;   o += al(np * s.G * s.D * 2);
   w.part_lse = o; o += al(np * s.G * 4);
-  w.cl = o;       o += al(cluster_ws(s.BH(), geo.M[1], static_cast<int64_t>(np)));
+  w.cl = o;       o += al(cluster_ws(s.BH(), geo.M[1], static_cast<int64_t>(np), static_cast<int>(ch)));
   // causal budgets above 32: the rows' log-sums between the per-leaf-block
   // merge and the tail merge, for callers that pass no lse
   w.row_lse = o;

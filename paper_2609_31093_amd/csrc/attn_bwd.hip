@@ -400,7 +400,7 @@ static BwdWs bwd_layout(const Shape& s, const Geo& geo) {
   w.dk = o;   o += al(kv);
   w.dv = o;   o += al(kv);
   w.part = o; o += al(np * s.G * s.D * 2);
-  w.cl = o;   o += al(cluster_ws(s.BH(), geo.M[1], static_cast<int64_t>(np)));
+  w.cl = o;   o += al(cluster_ws(s.BH(), geo.M[1], static_cast<int64_t>(np), static_cast<int>(ch)));
   w.total = o;
   return w;
 }

@@ -4,13 +4,13 @@
 //
 // A workgroup owns a chunk of rows of one (batch, KV head) and builds an LDS
 // histogram of the blocks its pairs reference; only the non-zero bins reach
-// global memory (one atomic per bin per chunk instead of one per pair).  An
-// exclusive scan turns the global counts into cluster offsets; the scatter
-// pass rebuilds the chunk histogram, reserves one contiguous range per
-// non-zero bin with a single global atomic, and places each pair with an LDS
-// atomic inside its range.  The order of pairs inside a cluster is therefore
-// not fixed, which no consumer depends on (every pair is processed on its
-// own).
+// global memory: one atomic per bin per chunk adds the chunk's count to the
+// bin's total and returns the chunk's offset inside the bin, which is kept
+// (one row of bins per chunk).  An exclusive scan turns the totals into
+// cluster offsets; the scatter pass starts each bin at its cluster offset
+// plus the chunk's offset and places each pair with an LDS atomic inside that
+// range.  The order of pairs inside a cluster is therefore not fixed, which
+// no consumer depends on (every pair is processed on its own).
 #include <algorithm>
 
 #include "common.h"
@@ -58,7 +58,8 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(int32_t* p, int64_t n) {
   for (int64_t i = blockIdx.x * 256LL + threadIdx.x; i < n; i += 256LL * gridDim.x) p[i] = 0;
 }
 
-__global__ __launch_bounds__(kClusterThreads) void cluster_hist_kernel(ClusterArgs a, int32_t* __restrict__ hist) {
+__global__ __launch_bounds__(kClusterThreads) void cluster_hist_kernel(ClusterArgs a, int32_t* __restrict__ hist,
+                                                                       int32_t* __restrict__ chunk_base) {
   extern __shared__ int32_t h[];
   const int bh = blockIdx.y;
   const int r0 = blockIdx.x * kClusterRows;
@@ -73,21 +74,21 @@ __global__ __launch_bounds__(kClusterThreads) void cluster_hist_kernel(ClusterAr
   }
   __syncthreads();
   int32_t* gh = hist + static_cast<int64_t>(bh) * a.M1;
+  int32_t* cb = chunk_base + (static_cast<int64_t>(bh) * gridDim.x + blockIdx.x) * a.M1;
   for (int i = threadIdx.x; i < a.M1; i += kClusterThreads) {
     const int n = h[i];
-    if (n) atomicAdd(&gh[i], n);
+    cb[i] = n ? atomicAdd(&gh[i], n) : 0;  // this chunk's offset inside bin i
   }
 }
 
-// Exclusive scans of the n counts into offs[0..n] (pair offsets, also copied
-// to cursor) and of their tile counts ceil(count / tile) into toffs[0..n].
+// Exclusive scans of the n counts into offs[0..n] (pair offsets) and of
+// their tile counts ceil(count / tile) into toffs[0..n].
 // Each thread owns a contiguous run of the counts; runs of up to kScanRun
 // are read into registers with independent loads.
 constexpr int kScanRun = 32;
 
 __global__ __launch_bounds__(1024) void cluster_scan_kernel(const int32_t* __restrict__ hist,
                                                             int32_t* __restrict__ offs,
-                                                            int32_t* __restrict__ cursor,
                                                             int32_t* __restrict__ toffs, int64_t n, int tile) {
   __shared__ int wsum[16], wtile[16];
   const int tid = threadIdx.x;
@@ -140,7 +141,6 @@ __global__ __launch_bounds__(1024) void cluster_scan_kernel(const int32_t* __res
     for (int j = 0; j < kScanRun; ++j) {
       if (j < cnt) {
         offs[i0 + j] = run;
-        cursor[i0 + j] = run;
         toffs[i0 + j] = trun;
       }
       run += v[j];
@@ -150,7 +150,6 @@ __global__ __launch_bounds__(1024) void cluster_scan_kernel(const int32_t* __res
     for (int64_t i = i0; i < i1; ++i) {
       const int c = hist[i];
       offs[i] = run;
-      cursor[i] = run;
       toffs[i] = trun;
       run += c;
       trun += (c + tile - 1) / tile;
@@ -171,7 +170,6 @@ __host__ __device__ __forceinline__ int scan_pad(int i) { return i + (i >> 4); }
 
 __global__ __launch_bounds__(1024) void cluster_scan_lds_kernel(const int32_t* __restrict__ hist,
                                                                 int32_t* __restrict__ offs,
-                                                                int32_t* __restrict__ cursor,
                                                                 int32_t* __restrict__ toffs, int n, int tile) {
   extern __shared__ int32_t sh[];
   __shared__ int wsum[16], wtile[16];
@@ -225,9 +223,7 @@ __global__ __launch_bounds__(1024) void cluster_scan_lds_kernel(const int32_t* _
   }
   __syncthreads();
   for (int e = tid; e < n; e += 1024) {
-    const int o = ho[scan_pad(e)];
-    offs[e] = o;
-    cursor[e] = o;
+    offs[e] = ho[scan_pad(e)];
     toffs[e] = ht[scan_pad(e)];
   }
   if (tid == 0) {
@@ -236,27 +232,20 @@ __global__ __launch_bounds__(1024) void cluster_scan_lds_kernel(const int32_t* _
   }
 }
 
-__global__ __launch_bounds__(kClusterThreads) void cluster_scatter_kernel(ClusterArgs a, int32_t* __restrict__ cursor,
+__global__ __launch_bounds__(kClusterThreads) void cluster_scatter_kernel(ClusterArgs a, const int32_t* __restrict__ offs,
+                                                                          const int32_t* __restrict__ chunk_base,
                                                                           int32_t* __restrict__ pairs) {
   extern __shared__ int32_t h[];
   const int bh = blockIdx.y;
   const int r0 = blockIdx.x * kClusterRows;
   const int nr = min(kClusterRows, a.nrows - r0);
-  for (int i = threadIdx.x; i < a.M1; i += kClusterThreads) h[i] = 0;
+  // bin i of this chunk starts at its cluster's offset plus the chunk's
+  // offset inside the cluster (reserved by cluster_hist_kernel)
+  const int32_t* go = offs + static_cast<int64_t>(bh) * a.M1;
+  const int32_t* cb = chunk_base + (static_cast<int64_t>(bh) * gridDim.x + blockIdx.x) * a.M1;
+  for (int i = threadIdx.x; i < a.M1; i += kClusterThreads) h[i] = go[i] + cb[i];
   __syncthreads();
   const int npairs = nr * a.S;
-  for (int e = threadIdx.x; e < npairs; e += kClusterThreads) {
-    const int r = r0 + e / a.S, slot = e % a.S;
-    int blk;
-    if (cluster_pair(a, bh, r, slot, blk)) atomicAdd(&h[blk], 1);
-  }
-  __syncthreads();
-  int32_t* gc = cursor + static_cast<int64_t>(bh) * a.M1;
-  for (int i = threadIdx.x; i < a.M1; i += kClusterThreads) {
-    const int n = h[i];
-    if (n) h[i] = atomicAdd(&gc[i], n);  // base of this chunk's range in bin i
-  }
-  __syncthreads();
   for (int e = threadIdx.x; e < npairs; e += kClusterThreads) {
     const int r = r0 + e / a.S, slot = e % a.S;
     int blk;
@@ -267,9 +256,10 @@ __global__ __launch_bounds__(kClusterThreads) void cluster_scatter_kernel(Cluste
   }
 }
 
-size_t cluster_ws(int BH, int M1, int64_t max_pairs) {
+size_t cluster_ws(int BH, int M1, int64_t max_pairs, int max_rows) {
   const size_t ncl = static_cast<size_t>(BH) * M1;
-  return 4 * ((ncl + 1) * 4 + 256) + static_cast<size_t>(max_pairs) * 4 + 256;
+  const size_t nchunk = static_cast<size_t>(BH) * ((max_rows + kClusterRows - 1) / kClusterRows);
+  return 3 * ((ncl + 1) * 4 + 256) + (nchunk * M1 * 4 + 256) + static_cast<size_t>(max_pairs) * 4 + 256;
 }
 
 int64_t cluster_max_chunks(int BH, int M1, int64_t max_pairs, int tile) {
@@ -284,31 +274,33 @@ hipError_t launch_cluster(const ClusterArgs& a, int BH, void* ws, ClusterOut* ou
       (a.mode == kClusterLeafParent && a.g < 2))
     return hipErrorInvalidValue;
   const int64_t ncl = static_cast<int64_t>(BH) * a.M1;
+  const int nchunk = (a.nrows + kClusterRows - 1) / kClusterRows;  // row chunks per (batch, KV head)
   char* base = static_cast<char*>(ws);
   int32_t* hist = reinterpret_cast<int32_t*>(base);
   int32_t* offs = reinterpret_cast<int32_t*>(base + al((ncl + 1) * 4));
-  int32_t* cursor = reinterpret_cast<int32_t*>(base + 2 * al((ncl + 1) * 4));
-  int32_t* toffs = reinterpret_cast<int32_t*>(base + 3 * al((ncl + 1) * 4));
-  int32_t* pairs = reinterpret_cast<int32_t*>(base + 4 * al((ncl + 1) * 4));
+  int32_t* toffs = reinterpret_cast<int32_t*>(base + 2 * al((ncl + 1) * 4));
+  int32_t* chunk_base = reinterpret_cast<int32_t*>(base + 3 * al((ncl + 1) * 4));
+  int32_t* pairs = reinterpret_cast<int32_t*>(base + 3 * al((ncl + 1) * 4) +
+                                              al(static_cast<size_t>(BH) * nchunk * a.M1 * 4));
   out->offs = offs;
   out->toffs = toffs;
   out->pairs = pairs;
   out->ncl = ncl;
   ProfScope ps("cluster_build", st);
   fill_zero_kernel<<<static_cast<unsigned>(std::min<int64_t>((ncl + 255) / 256, 4096)), 256, 0, st>>>(hist, ncl);
-  dim3 grid((a.nrows + kClusterRows - 1) / kClusterRows, BH);
+  dim3 grid(nchunk, BH);
   const size_t lds = static_cast<size_t>(a.M1) * 4;
-  cluster_hist_kernel<<<grid, kClusterThreads, lds, st>>>(a, hist);
+  cluster_hist_kernel<<<grid, kClusterThreads, lds, st>>>(a, hist, chunk_base);
   if (ncl <= kScanLdsMax) {
     const size_t slds = 2 * (static_cast<size_t>(scan_pad(static_cast<int>(ncl))) + 1) * sizeof(int32_t);
     if (slds > 65536)
       (void)hipFuncSetAttribute(reinterpret_cast<const void*>(cluster_scan_lds_kernel),
                                 hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(slds));
-    cluster_scan_lds_kernel<<<1, 1024, slds, st>>>(hist, offs, cursor, toffs, static_cast<int>(ncl), tile);
+    cluster_scan_lds_kernel<<<1, 1024, slds, st>>>(hist, offs, toffs, static_cast<int>(ncl), tile);
   } else {
-    cluster_scan_kernel<<<1, 1024, 0, st>>>(hist, offs, cursor, toffs, ncl, tile);
+    cluster_scan_kernel<<<1, 1024, 0, st>>>(hist, offs, toffs, ncl, tile);
   }
-  cluster_scatter_kernel<<<grid, kClusterThreads, lds, st>>>(a, cursor, pairs);
+  cluster_scatter_kernel<<<grid, kClusterThreads, lds, st>>>(a, offs, chunk_base, pairs);
   return hipGetLastError();
 }
 

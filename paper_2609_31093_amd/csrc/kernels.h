@@ -55,7 +55,9 @@ struct ClusterOut {
   const int32_t* pairs;  // (row - row0) << 8 | slot, grouped by (bh, block)
   int64_t ncl;           // BH*M1
 };
-size_t cluster_ws(int BH, int M1, int64_t max_pairs);
+// workspace of launch_cluster for up to max_pairs pairs and max_rows rows per
+// (batch, KV head) in one launch
+size_t cluster_ws(int BH, int M1, int64_t max_pairs, int max_rows);
 
 // Chunk w of the cluster list when the consumer takes up to `tile` pairs per
 // workgroup (the tile offsets of launch_cluster(..., tile)): its cluster (the

@@ -2506,7 +2506,7 @@ static TwoStageWs two_stage_layout(const Shape& s, const Geo& geo) {
   w.a1 = o;     o += align256(rows * s.gK() * 4);
   w.a1cnt = o;  o += align256(rows * 4);
   w.u1 = o;     o += align256(rows * s.gK() * 4);
-  w.cl = o;     o += align256(cluster_ws(s.BH(), geo.M[1], static_cast<int64_t>(rows) * s.gK()));
+  w.cl = o;     o += align256(cluster_ws(s.BH(), geo.M[1], static_cast<int64_t>(rows) * s.gK(), s.Nq));
   w.hilo = o;
   if (stage1_mfma_ok(s)) o += align256(static_cast<size_t>(s.BH()) * geo.R * s.D * 4);  // bf16 hi + lo per value
   w.total = o;
