@@ -100,7 +100,7 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
   constexpr int LPC = kBwdCols + 8;  // padded P^T / dS^T row (bf16, one row per key)
   constexpr int LQC = D + 8;         // padded q / do row (bf16, one row per column)
   constexpr bool KT = bwd_kt(C, D);
-  extern __shared__ uint16_t lds[];
+  extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* kl = lds;                                   // [C][LDK]
   uint16_t* vl = kl + C * LDK;                          // [C][LDK]
   uint16_t* kt = vl + C * LDK;                          // [D][LKT] K^T, two keys per word (if KT)

@@ -27,7 +27,7 @@ struct BsaArgs {
 template <typename T, int D, int GMAX>
 __global__ __launch_bounds__(64) void bsa_rows_kernel(BsaArgs a) {
   constexpr int DPL = D / 16;
-  extern __shared__ float sc[];  // [M1] scores, then [K] output scratch (as int)
+  extern __shared__ __align__(16) float sc[];  // [M1] scores, then [K] output scratch (as int)
   int* outl = reinterpret_cast<int*>(sc + a.M1);
   const int lane = threadIdx.x;
   const int grp = lane >> 4, sub = lane & 15;
@@ -257,7 +257,7 @@ __global__ __launch_bounds__(256, 2) void bsa_mfma_kernel(BsaArgs a, const uint1
   constexpr int LDS_ROW = D + 8;
   constexpr int CAP = 32;                      // blocks collected per query in the second scan
   constexpr int PRE = 2 * 64 * (D / 8) / 256;  // 16-byte staging loads per thread per chunk
-  extern __shared__ uint16_t lds[];
+  extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* shi = lds;                   // [64][LDS_ROW]
   uint16_t* slo = lds + 64 * LDS_ROW;    // [64][LDS_ROW]
   float* hred = reinterpret_cast<float*>(lds);  // pass-1 merge (over the chunk area and beyond)

@@ -68,7 +68,7 @@ template <typename T, int D>
 __global__ __launch_bounds__(256) void pool_leaf_kernel(const T* __restrict__ k, float* __restrict__ pyr,
                                                         Geo geo, int s_levels, int lpb) {
   constexpr int DPL = D / 16;
-  extern __shared__ float lds[];  // two buffers of LPB * D floats
+  extern __shared__ __align__(16) float lds[];  // two buffers of LPB * D floats
   float* buf0 = lds;
   float* buf1 = lds + lpb * D;
 
@@ -144,7 +144,7 @@ __global__ __launch_bounds__(256) void pool_top_kernel(float* __restrict__ pyr, 
 // the level-by-level chain does not wait on global memory; used when the two
 // largest levels fit the dynamic LDS.  Same arithmetic, same results.
 __global__ __launch_bounds__(1024) void pool_top_lds_kernel(float* __restrict__ pyr, Geo geo, int first_level, int D) {
-  extern __shared__ float lds[];
+  extern __shared__ __align__(16) float lds[];
   const int bh = blockIdx.x;
   float* pb = pyr + static_cast<int64_t>(bh) * geo.R * D;
   float* src = lds;
@@ -219,7 +219,7 @@ template <typename T, int D>
 __global__ __launch_bounds__(256) void pool_append_path_kernel(const T* __restrict__ k, float* __restrict__ pyr,
                                                                Geo geo) {
   constexpr int DPL = D / 16;
-  extern __shared__ float lds[];  // [D] changed child, then per level (g - 1) x D siblings
+  extern __shared__ __align__(16) float lds[];  // [D] changed child, then per level (g - 1) x D siblings
   float* val = lds;
   float* sib = lds + D;
   const int bh = blockIdx.x;

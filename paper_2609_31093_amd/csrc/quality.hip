@@ -40,7 +40,7 @@ __global__ __launch_bounds__(256) void quality_mass_kernel(QualityArgs a, const 
   constexpr int LDK = D + 8;
   constexpr int C = CT * 32;
   constexpr int MT = C / 16;
-  __shared__ uint16_t klds[C * LDK];
+  __shared__ __align__(16) uint16_t klds[C * LDK];
   __shared__ int cmax_w[4];
 
   const int bh = blockIdx.z;
@@ -155,7 +155,7 @@ __global__ __launch_bounds__(256) void quality_rank_kernel(QualityArgs a, const 
                                                            const int32_t* __restrict__ rows,
                                                            const float* __restrict__ mass,
                                                            float* __restrict__ metrics, int32_t* __restrict__ ref) {
-  extern __shared__ float P[];                                  // [M1] grouped mass
+  extern __shared__ __align__(16) float P[];                                  // [M1] grouped mass
   uint8_t* taken = reinterpret_cast<uint8_t*>(P + a.M1);        // [M1] in the reference set
   __shared__ float sv[4];
   __shared__ int si[4];

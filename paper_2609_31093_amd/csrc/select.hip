@@ -332,7 +332,7 @@ __global__ __launch_bounds__(256) void select_kernel(SelArgs a, int lds_words) {
   constexpr int NGRP = TEAM / 16;
   constexpr int NW = TEAM / 64;
   constexpr int ROWS = 256 / TEAM;
-  extern __shared__ int lds_i[];
+  extern __shared__ __align__(16) int lds_i[];
   const Geo& geo = a.geo;
   const int gK = a.gK;
   const int g = geo.g;
@@ -958,7 +958,7 @@ __global__ __launch_bounds__(kUnionWaves * 64) void stage1_union_kernel(SelArgs 
   constexpr int CPT = 16 / GC;  // union candidates per 16-row tile
   constexpr int R = kUnionRows;
   constexpr int UMAX = R * 128;
-  extern __shared__ int lds_u[];
+  extern __shared__ __align__(16) int lds_u[];
   const Geo& geo = a.geo;
   const int G = a.G, K = a.K, gK = a.gK;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -1231,7 +1231,7 @@ __global__ __launch_bounds__(256) void stage1_pair_kernel(SelArgs a, int row_wor
   constexpr int NCH = DPL / 4;      // 16-byte chunks per lane
   constexpr int NG = 32 / LPE;      // lane groups per half
   constexpr int UNR = DPL >= 32 ? 1 : (32 / DPL > 4 ? 4 : 32 / DPL);
-  extern __shared__ int lds_i[];
+  extern __shared__ __align__(16) int lds_i[];
   const Geo& geo = a.geo;
   const int g = geo.g, G = a.G, K = a.K, gK = a.gK;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -1665,7 +1665,7 @@ __global__ __launch_bounds__(NWAVE * 64) void stage1_g2_kernel(SelArgs a) {
   // coarsest down, whose eligible prefix (for the last row, plus one row for
   // the second child of the last eligible node) still fits the budget; each
   // row then reads them from LDS instead of through the L1 data path.
-  extern __shared__ float stg[];
+  extern __shared__ __align__(16) float stg[];
   int stage_lo = 1 << 30, stage_hi = -1;  // staged levels [stage_lo, stage_hi]
   auto stage_rows = [&](int cl, int lb) {
     const int e = a.causal ? anc_at(geo, cl, lb) + 2 : geo.M[lb];
@@ -1825,7 +1825,7 @@ __global__ __launch_bounds__(256) void leaf_score_kernel(LeafArgs a, const uint1
                                                          float* __restrict__ u1) {
   constexpr int LDR = D + 8;  // padded LDS row, in bf16 elements
   constexpr int KS = D / 16;
-  extern __shared__ uint16_t klds[];
+  extern __shared__ __align__(16) uint16_t klds[];
   int64_t cl;
   int beg, end;
   if (!cluster_chunk(offs, toffs, ncl, blockIdx.x, kLeafChunk, cl, beg, end)) return;
@@ -1920,7 +1920,7 @@ __global__ __launch_bounds__(256, KIND == kScoreLse ? 5 : 1) void leaf_parent_ke
                                                           float* __restrict__ u1) {
   constexpr int LDR = D + 8;
   constexpr int KS = D / 16;
-  extern __shared__ uint16_t klds[];
+  extern __shared__ __align__(16) uint16_t klds[];
   int64_t cl;
   int beg, end;
   if (!cluster_chunk(offs, toffs, ncl, blockIdx.x, kLeafChunk, cl, beg, end)) return;
@@ -2189,7 +2189,7 @@ __global__ __launch_bounds__(256) void stage1_row_kernel(SelArgs a) {
   constexpr int UNR = 4;  // child rows per 16-lane group in flight: 64 per round
   __shared__ int s_cand[64];
   __shared__ int s_n;
-  extern __shared__ float s_z[];  // [candidate * g + child][head], g*K*g*G floats
+  extern __shared__ __align__(16) float s_z[];  // [candidate * g + child][head], g*K*g*G floats
   const Geo& geo = a.geo;
   const int g = geo.g, G = a.G, K = a.K;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
