@@ -312,6 +312,9 @@ def main():
     ap.add_argument("--cold-steps", type=int, default=5,
                     help="further steps timed one by one after a cache-evicting write (0: none)")
     ap.add_argument("--no-bsa", action="store_true")
+    ap.add_argument("--union-min-tiles", type=int, default=None,
+                    help="row-tile union threshold of the attention (pisa_attn_union_min_tiles; "
+                         "negative: off); default: the library's")
     ap.add_argument("--sweep", default="",
                     help="comma-separated N values: time PISA selection and flat-BSA selection "
                          "(each including pooling) at every N with the workload's other shapes, "
@@ -350,6 +353,8 @@ def main():
         log(f"[bench] cpu baseline: {cpu['value']:.1f} tokens/s on {cpu['cores']} cores")
 
     from paper_2609_31093_amd import pisa
+    if args.union_min_tiles is not None:
+        pisa.pisa_attn_union_min_tiles(args.union_min_tiles)
 
     torch.cuda.set_device(0)
     tdt = torch.bfloat16 if w["dtype"] == "bf16" else torch.float32

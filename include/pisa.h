@@ -234,6 +234,17 @@ int pisa_sparse_attn_fwd(const pisa_problem* p, const void* q, const void* k, co
                          const int32_t* block_idx, void* o, float* lse, void* ws,
                          size_t ws_bytes, pisa_stream_t stream);
 
+/* Tuning of pisa_sparse_attn_fwd's row-tile path (same results either way, up
+ * to fp32 rounding order).  A row tile is 256/G consecutive query rows of one
+ * (batch, KV head); when the blocks its rows select number at most
+ * min(3K, 256), the whole tile can be attended by one workgroup that walks
+ * those blocks once, instead of by the block-centric kernels.  That path is
+ * taken, on calls with G in {1, 2, 4, 8, 16}, only when at least n tiles of
+ * the call qualify (so that it fills the device); n < 0 turns it off.
+ * Process-wide, read at each call's launch; default 1024.  Returns the
+ * previous value.  Host only: no device work. */
+int pisa_attn_union_min_tiles(int32_t n);
+
 /* Backward of the selected sparse attention with the block indices held
  * fixed (App. B: during backpropagation gradients flow through the attention
  * over the selected entries, not through the selection).  For every row and

@@ -9,6 +9,7 @@
 // end.  Outputs: o in the input dtype (round to nearest even for bf16), lse in
 // natural log.
 #include <algorithm>
+#include <atomic>
 
 #include "common.h"
 #include "kernels.h"
@@ -193,7 +194,15 @@ struct AttnBlockArgs {
   int row0, nrows;  // row chunk handled by this launch
   float qscale2;
   int Nkv;          // rows per (batch, KV head) in k and v
+  // rows attended by the row-tile union kernel (flag per tile of
+  // 1 << skip_shift rows); the block-centric kernels leave them alone
+  const uint8_t* skip = nullptr;
+  int skip_shift = 0, skip_tiles = 0;
 };
+
+__device__ __forceinline__ bool union_row(const AttnBlockArgs& a, int bh, int row) {
+  return a.skip && a.skip[static_cast<int64_t>(bh) * a.skip_tiles + (row >> a.skip_shift)];
+}
 
 __device__ __forceinline__ bf16x8a u4_as_bf16x8(uint4 r) { return __builtin_bit_cast(bf16x8a, r); }
 
@@ -216,7 +225,7 @@ __global__ __launch_bounds__(NW * 64, (CT >= 3 ? 1 : NW == 8 ? 4 : 3)) void attn
   constexpr int LDV = C + 4;       // padded V^T row
   constexpr int DT = D / 16;       // 16-row d tiles of O
   constexpr int TBS = D + 8;       // padded row of the partial transposition buffer
-  extern __shared__ uint16_t lds[];
+  extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* klds = lds;
   uint16_t* vt = lds + C * LDK;
   uint32_t* vt32 = reinterpret_cast<uint32_t*>(vt);
@@ -462,7 +471,7 @@ __global__ __launch_bounds__(NWL * 64, NWL == 8 ? 2 : 3) void attn_local_kernel(
   constexpr int NPASS = (QG + NWL - 1) / NWL;  // groups per wavefront
   constexpr int DPL = D / 16;            // merge: elements per lane
   constexpr int SROW = D + 4;            // merge: padded state row (floats)
-  extern __shared__ uint16_t lds[];
+  extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* klds = lds;
   uint16_t* vt = lds + C * LDK;
   uint32_t* vt32 = reinterpret_cast<uint32_t*>(vt);
@@ -473,6 +482,18 @@ __global__ __launch_bounds__(NWL * 64, NWL == 8 ? 2 : 3) void attn_local_kernel(
   const int c = (tq0 + a.row0) / C + static_cast<int>(blockIdx.x);
   const int p_lo = max(c * C, tq0 + a.row0), p_hi = min((c + 1) * C, tq0 + a.row0 + a.nrows);
   if (p_lo >= p_hi) return;
+  // rows attended by the row-tile union kernel: bit t - t_lo of umask for
+  // the block's tiles t_lo.. (at most C / 16 + 1 <= 9 of them)
+  uint32_t umask = 0;
+  int t_lo = 0;
+  if (a.skip) {
+    t_lo = (p_lo - tq0) >> a.skip_shift;
+    const int t_hi = (p_hi - 1 - tq0) >> a.skip_shift;
+    for (int t = t_lo; t <= t_hi; ++t)
+      umask |= (a.skip[static_cast<int64_t>(bh) * a.skip_tiles + t] ? 1u : 0u) << (t - t_lo);
+    if (umask == (2u << (t_hi - t_lo)) - 1u) return;  // every row of the block
+  }
+  auto urow = [&](int row) { return ((umask >> ((row >> a.skip_shift) - t_lo)) & 1u) != 0u; };
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int col = lane & 15, grp = lane >> 4;
   int sb[3];
@@ -484,7 +505,7 @@ __global__ __launch_bounds__(NWL * 64, NWL == 8 ? 2 : 3) void attn_local_kernel(
   for (int it = 0; it < NPASS * a.G; ++it) {
     const int hh = it / NPASS, qg = (it - hh * NPASS) * NWL + wave;
     const int p = c * C + qg * 16 + col;  // this lane's query position
-    const bool vq = qg < QG && p >= p_lo && p < p_hi;
+    const bool vq = qg < QG && p >= p_lo && p < p_hi && !urow(p - tq0);
     const int rowq = vq ? p - tq0 : p_lo - tq0;  // a row of the tile for lanes without a query
     const int32_t* sel = idx + (static_cast<int64_t>(bh) * a.Nq + rowq) * a.K;
     // which shared blocks this row selected (each of the 4 lanes of a column
@@ -619,7 +640,7 @@ __global__ __launch_bounds__(NWL * 64, NWL == 8 ? 2 : 3) void attn_local_kernel(
 #pragma unroll
     for (int r4 = 0; r4 < 4; ++r4) {
       const int pr = c * C + qg * 16 + r4 * 4 + grp;
-      const bool v4 = pr >= p_lo && pr < p_hi;
+      const bool v4 = pr >= p_lo && pr < p_hi && !urow(pr - tq0);
       const int32_t* sl = idx + (static_cast<int64_t>(bh) * a.Nq + (v4 ? pr - tq0 : p_lo - tq0)) * a.K;
       selA[r4] = (v4 && sub < a.K) ? sl[sub] : -1;
       selB[r4] = (v4 && sub + 16 < a.K) ? sl[sub + 16] : -1;
@@ -636,7 +657,7 @@ __global__ __launch_bounds__(NWL * 64, NWL == 8 ? 2 : 3) void attn_local_kernel(
     for (int r4 = 0; r4 < 4; ++r4) {
       const int rl = r4 * 4 + grp;  // row of the wavefront's 16
       const int pr = c * C + qg * 16 + rl;
-      const bool v4 = pr >= p_lo && pr < p_hi;
+      const bool v4 = pr >= p_lo && pr < p_hi && !urow(pr - tq0);
       const int rowm = v4 ? pr - tq0 : p_lo - tq0;
       const int64_t pb = (static_cast<int64_t>(bh) * a.nrows + (rowm - a.row0)) * a.K;
       float mm = st[16 * SROW + rl], ll = st[16 * SROW + 16 + rl];
@@ -714,6 +735,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnBlockArgs a, cons
   const int hk = hq / a.G, hh = hq - hk * a.G;
   const int bh = b * a.Hkv + hk;
   const int row = a.row0 + rr;
+  if (union_row(a, bh, row)) return;  // written by the row-tile union kernel
   const int32_t* sel = idx + (static_cast<int64_t>(bh) * a.Nq + row) * a.K;
   const int64_t orow = (static_cast<int64_t>(b) * a.H + hq) * a.Nq + row;
   float m = -INFINITY, s = 0.f, acc[DPL];
@@ -766,6 +788,422 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnBlockArgs a, cons
   }
 }
 
+// ----------------------------------------------------------------------------
+// Row-tile union attention, for selections where neighbouring query rows pick
+// mostly the same blocks (slowly drifting queries and keys).  A tile is
+// T = 256 / G consecutive rows of one (batch, KV head); its columns are the
+// (row, head) pairs, 16 per v_mfma_f32_16x16x32_bf16 column group, two groups
+// per wavefront, eight wavefronts per workgroup.  attn_union_plan_kernel
+// counts the distinct blocks the tile selects (its union U) and flags the
+// tile when |U| <= ulimit.  attn_union_kernel then walks U (ascending) once
+// per flagged tile: each block's keys and values are staged in LDS (the next
+// block's are loaded into registers meanwhile) and every column group one of
+// whose rows selected the block runs the online softmax over it (a column
+// masks the block off when its row did not select it, and the keys after its
+// position when causal).  o and lse are written directly: no partials.  The
+// block-centric kernels skip the rows of flagged tiles.
+// ----------------------------------------------------------------------------
+constexpr int kUnionWaves = 8;
+constexpr int kUnionGroups = 2;   // 16-column groups per wavefront
+constexpr int kUnionCols = kUnionWaves * kUnionGroups * 16;
+constexpr int kUnionMaxU = 256;   // union limit: at most min(3K, 256) blocks
+// Fewest flagged tiles the union kernel takes: four per CU of the 256-CU
+// device, so that its persistent grid (two workgroups per CU) runs at least
+// two rounds of tiles.
+constexpr int kUnionMinTiles = 1024;
+// Process-wide threshold (pisa_attn_union_min_tiles); negative: union kernel off.
+static std::atomic<int> g_union_min_tiles{kUnionMinTiles};
+
+// One workgroup of 256 threads per tile: |U| against ulimit.  The union of
+// four rows spread over the tile is counted first: when it already exceeds
+// ulimit, so does U, and the other rows are not read.
+__global__ __launch_bounds__(256) void attn_union_plan_kernel(AttnBlockArgs a, const int32_t* __restrict__ idx,
+                                                              uint8_t* __restrict__ flag, int T, int ulimit) {
+  extern __shared__ __align__(16) uint32_t bits[];  // [ceil(M1 / 32)]
+  __shared__ int s_cnt[2];
+  const int tid = threadIdx.x, tile = blockIdx.x, bh = blockIdx.y;
+  const int MW = (a.M1 + 31) / 32;
+  for (int e = tid; e < MW; e += 256) bits[e] = 0;
+  if (tid < 2) s_cnt[tid] = 0;
+  __syncthreads();
+  const int r0 = tile * T;
+  const int nr = min(T, a.Nq - r0);
+  const int32_t* lst = idx + (static_cast<int64_t>(bh) * a.Nq + r0) * a.K;
+  auto mark = [&](int e) {
+    const int x = lst[e];
+    if (x >= 0 && x < a.M1) atomicOr(&bits[x >> 5], 1u << (x & 31));
+  };
+  auto count = [&](int* dst) {
+    int c = 0;
+    for (int e = tid; e < MW; e += 256) c += __builtin_popcount(bits[e]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off);
+    if ((tid & 63) == 0) atomicAdd(dst, c);
+    __syncthreads();
+    return *dst;
+  };
+  // rows 0, nr/3, 2nr/3 and nr-1 (repeats are harmless: the bits are idempotent)
+  for (int e = tid; e < 4 * a.K; e += 256) {
+    const int j = e / a.K, row = j == 3 ? nr - 1 : j * nr / 3;
+    mark(row * a.K + e - j * a.K);
+  }
+  __syncthreads();
+  int u = count(&s_cnt[0]);
+  if (u <= ulimit) {
+    for (int e = tid; e < nr * a.K; e += 256) mark(e);
+    __syncthreads();
+    u = count(&s_cnt[1]);
+  }
+  if (tid == 0) flag[static_cast<int64_t>(bh) * a.skip_tiles + tile] = u <= ulimit ? 1 : 0;
+}
+
+// One workgroup of 1024 threads, four flags per thread per pass.  Fewer than
+// min_tiles flagged tiles would leave most of the chip idle behind a few
+// long tiles: their flags are cleared (the block-centric kernels then take
+// those rows) and the count is zero.  Otherwise the flagged tiles' ids
+// (bh * tiles + tile), ascending, and their count, for the union kernel's
+// persistent grid.
+__global__ __launch_bounds__(1024) void attn_union_compact_kernel(uint8_t* __restrict__ flag, int n, int min_tiles,
+                                                                  int32_t* __restrict__ list,
+                                                                  int32_t* __restrict__ count) {
+  __shared__ int wsum[16];
+  __shared__ int s_total;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  auto flags4 = [&](int i) -> uint32_t {  // flags i..i+3 as bytes (flag is 256-byte aligned)
+    if (i + 3 < n) return *reinterpret_cast<const uint32_t*>(flag + i);
+    uint32_t x = 0;
+    for (int j = 0; j < 4 && i + j < n; ++j) x |= static_cast<uint32_t>(flag[i + j]) << (8 * j);
+    return x;
+  };
+  int c = 0;
+  for (int i = 4 * tid; i < n; i += 4096) c += __builtin_popcount(flags4(i));
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) c += __shfl_xor(c, off);
+  if (tid == 0) s_total = 0;
+  __syncthreads();
+  if (lane == 0) atomicAdd(&s_total, c);
+  __syncthreads();
+  const int total = s_total;
+  if (total < min_tiles) {
+    for (int i = 4 * tid; i < n; i += 4096) {
+      if (i + 3 < n) *reinterpret_cast<uint32_t*>(flag + i) = 0u;
+      else for (int j = 0; i + j < n; ++j) flag[i + j] = 0;
+    }
+    if (tid == 0) *count = 0;
+    return;
+  }
+  int base = 0;
+  for (int c0 = 0; c0 < n; c0 += 4096) {
+    const int i = c0 + 4 * tid;
+    const uint32_t x = i < n ? flags4(i) : 0u;
+    const int mine = __builtin_popcount(x);
+    int inc = mine;  // inclusive scan over the wavefront
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(inc, off);
+      if (lane >= off) inc += y;
+    }
+    if (lane == 63) wsum[w] = inc;
+    __syncthreads();
+    int pre = 0, tot = 0;
+    for (int j = 0; j < 16; ++j) {
+      pre += j < w ? wsum[j] : 0;
+      tot += wsum[j];
+    }
+    int pos = base + pre + inc - mine;
+    for (int j = 0; j < 4; ++j)
+      if ((x >> (8 * j)) & 1u) list[pos++] = i + j;
+    base += tot;
+    __syncthreads();  // wsum is rewritten by the next chunk
+  }
+  if (tid == 0) *count = base;
+}
+
+template <int D, int CT, int G>
+__global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
+    AttnBlockArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
+    const int32_t* __restrict__ idx, uint16_t* __restrict__ o, float* __restrict__ lse,
+    const int32_t* __restrict__ tile_list, const int32_t* __restrict__ tile_count) {
+  constexpr int NW = kUnionWaves, NG = kUnionGroups;
+  constexpr int RW = 16 * NG / G, T = NW * RW;  // rows per wavefront, per tile
+  constexpr int KS = D / 32;
+  constexpr int LDK = D + 8;
+  constexpr int C = CT * 32;
+  constexpr int MT = C / 16;
+  constexpr int MC = (D == 128 && MT > 4) ? 2 : (MT <= 6 ? MT : 4);  // 16-key tiles per softmax chunk
+  static_assert(MT % MC == 0 && MC % 2 == 0, "blocks of 32, 64, 96 or 128 keys");
+  constexpr int LDV = C + 8;  // V^T row: 8-byte reads of a 16 x 4 lane tile hit distinct banks
+  constexpr int DT = D / 16;
+  constexpr int MWU = kUnionMaxU / 32;  // row-mask words
+  constexpr int KU = C * (D / 8);       // uint4 of keys per block
+  constexpr int VU = (C / 2) * (D / 8); // key pairs x 8 columns of values per block
+  constexpr int KPT = (KU + NW * 64 - 1) / (NW * 64), VPT = (VU + NW * 64 - 1) / (NW * 64);
+  extern __shared__ __align__(16) uint16_t lds[];
+  uint16_t* klds = lds;
+  uint16_t* vt = lds + C * LDK;
+  uint32_t* vt32 = reinterpret_cast<uint32_t*>(vt);
+  uint32_t* bitmap = reinterpret_cast<uint32_t*>(vt + D * LDV);  // [ceil(M1 / 32)]
+  const int MW = (a.M1 + 31) / 32;
+  int* wpre = reinterpret_cast<int*>(bitmap + MW);                // [MW] set bits before word w
+  int* ulist = wpre + MW;                                         // [kUnionMaxU] union, ascending
+  uint32_t* rmask = reinterpret_cast<uint32_t*>(ulist + kUnionMaxU);  // [T][MWU] row j selected U[u]
+  __shared__ int s_nu;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ntile = *tile_count;
+  // persistent workgroups over the flagged tiles
+  for (int li = blockIdx.x; li < ntile; li += gridDim.x) {
+  const int id = tile_list[li];
+  const int bh = id / a.skip_tiles, tile = id - bh * a.skip_tiles;
+  const int b = bh / a.Hkv, h = bh - b * a.Hkv;
+  const int r0 = tile * T;
+  const int32_t* lst = idx + static_cast<int64_t>(bh) * a.Nq * a.K;
+
+  __syncthreads();  // the previous tile's readers of the LDS are done
+  for (int e = tid; e < MW; e += NW * 64) bitmap[e] = 0;
+  for (int e = tid; e < T * MWU; e += NW * 64) rmask[e] = 0;
+  __syncthreads();
+  for (int e = tid; e < T * a.K; e += NW * 64) {
+    const int row = r0 + e / a.K;
+    if (row >= a.Nq) continue;
+    const int x = lst[static_cast<int64_t>(row) * a.K + e % a.K];
+    if (x >= 0 && x < a.M1) atomicOr(&bitmap[x >> 5], 1u << (x & 31));
+  }
+  __syncthreads();
+  if (wave == 0) {
+    const int per = (MW + 63) / 64;
+    const int w0 = min(MW, lane * per), w1 = min(MW, w0 + per);
+    int cnt = 0;
+    for (int w = w0; w < w1; ++w) cnt += __builtin_popcount(bitmap[w]);
+    int x = cnt;  // inclusive scan over the wavefront
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int y = __shfl_up(x, off);
+      if (lane >= off) x += y;
+    }
+    int run = x - cnt;
+    for (int w = w0; w < w1; ++w) {
+      wpre[w] = run;
+      run += __builtin_popcount(bitmap[w]);
+    }
+    if (lane == 63) s_nu = min(x, kUnionMaxU);  // the plan kernel flagged |U| <= ulimit <= kUnionMaxU
+  }
+  __syncthreads();
+  const int nu = s_nu;
+  for (int w = tid; w < MW; w += NW * 64) {
+    uint32_t bm = bitmap[w];
+    int pos = wpre[w];
+    while (bm && pos < kUnionMaxU) {
+      ulist[pos++] = w * 32 + __builtin_ctz(bm);
+      bm &= bm - 1;
+    }
+  }
+  for (int e = tid; e < T * a.K; e += NW * 64) {
+    const int j = e / a.K, row = r0 + j;
+    if (row >= a.Nq) continue;
+    const int x = lst[static_cast<int64_t>(row) * a.K + e % a.K];
+    if (x < 0 || x >= a.M1) continue;
+    const int u = wpre[x >> 5] + __builtin_popcount(bitmap[x >> 5] & ((1u << (x & 31)) - 1u));
+    if (u < kUnionMaxU) atomicOr(&rmask[j * MWU + (u >> 5)], 1u << (u & 31));
+  }
+
+  // this lane's columns: group cg holds row j = wave * RW + (cg * 16 + col) / G,
+  // head (cg * 16 + col) % G
+  const int col = lane & 15, grp = lane >> 4;
+  int jr[NG], tq[NG];
+  bool vrow[NG];
+  bf16x8a qb[NG][KS];
+  float m[NG], l[NG];
+  f32x4a oacc[NG][DT];
+#pragma unroll
+  for (int cg = 0; cg < NG; ++cg) {
+    const int cc = cg * 16 + col;
+    jr[cg] = wave * RW + cc / G;
+    const int row = r0 + jr[cg];
+    vrow[cg] = row < a.Nq;
+    const int rowc = vrow[cg] ? row : a.Nq - 1;
+    tq[cg] = a.N - a.Nq + rowc;
+    const uint16_t* qrow = q + ((static_cast<int64_t>(b) * a.H + h * G + cc % G) * a.Nq + rowc) * D + grp * 8;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) qb[cg][ks] = u4_as_bf16x8(*reinterpret_cast<const uint4*>(qrow + ks * 32));
+    m[cg] = -INFINITY;
+    l[cg] = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) oacc[cg][dt] = f32x4a{0.f, 0.f, 0.f, 0.f};
+  }
+
+  // staging registers: keys row-major, values as key pairs for the transpose
+  uint4 pk[KPT], pv0[VPT], pv1[VPT];
+  auto load = [&](int blk) __attribute__((always_inline)) {
+    const int rb = blk * C;
+    const int nkeys = min(C, a.N - rb);
+    const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.Nkv + rb) * D;
+    const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.Nkv + rb) * D;
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int e = tid + i * NW * 64;
+      const int r = e / (D / 8), c8 = (e % (D / 8)) * 8;
+      pk[i] = make_uint4(0, 0, 0, 0);
+      if (e < KU && r < nkeys) pk[i] = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int e = tid + i * NW * 64;
+      const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
+      pv0[i] = make_uint4(0, 0, 0, 0);
+      pv1[i] = make_uint4(0, 0, 0, 0);
+      if (e < VU && 2 * kp < nkeys) pv0[i] = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp) * D + c8);
+      if (e < VU && 2 * kp + 1 < nkeys)
+        pv1[i] = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp + 1) * D + c8);
+    }
+  };
+  auto store = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int e = tid + i * NW * 64;
+      const int r = e / (D / 8), c8 = (e % (D / 8)) * 8;
+      if (e < KU) *reinterpret_cast<uint4*>(klds + r * LDK + c8) = pk[i];
+    }
+#pragma unroll
+    for (int i = 0; i < VPT; ++i) {
+      const int e = tid + i * NW * 64;
+      const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
+      if (e >= VU) continue;
+      const uint32_t w0[4] = {pv0[i].x, pv0[i].y, pv0[i].z, pv0[i].w};
+      const uint32_t w1[4] = {pv1[i].x, pv1[i].y, pv1[i].z, pv1[i].w};
+#pragma unroll
+      for (int x = 0; x < 4; ++x) {
+        vt32[(c8 + 2 * x) * (LDV / 2) + kp] = (w0[x] & 0xFFFFu) | (w1[x] << 16);
+        vt32[(c8 + 2 * x + 1) * (LDV / 2) + kp] = (w0[x] >> 16) | (w1[x] & 0xFFFF0000u);
+      }
+    }
+  };
+
+  __syncthreads();  // ulist and rmask complete
+  for (int u = 0; u < nu; ++u) {
+    const int blk = ulist[u];
+    const int rb = blk * C;
+    const int nkeys = min(C, a.N - rb);
+    load(blk);
+    __syncthreads();  // the previous block's readers are done
+    store();
+    __syncthreads();
+    // Both column groups take every staged operand read: K and V^T tiles are
+    // read from LDS once per wavefront and feed one product per group.
+    int kmax[NG];
+    bool any = false;
+#pragma unroll
+    for (int cg = 0; cg < NG; ++cg) {
+      const bool sel = vrow[cg] && ((rmask[jr[cg] * MWU + (u >> 5)] >> (u & 31)) & 1u);
+      kmax[cg] = !sel ? 0 : (a.causal ? min(nkeys, tq[cg] - rb + 1) : nkeys);
+      any = any || sel;
+    }
+    if (__ballot(any) == 0) continue;  // none of the wavefront's rows selected the block
+    // keys in chunks of 64 (online softmax per chunk) to bound the registers
+#pragma unroll
+    for (int k0 = 0; k0 < MT; k0 += MC) {
+      f32x4a sa[NG][MC];
+#pragma unroll
+      for (int mt = 0; mt < MC; ++mt) {
+        f32x4a acc[NG];
+#pragma unroll
+        for (int cg = 0; cg < NG; ++cg) acc[cg] = f32x4a{0.f, 0.f, 0.f, 0.f};
+        const uint16_t* arow = klds + ((k0 + mt) * 16 + col) * LDK + grp * 8;
+        bf16x8a av[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) av[ks] = u4_as_bf16x8(*reinterpret_cast<const uint4*>(arow + ks * 32));
+        __builtin_amdgcn_sched_barrier(0);  // the reads leave together; the products wait for them in turn
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+          for (int cg = 0; cg < NG; ++cg)
+            acc[cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[ks], qb[cg][ks], acc[cg], 0, 0, 0);
+#pragma unroll
+        for (int cg = 0; cg < NG; ++cg) {
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int key = (k0 + mt) * 16 + 4 * grp + i;
+            acc[cg][i] = key < kmax[cg] ? acc[cg][i] * a.qscale2 : -INFINITY;
+          }
+          sa[cg][mt] = acc[cg];
+        }
+      }
+      float msafe[NG];
+#pragma unroll
+      for (int cg = 0; cg < NG; ++cg) {
+        float bm = -INFINITY;
+#pragma unroll
+        for (int mt = 0; mt < MC; ++mt)
+          bm = fmaxf(bm, fmaxf(fmaxf(sa[cg][mt][0], sa[cg][mt][1]), fmaxf(sa[cg][mt][2], sa[cg][mt][3])));
+        bm = fmaxf(bm, __shfl_xor(bm, 16));
+        bm = fmaxf(bm, __shfl_xor(bm, 32));
+        const float mn = fmaxf(m[cg], bm);
+        msafe[cg] = mn == -INFINITY ? 0.f : mn;
+        const float scl = fast_exp2(m[cg] - msafe[cg]);
+        l[cg] *= scl;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) oacc[cg][dt] *= scl;
+        m[cg] = mn;
+      }
+#pragma unroll
+      for (int s2 = 0; s2 < MC / 2; ++s2) {
+        bf16x8a pb[NG];
+#pragma unroll
+        for (int cg = 0; cg < NG; ++cg) {
+          float pv[8];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            pv[i] = fast_exp2(sa[cg][2 * s2][i] - msafe[cg]);
+            pv[4 + i] = fast_exp2(sa[cg][2 * s2 + 1][i] - msafe[cg]);
+          }
+#pragma unroll
+          for (int i = 0; i < 8; ++i) l[cg] += pv[i];
+          uint4 uu;
+          uu.x = pack2_bf16(pv[0], pv[1]);
+          uu.y = pack2_bf16(pv[2], pv[3]);
+          uu.z = pack2_bf16(pv[4], pv[5]);
+          uu.w = pack2_bf16(pv[6], pv[7]);
+          pb[cg] = u4_as_bf16x8(uu);
+        }
+        bf16x8a avv[DT];
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const uint16_t* vr = vt + (dt * 16 + col) * LDV + 4 * grp + 16 * k0 + 32 * s2;
+          const uint2 lo = *reinterpret_cast<const uint2*>(vr);
+          const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
+          avv[dt] = u4_as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int cg = 0; cg < NG; ++cg)
+            oacc[cg][dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(avv[dt], pb[cg], oacc[cg][dt], 0, 0, 0);
+      }
+    }
+  }
+#pragma unroll
+  for (int cg = 0; cg < NG; ++cg) {
+    float ll = l[cg];
+    ll += __shfl_xor(ll, 16);
+    ll += __shfl_xor(ll, 32);
+    if (!vrow[cg]) continue;
+    // oacc[cg][dt][i] = O[d = dt*16 + 4*grp + i][this column]
+    const int cc = cg * 16 + col;
+    const int64_t orow = (static_cast<int64_t>(b) * a.H + h * G + cc % G) * a.Nq + r0 + jr[cg];
+    const float inv = ll > 0.f ? 1.0f / ll : 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      uint2 w;
+      w.x = pack2_bf16(oacc[cg][dt][0] * inv, oacc[cg][dt][1] * inv);
+      w.y = pack2_bf16(oacc[cg][dt][2] * inv, oacc[cg][dt][3] * inv);
+      *reinterpret_cast<uint2*>(o + orow * D + dt * 16 + 4 * grp) = w;
+    }
+    if (lse && grp == 0) lse[orow] = ll > 0.f ? (m[cg] + fast_log2(ll)) * kLn2 : -INFINITY;
+  }
+  }
+}
+
 // Attention for few rows (decode): one workgroup per (row, slot) attends the
 // slot's key block for the G query heads of the KV head and leaves the same
 // partial as attn_block16_kernel (o normalised by its own sum in bf16, the
@@ -781,7 +1219,7 @@ __global__ __launch_bounds__(256) void attn_slot_kernel(AttnBlockArgs a, const u
                                                         float* __restrict__ part_lse) {
   constexpr int DPL = D / 16;
   constexpr int NPART = 256 / D;  // key subsets summed separately in the PV product
-  extern __shared__ uint16_t lds[];
+  extern __shared__ __align__(16) uint16_t lds[];
   const int C = a.C;
   uint16_t* ks = lds;                                          // [C][D]
   uint16_t* vs = lds + C * D;                                  // [C][D]
@@ -925,8 +1363,14 @@ static bool use_split_path(const Shape& s, const Geo& geo) {
 }
 
 struct AttnWs {
-  size_t part_o, part_lse, cl, row_lse, total;
+  size_t part_o, part_lse, cl, row_lse, uflag, ulist, total;
 };
+
+// The row-tile union kernel serves groups of 1, 2, 4, 8 or 16 heads.
+static bool union_ok(const Shape& s) {
+  return s.G == 1 || s.G == 2 || s.G == 4 || s.G == 8 || s.G == 16;
+}
+static int union_tile_rows(const Shape& s) { return kUnionCols / s.G; }
 
 static AttnWs attn_layout(const Shape& s, const Geo& geo) {
   const size_t ch = attn_chunk_rows(s);
@@ -941,6 +1385,13 @@ static AttnWs attn_layout(const Shape& s, const Geo& geo) {
   // merge and the tail merge, for callers that pass no lse
   w.row_lse = o;
   if (s.causal && s.K > 32) o += al(static_cast<size_t>(s.B) * s.H * s.Nq * 4);
+  // one flag per (batch, KV head, row tile) of the row-tile union kernel
+  const size_t ntile = union_ok(s) ? static_cast<size_t>(s.BH()) * ((s.Nq + union_tile_rows(s) - 1) / union_tile_rows(s)) : 0;
+  w.uflag = o;
+  o += al(ntile);
+  // the flagged tiles' ids and their count
+  w.ulist = o;
+  if (ntile) o += al((ntile + 1) * 4);
   w.total = o;
   return w;
 }
@@ -1009,17 +1460,72 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
   if (!lse && s.causal && s.K > 32) lse = reinterpret_cast<float*>(base + w.row_lse);
   const int ch = attn_chunk_rows(s);
   hipError_t e;
+  // Row tiles whose selections share blocks: attended whole by the union
+  // kernel first; the block-centric kernels below skip their rows.
+  const uint8_t* skip = nullptr;
+  int skip_shift = 0, skip_tiles = 0;
+  const int union_min = g_union_min_tiles.load(std::memory_order_relaxed);
+  if (union_ok(s) && union_min >= 0) {
+    const int T = union_tile_rows(s);
+    skip_tiles = (s.Nq + T - 1) / T;
+    while ((1 << skip_shift) < T) ++skip_shift;
+    uint8_t* flag = reinterpret_cast<uint8_t*>(base + w.uflag);
+    int32_t* tlist = reinterpret_cast<int32_t*>(base + w.ulist);
+    int32_t* tcount = tlist + static_cast<int64_t>(s.BH()) * skip_tiles;
+    skip = flag;
+    AttnBlockArgs ua{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], 0, s.Nq,
+                     kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv, nullptr, skip_shift, skip_tiles};
+    const int mw = (geo.M[1] + 31) / 32;
+    const int ulimit = std::min(3 * s.K, kUnionMaxU);
+    dim3 grid(static_cast<unsigned>(skip_tiles), s.BH());
+    {
+      ProfScope ps("attn_union_plan", st);
+      attn_union_plan_kernel<<<grid, 256, static_cast<size_t>(mw) * 4, st>>>(ua, idx, flag, T, ulimit);
+      attn_union_compact_kernel<<<1, 1024, 0, st>>>(flag, s.BH() * skip_tiles, union_min, tlist, tcount);
+      if ((e = hipGetLastError()) != hipSuccess) return e;
+    }
+    // persistent workgroups (at most two per CU are resident)
+    const unsigned ugrid = static_cast<unsigned>(std::min(s.BH() * skip_tiles, 512));
+    const size_t ulds = (static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 8)) * 2 +
+                        (static_cast<size_t>(2) * mw + kUnionMaxU + static_cast<size_t>(T) * (kUnionMaxU / 32)) * 4;
+    ProfScope ps("attn_union", st);
+    auto go = [&](auto kern) {
+      if (ulds > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                  hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(ulds));
+      kern<<<ugrid, kUnionWaves * 64, ulds, st>>>(ua, static_cast<const uint16_t*>(q),
+                                                  static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), idx,
+                                                  static_cast<uint16_t*>(o), lse, tlist, tcount);
+    };
+    auto by_g = [&](auto k1, auto k2, auto k4, auto k8, auto k16) {
+      switch (s.G) {
+        case 1: go(k1); break;
+        case 2: go(k2); break;
+        case 4: go(k4); break;
+        case 8: go(k8); break;
+        default: go(k16); break;
+      }
+    };
+#define PISA_UNION(CT) \
+    by_g(attn_union_kernel<D, CT, 1>, attn_union_kernel<D, CT, 2>, attn_union_kernel<D, CT, 4>, \
+         attn_union_kernel<D, CT, 8>, attn_union_kernel<D, CT, 16>)
+    if (s.C == 32) PISA_UNION(1);
+    else if (s.C == 64) PISA_UNION(2);
+    else if (s.C == 96) PISA_UNION(3);
+    else PISA_UNION(4);
+#undef PISA_UNION
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   for (int row0 = 0; row0 < s.Nq; row0 += ch) {
     const int nrows = std::min(ch, s.Nq - row0);
     // Causal: each row's first, previous and own block are attended per leaf
     // block by attn_local_kernel, which also merges the other partials.
     const bool local = s.causal != 0;
     ClusterArgs ca{idx, nullptr, s.K, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], local ? kClusterAttnFar : kClusterAttn,
-                   row0, nrows, s.g};
+                   row0, nrows, s.g, skip, skip_shift, skip_tiles};
     ClusterOut co{};
     if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st, kAttnChunk)) != hipSuccess) return e;
     AttnBlockArgs a{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], row0, nrows,
-                    kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv};
+                    kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv, skip, skip_shift, skip_tiles};
     {
       ProfScope ps("attn_block", st);
       dim3 grid(static_cast<unsigned>(
@@ -1115,3 +1621,7 @@ hipError_t launch_attention(const Shape& s, const Geo& geo, const void* q, const
 }
 
 }  // namespace pisa
+
+extern "C" int pisa_attn_union_min_tiles(int32_t n) {
+  return pisa::g_union_min_tiles.exchange(n < 0 ? -1 : n);
+}

@@ -29,6 +29,7 @@ __device__ __forceinline__ bool cluster_pair(const ClusterArgs& a, int bh, int r
   // attention lists come from the caller: entries past the last leaf block
   // are padding, like negative ones (the bins cover blocks 0 .. M1-1 only)
   if ((a.mode == kClusterAttn || a.mode == kClusterAttnFar) && blk >= a.M1) return false;
+  if (a.skip && a.skip[static_cast<int64_t>(bh) * a.skip_tiles + ((a.row0 + r) >> a.skip_shift)]) return false;
   if (a.mode == kClusterAttnFar) {
     const int c = (a.N - a.Nq + a.row0 + r) / a.C;
     return !(a.causal && (blk == 0 || blk == c || blk == c - 1));
@@ -60,7 +61,7 @@ __global__ __launch_bounds__(256) void fill_zero_kernel(int32_t* p, int64_t n) {
 
 __global__ __launch_bounds__(kClusterThreads) void cluster_hist_kernel(ClusterArgs a, int32_t* __restrict__ hist,
                                                                        int32_t* __restrict__ chunk_base) {
-  extern __shared__ int32_t h[];
+  extern __shared__ __align__(16) int32_t h[];
   const int bh = blockIdx.y;
   const int r0 = blockIdx.x * kClusterRows;
   const int nr = min(kClusterRows, a.nrows - r0);
@@ -171,7 +172,7 @@ __host__ __device__ __forceinline__ int scan_pad(int i) { return i + (i >> 4); }
 __global__ __launch_bounds__(1024) void cluster_scan_lds_kernel(const int32_t* __restrict__ hist,
                                                                 int32_t* __restrict__ offs,
                                                                 int32_t* __restrict__ toffs, int n, int tile) {
-  extern __shared__ int32_t sh[];
+  extern __shared__ __align__(16) int32_t sh[];
   __shared__ int wsum[16], wtile[16];
   int32_t* ho = sh;                       // counts, then offsets (padded)
   int32_t* ht = sh + scan_pad(n) + 1;     // tile offsets (padded)
@@ -235,7 +236,7 @@ __global__ __launch_bounds__(1024) void cluster_scan_lds_kernel(const int32_t* _
 __global__ __launch_bounds__(kClusterThreads) void cluster_scatter_kernel(ClusterArgs a, const int32_t* __restrict__ offs,
                                                                           const int32_t* __restrict__ chunk_base,
                                                                           int32_t* __restrict__ pairs) {
-  extern __shared__ int32_t h[];
+  extern __shared__ __align__(16) int32_t h[];
   const int bh = blockIdx.y;
   const int r0 = blockIdx.x * kClusterRows;
   const int nr = min(kClusterRows, a.nrows - r0);

@@ -47,6 +47,10 @@ struct ClusterArgs {
   int S, Nq, N, C, K, causal, M1, mode;  // M1: number of bins (leaf blocks, or parents)
   int row0, nrows;      // rows [row0, row0 + nrows) of every (batch, KV head)
   int g;                // fan-out (parent mode)
+  // attention modes: rows whose tile flag is set (skip[bh * skip_tiles +
+  // (row >> skip_shift)]) were attended by the row-tile union kernel
+  const uint8_t* skip = nullptr;
+  int skip_shift = 0, skip_tiles = 0;
 };
 constexpr int kClusterTile = 256;  // pairs per inner tile of the block attention's workgroup chunks
 struct ClusterOut {

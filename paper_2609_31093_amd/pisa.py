@@ -36,7 +36,7 @@ EXPORTS = (
     "pisa_num_levels", "pisa_pyramid_layout", "pisa_pyramid_bytes",
     "pisa_select_workspace_bytes", "pisa_bsa_workspace_bytes", "pisa_attn_workspace_bytes",
     "pisa_build_pyramid", "pisa_pyramid_append", "pisa_cache_capacity", "pisa_cache_grow", "pisa_select", "pisa_select_static", "pisa_select_flat_bsa",
-    "pisa_sparse_attn_fwd",
+    "pisa_sparse_attn_fwd", "pisa_attn_union_min_tiles",
     "pisa_attn_bwd_workspace_bytes", "pisa_sparse_attn_bwd",
     "pisa_quality_workspace_bytes", "pisa_selection_quality",
     "pisa_profile_enable", "pisa_profile_report", "pisa_status_string", "pisa_last_error",
@@ -89,6 +89,7 @@ def _load():
         "pisa_select_static": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp]),
         "pisa_select_flat_bsa": (ctypes.c_int, [P, vp, vp, vp, vp, sz, vp]),
         "pisa_sparse_attn_fwd": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
+        "pisa_attn_union_min_tiles": (ctypes.c_int, [i32]),
         "pisa_attn_bwd_workspace_bytes": (sz, [P]),
         "pisa_sparse_attn_bwd": (ctypes.c_int, [P, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]),
         "pisa_quality_workspace_bytes": (sz, [P, i32]),
@@ -232,6 +233,11 @@ def pisa_selection_quality(p: Problem, q, k, block_idx, rows, n_rows: int, metri
     return _check(_lib.pisa_selection_quality(ctypes.byref(p), _ptr(q), _ptr(k), _ptr(block_idx), _ptr(rows), n_rows,
                                               _ptr(metrics), _ptr(ref_idx), _ptr(ws), ws_bytes, _stream(stream)),
                   "pisa_selection_quality")
+
+
+def pisa_attn_union_min_tiles(n: int) -> int:
+    """Sets the row-tile union threshold of pisa_sparse_attn_fwd (n < 0: off); returns the previous one."""
+    return _lib.pisa_attn_union_min_tiles(int(n))
 
 
 def pisa_profile_enable(on: bool) -> int:
