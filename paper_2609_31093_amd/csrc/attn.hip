@@ -807,6 +807,28 @@ constexpr int kUnionWaves = 8;
 constexpr int kUnionGroups = 2;   // 16-column groups per wavefront
 constexpr int kUnionCols = kUnionWaves * kUnionGroups * 16;
 constexpr int kUnionMaxU = 256;   // union limit: at most min(3K, 256) blocks
+constexpr float kUnionSlack = 8.f;  // log2 units the running maximum may lag behind
+constexpr size_t kUnionMaxLds = 160 * 1024;  // LDS of one CU
+constexpr int kDeviceCUs = 256;
+typedef short v4s16 __attribute__((ext_vector_type(4)));
+// LDS byte address of a pointer into dynamic shared memory, made wave-uniform.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return __builtin_amdgcn_readfirstlane(
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const char*)p)));
+}
+// 16 bytes per lane from global memory straight into LDS at lds + 16 * lane.
+// Issued from inline assembly so that the compiler does not make the next
+// LDS read wait for it (it cannot tell the two stages apart); the consumer
+// waits for it with an explicit vmcnt wait and a barrier.
+__device__ __forceinline__ void lds_dma16(const void* src, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(src), "s"(lds) : "memory", "m0");
+}
+// Chunk-position swizzle of a staged key row (NCH 16-byte chunks per row):
+// the 16 rows of a K operand read get 16 distinct bank positions.
+template <int NCH>
+__device__ __forceinline__ int union_swz(int r) {
+  return NCH == 16 ? (r & 15) : ((r >> 1) & 7);
+}
 // Fewest flagged tiles the union kernel takes: four per CU of the 256-CU
 // device, so that its persistent grid (two workgroups per CU) runs at least
 // two rounds of tiles.
@@ -927,22 +949,23 @@ __global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
   constexpr int NW = kUnionWaves, NG = kUnionGroups;
   constexpr int RW = 16 * NG / G, T = NW * RW;  // rows per wavefront, per tile
   constexpr int KS = D / 32;
-  constexpr int LDK = D + 8;
   constexpr int C = CT * 32;
   constexpr int MT = C / 16;
   constexpr int MC = (D == 128 && MT > 4) ? 2 : (MT <= 6 ? MT : 4);  // 16-key tiles per softmax chunk
   static_assert(MT % MC == 0 && MC % 2 == 0, "blocks of 32, 64, 96 or 128 keys");
-  constexpr int LDV = C + 8;  // V^T row: 8-byte reads of a 16 x 4 lane tile hit distinct banks
   constexpr int DT = D / 16;
   constexpr int MWU = kUnionMaxU / 32;  // row-mask words
-  constexpr int KU = C * (D / 8);       // uint4 of keys per block
-  constexpr int VU = (C / 2) * (D / 8); // key pairs x 8 columns of values per block
-  constexpr int KPT = (KU + NW * 64 - 1) / (NW * 64), VPT = (VU + NW * 64 - 1) / (NW * 64);
+  constexpr int NCH = D / 8;            // 16-byte chunks per key row
+  constexpr int RPI = 64 / NCH;         // key rows per direct-to-LDS load instruction
+  constexpr int BLK = C * D;            // elements of one staged K (or V) block
+  static_assert(D == 64 || D == 128, "head dimension 64 or 128");
+  // Two stages of [K block, V block], both row-major with the 16-byte chunks
+  // of row r stored at chunk position c ^ union_swz<NCH>(r): the K operand
+  // reads (16 rows x one chunk per 16 lanes) and the transposing V reads
+  // (16 rows x 32 bytes per wavefront) then spread over all banks.
   extern __shared__ __align__(16) uint16_t lds[];
-  uint16_t* klds = lds;
-  uint16_t* vt = lds + C * LDK;
-  uint32_t* vt32 = reinterpret_cast<uint32_t*>(vt);
-  uint32_t* bitmap = reinterpret_cast<uint32_t*>(vt + D * LDV);  // [ceil(M1 / 32)]
+  uint16_t* stage = lds;
+  uint32_t* bitmap = reinterpret_cast<uint32_t*>(lds + 4 * BLK);  // [ceil(M1 / 32)]
   const int MW = (a.M1 + 31) / 32;
   int* wpre = reinterpret_cast<int*>(bitmap + MW);                // [MW] set bits before word w
   int* ulist = wpre + MW;                                         // [kUnionMaxU] union, ascending
@@ -1032,73 +1055,64 @@ __global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
     for (int dt = 0; dt < DT; ++dt) oacc[cg][dt] = f32x4a{0.f, 0.f, 0.f, 0.f};
   }
 
-  // staging registers: keys row-major, values as key pairs for the transpose
-  uint4 pk[KPT], pv0[VPT], pv1[VPT];
-  auto load = [&](int blk) __attribute__((always_inline)) {
+  // Block blk's keys and values straight from global memory into stage buf:
+  // each instruction fills RPI rows (lane L: row L / NCH, chunk position
+  // L % NCH, which holds logical chunk (L % NCH) ^ swz(row)).  Rows past the
+  // sequence's end repeat its last row (finite values; their keys are masked).
+  auto issue = [&](int blk, int buf) __attribute__((always_inline)) {
     const int rb = blk * C;
-    const int nkeys = min(C, a.N - rb);
+    const int last = min(C, a.N - rb) - 1;
     const uint16_t* kb = k + (static_cast<int64_t>(bh) * a.Nkv + rb) * D;
     const uint16_t* vb = v + (static_cast<int64_t>(bh) * a.Nkv + rb) * D;
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int e = tid + i * NW * 64;
-      const int r = e / (D / 8), c8 = (e % (D / 8)) * 8;
-      pk[i] = make_uint4(0, 0, 0, 0);
-      if (e < KU && r < nkeys) pk[i] = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int e = tid + i * NW * 64;
-      const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
-      pv0[i] = make_uint4(0, 0, 0, 0);
-      pv1[i] = make_uint4(0, 0, 0, 0);
-      if (e < VU && 2 * kp < nkeys) pv0[i] = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp) * D + c8);
-      if (e < VU && 2 * kp + 1 < nkeys)
-        pv1[i] = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(2 * kp + 1) * D + c8);
+    uint16_t* kd = stage + buf * 2 * BLK;
+    for (int ins = wave; ins < C / RPI; ins += NW) {
+      const int row = ins * RPI + lane / NCH;
+      const int64_t src = static_cast<int64_t>(min(row, last)) * D + ((lane % NCH) ^ union_swz<NCH>(row)) * 8;
+      const uint32_t dk = lds_addr(kd + ins * RPI * D);
+      lds_dma16(kb + src, dk);
+      lds_dma16(vb + src, dk + BLK * 2);
     }
   };
-  auto store = [&]() __attribute__((always_inline)) {
+  // this lane's K operand offsets (elements within a block): row tile*16 + col,
+  // logical chunk 4 ks + grp
+  int koff[KS];
 #pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int e = tid + i * NW * 64;
-      const int r = e / (D / 8), c8 = (e % (D / 8)) * 8;
-      if (e < KU) *reinterpret_cast<uint4*>(klds + r * LDK + c8) = pk[i];
-    }
+  for (int ks = 0; ks < KS; ++ks) koff[ks] = col * D + ((4 * ks + grp) ^ union_swz<NCH>(col)) * 8;
+  // V operand (transposing reads): lane i = col of group grp reads 8 bytes of
+  // row 4 grp + i / 4 (+16 for the second half of a 32-key step) at column
+  // 16 dt + 4 (i % 4)
+  const int vr0 = 4 * grp + col / 4;
+  int voff[DT];
 #pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int e = tid + i * NW * 64;
-      const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
-      if (e >= VU) continue;
-      const uint32_t w0[4] = {pv0[i].x, pv0[i].y, pv0[i].z, pv0[i].w};
-      const uint32_t w1[4] = {pv1[i].x, pv1[i].y, pv1[i].z, pv1[i].w};
-#pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        vt32[(c8 + 2 * x) * (LDV / 2) + kp] = (w0[x] & 0xFFFFu) | (w1[x] << 16);
-        vt32[(c8 + 2 * x + 1) * (LDV / 2) + kp] = (w0[x] >> 16) | (w1[x] & 0xFFFF0000u);
-      }
-    }
-  };
+  for (int dt = 0; dt < DT; ++dt)
+    voff[dt] = vr0 * D + ((2 * dt + (col & 3) / 2) ^ union_swz<NCH>(vr0)) * 8 + (col & 1) * 4;
 
   __syncthreads();  // ulist and rmask complete
+  if (nu > 0) issue(ulist[0], 0);
   for (int u = 0; u < nu; ++u) {
     const int blk = ulist[u];
     const int rb = blk * C;
     const int nkeys = min(C, a.N - rb);
-    load(blk);
-    __syncthreads();  // the previous block's readers are done
-    store();
-    __syncthreads();
+    __builtin_amdgcn_s_waitcnt(0);  // this wavefront's loads of block u have landed
+    __syncthreads();                // every wavefront's have, and block u - 1 is done
+    if (u + 1 < nu) issue(ulist[u + 1], (u + 1) & 1);
+    const uint16_t* klds = stage + (u & 1) * 2 * BLK;
+    const uint16_t* vlds = klds + BLK;
     // Both column groups take every staged operand read: K and V^T tiles are
     // read from LDS once per wavefront and feed one product per group.
     int kmax[NG];
-    bool any = false;
+    bool any = false, full = true;
 #pragma unroll
     for (int cg = 0; cg < NG; ++cg) {
       const bool sel = vrow[cg] && ((rmask[jr[cg] * MWU + (u >> 5)] >> (u & 31)) & 1u);
-      kmax[cg] = !sel ? 0 : (a.causal ? min(nkeys, tq[cg] - rb + 1) : nkeys);
-      any = any || sel;
+      // keys the column sees (0 also for a selected block after its position)
+      kmax[cg] = !sel ? 0 : (a.causal ? max(0, min(nkeys, tq[cg] - rb + 1)) : nkeys);
+      any = any || kmax[cg] > 0;
+      full = full && kmax[cg] == C;
     }
-    if (__ballot(any) == 0) continue;  // none of the wavefront's rows selected the block
+    if (__ballot(any) == 0) continue;  // no column of the wavefront sees a key of the block
+    // every column of the wavefront sees every key of the block: no masking
+    const bool wfull = __ballot(!full) == 0;
     // keys in chunks of 64 (online softmax per chunk) to bound the registers
 #pragma unroll
     for (int k0 = 0; k0 < MT; k0 += MC) {
@@ -1108,43 +1122,64 @@ __global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
         f32x4a acc[NG];
 #pragma unroll
         for (int cg = 0; cg < NG; ++cg) acc[cg] = f32x4a{0.f, 0.f, 0.f, 0.f};
-        const uint16_t* arow = klds + ((k0 + mt) * 16 + col) * LDK + grp * 8;
+        const uint16_t* arow = klds + (k0 + mt) * 16 * D;
         bf16x8a av[KS];
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) av[ks] = u4_as_bf16x8(*reinterpret_cast<const uint4*>(arow + ks * 32));
+        for (int ks = 0; ks < KS; ++ks) av[ks] = u4_as_bf16x8(*reinterpret_cast<const uint4*>(arow + koff[ks]));
         __builtin_amdgcn_sched_barrier(0);  // the reads leave together; the products wait for them in turn
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
 #pragma unroll
           for (int cg = 0; cg < NG; ++cg)
             acc[cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[ks], qb[cg][ks], acc[cg], 0, 0, 0);
+        // raw logits (the log2e / sqrt(d) scale is applied in the exponent)
 #pragma unroll
         for (int cg = 0; cg < NG; ++cg) {
+          if (!wfull) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int key = (k0 + mt) * 16 + 4 * grp + i;
-            acc[cg][i] = key < kmax[cg] ? acc[cg][i] * a.qscale2 : -INFINITY;
+            for (int i = 0; i < 4; ++i) {
+              const int key = (k0 + mt) * 16 + 4 * grp + i;
+              acc[cg][i] = key < kmax[cg] ? acc[cg][i] : -INFINITY;
+            }
           }
           sa[cg][mt] = acc[cg];
         }
       }
-      float msafe[NG];
+      // Online softmax with a lazily raised reference: m only moves (and
+      // the accumulators are rescaled) when the chunk's maximum exceeds it
+      // by more than kUnionSlack, so the exponentials stay below
+      // 2^kUnionSlack; in most chunks no column of the wavefront moves.
+      // Each lane tests its own logits first; only when one of them exceeds
+      // its column's reference does the wavefront reduce the column maxima
+      // across lanes and move the references.
+      float lm[NG];
+      bool over = false;
 #pragma unroll
       for (int cg = 0; cg < NG; ++cg) {
         float bm = -INFINITY;
 #pragma unroll
         for (int mt = 0; mt < MC; ++mt)
           bm = fmaxf(bm, fmaxf(fmaxf(sa[cg][mt][0], sa[cg][mt][1]), fmaxf(sa[cg][mt][2], sa[cg][mt][3])));
-        bm = fmaxf(bm, __shfl_xor(bm, 16));
-        bm = fmaxf(bm, __shfl_xor(bm, 32));
-        const float mn = fmaxf(m[cg], bm);
-        msafe[cg] = mn == -INFINITY ? 0.f : mn;
-        const float scl = fast_exp2(m[cg] - msafe[cg]);
-        l[cg] *= scl;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) oacc[cg][dt] *= scl;
-        m[cg] = mn;
+        lm[cg] = bm * a.qscale2;
+        over = over || lm[cg] > m[cg] + kUnionSlack;
       }
+      if (__ballot(over) != 0) {
+#pragma unroll
+        for (int cg = 0; cg < NG; ++cg) {
+          float bm = lm[cg];
+          bm = fmaxf(bm, __shfl_xor(bm, 16));
+          bm = fmaxf(bm, __shfl_xor(bm, 32));
+          const float nm = bm > m[cg] + kUnionSlack ? bm : m[cg];
+          const float scl = nm != m[cg] ? fast_exp2(m[cg] - nm) : 1.f;
+          l[cg] *= scl;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) oacc[cg][dt] *= scl;
+          m[cg] = nm;
+        }
+      }
+      float nms[NG];  // -m, or 0 while no key was seen (then every logit is -inf)
+#pragma unroll
+      for (int cg = 0; cg < NG; ++cg) nms[cg] = m[cg] == -INFINITY ? 0.f : -m[cg];
 #pragma unroll
       for (int s2 = 0; s2 < MC / 2; ++s2) {
         bf16x8a pb[NG];
@@ -1153,8 +1188,8 @@ __global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
           float pv[8];
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
-            pv[i] = fast_exp2(sa[cg][2 * s2][i] - msafe[cg]);
-            pv[4 + i] = fast_exp2(sa[cg][2 * s2 + 1][i] - msafe[cg]);
+            pv[i] = fast_exp2(fmaf(sa[cg][2 * s2][i], a.qscale2, nms[cg]));
+            pv[4 + i] = fast_exp2(fmaf(sa[cg][2 * s2 + 1][i], a.qscale2, nms[cg]));
           }
 #pragma unroll
           for (int i = 0; i < 8; ++i) l[cg] += pv[i];
@@ -1166,12 +1201,14 @@ __global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
           pb[cg] = u4_as_bf16x8(uu);
         }
         bf16x8a avv[DT];
+        const uint16_t* vr = vlds + (k0 + 2 * s2) * 16 * D;  // keys of tiles 2 s2, 2 s2 + 1 of the chunk
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          const uint16_t* vr = vt + (dt * 16 + col) * LDV + 4 * grp + 16 * k0 + 32 * s2;
-          const uint2 lo = *reinterpret_cast<const uint2*>(vr);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vr + 16);
-          avv[dt] = u4_as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
+          const v4s16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) v4s16*)(vr + voff[dt]));
+          const v4s16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) v4s16*)(vr + 16 * D + voff[dt]));
+          avv[dt] = __builtin_bit_cast(bf16x8a, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         }
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
@@ -1465,7 +1502,15 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
   const uint8_t* skip = nullptr;
   int skip_shift = 0, skip_tiles = 0;
   const int union_min = g_union_min_tiles.load(std::memory_order_relaxed);
-  if (union_ok(s) && union_min >= 0) {
+  const int mw = (geo.M[1] + 31) / 32;
+  // the union kernel's LDS: two stages of a K and a V block, then the
+  // union's bookkeeping (block bitmap, its prefix counts, the union, the
+  // rows' masks over it); beyond the device's LDS the block-centric path
+  // takes every row
+  const size_t ulds = static_cast<size_t>(4) * s.C * D * 2 +
+                      (static_cast<size_t>(2) * mw + kUnionMaxU +
+                       static_cast<size_t>(union_ok(s) ? union_tile_rows(s) : 0) * (kUnionMaxU / 32)) * 4;
+  if (union_ok(s) && union_min >= 0 && ulds <= kUnionMaxLds) {
     const int T = union_tile_rows(s);
     skip_tiles = (s.Nq + T - 1) / T;
     while ((1 << skip_shift) < T) ++skip_shift;
@@ -1475,7 +1520,6 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
     skip = flag;
     AttnBlockArgs ua{s.H, s.Hkv, s.G, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], 0, s.Nq,
                      kLog2e / sqrtf(static_cast<float>(s.D)), s.Nkv, nullptr, skip_shift, skip_tiles};
-    const int mw = (geo.M[1] + 31) / 32;
     const int ulimit = std::min(3 * s.K, kUnionMaxU);
     dim3 grid(static_cast<unsigned>(skip_tiles), s.BH());
     {
@@ -1484,14 +1528,16 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
       attn_union_compact_kernel<<<1, 1024, 0, st>>>(flag, s.BH() * skip_tiles, union_min, tlist, tcount);
       if ((e = hipGetLastError()) != hipSuccess) return e;
     }
-    // persistent workgroups (at most two per CU are resident)
-    const unsigned ugrid = static_cast<unsigned>(std::min(s.BH() * skip_tiles, 512));
-    const size_t ulds = (static_cast<size_t>(s.C) * (D + 8) + static_cast<size_t>(D) * (s.C + 8)) * 2 +
-                        (static_cast<size_t>(2) * mw + kUnionMaxU + static_cast<size_t>(T) * (kUnionMaxU / 32)) * 4;
     ProfScope ps("attn_union", st);
     auto go = [&](auto kern) {
       if (ulds > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
                                                   hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(ulds));
+      // persistent workgroups: as many as are resident at once
+      int per_cu = 0;
+      if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kUnionWaves * 64, ulds) != hipSuccess ||
+          per_cu < 1)
+        per_cu = 1;
+      const unsigned ugrid = static_cast<unsigned>(std::min(s.BH() * skip_tiles, per_cu * kDeviceCUs));
       kern<<<ugrid, kUnionWaves * 64, ulds, st>>>(ua, static_cast<const uint16_t*>(q),
                                                   static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), idx,
                                                   static_cast<uint16_t*>(o), lse, tlist, tcount);
