@@ -38,8 +38,14 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def algorithmic_work(w, pairs_scored, attn_pairs, far_key_pairs=None, far_slots=None):
-    """Algorithmic bytes / flops per launch of each kernel (see the design notes)."""
+def algorithmic_work(w, pairs_scored, attn_pairs, far_key_pairs=None, far_slots=None, union_key_pairs=0,
+                     block_rows=None):
+    """Algorithmic bytes / flops per launch of each kernel (see the design notes).
+
+    far_key_pairs / far_slots count only the rows left to the block-centric
+    kernels (block_rows of them per (batch, KV head) group), union_key_pairs
+    the exact (query head, key) pairs of the rows the row-tile union kernel
+    attended."""
     B, H, Hkv, N, Nq, d, C, g, K = (w[k] for k in ("B", "H", "Hkv", "N", "Nq", "d", "C", "g", "K"))
     G = H // Hkv
     es = 2 if w["dtype"] == "bf16" else 4
@@ -76,16 +82,52 @@ def algorithmic_work(w, pairs_scored, attn_pairs, far_key_pairs=None, far_slots=
         # row's first, previous and own; the per-leaf-block kernel reads those
         # slots' partials (bf16 o + fp32 log-sum) and q, and writes o and lse
         out["attn_block"] = ("mfma", far_key_pairs * 4 * d)
-        out["attn_local"] = ("hbm", far_slots * G * (2 * d + 4) + B * H * Nq * (2 * d + 2 * d + 4))
+        nrows = B * Hkv * Nq if block_rows is None else block_rows
+        out["attn_local"] = ("hbm", far_slots * G * (2 * d + 4) + nrows * G * (2 * d + 2 * d + 4))
     else:
         out["attn_block"] = ("mfma", attn_pairs * 4 * d)
     rows = B * Hkv * Nq
+    if union_key_pairs:
+        out["attn_union"] = ("mfma", union_key_pairs * 4 * d)
+    out["attn_union_plan"] = ("hbm", rows * K * 4)
     out["final_topk"] = ("hbm", rows * (g * K * 8 + 4 + K * 4))
     out["cluster_build"] = ("hbm", rows * g * K * 4 * 3)
     return out
 
 
-def attention_sharing(idx, w):
+def union_rows(idx_t, w, min_tiles):
+    """Rows [B, Hkv, Nq] that pisa_sparse_attn_fwd's row-tile union kernel
+    attends, by the library's rule: tiles of 256 / G consecutive rows of one
+    (batch, KV head) whose selections name at most min(3K, 256) distinct leaf
+    blocks, taken when at least min_tiles tiles qualify, G in {1, 2, 4, 8, 16}
+    and the kernel's LDS (two stages of a K and a V block plus its
+    bookkeeping) fits 160 KB.  Returns (rows, stagings: the blocks the kernel
+    stages, one per distinct block of each tile it takes), or None when it
+    takes no row."""
+    import torch
+
+    B, H, Hkv, N, Nq, d, C, K = (w[k] for k in ("B", "H", "Hkv", "N", "Nq", "d", "C", "K"))
+    G = H // Hkv
+    M1 = -(-N // C)
+    if G not in (1, 2, 4, 8, 16) or min_tiles < 0 or w["dtype"] != "bf16":
+        return None
+    T = 256 // G
+    if 4 * C * d * 2 + (2 * (-(-M1 // 32)) + 256 + T * 8) * 4 > 160 * 1024:
+        return None
+    tiles = -(-Nq // T)
+    x = idx_t.reshape(B * Hkv, Nq, K)
+    x = torch.where((x >= 0) & (x < M1), x, torch.full_like(x, M1))
+    if tiles * T > Nq:
+        x = torch.cat([x, torch.full((B * Hkv, tiles * T - Nq, K), M1, dtype=x.dtype, device=x.device)], dim=1)
+    xs = torch.sort(x.reshape(B * Hkv, tiles, T * K), dim=-1).values
+    distinct = (xs[..., :1] < M1).sum(-1) + ((xs[..., 1:] != xs[..., :-1]) & (xs[..., 1:] < M1)).sum(-1)
+    ok = distinct <= min(3 * K, 256)
+    if int(ok.sum().item()) < max(min_tiles, 1):
+        return None
+    return ok.repeat_interleave(T, dim=1)[:, :Nq].reshape(B, Hkv, Nq), int((distinct * ok).sum().item())
+
+
+def attention_sharing(idx, w, union=None):
     """Block sharing of the block-centric attention, from a selection
     (counted on the GPU, outside any timed region): (query head, row, block)
     triples attended divided by the K/V block stagings the kernels make.  A far
@@ -93,7 +135,9 @@ def attention_sharing(idx, w):
     chunk of up to 1024 (row, slot) pairs of its cluster and serves every query
     head of the pair; causal rows' first, previous and own blocks are staged by
     the per-leaf-block kernel once per (query leaf block, query head, pass of
-    its row groups).  None where another attention path runs."""
+    its row groups); the rows of the row-tile union kernel's tiles (union, from
+    union_rows) are served by one staging per distinct block of their tile.
+    None where another attention path runs."""
     import torch
 
     B, H, Hkv, N, Nq, C, K = (w[k] for k in ("B", "H", "Hkv", "N", "Nq", "C", "K"))
@@ -106,6 +150,11 @@ def attention_sharing(idx, w):
     c_row = t_pos // C
     valid = (it >= 0) & (it < M1)
     forced = (it == 0) | (it == c_row) | (it == c_row - 1) if w["causal"] else torch.zeros_like(valid)
+    urow = torch.zeros((B, Hkv, Nq, 1), dtype=torch.bool, device=idx.device) if union is None \
+        else union[0].unsqueeze(-1)
+    union_triples = int((valid & urow).sum().item()) * G
+    union_loads = 0 if union is None else union[1]
+    valid = valid & ~urow
     far = valid & ~forced
     bh = torch.arange(B * Hkv, device=idx.device).view(B, Hkv, 1, 1)
     cl = (bh * M1 + it)[far]
@@ -116,13 +165,20 @@ def attention_sharing(idx, w):
     if w["causal"]:
         nwl = 8 if C == 128 else 4
         npass = -(-(C // 16) // nwl)
-        cs = torch.unique(c_row.flatten())
+        # one workgroup per (batch, KV head, query leaf block) holding a row
+        # the block-centric path serves
+        keys = (bh * M1 + c_row).expand(B, Hkv, Nq, 1)[~urow]
+        cs = torch.unique(keys) % M1
         nsb = 1 + (cs - 1 > 0).long() + (cs > 0).long()
-        local_loads = B * Hkv * int(nsb.sum().item()) * npass * G
+        local_loads = int(nsb.sum().item()) * npass * G
         local_triples = int((valid & forced).sum().item()) * G
-    return {"factor": (far_triples + local_triples) / max(1, far_loads + local_loads),
-            "far": far_triples / max(1, far_loads), "local": local_triples / max(1, local_loads) if local_loads else None,
-            "triples": far_triples + local_triples, "block_stagings": far_loads + local_loads,
+    triples = far_triples + local_triples + union_triples
+    loads = far_loads + local_loads + union_loads
+    return {"factor": triples / max(1, loads),
+            "far": far_triples / max(1, far_loads) if far_loads else None,
+            "local": local_triples / max(1, local_loads) if local_loads else None,
+            "union": union_triples / max(1, union_loads) if union_loads else None,
+            "triples": triples, "block_stagings": loads,
             "what": "(query head, row, block) triples attended / K-V block stagings into LDS by the attention kernels"}
 
 
@@ -439,11 +495,20 @@ def main():
     attn_pairs = int((cnt * valid).sum().item()) * (H // Hkv)
     c_row = (t_pos // C)
     far = valid & (idx_t != 0) & (idx_t != c_row) & (idx_t != c_row - 1)
-    far_key_pairs = int((cnt * far).sum().item()) * (H // Hkv)
-    far_slots = int(far.sum().item())
+    # rows the row-tile union kernel took: their work goes to it, the rest to
+    # the block-centric kernels
+    umin = pisa.pisa_attn_union_min_tiles(0)
+    pisa.pisa_attn_union_min_tiles(umin)
+    union = union_rows(idx_t, w, umin)
+    brow = torch.ones((B, Hkv, Nq, 1), dtype=torch.bool, device="cuda") if union is None \
+        else ~union[0].unsqueeze(-1)
+    far_key_pairs = int((cnt * (far & brow)).sum().item()) * (H // Hkv)
+    far_slots = int((far & brow).sum().item())
+    union_key_pairs = int((cnt * (valid & ~brow)).sum().item()) * (H // Hkv)
+    block_rows = int(brow.sum().item())
     # leaf pairs scored (upper bound): every row may score g*K candidates minus the 3 forced
     pairs_scored = B * Hkv * Nq * max(0, g * K - (3 if w["causal"] else 0))
-    work = algorithmic_work(w, pairs_scored, attn_pairs, far_key_pairs, far_slots)
+    work = algorithmic_work(w, pairs_scored, attn_pairs, far_key_pairs, far_slots, union_key_pairs, block_rows)
     kernels = {name: {"launches": n // args.steps if n >= args.steps else n,
                       "ms_per_step": tot / args.steps, "avg_ms": tot / max(n, 1)}
                for name, (n, tot) in kern.items()}
@@ -552,7 +617,7 @@ def main():
         "cpu_baseline": cpu,
         "fractions": fractions,
         "probes": probes,
-        "attention_sharing": attention_sharing(idx, w),
+        "attention_sharing": attention_sharing(idx, w, union),
         "per_kernel_roofline": per_kernel,
     }
     print(json.dumps(res), flush=True)
