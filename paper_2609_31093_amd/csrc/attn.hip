@@ -809,6 +809,8 @@ constexpr int kUnionCols = kUnionWaves * kUnionGroups * 16;
 constexpr int kUnionMaxU = 256;   // union limit: at most min(3K, 256) blocks
 constexpr float kUnionSlack = 8.f;  // log2 units the running maximum may lag behind
 constexpr size_t kUnionMaxLds = 160 * 1024;  // LDS of one CU
+constexpr int kUnionMergeBatch = 4;  // LOCAL: partials requested together
+constexpr int kLocalWaves = 4;       // LOCAL: wavefronts per workgroup (several workgroups per CU)
 constexpr int kDeviceCUs = 256;
 typedef short v4s16 __attribute__((ext_vector_type(4)));
 // LDS byte address of a pointer into dynamic shared memory, made wave-uniform.
@@ -941,12 +943,19 @@ __global__ __launch_bounds__(1024) void attn_union_compact_kernel(uint8_t* __res
   if (tid == 0) *count = base;
 }
 
-template <int D, int CT, int G>
-__global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
+// LOCAL (causal, block-centric path): the tiles of the chunk [a.row0,
+// a.row0 + a.nrows) that the union kernel did not take, each over the union
+// of its rows' first, previous and own blocks only (the ones they selected);
+// every column then merges the partials the block-centric kernel wrote for
+// its row's other slots before o and lse are written.  ltiles: tiles per
+// (batch, KV head) in the chunk, lcount: ltiles times the groups.
+template <int D, int CT, int G, bool LOCAL>
+__global__ __launch_bounds__((LOCAL ? kLocalWaves : kUnionWaves) * 64, 2) void attn_union_kernel(
     AttnBlockArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const int32_t* __restrict__ idx, uint16_t* __restrict__ o, float* __restrict__ lse,
-    const int32_t* __restrict__ tile_list, const int32_t* __restrict__ tile_count) {
-  constexpr int NW = kUnionWaves, NG = kUnionGroups;
+    const int32_t* __restrict__ tile_list, const int32_t* __restrict__ tile_count,
+    const uint16_t* __restrict__ part_o, const float* __restrict__ part_lse, int ltiles, int lcount) {
+  constexpr int NW = LOCAL ? kLocalWaves : kUnionWaves, NG = kUnionGroups;
   constexpr int RW = 16 * NG / G, T = NW * RW;  // rows per wavefront, per tile
   constexpr int KS = D / 32;
   constexpr int C = CT * 32;
@@ -973,14 +982,33 @@ __global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
   __shared__ int s_nu;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int ntile = *tile_count;
-  // persistent workgroups over the flagged tiles
+  const int ntile = LOCAL ? lcount : *tile_count;
+  const int rend = LOCAL ? min(a.Nq, a.row0 + a.nrows) : a.Nq;  // rows of this launch end here
+  // persistent workgroups over the tiles
   for (int li = blockIdx.x; li < ntile; li += gridDim.x) {
-  const int id = tile_list[li];
-  const int bh = id / a.skip_tiles, tile = id - bh * a.skip_tiles;
+  int bh, tile;
+  if constexpr (LOCAL) {
+    bh = li / ltiles;
+    tile = a.row0 / T + (li - bh * ltiles);
+    // the union kernel's tiles (T divides its tile rows)
+    if (a.skip && a.skip[static_cast<int64_t>(bh) * a.skip_tiles + ((tile * T) >> a.skip_shift)]) continue;
+  } else {
+    const int id = tile_list[li];
+    bh = id / a.skip_tiles;
+    tile = id - bh * a.skip_tiles;
+  }
   const int b = bh / a.Hkv, h = bh - b * a.Hkv;
   const int r0 = tile * T;
   const int32_t* lst = idx + static_cast<int64_t>(bh) * a.Nq * a.K;
+  // LOCAL: only a row's first, previous and own blocks (App. B's forced set)
+  auto take = [&](int row, int x) {
+    if (x < 0 || x >= a.M1) return false;
+    if constexpr (LOCAL) {
+      const int cr = (a.N - a.Nq + row) / C;
+      return x == 0 || x == cr || x == cr - 1;
+    }
+    return true;
+  };
 
   __syncthreads();  // the previous tile's readers of the LDS are done
   for (int e = tid; e < MW; e += NW * 64) bitmap[e] = 0;
@@ -988,9 +1016,9 @@ __global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
   __syncthreads();
   for (int e = tid; e < T * a.K; e += NW * 64) {
     const int row = r0 + e / a.K;
-    if (row >= a.Nq) continue;
+    if (row >= rend) continue;
     const int x = lst[static_cast<int64_t>(row) * a.K + e % a.K];
-    if (x >= 0 && x < a.M1) atomicOr(&bitmap[x >> 5], 1u << (x & 31));
+    if (take(row, x)) atomicOr(&bitmap[x >> 5], 1u << (x & 31));
   }
   __syncthreads();
   if (wave == 0) {
@@ -1023,9 +1051,9 @@ __global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
   }
   for (int e = tid; e < T * a.K; e += NW * 64) {
     const int j = e / a.K, row = r0 + j;
-    if (row >= a.Nq) continue;
+    if (row >= rend) continue;
     const int x = lst[static_cast<int64_t>(row) * a.K + e % a.K];
-    if (x < 0 || x >= a.M1) continue;
+    if (!take(row, x)) continue;
     const int u = wpre[x >> 5] + __builtin_popcount(bitmap[x >> 5] & ((1u << (x & 31)) - 1u));
     if (u < kUnionMaxU) atomicOr(&rmask[j * MWU + (u >> 5)], 1u << (u & 31));
   }
@@ -1043,8 +1071,8 @@ __global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
     const int cc = cg * 16 + col;
     jr[cg] = wave * RW + cc / G;
     const int row = r0 + jr[cg];
-    vrow[cg] = row < a.Nq;
-    const int rowc = vrow[cg] ? row : a.Nq - 1;
+    vrow[cg] = row < rend;
+    const int rowc = vrow[cg] ? row : r0;
     tq[cg] = a.N - a.Nq + rowc;
     const uint16_t* qrow = q + ((static_cast<int64_t>(b) * a.H + h * G + cc % G) * a.Nq + rowc) * D + grp * 8;
 #pragma unroll
@@ -1224,9 +1252,50 @@ __global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
     float ll = l[cg];
     ll += __shfl_xor(ll, 16);
     ll += __shfl_xor(ll, 32);
+    float mm = m[cg];
+    const int cc = cg * 16 + col;
+    if constexpr (LOCAL) {
+      // merge the partials (o normalised, log2-sum) of the row's other slots;
+      // a lane reads the 4 values of each 16-wide d tile it holds
+      const int row = tq[cg] - (a.N - a.Nq);
+      const int cr = tq[cg] / C;
+      const int32_t* sl = lst + static_cast<int64_t>(row) * a.K;
+      const int64_t pb = (static_cast<int64_t>(bh) * a.nrows + (row - a.row0)) * a.K;
+      for (int s0 = 0; s0 < a.K; s0 += kUnionMergeBatch) {
+        float ls[kUnionMergeBatch];
+        uint2 xo[kUnionMergeBatch][DT];
+#pragma unroll
+        for (int u = 0; u < kUnionMergeBatch; ++u) {
+          const int sx = s0 + u;
+          const int x = sx < a.K ? sl[sx] : -1;
+          const bool far = x >= 0 && x < a.M1 && x != 0 && x != cr && x != cr - 1;
+          ls[u] = far ? part_lse[(pb + sx) * G + cc % G] : -INFINITY;
+        }
+#pragma unroll
+        for (int u = 0; u < kUnionMergeBatch; ++u) {
+          const uint16_t* pr = part_o + ((pb + (ls[u] != -INFINITY ? s0 + u : 0)) * G + cc % G) * D + 4 * grp;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) xo[u][dt] = *reinterpret_cast<const uint2*>(pr + dt * 16);
+        }
+#pragma unroll
+        for (int u = 0; u < kUnionMergeBatch; ++u) {
+          if (ls[u] == -INFINITY) continue;
+          const float mn = fmaxf(mm, ls[u]);
+          const float c0 = fast_exp2(mm - mn), c1 = fast_exp2(ls[u] - mn);
+          ll = ll * c0 + c1;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) {
+            oacc[cg][dt][0] = oacc[cg][dt][0] * c0 + __uint_as_float(xo[u][dt].x << 16) * c1;
+            oacc[cg][dt][1] = oacc[cg][dt][1] * c0 + __uint_as_float(xo[u][dt].x & 0xFFFF0000u) * c1;
+            oacc[cg][dt][2] = oacc[cg][dt][2] * c0 + __uint_as_float(xo[u][dt].y << 16) * c1;
+            oacc[cg][dt][3] = oacc[cg][dt][3] * c0 + __uint_as_float(xo[u][dt].y & 0xFFFF0000u) * c1;
+          }
+          mm = mn;
+        }
+      }
+    }
     if (!vrow[cg]) continue;
     // oacc[cg][dt][i] = O[d = dt*16 + 4*grp + i][this column]
-    const int cc = cg * 16 + col;
     const int64_t orow = (static_cast<int64_t>(b) * a.H + h * G + cc % G) * a.Nq + r0 + jr[cg];
     const float inv = ll > 0.f ? 1.0f / ll : 0.f;
 #pragma unroll
@@ -1236,7 +1305,7 @@ __global__ __launch_bounds__(kUnionWaves * 64, 2) void attn_union_kernel(
       w.y = pack2_bf16(oacc[cg][dt][2] * inv, oacc[cg][dt][3] * inv);
       *reinterpret_cast<uint2*>(o + orow * D + dt * 16 + 4 * grp) = w;
     }
-    if (lse && grp == 0) lse[orow] = ll > 0.f ? (m[cg] + fast_log2(ll)) * kLn2 : -INFINITY;
+    if (lse && grp == 0) lse[orow] = ll > 0.f ? (mm + fast_log2(ll)) * kLn2 : -INFINITY;
   }
   }
 }
@@ -1389,7 +1458,10 @@ constexpr size_t kPartialBudget = size_t(6) << 30;
 
 static int attn_chunk_rows(const Shape& s) {
   const size_t per_row = static_cast<size_t>(s.BH()) * s.K * s.G * (s.D * 2 + 4);
-  const size_t rows = kPartialBudget / per_row;
+  size_t rows = kPartialBudget / per_row;
+  // several chunks: whole 256-row tiles each, so that the row-tile kernels'
+  // tiles line up with every chunk
+  if (rows < static_cast<size_t>(s.Nq) && rows >= 256) rows = rows / 256 * 256;
   return static_cast<int>(std::min<size_t>(s.Nq, std::max<size_t>(rows, 1)));
 }
 
@@ -1510,7 +1582,8 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
   const size_t ulds = static_cast<size_t>(4) * s.C * D * 2 +
                       (static_cast<size_t>(2) * mw + kUnionMaxU +
                        static_cast<size_t>(union_ok(s) ? union_tile_rows(s) : 0) * (kUnionMaxU / 32)) * 4;
-  if (union_ok(s) && union_min >= 0 && ulds <= kUnionMaxLds) {
+  const bool union_lds_ok = ulds <= kUnionMaxLds;
+  if (union_ok(s) && union_min >= 0 && union_lds_ok) {
     const int T = union_tile_rows(s);
     skip_tiles = (s.Nq + T - 1) / T;
     while ((1 << skip_shift) < T) ++skip_shift;
@@ -1540,7 +1613,7 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
       const unsigned ugrid = static_cast<unsigned>(std::min(s.BH() * skip_tiles, per_cu * kDeviceCUs));
       kern<<<ugrid, kUnionWaves * 64, ulds, st>>>(ua, static_cast<const uint16_t*>(q),
                                                   static_cast<const uint16_t*>(k), static_cast<const uint16_t*>(v), idx,
-                                                  static_cast<uint16_t*>(o), lse, tlist, tcount);
+                                                  static_cast<uint16_t*>(o), lse, tlist, tcount, nullptr, nullptr, 0, 0);
     };
     auto by_g = [&](auto k1, auto k2, auto k4, auto k8, auto k16) {
       switch (s.G) {
@@ -1552,8 +1625,8 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
       }
     };
 #define PISA_UNION(CT) \
-    by_g(attn_union_kernel<D, CT, 1>, attn_union_kernel<D, CT, 2>, attn_union_kernel<D, CT, 4>, \
-         attn_union_kernel<D, CT, 8>, attn_union_kernel<D, CT, 16>)
+    by_g(attn_union_kernel<D, CT, 1, false>, attn_union_kernel<D, CT, 2, false>, attn_union_kernel<D, CT, 4, false>, \
+         attn_union_kernel<D, CT, 8, false>, attn_union_kernel<D, CT, 16, false>)
     if (s.C == 32) PISA_UNION(1);
     else if (s.C == 64) PISA_UNION(2);
     else if (s.C == 96) PISA_UNION(3);
@@ -1597,7 +1670,47 @@ static hipError_t launch_block_path(const Shape& s, const Geo& geo, const void* 
       else
         go(attn_block16_kernel<D, 4, kAttnBlockWaves>, kAttnBlockWaves);
     }
-    if (local) {
+    // With several heads per KV head, the row tiles of this chunk that the
+    // union kernel did not take go through its LOCAL mode: the forced blocks
+    // staged once per tile for every head, then the far partials merged.
+    const int lT = union_ok(s) ? kLocalWaves * kUnionGroups * 16 / s.G : 0;
+    const size_t llds = static_cast<size_t>(4) * s.C * D * 2 +
+                        (static_cast<size_t>(2) * mw + kUnionMaxU + static_cast<size_t>(lT) * (kUnionMaxU / 32)) * 4;
+    if (local && s.G > 1 && union_ok(s) && llds <= kUnionMaxLds && row0 % lT == 0) {
+      ProfScope ps("attn_local", st);
+      const int ltiles = (row0 + nrows + lT - 1) / lT - row0 / lT;
+      const int lcount = s.BH() * ltiles;
+      const uint16_t* qq = static_cast<const uint16_t*>(q);
+      const uint16_t* kk = static_cast<const uint16_t*>(k);
+      const uint16_t* vv = static_cast<const uint16_t*>(v);
+      auto go = [&](auto kern) {
+        if (llds > 65536) (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
+                                                    hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(llds));
+        int per_cu = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kern, kLocalWaves * 64, llds) != hipSuccess ||
+            per_cu < 1)
+          per_cu = 1;
+        const unsigned lgrid = static_cast<unsigned>(std::min(lcount, per_cu * kDeviceCUs));
+        kern<<<lgrid, kLocalWaves * 64, llds, st>>>(a, qq, kk, vv, idx, static_cast<uint16_t*>(o), lse, nullptr,
+                                                    nullptr, part_o, part_lse, ltiles, lcount);
+      };
+      auto by_g = [&](auto k2, auto k4, auto k8, auto k16) {
+        switch (s.G) {
+          case 2: go(k2); break;
+          case 4: go(k4); break;
+          case 8: go(k8); break;
+          default: go(k16); break;
+        }
+      };
+#define PISA_LOCAL(CT) \
+      by_g(attn_union_kernel<D, CT, 2, true>, attn_union_kernel<D, CT, 4, true>, attn_union_kernel<D, CT, 8, true>, \
+           attn_union_kernel<D, CT, 16, true>)
+      if (s.C == 32) PISA_LOCAL(1);
+      else if (s.C == 64) PISA_LOCAL(2);
+      else if (s.C == 96) PISA_LOCAL(3);
+      else PISA_LOCAL(4);
+#undef PISA_LOCAL
+    } else if (local) {
       ProfScope ps("attn_local", st);
       const int tq0 = s.N - s.Nq;
       const int nblk = (tq0 + row0 + nrows - 1) / s.C - (tq0 + row0) / s.C + 1;
