@@ -135,8 +135,10 @@ def attention_sharing(idx, w, union=None):
     chunk of up to 1024 (row, slot) pairs of its cluster and serves every query
     head of the pair; causal rows' first, previous and own blocks are staged by
     the per-leaf-block kernel once per (query leaf block, query head, pass of
-    its row groups); the rows of the row-tile union kernel's tiles (union, from
-    union_rows) are served by one staging per distinct block of their tile.
+    its row groups), or, with several heads per KV head, once per tile of
+    128 / G rows for all heads; the rows of the row-tile union kernel's tiles
+    (union, from union_rows) are served by one staging per distinct block of
+    their tile.
     None where another attention path runs."""
     import torch
 
@@ -162,7 +164,18 @@ def attention_sharing(idx, w, union=None):
     far_loads = int(((counts + 1023) // 1024).sum().item())
     far_triples = int(far.sum().item()) * G
     local_loads = local_triples = 0
-    if w["causal"]:
+    d = w["d"]
+    lT = 128 // G
+    local_tiles = (w["causal"] and G in (2, 4, 8, 16)
+                   and 4 * C * d * 2 + (2 * (-(-M1 // 32)) + 256 + lT * 8) * 4 <= 160 * 1024)
+    if local_tiles:
+        # several heads per KV head: tiles of 128 / G rows stage each distinct
+        # forced block their rows selected once for all heads
+        tile = (torch.arange(Nq, device=idx.device) // lT).view(1, 1, Nq, 1)
+        key = ((bh * (-(-Nq // lT)) + tile) * M1 + it)[valid & forced]
+        local_loads = int(torch.unique(key).numel())
+        local_triples = int((valid & forced).sum().item()) * G
+    elif w["causal"]:
         nwl = 8 if C == 128 else 4
         npass = -(-(C // 16) // nwl)
         # one workgroup per (batch, KV head, query leaf block) holding a row
