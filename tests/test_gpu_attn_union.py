@@ -213,3 +213,34 @@ def test_union_threshold_and_off(mode, union_min_tiles):
     empty = np.isneginf(want_lse)
     assert np.array_equal(np.isneginf(got_lse), empty)
     assert np.abs(got_lse[~empty] - want_lse[~empty]).max() <= 1e-3
+
+
+def test_forced_block_tiles_across_row_chunks():
+    """8 heads per KV head with a budget of 64: the per-slot partials of
+    60000 rows exceed the 6 GiB the block-centric path holds at once, so the
+    attention runs in three row chunks (whole 256-row tiles each) and every
+    chunk's forced-block tiles merge 61 far partials per (row, head) (no
+    separate tail merge).  The selection is the library's own; rows on both
+    sides of each chunk boundary and random rows against the oracle."""
+    B, H, Hkv, d, C, g, K = 1, 16, 2, 128, 64, 2, 64
+    N = Nq = 60000
+    G = H // Hkv
+    per_row = B * Hkv * K * G * (2 * d + 4)
+    ch = (6 << 30) // per_row // 256 * 256
+    assert ch < Nq < 3 * ch
+    print("case chunks", ch, flush=True)
+    x = inputs.random_qkv(B, H, Hkv, Nq, N, d, "bf16", seed=29)
+    q, k, v = dev(x["q"], "bf16"), dev(x["k"], "bf16"), dev(x["v"], "bf16")
+    p = pisa.make_problem(B, H, Hkv, Nq, N, d, C, g, K, 1, "bf16")
+    idx = pisa.select(p, q, k, pisa.build_pyramid(p, k))
+    o, lse = pisa.sparse_attn_fwd(p, q, k, v, idx)
+    torch.cuda.synchronize()
+    idx_np = idx.cpu().numpy()
+    rng = np.random.default_rng(4)
+    rows = np.unique(np.concatenate([[0, 1, ch - 1, ch, 2 * ch - 1, 2 * ch, Nq - 1],
+                                     rng.choice(Nq, 25, replace=False)]))
+    want_o, want_lse = O.sparse_attention(x["q"], x["k"], x["v"], idx_np[:, :, rows], C, True, rows=rows)
+    got_o = o.float().cpu().numpy()[:, :, rows]
+    got_lse = lse.cpu().numpy()[:, :, rows]
+    assert np.abs(got_o - want_o).max() <= 2e-2
+    assert np.abs(got_lse - want_lse).max() <= 1e-3
