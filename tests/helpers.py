@@ -173,3 +173,50 @@ def check_flat_bsa_rows(q, k, C, K, causal, gpu_idx, rows, tol=1e-3, heads=None)
                         f"flat-BSA row {(b, h, int(r))}: gpu {got} not admissible (oracle {want}, gap {gap})"
                     st["near_tie_other_admissible"] += 1
     return st
+
+
+def pyramid_error_bound(k, C, g, levels_of=None):
+    """Per-element bound on |float32 pyramid - exact pyramid|, in the layout of
+    oracle.pyramid ([B, Hkv, R, d]).
+
+    Every node is a float32 mean: the sum of its n inputs in any order errs by
+    at most gamma_{n-1} * sum |x| (gamma_m = m u / (1 - m u), u = 2^-24), and
+    the division (or multiplication by a rounded 1/n) adds at most 2u of the
+    result.  A leaf's inputs are exact (bf16 or fp32 keys); a coarser node's
+    are its children as computed, each off by at most its own bound B_j, so
+    the node's bound is max_j B_j (the mean of the perturbations) plus
+    gamma_{n-1} * mean_j (|x_j| + B_j) plus 3u (|mean| + max_j B_j).  The
+    magnitudes come from the exact (float64) pyramid of the oracle
+    (levels_of: {(b, h): oracle.build_pyramid levels} already at hand)."""
+    import oracle as O
+
+    u = 2.0 ** -24
+    gam = lambda n: n * u / (1.0 - n * u)
+    k = np.asarray(k, dtype=np.float64)
+    B, Hkv, N, d = k.shape
+    out = None
+    for b in range(B):
+        for h in range(Hkv):
+            levels = levels_of[(b, h)] if levels_of and (b, h) in levels_of else O.build_pyramid(k[b, h], C, g)
+            M1 = levels[0].shape[0]
+            kabs = np.zeros((M1 * C, d))
+            kabs[:N] = np.abs(k[b, h])
+            cnt = np.minimum(C, N - np.arange(M1) * C).astype(np.float64)
+            absmean = kabs.reshape(M1, C, d).sum(axis=1) / cnt[:, None]
+            bounds = [gam(cnt - 1)[:, None] * absmean + 3 * u * np.abs(levels[0])]
+            for lv in range(1, len(levels)):
+                cb, cx = bounds[-1], np.abs(levels[lv - 1])
+                M = levels[lv].shape[0]
+                nc = np.minimum(g, cb.shape[0] - np.arange(M) * g).astype(np.float64)
+                pb = np.zeros((M * g, d))
+                px = np.zeros((M * g, d))
+                pb[:cb.shape[0]] = cb
+                px[:cb.shape[0]] = cx
+                bmax = pb.reshape(M, g, d).max(axis=1)
+                mabs = (px + pb).reshape(M, g, d).sum(axis=1) / nc[:, None]
+                bounds.append(bmax + gam(nc - 1)[:, None] * mabs + 3 * u * (np.abs(levels[lv]) + bmax))
+            rows = O.pyramid_rows(bounds)
+            if out is None:
+                out = np.empty((B, Hkv, rows.shape[0], d))
+            out[b, h] = rows
+    return out

@@ -15,7 +15,7 @@ import torch
 
 import oracle as O
 from paper_2609_31093_amd import inputs
-from tests.helpers import check_flat_bsa_rows, check_selection_rows, check_valid_all_rows
+from tests.helpers import check_flat_bsa_rows, check_selection_rows, check_valid_all_rows, pyramid_error_bound
 
 pytestmark = pytest.mark.gpu
 
@@ -81,10 +81,11 @@ def test_fullsize_workload(name):
         levels = O.build_pyramid(kh, C, g)
         # pyramid: every level's first, middle and last nodes
         got_pyr = pyr[0, h].cpu().numpy()
+        bound = pyramid_error_bound(x["k"][:, h:h + 1], C, g, levels_of={(0, 0): levels})[0, 0]
         for lv, S in enumerate(levels[:-1] if len(levels) > 1 else levels, start=1):
             for i in sorted({0, S.shape[0] // 2, S.shape[0] - 1}):
-                err = np.abs(got_pyr[offs[lv - 1] + i] - S[i]).max()
-                assert err <= (C + len(sizes) * g) * 2.0 ** -24 * float(np.abs(kh).max()), (lv, i, err)
+                err = np.abs(got_pyr[offs[lv - 1] + i] - S[i])
+                assert np.all(err <= bound[offs[lv - 1] + i]), (lv, i, float(err.max()))
         st = check_selection_rows(x["q"], x["k"], C, g, K, causal, idx_np[:, h:h + 1][:, :, rows], rows,
                                   gpu_score=sc_np[:, h:h + 1][:, :, rows], heads=[h], levels={(0, h): levels})
         for key, val in st.items():
