@@ -812,7 +812,6 @@ constexpr size_t kUnionMaxLds = 160 * 1024;  // LDS of one CU
 constexpr int kUnionMergeBatch = 4;  // LOCAL: partials requested together
 constexpr int kLocalWaves = 4;       // LOCAL: wavefronts per workgroup (several workgroups per CU)
 constexpr int kDeviceCUs = 256;
-typedef short v4s16 __attribute__((ext_vector_type(4)));
 // LDS byte address of a pointer into dynamic shared memory, made wave-uniform.
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return __builtin_amdgcn_readfirstlane(
@@ -1232,10 +1231,8 @@ __global__ __launch_bounds__((LOCAL ? kLocalWaves : kUnionWaves) * 64, 2) void a
         const uint16_t* vr = vlds + (k0 + 2 * s2) * 16 * D;  // keys of tiles 2 s2, 2 s2 + 1 of the chunk
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
-          const v4s16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) v4s16*)(vr + voff[dt]));
-          const v4s16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) v4s16*)(vr + 16 * D + voff[dt]));
+          const v4s16 lo = lds_read_tr16x4(vr + voff[dt]);
+          const v4s16 hi = lds_read_tr16x4(vr + 16 * D + voff[dt]);
           avv[dt] = __builtin_bit_cast(bf16x8a, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         }
         __builtin_amdgcn_sched_barrier(0);

@@ -55,12 +55,9 @@ __device__ __forceinline__ void store_bf16_part(uint16_t* p, const float (&x)[DP
   }
 }
 
-// K^T staged in LDS for the dq product when it fits beside the other tiles;
-// otherwise its operand is read from the row-major K with strided loads.
-__host__ __device__ constexpr bool bwd_kt(int C, int D) { return C <= 96 || D <= 64; }
 __host__ __device__ constexpr size_t bwd_lds_elems(int C, int D) {
-  return 2 * static_cast<size_t>(C) * (D + 8) + (bwd_kt(C, D) ? static_cast<size_t>(D) * (C + 4) : 0) +
-         2 * static_cast<size_t>(C) * (kBwdCols + 8) + 2 * static_cast<size_t>(kBwdCols) * (D + 8) +
+  return 2 * static_cast<size_t>(C) * (D + 8) +
+         2 * static_cast<size_t>(kBwdCols) * (C + 8) + 2 * static_cast<size_t>(kBwdCols) * (D + 8) +
          4 * 16 * static_cast<size_t>(D + 8);
 }
 
@@ -94,20 +91,16 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
   constexpr int LDK = D + 8;      // padded K / V row (bf16)
   constexpr int C = CT * 32;      // keys per block
   constexpr int MT = C / 16;      // 16-key tiles
-  constexpr int LKT = C + 4;      // padded K^T row
   constexpr int DT = D / 16;      // 16-dim tiles
   constexpr int DTW = DT / 4;     // 16-dim tiles of dK, dV per wavefront
-  constexpr int LPC = kBwdCols + 8;  // padded P^T / dS^T row (bf16, one row per key)
+  constexpr int LPK = C + 8;         // padded P / dS row (bf16, one row per column, keys along it)
   constexpr int LQC = D + 8;         // padded q / do row (bf16, one row per column)
-  constexpr bool KT = bwd_kt(C, D);
   extern __shared__ __align__(16) uint16_t lds[];
   uint16_t* kl = lds;                                   // [C][LDK]
   uint16_t* vl = kl + C * LDK;                          // [C][LDK]
-  uint16_t* kt = vl + C * LDK;                          // [D][LKT] K^T, two keys per word (if KT)
-  uint32_t* kt32 = reinterpret_cast<uint32_t*>(kt);
-  uint16_t* pt = kt + (KT ? D * LKT : 0);               // [C][LPC] P^T
-  uint16_t* st = pt + C * LPC;                          // [C][LPC] dS^T
-  uint16_t* qr = st + C * LPC;                          // [64][LQC] q of the group's columns
+  uint16_t* pt = vl + C * LDK;                          // [64][LPK] P of the group's columns
+  uint16_t* st = pt + kBwdCols * LPK;                   // [64][LPK] dS
+  uint16_t* qr = st + kBwdCols * LPK;                   // [64][LQC] q of the group's columns
   uint16_t* dr = qr + kBwdCols * LQC;                   // [64][LQC] do of the group's columns
   uint16_t* tb = dr + kBwdCols * LQC + (threadIdx.x >> 6) * 16 * LQC;  // [16][LQC] this wavefront's dq rows
 
@@ -133,19 +126,6 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
     }
     *reinterpret_cast<uint4*>(kl + r * LDK + c8) = kv;
     *reinterpret_cast<uint4*>(vl + r * LDK + c8) = vv;
-  }
-  for (int e = threadIdx.x; KT && e < (C / 2) * (D / 8); e += 256) {
-    const int kp = e % (C / 2), c8 = (e / (C / 2)) * 8;
-    uint4 k0 = make_uint4(0, 0, 0, 0), k1 = make_uint4(0, 0, 0, 0);
-    if (2 * kp < nkeys) k0 = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(2 * kp) * D + c8);
-    if (2 * kp + 1 < nkeys) k1 = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(2 * kp + 1) * D + c8);
-    const uint32_t w0[4] = {k0.x, k0.y, k0.z, k0.w};
-    const uint32_t w1[4] = {k1.x, k1.y, k1.z, k1.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      kt32[(c8 + 2 * i) * (LKT / 2) + kp] = (w0[i] & 0xFFFFu) | (w1[i] << 16);
-      kt32[(c8 + 2 * i + 1) * (LKT / 2) + kp] = (w0[i] >> 16) | (w1[i] & 0xFFFF0000u);
-    }
   }
 
   // dV, dK of this wavefront's dims: [key tile][dim tile j: dt = wave*DTW + j]
@@ -222,22 +202,16 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
       u.z = pack2_bf16(dsv[2 * s2 + 1][0], dsv[2 * s2 + 1][1]);
       u.w = pack2_bf16(dsv[2 * s2 + 1][2], dsv[2 * s2 + 1][3]);
       const bf16x8b2 sb = u4_bf16x8b2(u);
+      // K^T operand from the row-major K: keys 32 s2 + 4 grp + 0..3 and
+      // 32 s2 + 16 + 4 grp + 0..3 (dS's operand order) of dim dt*16 + col,
+      // by transposing reads (lane col: key row 4 grp + col / 4, dims 4 (col % 4))
+      const uint16_t* kr = kl + (32 * s2 + 4 * grp + col / 4) * LDK + 4 * (col & 3);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        uint4 ak;
-        if constexpr (KT) {
-          const uint16_t* krt = kt + (dt * 16 + col) * LKT + 4 * grp + 32 * s2;
-          const uint2 lo = *reinterpret_cast<const uint2*>(krt);
-          const uint2 hi = *reinterpret_cast<const uint2*>(krt + 16);
-          ak = make_uint4(lo.x, lo.y, hi.x, hi.y);
-        } else {
-          uint16_t xk[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e)
-            xk[e] = kl[(32 * s2 + 4 * grp + (e & 3) + (e >> 2) * 16) * LDK + dt * 16 + col];
-          ak = __builtin_bit_cast(uint4, xk);
-        }
-        qacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(u4_bf16x8b2(ak), sb, qacc[dt], 0, 0, 0);
+        const v4s16 lo = lds_read_tr16x4(kr + dt * 16);
+        const v4s16 hi = lds_read_tr16x4(kr + 16 * LDK + dt * 16);
+        const bf16x8b2 ak = __builtin_bit_cast(bf16x8b2, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        qacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, sb, qacc[dt], 0, 0, 0);
       }
     }
     {
@@ -263,38 +237,39 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
       }
       wave_sync();
     }
-    // P^T and dS^T of the group, one row per key
+    // P and dS of the group, one row per column (this lane's 4 keys of each
+    // 16-key tile in one 8-byte store)
 #pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = mt * 16 + 4 * grp + i;
-        pt[key * LPC + wave * 16 + col] = f32_to_bf16_rne(pv[mt][i]);
-        st[key * LPC + wave * 16 + col] = f32_to_bf16_rne(dsv[mt][i]);
-      }
+    for (int mt = 0; mt < MT; ++mt) {
+      const int o = (wave * 16 + col) * LPK + mt * 16 + 4 * grp;
+      *reinterpret_cast<uint2*>(pt + o) = make_uint2(pack2_bf16(pv[mt][0], pv[mt][1]), pack2_bf16(pv[mt][2], pv[mt][3]));
+      *reinterpret_cast<uint2*>(st + o) =
+          make_uint2(pack2_bf16(dsv[mt][0], dsv[mt][1]), pack2_bf16(dsv[mt][2], dsv[mt][3]));
+    }
     __syncthreads();
     // dV[key][d] += sum_c P^T[key][c] do[c][d];  dK[key][d] += sum_c dS^T[key][c] q[c][d]
+    // Every operand below holds 8 consecutive columns kk*32 + 8 grp + 0..7 of
+    // one key (P, dS) or one dim (do, q): two transposing reads of 4 rows,
+    // lane col reading row 8 grp + col / 4 (+4) at element 4 (col % 4).
 #pragma unroll
     for (int kk = 0; kk < kBwdCols / 32; ++kk) {
+      const int ar = kk * 32 + 8 * grp + col / 4;
+      const int ae = 4 * (col & 3);
+      auto tr8 = [&](const uint16_t* base, int ld) {
+        const v4s16 lo = lds_read_tr16x4(base + ar * ld + ae);
+        const v4s16 hi = lds_read_tr16x4(base + (ar + 4) * ld + ae);
+        return __builtin_bit_cast(bf16x8b2, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      };
       bf16x8b2 bdo[DTW], bq[DTW];
 #pragma unroll
       for (int jj = 0; jj < DTW; ++jj) {
-        const int dcol = (wave * DTW + jj) * 16 + col;
-        uint16_t xd[8], xq[8];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          xd[e] = dr[(kk * 32 + grp * 8 + e) * LQC + dcol];
-          xq[e] = qr[(kk * 32 + grp * 8 + e) * LQC + dcol];
-        }
-        bdo[jj] = __builtin_bit_cast(bf16x8b2, xd);
-        bq[jj] = __builtin_bit_cast(bf16x8b2, xq);
+        bdo[jj] = tr8(dr + (wave * DTW + jj) * 16, LQC);
+        bq[jj] = tr8(qr + (wave * DTW + jj) * 16, LQC);
       }
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const bf16x8b2 ap =
-            u4_bf16x8b2(*reinterpret_cast<const uint4*>(pt + (mt * 16 + col) * LPC + kk * 32 + grp * 8));
-        const bf16x8b2 as =
-            u4_bf16x8b2(*reinterpret_cast<const uint4*>(st + (mt * 16 + col) * LPC + kk * 32 + grp * 8));
+        const bf16x8b2 ap = tr8(pt + mt * 16, LPK);
+        const bf16x8b2 as = tr8(st + mt * 16, LPK);
 #pragma unroll
         for (int jj = 0; jj < DTW; ++jj) {
           accv[mt][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap, bdo[jj], accv[mt][jj], 0, 0, 0);

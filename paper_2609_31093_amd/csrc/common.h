@@ -54,6 +54,17 @@ __device__ __forceinline__ int anc_at(const Geo& geo, int x, int l) {
 typedef float f32x2_t __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 
+typedef short v4s16 __attribute__((ext_vector_type(4)));
+
+// Transposing LDS read (ds_read_b64_tr_b16): in each group of 16 lanes, lane
+// i receives element i % 4 of the 8-byte reads of lanes 4j + i / 4, j = 0..3.
+// With lane s reading 4 consecutive bf16 of row s / 4 at column 4 (s % 4),
+// lane i gets column i of those 4 rows: an MFMA operand's 4 consecutive
+// k-elements from a row-major tile whose rows are the k index.
+__device__ __forceinline__ v4s16 lds_read_tr16x4(const uint16_t* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) v4s16*)(p));
+}
+
 // Two floats to packed bf16 (round to nearest even, hardware conversion).
 __device__ __forceinline__ uint32_t pack2_bf16(float a, float b) {
   const f32x2_t v = {a, b};
