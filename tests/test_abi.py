@@ -268,3 +268,14 @@ def test_cache_grow_validates_before_launch():
     assert call(ko=big * 2) == pisa.PISA_ERR_INVALID_ARG            # keys without the other three pointers
     assert call(ko=big * 2, kn=big * 3, vo=big * 4, vn=big * 3 + 4096) == pisa.PISA_ERR_INVALID_ARG  # k_new, v_new overlap
     assert call(pp=_good(d=96)) == pisa.PISA_ERR_UNSUPPORTED
+
+
+def test_union_threshold_knob_returns_previous_value():
+    prev = pisa.pisa_attn_union_min_tiles(5)
+    try:
+        assert prev == 1024  # the library's default
+        assert pisa.pisa_attn_union_min_tiles(-7) == 5
+        assert pisa.pisa_attn_union_min_tiles(0) == -1  # any negative value means off
+        assert pisa.pisa_attn_union_min_tiles(prev) == 0
+    finally:
+        pisa.pisa_attn_union_min_tiles(prev)
