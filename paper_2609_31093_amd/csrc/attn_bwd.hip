@@ -55,10 +55,30 @@ __device__ __forceinline__ void store_bf16_part(uint16_t* p, const float (&x)[DP
   }
 }
 
+// Blocks of 64 keys use a compact LDS layout: every tile unpadded, the
+// 16-byte chunks of each row XOR-swizzled, and each wavefront's dq staging
+// rows laid over its own P and dS rows, so that (at d = 128) the workgroup
+// needs 80 KB and two fit a CU.  Other block sizes keep padded rows.
+__host__ __device__ constexpr bool bwd_compact(int C) { return C == 64; }
+__host__ __device__ constexpr int bwd_region(int C, int D) { return 2 * 16 * C > 16 * D ? 2 * 16 * C : 16 * D; }
 __host__ __device__ constexpr size_t bwd_lds_elems(int C, int D) {
-  return 2 * static_cast<size_t>(C) * (D + 8) +
-         2 * static_cast<size_t>(kBwdCols) * (C + 8) + 2 * static_cast<size_t>(kBwdCols) * (D + 8) +
-         4 * 16 * static_cast<size_t>(D + 8);
+  return bwd_compact(C)
+             ? 2 * static_cast<size_t>(C) * D + 2 * static_cast<size_t>(kBwdCols) * D + 4 * static_cast<size_t>(bwd_region(C, D))
+             : 2 * static_cast<size_t>(C) * (D + 8) + 2 * static_cast<size_t>(kBwdCols) * (C + 8) +
+                   2 * static_cast<size_t>(kBwdCols) * (D + 8) + 4 * 16 * static_cast<size_t>(D + 8);
+}
+
+// Chunk swizzles of the compact layout (NCH 16-byte chunks per row): one for
+// tiles read 16 consecutive rows at a time (K, V, the dq staging rows), one
+// for tiles read by the transposing loads of rows 8 g + j (q, do, P, dS);
+// either spreads each read over the banks in the fewest cycles.
+template <int NCH>
+__device__ __forceinline__ int bwd_swz_rows(int r) {
+  return NCH == 16 ? (r & 15) : ((r >> 1) & 7);
+}
+template <int NCH>
+__device__ __forceinline__ int bwd_swz_cols(int r) {
+  return NCH == 16 ? ((r & 15) ^ ((r >> 2) & 12)) : 2 * (((r >> 3) + (r >> 1)) & 3);
 }
 
 // stat[(b*H + h)*Nq + row] = (lse * log2(e), do . o): 16 lanes per (row, head).
@@ -81,8 +101,10 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(AttnBwdArgs a, const
   if (sub == 0) stat[rh] = make_float2(lse[rh] * kLog2e, s);
 }
 
+// With the compact layout two workgroups fit a CU: registers for two
+// wavefronts per SIMD (256 each); otherwise one.
 template <int D, int CT>
-__global__ __launch_bounds__(256) void attn_bwd_block_kernel(
+__global__ __launch_bounds__(256, bwd_compact(CT * 32) ? 2 : 1) void attn_bwd_block_kernel(
     AttnBwdArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dO, const float2* __restrict__ stat, const int32_t* __restrict__ offs,
     const int32_t* __restrict__ toffs, int64_t ncl, const int32_t* __restrict__ pairs, uint16_t* __restrict__ part_dq,
@@ -95,14 +117,35 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
   constexpr int DTW = DT / 4;     // 16-dim tiles of dK, dV per wavefront
   constexpr int LPK = C + 8;         // padded P / dS row (bf16, one row per column, keys along it)
   constexpr int LQC = D + 8;         // padded q / do row (bf16, one row per column)
+  constexpr bool CMP = bwd_compact(C);
+  constexpr int NCD = D / 8, NCC = C / 8;  // 16-byte chunks per row of D / of C elements
+  constexpr int RW = bwd_region(C, D);     // compact: elements of a wavefront's P + dS (+ dq staging) region
   extern __shared__ __align__(16) uint16_t lds[];
-  uint16_t* kl = lds;                                   // [C][LDK]
-  uint16_t* vl = kl + C * LDK;                          // [C][LDK]
-  uint16_t* pt = vl + C * LDK;                          // [64][LPK] P of the group's columns
-  uint16_t* st = pt + kBwdCols * LPK;                   // [64][LPK] dS
-  uint16_t* qr = st + kBwdCols * LPK;                   // [64][LQC] q of the group's columns
-  uint16_t* dr = qr + kBwdCols * LQC;                   // [64][LQC] do of the group's columns
-  uint16_t* tb = dr + kBwdCols * LQC + (threadIdx.x >> 6) * 16 * LQC;  // [16][LQC] this wavefront's dq rows
+  // padded: K, V [C][LDK]; P, dS [64][LPK]; q, do [64][LQC]; dq staging [4][16][LQC]
+  // compact: K, V [C][D]; q, do [64][D]; then per wavefront [P 16 x C][dS 16 x C],
+  // whose first 16 x D elements also hold that wavefront's dq staging rows
+  uint16_t* kl = lds;
+  uint16_t* vl = kl + C * (CMP ? D : LDK);
+  uint16_t* qr = vl + C * (CMP ? D : LDK);
+  uint16_t* dr = qr + kBwdCols * (CMP ? D : LQC);
+  uint16_t* pt = dr + kBwdCols * (CMP ? D : LQC);       // padded: P; compact: the wavefront regions
+  uint16_t* st = pt + (CMP ? 0 : kBwdCols * LPK);       // padded: dS
+  uint16_t* tb = CMP ? pt + (threadIdx.x >> 6) * RW : st + kBwdCols * LPK + (threadIdx.x >> 6) * 16 * LQC;
+  // element e (a multiple of 4) of row r of each tile
+  auto at_kv = [&](uint16_t* base, int r, int e) {
+    return CMP ? base + r * D + (((e >> 3) ^ bwd_swz_rows<NCD>(r)) << 3) + (e & 7) : base + r * LDK + e;
+  };
+  auto at_qd = [&](uint16_t* base, int r, int e) {
+    return CMP ? base + r * D + (((e >> 3) ^ bwd_swz_cols<NCD>(r)) << 3) + (e & 7) : base + r * LQC + e;
+  };
+  auto at_ps = [&](bool ds, int r, int e) {
+    return CMP ? pt + (r >> 4) * RW + (ds ? 16 * C : 0) + (r & 15) * C + (((e >> 3) ^ bwd_swz_cols<NCC>(r)) << 3) +
+                     (e & 7)
+               : (ds ? st : pt) + r * LPK + e;
+  };
+  auto at_tb = [&](int r, int e) {
+    return CMP ? tb + r * D + (((e >> 3) ^ bwd_swz_rows<NCD>(r)) << 3) + (e & 7) : tb + r * LQC + e;
+  };
 
   int64_t cl;
   int beg, end;
@@ -124,8 +167,8 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
       kv = *reinterpret_cast<const uint4*>(kb + static_cast<int64_t>(r) * D + c8);
       vv = *reinterpret_cast<const uint4*>(vb + static_cast<int64_t>(r) * D + c8);
     }
-    *reinterpret_cast<uint4*>(kl + r * LDK + c8) = kv;
-    *reinterpret_cast<uint4*>(vl + r * LDK + c8) = vv;
+    *reinterpret_cast<uint4*>(at_kv(kl, r, c8)) = kv;
+    *reinterpret_cast<uint4*>(at_kv(vl, r, c8)) = vv;
   }
 
   // dV, dK of this wavefront's dims: [key tile][dim tile j: dt = wave*DTW + j]
@@ -163,8 +206,8 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
         qb[ks] = u4_bf16x8b2(uq);
         db[ks] = u4_bf16x8b2(ud);
         // the group's q and do rows for the dK / dV products
-        *reinterpret_cast<uint4*>(qr + (wave * 16 + col) * LQC + ks * 32 + grp * 8) = uq;
-        *reinterpret_cast<uint4*>(dr + (wave * 16 + col) * LQC + ks * 32 + grp * 8) = ud;
+        *reinterpret_cast<uint4*>(at_qd(qr, wave * 16 + col, ks * 32 + grp * 8)) = uq;
+        *reinterpret_cast<uint4*>(at_qd(dr, wave * 16 + col, ks * 32 + grp * 8)) = ud;
       }
     }
     const float2 sd = pr >= 0 ? stat[qrow] : make_float2(0.f, 0.f);
@@ -173,14 +216,12 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
       f32x4b2 sacc = {0.f, 0.f, 0.f, 0.f}, pacc = {0.f, 0.f, 0.f, 0.f};
-      const uint16_t* krow = kl + (mt * 16 + col) * LDK + grp * 8;
-      const uint16_t* vrow = vl + (mt * 16 + col) * LDK + grp * 8;
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
-        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(u4_bf16x8b2(*reinterpret_cast<const uint4*>(krow + ks * 32)),
-                                                      qb[ks], sacc, 0, 0, 0);
-        pacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(u4_bf16x8b2(*reinterpret_cast<const uint4*>(vrow + ks * 32)),
-                                                      db[ks], pacc, 0, 0, 0);
+        const uint4 ka = *reinterpret_cast<const uint4*>(at_kv(kl, mt * 16 + col, ks * 32 + grp * 8));
+        const uint4 va = *reinterpret_cast<const uint4*>(at_kv(vl, mt * 16 + col, ks * 32 + grp * 8));
+        sacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(u4_bf16x8b2(ka), qb[ks], sacc, 0, 0, 0);
+        pacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(u4_bf16x8b2(va), db[ks], pacc, 0, 0, 0);
       }
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
@@ -205,11 +246,11 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
       // K^T operand from the row-major K: keys 32 s2 + 4 grp + 0..3 and
       // 32 s2 + 16 + 4 grp + 0..3 (dS's operand order) of dim dt*16 + col,
       // by transposing reads (lane col: key row 4 grp + col / 4, dims 4 (col % 4))
-      const uint16_t* kr = kl + (32 * s2 + 4 * grp + col / 4) * LDK + 4 * (col & 3);
+      const int kr = 32 * s2 + 4 * grp + col / 4;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const v4s16 lo = lds_read_tr16x4(kr + dt * 16);
-        const v4s16 hi = lds_read_tr16x4(kr + 16 * LDK + dt * 16);
+        const v4s16 lo = lds_read_tr16x4(at_kv(kl, kr, dt * 16 + 4 * (col & 3)));
+        const v4s16 hi = lds_read_tr16x4(at_kv(kl, kr + 16, dt * 16 + 4 * (col & 3)));
         const bf16x8b2 ak = __builtin_bit_cast(bf16x8b2, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         qacc[dt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ak, sb, qacc[dt], 0, 0, 0);
       }
@@ -223,7 +264,7 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
         uint2 w;
         w.x = pack2_bf16(qacc[dt][0] * a.rscale, qacc[dt][1] * a.rscale);
         w.y = pack2_bf16(qacc[dt][2] * a.rscale, qacc[dt][3] * a.rscale);
-        *reinterpret_cast<uint2*>(tb + col * LQC + dt * 16 + 4 * grp) = w;
+        *reinterpret_cast<uint2*>(at_tb(col, dt * 16 + 4 * grp)) = w;
       }
       wave_sync();
 #pragma unroll
@@ -232,7 +273,7 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
         const int r = e / (D / 8), c8 = (e - r * (D / 8)) * 8;
         const int64_t px = __shfl(pidx, r);  // lanes 0-15 hold columns 0-15
         const bool ok = __shfl(pr, r) >= 0;
-        const uint4 x = *reinterpret_cast<const uint4*>(tb + r * LQC + c8);
+        const uint4 x = *reinterpret_cast<const uint4*>(at_tb(r, c8));
         if (ok) *reinterpret_cast<uint4*>(part_dq + px * D + c8) = x;
       }
       wave_sync();
@@ -241,9 +282,9 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
     // 16-key tile in one 8-byte store)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt) {
-      const int o = (wave * 16 + col) * LPK + mt * 16 + 4 * grp;
-      *reinterpret_cast<uint2*>(pt + o) = make_uint2(pack2_bf16(pv[mt][0], pv[mt][1]), pack2_bf16(pv[mt][2], pv[mt][3]));
-      *reinterpret_cast<uint2*>(st + o) =
+      *reinterpret_cast<uint2*>(at_ps(false, wave * 16 + col, mt * 16 + 4 * grp)) =
+          make_uint2(pack2_bf16(pv[mt][0], pv[mt][1]), pack2_bf16(pv[mt][2], pv[mt][3]));
+      *reinterpret_cast<uint2*>(at_ps(true, wave * 16 + col, mt * 16 + 4 * grp)) =
           make_uint2(pack2_bf16(dsv[mt][0], dsv[mt][1]), pack2_bf16(dsv[mt][2], dsv[mt][3]));
     }
     __syncthreads();
@@ -255,21 +296,21 @@ __global__ __launch_bounds__(256) void attn_bwd_block_kernel(
     for (int kk = 0; kk < kBwdCols / 32; ++kk) {
       const int ar = kk * 32 + 8 * grp + col / 4;
       const int ae = 4 * (col & 3);
-      auto tr8 = [&](const uint16_t* base, int ld) {
-        const v4s16 lo = lds_read_tr16x4(base + ar * ld + ae);
-        const v4s16 hi = lds_read_tr16x4(base + (ar + 4) * ld + ae);
+      auto join = [](v4s16 lo, v4s16 hi) {
         return __builtin_bit_cast(bf16x8b2, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
       };
       bf16x8b2 bdo[DTW], bq[DTW];
 #pragma unroll
       for (int jj = 0; jj < DTW; ++jj) {
-        bdo[jj] = tr8(dr + (wave * DTW + jj) * 16, LQC);
-        bq[jj] = tr8(qr + (wave * DTW + jj) * 16, LQC);
+        const int e = (wave * DTW + jj) * 16 + ae;
+        bdo[jj] = join(lds_read_tr16x4(at_qd(dr, ar, e)), lds_read_tr16x4(at_qd(dr, ar + 4, e)));
+        bq[jj] = join(lds_read_tr16x4(at_qd(qr, ar, e)), lds_read_tr16x4(at_qd(qr, ar + 4, e)));
       }
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt) {
-        const bf16x8b2 ap = tr8(pt + mt * 16, LPK);
-        const bf16x8b2 as = tr8(st + mt * 16, LPK);
+        const int e = mt * 16 + ae;
+        const bf16x8b2 ap = join(lds_read_tr16x4(at_ps(false, ar, e)), lds_read_tr16x4(at_ps(false, ar + 4, e)));
+        const bf16x8b2 as = join(lds_read_tr16x4(at_ps(true, ar, e)), lds_read_tr16x4(at_ps(true, ar + 4, e)));
 #pragma unroll
         for (int jj = 0; jj < DTW; ++jj) {
           accv[mt][jj] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ap, bdo[jj], accv[mt][jj], 0, 0, 0);
