@@ -228,8 +228,10 @@ int pisa_select_flat_bsa(const pisa_problem* p, const void* q, const float* pyra
  * causal mode a block that starts after the query contributes nothing either
  * (all of its tokens are masked).  The entries of a row need not be sorted
  * but must be distinct (pisa_select writes them so): a block listed twice is
- * attended twice.  Writes o (problem dtype) and lse (nullable); a row with no
- * visible token gets o = 0 and lse = -inf. */
+ * attended once or twice depending on the kernel that takes the row (the
+ * row-tile kernels, and a row's first, previous and own blocks, count it
+ * once).  Writes o (problem dtype) and lse (nullable); a row with no visible
+ * token gets o = 0 and lse = -inf. */
 int pisa_sparse_attn_fwd(const pisa_problem* p, const void* q, const void* k, const void* v,
                          const int32_t* block_idx, void* o, float* lse, void* ws,
                          size_t ws_bytes, pisa_stream_t stream);
