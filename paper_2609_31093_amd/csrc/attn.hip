@@ -1252,28 +1252,27 @@ __global__ __launch_bounds__((LOCAL ? kLocalWaves : kUnionWaves) * 64, 2) void a
     float mm = m[cg];
     const int cc = cg * 16 + col;
     if constexpr (LOCAL) {
-      // merge the partials (o normalised, log2-sum) of the row's other slots;
-      // a lane reads the 4 values of each 16-wide d tile it holds
+      // merge the partials (o normalised, log2-sum) of the row's other
+      // slots.  The four lanes of a column request the slot indices, then
+      // the log-sums, of slots grp, grp + 4, ... (the first 32) all at once;
+      // the partials (each lane the 4 values of each 16-wide d tile it
+      // holds) follow in batches of four slots.
       const int row = tq[cg] - (a.N - a.Nq);
       const int cr = tq[cg] / C;
+      const int hq = cc % G;
       const int32_t* sl = lst + static_cast<int64_t>(row) * a.K;
       const int64_t pb = (static_cast<int64_t>(bh) * a.nrows + (row - a.row0)) * a.K;
-      for (int s0 = 0; s0 < a.K; s0 += kUnionMergeBatch) {
-        float ls[kUnionMergeBatch];
-        uint2 xo[kUnionMergeBatch][DT];
+      auto far = [&](int x) { return x >= 0 && x < a.M1 && x != 0 && x != cr && x != cr - 1; };
+      constexpr int KB = 8;  // the first 4 * KB slots: KB per lane
+      int xs[KB];
+      float lsv[KB];
 #pragma unroll
-        for (int u = 0; u < kUnionMergeBatch; ++u) {
-          const int sx = s0 + u;
-          const int x = sx < a.K ? sl[sx] : -1;
-          const bool far = x >= 0 && x < a.M1 && x != 0 && x != cr && x != cr - 1;
-          ls[u] = far ? part_lse[(pb + sx) * G + cc % G] : -INFINITY;
-        }
+      for (int i = 0; i < KB; ++i) xs[i] = 4 * i + grp < a.K ? sl[4 * i + grp] : -1;
 #pragma unroll
-        for (int u = 0; u < kUnionMergeBatch; ++u) {
-          const uint16_t* pr = part_o + ((pb + (ls[u] != -INFINITY ? s0 + u : 0)) * G + cc % G) * D + 4 * grp;
-#pragma unroll
-          for (int dt = 0; dt < DT; ++dt) xo[u][dt] = *reinterpret_cast<const uint2*>(pr + dt * 16);
-        }
+      for (int i = 0; i < KB; ++i) lsv[i] = far(xs[i]) ? part_lse[(pb + 4 * i + grp) * G + hq] : -INFINITY;
+      const uint16_t* pcol = part_o + (pb * G + hq) * D + 4 * grp;  // slot s at pcol + s * G * D
+      auto merge = [&](const float (&ls)[kUnionMergeBatch], const uint2 (&xo)[kUnionMergeBatch][DT])
+                       __attribute__((always_inline)) {
 #pragma unroll
         for (int u = 0; u < kUnionMergeBatch; ++u) {
           if (ls[u] == -INFINITY) continue;
@@ -1289,6 +1288,45 @@ __global__ __launch_bounds__((LOCAL ? kLocalWaves : kUnionWaves) * 64, 2) void a
           }
           mm = mn;
         }
+      };
+      static_assert(kUnionMergeBatch == 4, "a batch is the four slots of one register of lsv");
+      // batch i = slots 4 i .. 4 i + 3; slot 4 i + u is held by lane col + 16 u
+      auto fetch = [&](int i, float (&ls)[kUnionMergeBatch], uint2 (&xo)[kUnionMergeBatch][DT])
+                       __attribute__((always_inline)) {
+#pragma unroll
+        for (int u = 0; u < kUnionMergeBatch; ++u) {
+          ls[u] = __shfl(lsv[i], col | (u << 4));
+          const uint16_t* pr = pcol + static_cast<int64_t>(ls[u] != -INFINITY ? 4 * i + u : 0) * G * D;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) xo[u][dt] = *reinterpret_cast<const uint2*>(pr + dt * 16);
+        }
+      };
+      const int nb = min(a.K, 4 * KB);
+#pragma unroll
+      for (int i = 0; i < KB; ++i) {
+        if (4 * i >= nb) break;
+        float ls[kUnionMergeBatch];
+        uint2 xo[kUnionMergeBatch][DT];
+        fetch(i, ls, xo);
+        merge(ls, xo);
+      }
+      // slots 32 and up (budgets above 32), a batch at a time
+      for (int s0 = 4 * KB; s0 < a.K; s0 += kUnionMergeBatch) {
+        float ls[kUnionMergeBatch];
+        uint2 xo[kUnionMergeBatch][DT];
+#pragma unroll
+        for (int u = 0; u < kUnionMergeBatch; ++u) {
+          const int sx = s0 + u;
+          const int x = sx < a.K ? sl[sx] : -1;
+          ls[u] = far(x) ? part_lse[(pb + sx) * G + hq] : -INFINITY;
+        }
+#pragma unroll
+        for (int u = 0; u < kUnionMergeBatch; ++u) {
+          const uint16_t* pr = pcol + static_cast<int64_t>(ls[u] != -INFINITY ? s0 + u : 0) * G * D;
+#pragma unroll
+          for (int dt = 0; dt < DT; ++dt) xo[u][dt] = *reinterpret_cast<const uint2*>(pr + dt * 16);
+        }
+        merge(ls, xo);
       }
     }
     if (!vrow[cg]) continue;
