@@ -754,21 +754,42 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnBlockArgs a, cons
       }
     }
   }
-  for (int slot = slot0 + grp; slot < a.K; slot += 4) {
-    const int blk = sel[slot];
-    if (blk < 0 || blk >= a.M1) continue;  // padding (no partial was written)
-    if (TAIL && (blk == 0 || blk == c || blk == c - 1)) continue;
-    const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + slot) * a.G + hh;
-    const float ls = part_lse[pidx];
-    if (ls == -INFINITY) continue;
-    float x[DPL];
-    load_row_part<uint16_t, DPL>(part_o + pidx * D + sub * DPL, x);
-    const float mn = fmaxf(m, ls);
-    const float c0 = fast_exp2(m - mn), c1 = fast_exp2(ls - mn);
-    s = s * c0 + c1;
+  // The group takes slots grp, grp + 4, ...: SPL of them at a time, their
+  // block indices, then their log-sums, then their partials each requested
+  // together.
+  constexpr int SPL = 4;
+  const int64_t pbase = (static_cast<int64_t>(bh) * a.nrows + rr) * a.K;
+  for (int s0 = slot0 + grp; s0 < a.K; s0 += 4 * SPL) {
+    int blk[SPL];
+    float ls[SPL];
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) acc[e] = acc[e] * c0 + x[e] * c1;
-    m = mn;
+    for (int i = 0; i < SPL; ++i) blk[i] = s0 + 4 * i < a.K ? sel[s0 + 4 * i] : -1;
+#pragma unroll
+    for (int i = 0; i < SPL; ++i) {
+      // padding (no partial was written); TAIL: the blocks merged before
+      const bool take = blk[i] >= 0 && blk[i] < a.M1 && !(TAIL && (blk[i] == 0 || blk[i] == c || blk[i] == c - 1));
+      ls[i] = take ? part_lse[(pbase + s0 + 4 * i) * a.G + hh] : -INFINITY;
+    }
+    float x[SPL][DPL];
+#pragma unroll
+    for (int i = 0; i < SPL; ++i) {
+      if (ls[i] != -INFINITY) {
+        load_row_part<uint16_t, DPL>(part_o + ((pbase + s0 + 4 * i) * a.G + hh) * D + sub * DPL, x[i]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) x[i][e] = 0.f;
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < SPL; ++i) {
+      if (ls[i] == -INFINITY) continue;
+      const float mn = fmaxf(m, ls[i]);
+      const float c0 = fast_exp2(m - mn), c1 = fast_exp2(ls[i] - mn);
+      s = s * c0 + c1;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) acc[e] = acc[e] * c0 + x[i][e] * c1;
+      m = mn;
+    }
   }
 #pragma unroll
   for (int msk = 16; msk <= 32; msk <<= 1) {

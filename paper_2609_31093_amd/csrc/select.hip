@@ -2200,22 +2200,6 @@ __global__ __launch_bounds__(256) void stage1_row_kernel(SelArgs a) {
   const int t = geo.N - a.Nq + row;
   const int c = t / geo.C;
 
-  float qv[GMAX][DPL];
-  {
-    const T* qb = static_cast<const T*>(a.q);
-#pragma unroll
-    for (int hh = 0; hh < GMAX; ++hh) {
-      if (hh < G) {
-        const int64_t off = ((static_cast<int64_t>(b) * a.H + h * G + hh) * a.Nq + row) * D + sub * DPL;
-        load_row_part<T, DPL>(qb + off, qv[hh]);
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) qv[hh][e] *= a.qscale2;
-      } else {
-#pragma unroll
-        for (int e = 0; e < DPL; ++e) qv[hh][e] = 0.f;
-      }
-    }
-  }
   auto n_eligible = [&](int lev) { return a.causal ? min(anc_at(geo, c, lev) + 1, geo.M[lev]) : geo.M[lev]; };
   int start = 1;
   for (int lev = geo.L; lev >= 2; --lev) {
@@ -2232,6 +2216,26 @@ __global__ __launch_bounds__(256) void stage1_row_kernel(SelArgs a) {
     if (lane == 0) s_n = nA;
   }
   __syncthreads();
+  // q is requested with the first level's child rows (a barrier waits for
+  // every outstanding load, and scaling q right after its load would too)
+  float qv[GMAX][DPL];
+  bool need_q = true;
+  auto load_q = [&]() __attribute__((always_inline)) {
+    const T* qb = static_cast<const T*>(a.q);
+#pragma unroll
+    for (int hh = 0; hh < GMAX; ++hh) {
+      if (hh < G) {
+        const int64_t off = ((static_cast<int64_t>(b) * a.H + h * G + hh) * a.Nq + row) * D + sub * DPL;
+        load_row_part<T, DPL>(qb + off, qv[hh]);
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) qv[hh][e] *= a.qscale2;
+      } else {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) qv[hh][e] = 0.f;
+      }
+    }
+    need_q = false;
+  };
 
   for (int lev = start; lev >= 2; --lev) {
     nA = s_n;
@@ -2255,6 +2259,7 @@ __global__ __launch_bounds__(256) void stage1_row_kernel(SelArgs a) {
           for (int i = 0; i < DPL; ++i) x[u][i] = 0.f;
         }
       }
+      if (need_q) load_q();
 #pragma unroll
       for (int u = 0; u < UNR; ++u) {
         const int e = e0 + 16 * u;
@@ -2338,16 +2343,14 @@ __global__ __launch_bounds__(256) void leaf_slot_kernel(SelArgs a, const int32_t
   const Geo& geo = a.geo;
   const int slot = blockIdx.x;
   const int64_t rg = blockIdx.y;  // bh * Nq + row
-  const int n = a1cnt[rg];
-  if (slot >= n || n <= a.K) return;
-  const int node = a1[rg * a.gK + slot];
   const int bh = static_cast<int>(rg / a.Nq), row = static_cast<int>(rg - static_cast<int64_t>(bh) * a.Nq);
-  const int c = (geo.N - a.Nq + row) / geo.C;
-  if (a.causal && (node == 0 || node == c || node == c - 1)) return;  // forced: never scored
   const int b = bh / a.Hkv, h = bh - b * a.Hkv;
   const int G = a.G;
   const int tid = threadIdx.x, grp = tid >> 4, sub = tid & 15;
-
+  // the candidate count, the slot's node (in bounds: slot < g*K) and q are
+  // requested together
+  const int n = a1cnt[rg];
+  const int node = a1[rg * a.gK + slot];
   float qv[GMAX][DPL];
   {
     const T* qb = static_cast<const T*>(a.q);
@@ -2364,6 +2367,9 @@ __global__ __launch_bounds__(256) void leaf_slot_kernel(SelArgs a, const int32_t
       }
     }
   }
+  if (slot >= n || n <= a.K) return;
+  const int c = (geo.N - a.Nq + row) / geo.C;
+  if (a.causal && (node == 0 || node == c || node == c - 1)) return;  // forced: never scored
   const int r0 = node * geo.C;
   const int nrows = min(geo.C, geo.N - r0);
   const T* kb = static_cast<const T*>(a.k) + (static_cast<int64_t>(bh) * geo.Nkv + r0) * D + sub * DPL;
