@@ -18,9 +18,13 @@
 // the forward's o partials); P^T, dS^T, q and do of the group go to LDS and
 // the four wavefronts then add dV += P^T do and dK += dS^T q for their
 // quarter of the head dimension, accumulating over the whole chunk in
-// registers.  At the end each chunk adds its dK, dV into fp32 accumulators.
+// registers.  At the end a chunk writes its dK, dV rows in the problem dtype
+// when it is its block's only chunk and the launch covers every row, else
+// adds them into fp32 accumulators.
 // attn_bwd_dq_kernel: dq of each row = the sum of its slots' partials.
-// attn_bwd_finalize_kernel: dK, dV accumulators to the problem dtype.
+// attn_bwd_blocks_kernel / attn_bwd_finalize_kernel: the accumulators (of the
+// blocks with several chunks, or all of them) to the problem dtype, and zero
+// rows for keys nothing selected.
 #include <algorithm>
 
 #include "common.h"
@@ -40,6 +44,9 @@ struct AttnBwdArgs {
   float qscale2;    // log2(e) / sqrt(d)
   float rscale;     // 1 / sqrt(d)
   int Nkv;          // rows per (batch, KV head) in k, v, dk, dv
+  // one launch covers every row: a block whose pairs fit one chunk writes
+  // its dK, dV rows directly in the problem dtype
+  int direct = 0;
 };
 
 __device__ __forceinline__ bf16x8b2 u4_bf16x8b2(uint4 r) { return __builtin_bit_cast(bf16x8b2, r); }
@@ -108,7 +115,8 @@ __global__ __launch_bounds__(256, bwd_compact(CT * 32) ? 2 : 1) void attn_bwd_bl
     AttnBwdArgs a, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k, const uint16_t* __restrict__ v,
     const uint16_t* __restrict__ dO, const float2* __restrict__ stat, const int32_t* __restrict__ offs,
     const int32_t* __restrict__ toffs, int64_t ncl, const int32_t* __restrict__ pairs, uint16_t* __restrict__ part_dq,
-    float* __restrict__ dk_acc, float* __restrict__ dv_acc) {
+    float* __restrict__ dk_acc, float* __restrict__ dv_acc, uint16_t* __restrict__ dk_out,
+    uint16_t* __restrict__ dv_out) {
   constexpr int KS = D / 32;      // 32-dim k-steps of S^T and dP^T
   constexpr int LDK = D + 8;      // padded K / V row (bf16)
   constexpr int C = CT * 32;      // keys per block
@@ -322,6 +330,29 @@ __global__ __launch_bounds__(256, bwd_compact(CT * 32) ? 2 : 1) void attn_bwd_bl
   }
 
   // accv[mt][jj][i]: key mt*16 + 4*grp + i, dim (wave*DTW + jj)*16 + col
+  if (a.direct && toffs[cl + 1] - toffs[cl] == 1) {
+    // the block's only chunk: dV, dK in the problem dtype, two dims per
+    // 4-byte store (even lanes dV, odd lanes dK, each with its neighbour's value)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = mt * 16 + 4 * grp + i;
+        if (key >= nkeys) continue;  // the same for both lanes of a pair
+        const int64_t base = (static_cast<int64_t>(bh) * a.Nkv + r0 + key) * D;
+#pragma unroll
+        for (int jj = 0; jj < DTW; ++jj) {
+          const int dcol = (wave * DTW + jj) * 16 + (col & ~1);
+          const float vv = accv[mt][jj][i], kv = acck[mt][jj][i] * a.rscale;
+          const float vn = __shfl_xor(vv, 1), kn = __shfl_xor(kv, 1);
+          if (col & 1)
+            *reinterpret_cast<uint32_t*>(dk_out + base + dcol) = pack2_bf16(kn, kv);
+          else
+            *reinterpret_cast<uint32_t*>(dv_out + base + dcol) = pack2_bf16(vv, vn);
+        }
+      }
+    return;
+  }
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -385,6 +416,53 @@ __global__ __launch_bounds__(256) void fill_zero_f32_kernel(float* p, int64_t n)
   for (int64_t i = blockIdx.x * 256LL + threadIdx.x; i < n; i += 256LL * gridDim.x) p[i] = 0.f;
 }
 
+// Direct launches: one wavefront per (batch x KV head, key block), from the
+// cluster's chunk offsets.  Before the block kernel: the fp32 accumulator rows
+// of blocks with several chunks are cleared.  After it: those rows go to the
+// problem dtype, and blocks no pair selected get zero rows (a block with one
+// chunk was written by the block kernel itself).
+template <int D, bool AFTER>
+__global__ __launch_bounds__(256) void attn_bwd_blocks_kernel(AttnBwdArgs a, int BH, const int32_t* __restrict__ toffs,
+                                                              float* __restrict__ dk_acc, float* __restrict__ dv_acc,
+                                                              uint16_t* __restrict__ dk, uint16_t* __restrict__ dv) {
+  const int64_t w = static_cast<int64_t>(blockIdx.x) * 4 + (threadIdx.x >> 6);
+  if (w >= static_cast<int64_t>(BH) * a.M1) return;
+  const int lane = threadIdx.x & 63;
+  const int nch = toffs[w + 1] - toffs[w];
+  if (nch == 1 || (!AFTER && nch == 0)) return;
+  const int bh = static_cast<int>(w / a.M1), blk = static_cast<int>(w - static_cast<int64_t>(bh) * a.M1);
+  const int r0 = blk * a.C;
+  const int64_t e0 = (static_cast<int64_t>(bh) * a.Nkv + r0) * D;
+  const int n4 = min(a.C, a.N - r0) * D / 4;  // float4 groups of the block's rows
+  for (int e = lane; e < n4; e += 64) {
+    if constexpr (!AFTER) {
+      reinterpret_cast<float4*>(dk_acc + e0)[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+      reinterpret_cast<float4*>(dv_acc + e0)[e] = make_float4(0.f, 0.f, 0.f, 0.f);
+    } else {
+      float4 x = make_float4(0.f, 0.f, 0.f, 0.f), y = x;
+      if (nch > 1) {
+        x = reinterpret_cast<const float4*>(dk_acc + e0)[e];
+        y = reinterpret_cast<const float4*>(dv_acc + e0)[e];
+      }
+      reinterpret_cast<uint2*>(dk + e0)[e] = make_uint2(pack2_bf16(x.x, x.y), pack2_bf16(x.z, x.w));
+      reinterpret_cast<uint2*>(dv + e0)[e] = make_uint2(pack2_bf16(y.x, y.y), pack2_bf16(y.z, y.w));
+    }
+  }
+}
+
+// Zero rows [N, Nkv) of every (batch, KV head) of dk and dv.
+template <int D>
+__global__ __launch_bounds__(256) void attn_bwd_tail_kernel(int BH, int N, int Nkv, uint16_t* __restrict__ dk,
+                                                            uint16_t* __restrict__ dv) {
+  const int64_t per = static_cast<int64_t>(Nkv - N) * D / 4;  // uint2 groups per head
+  for (int64_t i = blockIdx.x * 256LL + threadIdx.x; i < BH * per; i += 256LL * gridDim.x) {
+    const int64_t bh = i / per, e = i - bh * per;
+    const int64_t off = (bh * Nkv + N) * D / 4 + e;
+    reinterpret_cast<uint2*>(dk)[off] = make_uint2(0u, 0u);
+    reinterpret_cast<uint2*>(dv)[off] = make_uint2(0u, 0u);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Host side.
 // ---------------------------------------------------------------------------
@@ -441,25 +519,36 @@ static hipError_t launch_bwd_d(const Shape& s, const Geo& geo, const void* q, co
                 kLog2e / sqrtf(static_cast<float>(s.D)), 1.0f / sqrtf(static_cast<float>(s.D)), s.Nkv};
   hipError_t e;
   const int64_t nkv = static_cast<int64_t>(s.BH()) * s.Nkv * D;
+  const int ch = bwd_chunk_rows(s);
+  a.direct = ch >= s.Nq ? 1 : 0;
+  const int64_t nblk = static_cast<int64_t>(s.BH()) * geo.M[1];
+  uint16_t* dk16 = static_cast<uint16_t*>(dk);
+  uint16_t* dv16 = static_cast<uint16_t*>(dv);
   {
     ProfScope ps("attn_bwd_prep", st);
-    fill_zero_f32_kernel<<<static_cast<unsigned>(std::min<int64_t>((nkv + 255) / 256, 8192)), 256, 0, st>>>(dk_acc,
-                                                                                                           nkv);
-    fill_zero_f32_kernel<<<static_cast<unsigned>(std::min<int64_t>((nkv + 255) / 256, 8192)), 256, 0, st>>>(dv_acc,
-                                                                                                           nkv);
+    if (!a.direct) {
+      fill_zero_f32_kernel<<<static_cast<unsigned>(std::min<int64_t>((nkv + 255) / 256, 8192)), 256, 0, st>>>(
+          dk_acc, nkv);
+      fill_zero_f32_kernel<<<static_cast<unsigned>(std::min<int64_t>((nkv + 255) / 256, 8192)), 256, 0, st>>>(
+          dv_acc, nkv);
+    }
     const int64_t nrh = static_cast<int64_t>(s.B) * s.H * s.Nq;
     attn_bwd_prep_kernel<D><<<static_cast<unsigned>((nrh + 15) / 16), 256, 0, st>>>(
         a, static_cast<const uint16_t*>(o), dd, lse, stat, nrh);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
-  const int ch = bwd_chunk_rows(s);
+  ClusterOut co{};
   for (int row0 = 0; row0 < s.Nq; row0 += ch) {
     const int nrows = std::min(ch, s.Nq - row0);
     a.row0 = row0;
     a.nrows = nrows;
     ClusterArgs ca{idx, nullptr, s.K, s.Nq, s.N, s.C, s.K, s.causal, geo.M[1], kClusterAttn, row0, nrows, s.g};
-    ClusterOut co{};
     if ((e = launch_cluster(ca, s.BH(), base + w.cl, &co, st, kBwdChunk)) != hipSuccess) return e;
+    if (a.direct) {
+      ProfScope ps("attn_bwd_prep", st);
+      attn_bwd_blocks_kernel<D, false><<<static_cast<unsigned>((nblk + 3) / 4), 256, 0, st>>>(
+          a, s.BH(), co.toffs, dk_acc, dv_acc, dk16, dv16);
+    }
     {
       ProfScope ps("attn_bwd_block", st);
       const int64_t np = static_cast<int64_t>(s.BH()) * nrows * s.K;
@@ -469,7 +558,7 @@ static hipError_t launch_bwd_d(const Shape& s, const Geo& geo, const void* q, co
         (void)hipFuncSetAttribute(reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize,
                                   static_cast<int>(lds));
         kern<<<grid, 256, lds, st>>>(a, qq, kk, vv, dd, stat, co.offs, co.toffs, co.ncl, co.pairs, part, dk_acc,
-                                     dv_acc);
+                                     dv_acc, dk16, dv16);
       };
       if (s.C == 32)
         go(attn_bwd_block_kernel<D, 1>);
@@ -489,9 +578,19 @@ static hipError_t launch_bwd_d(const Shape& s, const Geo& geo, const void* q, co
   }
   {
     ProfScope ps("attn_bwd_finalize", st);
-    const int64_t n4 = nkv / 4;
-    attn_bwd_finalize_kernel<<<static_cast<unsigned>((n4 + 255) / 256), 256, 0, st>>>(
-        dk_acc, dv_acc, static_cast<uint16_t*>(dk), static_cast<uint16_t*>(dv), n4);
+    if (a.direct) {
+      attn_bwd_blocks_kernel<D, true><<<static_cast<unsigned>((nblk + 3) / 4), 256, 0, st>>>(
+          a, s.BH(), co.toffs, dk_acc, dv_acc, dk16, dv16);
+      if (s.Nkv > s.N) {
+        const int64_t tail = static_cast<int64_t>(s.BH()) * (s.Nkv - s.N) * D / 4;
+        attn_bwd_tail_kernel<D><<<static_cast<unsigned>(std::min<int64_t>((tail + 255) / 256, 8192)), 256, 0, st>>>(
+            s.BH(), s.N, s.Nkv, dk16, dv16);
+      }
+    } else {
+      const int64_t n4 = nkv / 4;
+      attn_bwd_finalize_kernel<<<static_cast<unsigned>((n4 + 255) / 256), 256, 0, st>>>(dk_acc, dv_acc, dk16, dv16,
+                                                                                         n4);
+    }
   }
   return hipGetLastError();
 }

@@ -85,6 +85,38 @@ def test_attention_backward_untouched_rows_are_zero():
     assert (dk[0, 0, reached.cuda()] != 0).any()
 
 
+def test_attention_backward_reserved_rows():
+    """With rows reserved past N (Ncap > N, the decode cache's layout; the
+    reserved k and v rows hold NaN), dq equals the unreserved run's bit for
+    bit, dk and dv on rows [0, N) equal it up to the fp32 summation order (the
+    pair order inside a block's cluster varies between runs), and dk, dv are
+    zero on rows [N, Ncap) whatever the buffers held before."""
+    B, H, Hkv, Nq, N, d, C, K, cap = 1, 4, 2, 700, 1000, 128, 64, 5, 1300
+    x = inputs.random_qkv(B, H, Hkv, Nq, N, d, "bf16", seed=8)
+    q, k, v = (torch.from_numpy(x[n]).to(torch.bfloat16).cuda() for n in "qkv")
+    d_o = torch.randn((B, H, Nq, d), device="cuda").to(torch.bfloat16)
+    p = pisa.make_problem(B, H, Hkv, Nq, N, d, C, 2, K, 1, "bf16")
+    idx = pisa.select(p, q, k, pisa.build_pyramid(p, k))
+    o, lse = pisa.sparse_attn_fwd(p, q, k, v, idx)
+    dq0, dk0, dv0 = pisa.sparse_attn_bwd(p, q, k, v, idx, o, lse, d_o)
+    pc = pisa.make_problem(B, H, Hkv, Nq, N, d, C, 2, K, 1, "bf16", Ncap=cap)
+    kc = torch.full((B, Hkv, cap, d), float("nan"), device="cuda", dtype=torch.bfloat16)
+    vc = kc.clone()
+    kc[:, :, :N] = k
+    vc[:, :, :N] = v
+    dq = torch.full_like(q, float("nan"))
+    dk = torch.full_like(kc, float("nan"))
+    dv = torch.full_like(vc, float("nan"))
+    nb = pisa.pisa_attn_bwd_workspace_bytes(pc)
+    ws = torch.empty(max(nb, 1), dtype=torch.uint8, device="cuda")
+    pisa.pisa_sparse_attn_bwd(pc, q, kc, vc, idx, o, lse, d_o, dq, dk, dv, ws, nb, None)
+    torch.cuda.synchronize()
+    assert torch.equal(dq, dq0)
+    for got, want in ((dk[:, :, :N], dk0), (dv[:, :, :N], dv0)):
+        assert torch.allclose(got.float(), want.float(), rtol=2e-2, atol=2e-2 * float(want.float().abs().max()))
+    assert (dk[:, :, N:] == 0).all() and (dv[:, :, N:] == 0).all()
+
+
 def test_attention_backward_needles_128k():
     """At the needle workload's full size, in the launch configuration bench.py
     --backward times: dq of sampled rows against the oracle (a row's dq depends
