@@ -156,6 +156,43 @@ def test_attention_backward_needles_128k():
     assert np.abs(got - want).max() <= REL * np.abs(want).max()
 
 
+def test_attention_backward_across_row_chunks():
+    """More (row, slot) pairs than one launch's partial budget (4 GiB of dq
+    partials), so the rows go in four chunks and every key block adds into the
+    fp32 accumulators across launches: sampled rows' dq against the oracle and
+    the two per-KV-head identities of the full-size test."""
+    B, H, Hkv, Nq, N, d, C, g, K = 1, 16, 2, 60000, 60000, 128, 64, 2, 64
+    x = inputs.random_qkv(B, H, Hkv, Nq, N, d, "bf16", seed=12)
+    q, k, v = (torch.from_numpy(x[n]).to(torch.bfloat16).cuda() for n in "qkv")
+    gen = torch.Generator(device="cuda").manual_seed(13)
+    d_o = torch.randn((B, H, Nq, d), device="cuda", generator=gen).to(torch.bfloat16)
+    p = pisa.make_problem(B, H, Hkv, Nq, N, d, C, g, K, 1, "bf16")
+    per_row = B * Hkv * K * (H // Hkv) * d * 2  # bytes of dq partials per row
+    assert per_row * Nq > 3 * (4 << 30), "the shape must span several row chunks"
+    idx = pisa.select(p, q, k, pisa.build_pyramid(p, k))
+    o, lse = pisa.sparse_attn_fwd(p, q, k, v, idx)
+    dq, dk, dv = pisa.sparse_attn_bwd(p, q, k, v, idx, o, lse, d_o)
+    torch.cuda.synchronize()
+    sdv = dv.double().sum(2)
+    sdo = d_o.double().view(B, Hkv, H // Hkv, Nq, d).sum((2, 3))
+    assert (sdv - sdo).abs().max().item() <= 1e-2 * sdo.abs().max().item() + 1.0
+    sdk = dk.double().sum(2)
+    assert sdk.abs().max().item() <= 2e-3 * dk.double().abs().sum(2).max().item()
+    rows = [0, 1, 16383, 16384, 30000, 32768, Nq - 1]  # both sides of the chunk boundaries
+    do_np = d_o.float().cpu().numpy()
+    sel = idx.cpu().numpy()
+    want, got = [], []
+    for hq in (0, 11):
+        hk = hq // (H // Hkv)
+        kh, vh = x["k"][0, hk].astype(np.float64), x["v"][0, hk].astype(np.float64)
+        for r in rows:
+            t = N - Nq + r
+            want.append(O.attention_row_bwd(x["q"][0, hq, r], kh, vh, sel[0, hk, r], t, C, True, do_np[0, hq, r])[0])
+            got.append(dq[0, hq, r].float().cpu().numpy())
+    want, got = np.array(want), np.array(got)
+    assert np.abs(got - want).max() <= REL * np.abs(want).max()
+
+
 def test_backward_out_of_range_indices_are_padding():
     """Entries at or past ceil(N/C) add nothing to any gradient."""
     B, H, Hkv, Nq, N, d, C, K, causal = SHAPES["gqa2-c64"]
