@@ -387,13 +387,33 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_kernel(AttnBwdArgs a, const i
   float acc[DPL];
 #pragma unroll
   for (int e = 0; e < DPL; ++e) acc[e] = 0.f;
-  for (int s = 0; s < a.K; ++s) {
-    if (sel[s] < 0 || sel[s] >= a.M1) continue;  // padding: no partial was written
-    const int64_t pidx = ((static_cast<int64_t>(bh) * a.nrows + rr) * a.K + s) * a.G + hh;
-    float x[DPL];
-    load_row_part<uint16_t, DPL>(part_dq + pidx * D + sub * DPL, x);
+  // four slots' indices, then their partials, requested together (the sum
+  // keeps the slot order)
+  constexpr int SB = 4;
+  const int64_t pbase = (static_cast<int64_t>(bh) * a.nrows + rr) * a.K;
+  for (int s0 = 0; s0 < a.K; s0 += SB) {
+    bool use[SB];
 #pragma unroll
-    for (int e = 0; e < DPL; ++e) acc[e] += x[e];
+    for (int u = 0; u < SB; ++u) {
+      const int x = s0 + u < a.K ? sel[s0 + u] : -1;
+      use[u] = x >= 0 && x < a.M1;  // padding: no partial was written
+    }
+    float x[SB][DPL];
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      if (use[u]) {
+        load_row_part<uint16_t, DPL>(part_dq + ((pbase + s0 + u) * a.G + hh) * D + sub * DPL, x[u]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) x[u][e] = 0.f;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < SB; ++u) {
+      if (!use[u]) continue;
+#pragma unroll
+      for (int e = 0; e < DPL; ++e) acc[e] += x[u][e];
+    }
   }
   const int64_t orow = (static_cast<int64_t>(b) * a.H + hq) * a.Nq + row;
   store_bf16_part<DPL>(dq + orow * D + sub * DPL, acc);
