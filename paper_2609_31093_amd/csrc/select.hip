@@ -1742,53 +1742,75 @@ __global__ __launch_bounds__(NWAVE * 64) void stage1_g2_kernel(SelArgs a) {
   g2_store_leaves(a, bh, row, live, hl, hbase, node);
 }
 
-// Final Top-K for g*K <= 32: two rows per wavefront, one candidate per lane
-// (the candidates arrive in ascending block order).  sort32 ranks them
+// Final Top-K for g*K <= 32: a row per 32-lane half of a wavefront (RP such
+// pairs of rows per wavefront), one candidate per lane (the candidates
+// arrive in ascending block order).  sort32 ranks them
 // (forced and unranked rows keyed +inf); the rank of each lane's own
 // candidate comes back through LDS and the kept ones are compacted in their
 // original, ascending order with a prefix sum.
+template <int RP>
 __global__ __launch_bounds__(256) void final_topk_pair_kernel(TopkArgsP a, const int32_t* __restrict__ a1,
                                                               const int32_t* __restrict__ a1cnt,
                                                               const float* __restrict__ u1,
                                                               int32_t* __restrict__ idx, float* __restrict__ score) {
-  __shared__ int s_rank[4][64];
+  __shared__ int s_rank[4][RP][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int half = lane >> 5, hl = lane & 31;
-  const int64_t rg = (blockIdx.x * 4LL + wave) * 2 + half;
-  const bool live = rg < a.rows;
-  const int64_t rgc = live ? rg : a.rows - 1;
-  const int row = static_cast<int>(rgc % a.Nq);
-  const int c = (a.N - a.Nq + row) / a.C;
-  // the three loads of a row are independent (slots past the count hold
-  // stale workspace values that are masked below)
-  const int slot = min(hl, a.gK - 1);
-  const int n = a1cnt[rgc];
-  const int node_raw = a1[rgc * a.gK + slot];
-  const float u_raw = u1[rgc * a.gK + slot];
-  const bool ranked = n > a.K;
-  const bool valid = hl < n;
-  const int node = valid ? node_raw : -1;
-  const bool isf = a.causal && valid && (node == 0 || node == c || node == c - 1);
-  float key = -INFINITY;
-  if (valid) key = (ranked && !isf) ? u_raw : INFINITY;
-  const float own = key;
-  int pack = valid ? (node << 6) | hl : 0x7FFFFFC0 | hl;
-  // lane p of the sorted half holds rank p (with K = 16 only the best 16 are
+  // RP pairs of rows per wavefront, processed side by side (independent
+  // chains whose memory and lane-exchange latencies overlap)
+  int64_t rg[RP];
+  bool live[RP];
+  int n[RP], node_raw[RP], c[RP];
+  float u_raw[RP];
+#pragma unroll
+  for (int p = 0; p < RP; ++p) {
+    rg[p] = ((blockIdx.x * 4LL + wave) * RP + p) * 2 + half;
+    live[p] = rg[p] < a.rows;
+    const int64_t rgc = live[p] ? rg[p] : a.rows - 1;
+    const int row = static_cast<int>(rgc % a.Nq);
+    c[p] = (a.N - a.Nq + row) / a.C;
+    // the three loads of a row are independent (slots past the count hold
+    // stale workspace values that are masked below)
+    const int slot = min(hl, a.gK - 1);
+    n[p] = a1cnt[rgc];
+    node_raw[p] = a1[rgc * a.gK + slot];
+    u_raw[p] = u1[rgc * a.gK + slot];
+  }
+  float key[RP], own[RP];
+  int pack[RP], node[RP];
+  bool valid[RP];
+#pragma unroll
+  for (int p = 0; p < RP; ++p) {
+    const bool ranked = n[p] > a.K;
+    valid[p] = hl < n[p];
+    node[p] = valid[p] ? node_raw[p] : -1;
+    const bool isf = a.causal && valid[p] && (node[p] == 0 || node[p] == c[p] || node[p] == c[p] - 1);
+    key[p] = -INFINITY;
+    if (valid[p]) key[p] = (ranked && !isf) ? u_raw[p] : INFINITY;
+    own[p] = key[p];
+    pack[p] = valid[p] ? (node[p] << 6) | hl : 0x7FFFFFC0 | hl;
+  }
+  // lane q of the sorted half holds rank q (with K = 16 only the best 16 are
   // separated from the rest); send it back to the source lane
-  sort32_top16(key, pack, hl, a.K != 16);
-  s_rank[wave][(lane & 32) + (pack & 63)] = hl;
+#pragma unroll
+  for (int p = 0; p < RP; ++p) sort32_top16(key[p], pack[p], hl, a.K != 16);
+#pragma unroll
+  for (int p = 0; p < RP; ++p) s_rank[wave][p][(lane & 32) + (pack[p] & 63)] = hl;
   wave_sync();
-  const bool kept = valid && s_rank[wave][lane] < a.K;
-  const int incl = scan32(kept ? 1 : 0, hl);
-  if (live) {
-    const int total = half_total(incl, lane);
-    if (kept) {
-      idx[rg * a.K + incl - 1] = node;
-      if (score) score[rg * a.K + incl - 1] = (own == INFINITY) ? INFINITY : own * kLn2;
-    }
-    if (hl >= total && hl < a.K) {
-      idx[rg * a.K + hl] = -1;
-      if (score) score[rg * a.K + hl] = -INFINITY;
+#pragma unroll
+  for (int p = 0; p < RP; ++p) {
+    const bool kept = valid[p] && s_rank[wave][p][lane] < a.K;
+    const int incl = scan32(kept ? 1 : 0, hl);
+    if (live[p]) {
+      const int total = half_total(incl, lane);
+      if (kept) {
+        idx[rg[p] * a.K + incl - 1] = node[p];
+        if (score) score[rg[p] * a.K + incl - 1] = (own[p] == INFINITY) ? INFINITY : own[p] * kLn2;
+      }
+      if (hl >= total && hl < a.K) {
+        idx[rg[p] * a.K + hl] = -1;
+        if (score) score[rg[p] * a.K + hl] = -INFINITY;
+      }
     }
   }
 }
@@ -2295,7 +2317,12 @@ __global__ __launch_bounds__(256) void stage1_row_kernel(SelArgs a) {
       bool kept = valid;
       if (ranked) {
         int pack = valid ? node : 0x7FFFFFC0 | lane;
-        sort64(key, pack, lane);
+        // at most 32 candidates (g*K <= 32) sit in lanes 0-31: a 32-lane
+        // sort (with K = 16 only the best 16 separated from the rest) ranks them
+        if (a.gK <= 32)
+          sort32_top16(key, pack, lane & 31, K != 16);
+        else
+          sort64(key, pack, lane);
         kept = lane < K && key != -INFINITY;
         knode = pack;
       }
@@ -2318,7 +2345,10 @@ __global__ __launch_bounds__(256) void stage1_row_kernel(SelArgs a) {
     // leaf candidate set, ascending
     float akey = node >= 0 ? -static_cast<float>(node) : -INFINITY;
     int apack = node >= 0 ? node : 0x7FFFFFC0 | lane;
-    sort64(akey, apack, lane);
+    if (a.gK <= 32)
+      sort32(akey, apack, lane & 31);
+    else
+      sort64(akey, apack, lane);
     const int64_t orow = static_cast<int64_t>(bh) * a.Nq + row;
     if (lane < a.gK) a.a1[orow * a.gK + lane] = lane < nA ? apack : -1;
     if (lane == 0) a.a1cnt[orow] = nA;
@@ -2528,7 +2558,12 @@ static hipError_t launch_final_topk(const Shape& s, const int32_t* a1, const int
   ProfScope ps("final_topk", st);
   if (s.gK() <= 32) {
     TopkArgsP ta{s.Nq, s.N, s.C, s.K, s.gK(), s.causal, rows};
-    final_topk_pair_kernel<<<static_cast<unsigned>((rows + 7) / 8), 256, 0, st>>>(ta, a1, a1cnt, u1, idx, score);
+    if (rows >= 65536)  // two row pairs per wavefront once the grid fills the GPU several times over
+      final_topk_pair_kernel<2><<<static_cast<unsigned>((rows + 15) / 16), 256, 0, st>>>(ta, a1, a1cnt, u1, idx,
+                                                                                        score);
+    else
+      final_topk_pair_kernel<1><<<static_cast<unsigned>((rows + 7) / 8), 256, 0, st>>>(ta, a1, a1cnt, u1, idx,
+                                                                                       score);
   } else {
     TopkArgs ta{s.Nq, s.N, s.C, s.K, s.gK(), s.causal, rows};
     final_topk_kernel<<<static_cast<unsigned>((rows + 3) / 4), 256, 0, st>>>(ta, a1, a1cnt, u1, idx, score);
