@@ -20,7 +20,8 @@ import torch
 
 import oracle as O
 from paper_2609_31093_amd import inputs
-from tests.helpers import check_flat_bsa_rows, check_selection_rows, check_selection_valid, dev, pyramid_error_bound
+from tests.helpers import (check_flat_bsa_rows, check_selection_rows, check_selection_valid, check_valid_all_rows, dev,
+                           pyramid_error_bound)
 
 pytestmark = pytest.mark.gpu
 
@@ -334,3 +335,21 @@ def test_flat_bsa_all_scores_tied(G):
         c = (N - Nq + r) // C
         want = sorted({0, c - 1, c} | set(range(1, K - 2)))   # K - 3 unforced: blocks 1 .. K - 3
         assert list(idx[0, 0, r]) == want, (r, idx[0, 0, r])
+
+
+def test_select_large_ragged_grid():
+    """A grid past 65536 (batch x KV head x row) rows whose count is not a
+    multiple of the final Top-K's rows per workgroup (16 there, two row pairs
+    per wavefront): the last rows and sampled others against the oracle, and
+    every row a valid selection."""
+    B, H, Hkv, N, d, C, g, K = 1, 1, 1, 65541, 128, 64, 2, 16
+    x = inputs.random_qkv(B, H, Hkv, N, N, d, "bf16", seed=21)
+    q, k = (torch.from_numpy(x[n]).to(torch.bfloat16).cuda() for n in "qk")
+    p = pisa.make_problem(B, H, Hkv, N, N, d, C, g, K, 1, "bf16")
+    assert (B * Hkv * N) % 16 != 0 and B * Hkv * N >= 65536
+    idx, sc = pisa.select(p, q, k, pisa.build_pyramid(p, k), with_score=True)
+    torch.cuda.synchronize()
+    idx_np = idx.cpu().numpy()
+    check_valid_all_rows(idx_np, N, N, C, K, True)
+    rows = np.unique(np.concatenate([np.arange(N - 18, N), np.random.default_rng(22).choice(N, 14, replace=False)]))
+    check_selection_rows(x["q"], x["k"], C, g, K, True, idx_np[:, :, rows], rows, gpu_score=sc.cpu().numpy()[:, :, rows])
